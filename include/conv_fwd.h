@@ -1,0 +1,179 @@
+/*
+ * conv_fwd.h -- C ABI of the MI355X (gfx950) forward-convolution library.
+ *
+ * The operation (Sec. 1, Eq. (1); loop bounds of Listing 2):
+ *
+ *   Out[n][k][h][w] = sum_{c<C, r<R, s<S} In[n][c][h+r][w+s] * Ker[k][c][r][s]
+ *
+ * for n < N, k < K, h < P = H-R+1, w < Q = W-S+1.  H and W are the *input*
+ * height and width (caption of Table 1); the correlation is valid (no
+ * padding), stride 1, with no kernel flip.  Out is overwritten (beta = 0).
+ *
+ * Layouts (Sec. 9, artifact appendix): In is NCHW, Ker is KCRS, Out is NKPQ;
+ * all dense, contiguous, row-major.  Only element alignment is required.
+ *
+ * Loop order and tile sizes are chosen per shape by a tile selector built on
+ * the paper's data-movement model (Sec. 3-5, Algorithm 1 of Sec. 8),
+ * re-derived for the gfx950 memory hierarchy; see conv_fwd_plan.
+ *
+ * Ownership: every tensor pointer is DEVICE memory allocated and freed by
+ * the caller.  The library keeps a host-side plan cache only and makes no
+ * device allocation.  In, Ker and Out must not overlap.
+ *
+ * Asynchrony: the compute calls enqueue kernels on `stream` (a hipStream_t;
+ * NULL = the default stream) and return without synchronising.  A return of
+ * CONV_OK means the launch was enqueued; faults inside the kernel surface at
+ * the caller's next synchronisation.
+ *
+ * Errors: on any error the call launches nothing and leaves Out untouched.
+ * Thread safety: all entry points are reentrant.
+ */
+#ifndef CONV_FWD_H
+#define CONV_FWD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CONV_OK = 0,
+  CONV_EINVAL = -1,  /* an extent <= 0, R > H, S > W, or a bad plan/option */
+  CONV_ENULL = -2,   /* a null tensor or output-struct pointer */
+  CONV_ERANGE = -3,  /* a tensor of 2^31 elements or more */
+  CONV_ENOPLAN = -4, /* no kernel configuration fits the shape */
+  CONV_EHIP = -5     /* the HIP runtime reported an error at launch */
+} conv_status_t;
+
+/* Element types of In and Ker (Out and accumulation are always fp32). */
+enum { CONV_DTYPE_F32 = 0, CONV_DTYPE_BF16 = 1 };
+
+/* Memory levels of the model, innermost first. */
+enum {
+  CONV_LVL_REG = 0,  /* LDS -> VGPR operand traffic of the wave tiles      */
+  CONV_LVL_LDS = 1,  /* L2 -> LDS traffic of the workgroup tiles           */
+  CONV_LVL_L2 = 2,   /* MALL/HBM -> L2 traffic of the per-XCD tile sets    */
+  CONV_LVL_HBM = 3,  /* device-memory traffic (compulsory In, Ker, Out)    */
+  CONV_NUM_LVLS = 4
+};
+
+/*
+ * A tile plan: one point of the search space of Algorithm 1 (Sec. 8) for the
+ * gfx950 kernel, with the model's prediction of its data movement.
+ *
+ * The workgroup (LDS-level) tile covers `tile_k` output channels and a block
+ * of output pixels: `tile_rows` consecutive output rows of the flattened
+ * (n, h) row index times `tile_cols` consecutive columns, with `tile_c` input
+ * channels staged per pipeline step (all R x S taps at once).  The wave
+ * (register-level) tile is `wave_k` x `wave_px`; accumulators stay in
+ * registers for the whole reduction (the Out-stationary classes
+ * <{n,k,h,w},{c,r},s> / <{n,k,h,w},{c,s},r> of Sec. 4).
+ */
+typedef struct {
+  int dtype;          /* CONV_DTYPE_*                                        */
+  int variant;        /* internal kernel variant id (opaque)                 */
+  int tile_k;         /* output channels per workgroup                      */
+  int tile_rows;      /* output rows (flattened n*P+h) per workgroup         */
+  int tile_cols;      /* output columns per workgroup                        */
+  int tile_c;         /* input channels per pipeline step                    */
+  int wave_k;         /* output channels per wave                            */
+  int wave_px;        /* output pixels per wave (multiple of 16)             */
+  int waves_k;        /* waves along k in a workgroup                        */
+  int waves_px;       /* waves along pixels in a workgroup                   */
+  int grid_order;     /* 0: k tiles innermost in the workgroup order (In reuse
+                         in L2); 1: pixel tiles innermost (Ker reuse)        */
+  int lds_bytes;      /* dynamic LDS per workgroup                           */
+  int64_t num_wg;     /* workgroups launched                                 */
+  int class_lvl[CONV_NUM_LVLS]; /* paper class 1..8 (Sec. 4) per level, 0 = n/a */
+  double pred_bytes[CONV_NUM_LVLS]; /* modelled bytes moved at each level    */
+  double pred_us[CONV_NUM_LVLS];    /* bytes / bandwidth of each level, us   */
+  double pred_mfma_us;              /* MFMA time incl. padding and waves, us */
+  double pred_total_us;             /* max over the above (Sec. 5 min-max)   */
+} conv_plan_t;
+
+/*
+ * fp32 forward convolution, Eq. (1).
+ *   In  : [N][C][H][W]           fp32, device
+ *   Ker : [K][C][R][S]           fp32, device
+ *   Out : [N][K][H-R+1][W-S+1]   fp32, device, overwritten
+ * Returns a conv_status_t.
+ */
+int conv_fwd(int N, int C, int K, int H, int W, int R, int S,
+             const float* In, const float* Ker, float* Out, void* stream);
+
+/*
+ * bf16-input forward convolution, Eq. (1): In and Ker hold bfloat16 bit
+ * patterns (uint16, same layouts as above); products and sums are formed in
+ * fp32 and Out is fp32.  Returns a conv_status_t.
+ */
+int conv_fwd_bf16(int N, int C, int K, int H, int W, int R, int S,
+                  const uint16_t* In, const uint16_t* Ker, float* Out, void* stream);
+
+/*
+ * Host-only: the tile plan the selector picks for this shape and dtype
+ * (CONV_DTYPE_*), with its modelled per-level bytes.  Cached per shape.
+ * Makes no HIP call.  Returns a conv_status_t.
+ */
+int conv_fwd_plan(int N, int C, int K, int H, int W, int R, int S, int dtype,
+                  conv_plan_t* plan_out);
+
+/*
+ * Forward convolution with an explicit plan (as returned by conv_fwd_plan,
+ * possibly with other tile fields, e.g. for model-validation sweeps).  The
+ * plan is re-validated: only its dtype, variant, tile_* , wave_*, waves_* and
+ * grid_order fields are read; the rest is recomputed.  `In`/`Ker` are fp32
+ * or bf16 per plan->dtype.  Returns CONV_EINVAL for a plan the kernels cannot
+ * run, else as conv_fwd.
+ */
+int conv_fwd_with_plan(int N, int C, int K, int H, int W, int R, int S,
+                       const void* In, const void* Ker, float* Out,
+                       const conv_plan_t* plan, void* stream);
+
+/*
+ * Host-only: every candidate plan the selector scores for this shape (the
+ * feasible kernel configurations), best first.  Writes at most `cap` plans
+ * to `plans` (may be NULL when cap == 0) and returns the number of
+ * candidates, or a negative conv_status_t.
+ */
+int conv_fwd_candidates(int N, int C, int K, int H, int W, int R, int S, int dtype,
+                        conv_plan_t* plans, int cap);
+
+/*
+ * Host-only: the paper's single-level data-movement volume (Sec. 3.2) for a
+ * tile-loop permutation.  perm[0..6] lists the loops outermost first, coded
+ * n=0, k=1, c=2, r=3, s=4, h=5, w=6; N[] and T[] are problem extents and
+ * tile sizes in the same coding (h, w extents are output extents).  Writes
+ * the In, Ker and Out volumes in elements to dv[0..2], Out multiplied by
+ * out_factor (2 in the paper: read and write).  Returns a conv_status_t.
+ */
+int conv_model_volume(const int perm[7], const int64_t N[7], const int64_t T[7],
+                      int out_factor, double dv[3]);
+
+/*
+ * Host-only introspection: the launch geometry a plan resolves to for this
+ * shape, as CONV_GEOM_FIELDS int32 values in this order:
+ *   kernel view of the problem N, C, K, H, W, R, S, P, Q (a 1x1 problem is
+ *   presented as one row of H*W pixels per image);
+ *   tile rows, tile cols; row tiles, column tiles, k tiles;
+ *   LDS In rows, In row pitch, In channel stride; LDS Ker row pitch;
+ *   waves along k, waves along pixels; grid order; workgroups;
+ *   LDS In / Ker elements per buffer; staging loads per thread (In, Ker);
+ *   pipeline steps; then the kernel variant's k blocks per wave, pixel blocks
+ *   per wave, channels per step, compile-time R, S (0 = runtime), staging
+ *   capacity (In, Ker), Ker vector width, threads per workgroup; LDS bytes.
+ * Writes min(cap, CONV_GEOM_FIELDS) values and returns CONV_GEOM_FIELDS, or
+ * a negative conv_status_t (CONV_EINVAL for a plan the kernels cannot run).
+ */
+#define CONV_GEOM_FIELDS 40
+int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S,
+                      const conv_plan_t* plan, int32_t* out, int cap);
+
+/* Static string for a conv_status_t. */
+const char* conv_fwd_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CONV_FWD_H */

@@ -1,0 +1,211 @@
+"""Python binding of the C ABI in ``include/conv_fwd.h`` (ctypes).
+
+Argument marshalling only: every step of the computation runs in the HIP
+library ``libconvfwd.so``.  PyTorch provides device memory and the current
+stream.  There is no fallback: if the library is missing, or a tensor is not
+on the GPU, the call raises.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libconvfwd.so")
+
+CONV_OK, CONV_EINVAL, CONV_ENULL, CONV_ERANGE, CONV_ENOPLAN, CONV_EHIP = 0, -1, -2, -3, -4, -5
+CONV_DTYPE_F32, CONV_DTYPE_BF16 = 0, 1
+LEVELS = ("reg", "lds", "l2", "hbm")
+ITER_CODE = {"n": 0, "k": 1, "c": 2, "r": 3, "s": 4, "h": 5, "w": 6}
+
+_i32, _i64, _dbl, _vp = ctypes.c_int, ctypes.c_int64, ctypes.c_double, ctypes.c_void_p
+
+
+class ConvPlan(ctypes.Structure):
+    """Mirror of ``conv_plan_t``."""
+    _fields_ = [
+        ("dtype", _i32), ("variant", _i32), ("tile_k", _i32), ("tile_rows", _i32),
+        ("tile_cols", _i32), ("tile_c", _i32), ("wave_k", _i32), ("wave_px", _i32),
+        ("waves_k", _i32), ("waves_px", _i32), ("grid_order", _i32), ("lds_bytes", _i32),
+        ("num_wg", _i64), ("class_lvl", _i32 * 4), ("pred_bytes", _dbl * 4),
+        ("pred_us", _dbl * 4), ("pred_mfma_us", _dbl), ("pred_total_us", _dbl),
+    ]
+
+    def to_dict(self):
+        d = {f: getattr(self, f) for f, _ in self._fields_[:13]}
+        d["class_lvl"] = dict(zip(LEVELS, list(self.class_lvl)))
+        d["pred_bytes"] = dict(zip(LEVELS, list(self.pred_bytes)))
+        d["pred_us"] = dict(zip(LEVELS, list(self.pred_us)))
+        d["pred_mfma_us"] = self.pred_mfma_us
+        d["pred_total_us"] = self.pred_total_us
+        return d
+
+    @classmethod
+    def from_dict(cls, d):
+        p = cls()
+        for f, _ in cls._fields_[:13]:
+            if f in d:
+                setattr(p, f, d[f])
+        return p
+
+
+class ConvError(RuntimeError):
+    def __init__(self, status, what):
+        self.status = status
+        super().__init__(f"{what}: {strerror(status)} (status {status})")
+
+
+_lib = None
+
+
+def lib():
+    """The loaded HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing; build it with `python -m paper_2101_09808_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        shape7 = [_i32] * 7
+        L.conv_fwd.argtypes = shape7 + [_vp, _vp, _vp, _vp]
+        L.conv_fwd.restype = _i32
+        L.conv_fwd_bf16.argtypes = shape7 + [_vp, _vp, _vp, _vp]
+        L.conv_fwd_bf16.restype = _i32
+        L.conv_fwd_plan.argtypes = shape7 + [_i32, ctypes.POINTER(ConvPlan)]
+        L.conv_fwd_plan.restype = _i32
+        L.conv_fwd_with_plan.argtypes = shape7 + [_vp, _vp, _vp, ctypes.POINTER(ConvPlan), _vp]
+        L.conv_fwd_with_plan.restype = _i32
+        L.conv_fwd_candidates.argtypes = shape7 + [_i32, ctypes.POINTER(ConvPlan), _i32]
+        L.conv_fwd_candidates.restype = _i32
+        L.conv_model_volume.argtypes = [ctypes.POINTER(_i32), ctypes.POINTER(_i64),
+                                        ctypes.POINTER(_i64), _i32, ctypes.POINTER(_dbl)]
+        L.conv_model_volume.restype = _i32
+        L.conv_fwd_geometry.argtypes = shape7 + [ctypes.POINTER(ConvPlan), ctypes.POINTER(_i32), _i32]
+        L.conv_fwd_geometry.restype = _i32
+        L.conv_fwd_strerror.argtypes = [_i32]
+        L.conv_fwd_strerror.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def strerror(status):
+    return lib().conv_fwd_strerror(int(status)).decode()
+
+
+def _stream_ptr(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check_inputs(In, Ker, dtype):
+    if not (isinstance(In, torch.Tensor) and isinstance(Ker, torch.Tensor)):
+        raise TypeError("In and Ker must be torch tensors")
+    if not (In.is_cuda and Ker.is_cuda):
+        raise ValueError("In and Ker must be GPU tensors (the library has no CPU path)")
+    if In.dtype != dtype or Ker.dtype != dtype:
+        raise TypeError(f"expected {dtype} tensors, got {In.dtype} and {Ker.dtype}")
+    if In.dim() != 4 or Ker.dim() != 4:
+        raise ValueError("In must be [N,C,H,W] and Ker [K,C,R,S]")
+    if not (In.is_contiguous() and Ker.is_contiguous()):
+        raise ValueError("In and Ker must be contiguous (NCHW / KCRS)")
+    N, C, H, W = In.shape
+    K, C2, R, S = Ker.shape
+    if C2 != C:
+        raise ValueError(f"channel mismatch: In has {C}, Ker has {C2}")
+    return N, C, K, H, W, R, S
+
+
+def _out_for(In, shape, out):
+    N, C, K, H, W, R, S = shape
+    oshape = (N, K, H - R + 1, W - S + 1)
+    if out is None:
+        return torch.empty(oshape, dtype=torch.float32, device=In.device)
+    if out.shape != oshape or out.dtype != torch.float32 or not out.is_contiguous() or out.device != In.device:
+        raise ValueError(f"out must be a contiguous float32 {oshape} tensor on {In.device}")
+    return out
+
+
+def conv_fwd(In, Ker, out=None, stream=None):
+    """Eq. (1) for fp32 In [N,C,H,W] and Ker [K,C,R,S]; returns fp32 Out [N,K,P,Q]."""
+    shape = _check_inputs(In, Ker, torch.float32)
+    out = _out_for(In, shape, out)
+    st = lib().conv_fwd(*shape, In.data_ptr(), Ker.data_ptr(), out.data_ptr(), _stream_ptr(stream))
+    if st != CONV_OK:
+        raise ConvError(st, "conv_fwd")
+    return out
+
+
+def conv_fwd_bf16(In, Ker, out=None, stream=None):
+    """Eq. (1) for bf16 In and Ker, fp32 accumulation and fp32 Out."""
+    shape = _check_inputs(In, Ker, torch.bfloat16)
+    out = _out_for(In, shape, out)
+    st = lib().conv_fwd_bf16(*shape, In.data_ptr(), Ker.data_ptr(), out.data_ptr(), _stream_ptr(stream))
+    if st != CONV_OK:
+        raise ConvError(st, "conv_fwd_bf16")
+    return out
+
+
+def conv_fwd_with_plan(In, Ker, plan, out=None, stream=None):
+    """Eq. (1) with an explicit tile plan (a ConvPlan or its dict)."""
+    if isinstance(plan, dict):
+        plan = ConvPlan.from_dict(plan)
+    dtype = torch.bfloat16 if plan.dtype == CONV_DTYPE_BF16 else torch.float32
+    shape = _check_inputs(In, Ker, dtype)
+    out = _out_for(In, shape, out)
+    st = lib().conv_fwd_with_plan(*shape, In.data_ptr(), Ker.data_ptr(), out.data_ptr(),
+                                  ctypes.byref(plan), _stream_ptr(stream))
+    if st != CONV_OK:
+        raise ConvError(st, "conv_fwd_with_plan")
+    return out
+
+
+def conv_fwd_plan(N, C, K, H, W, R, S, dtype=CONV_DTYPE_F32):
+    """The selector's plan for a shape (host only) as a dict."""
+    p = ConvPlan()
+    st = lib().conv_fwd_plan(N, C, K, H, W, R, S, dtype, ctypes.byref(p))
+    if st != CONV_OK:
+        raise ConvError(st, "conv_fwd_plan")
+    return p.to_dict()
+
+
+def conv_fwd_candidates(N, C, K, H, W, R, S, dtype=CONV_DTYPE_F32, cap=4096):
+    """All candidate plans the selector scores for a shape, best first."""
+    buf = (ConvPlan * cap)()
+    n = lib().conv_fwd_candidates(N, C, K, H, W, R, S, dtype, buf, cap)
+    if n < 0:
+        raise ConvError(n, "conv_fwd_candidates")
+    return [buf[i].to_dict() for i in range(min(n, cap))]
+
+
+def conv_model_volume(perm, N, T, out_factor=2):
+    """The paper's single-level volumes (In, Ker, Out) for a permutation of
+    'nkcrshw' (outermost first) and dicts of extents / tile sizes."""
+    order = [ITER_CODE[x] for x in perm]
+    keys = sorted(ITER_CODE, key=ITER_CODE.get)
+    Na = (_i64 * 7)(*[int(N[k]) for k in keys])
+    Ta = (_i64 * 7)(*[int(T[k]) for k in keys])
+    dv = (_dbl * 3)()
+    st = lib().conv_model_volume((_i32 * 7)(*order), Na, Ta, out_factor, dv)
+    if st != CONV_OK:
+        raise ConvError(st, "conv_model_volume")
+    return {"In": dv[0], "Ker": dv[1], "Out": dv[2]}
+
+
+GEOM_FIELDS = (
+    "N", "C", "K", "H", "W", "R", "S", "P", "Q",
+    "tr", "tw", "tiles_rows", "tiles_cols", "tiles_k",
+    "in_rows", "in_wp", "in_cstride", "ker_rstride",
+    "nwk", "nwp", "order", "num_tiles",
+    "lds_in_elems", "lds_ker_elems", "ni_in", "ni_ker", "nchunks",
+    "wk", "wp", "tc", "rc", "sc", "max_ni", "max_nk", "ker_vec", "threads", "lds_bytes",
+)
+
+
+def conv_fwd_geometry(N, C, K, H, W, R, S, plan):
+    """The launch geometry a plan resolves to (host only), as a dict."""
+    if isinstance(plan, dict):
+        plan = ConvPlan.from_dict(plan)
+    buf = (_i32 * 40)()
+    st = lib().conv_fwd_geometry(N, C, K, H, W, R, S, ctypes.byref(plan), buf, 40)
+    if st < 0:
+        raise ConvError(st, "conv_fwd_geometry")
+    return dict(zip(GEOM_FIELDS, list(buf)[:len(GEOM_FIELDS)]))

@@ -1,0 +1,191 @@
+// C ABI of the convolution library: argument validation, the per-shape plan
+// cache and dispatch to the kernels.  The declarations and their contracts
+// are in include/conv_fwd.h.
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <tuple>
+
+#include "conv_internal.h"
+
+using namespace convfwd;
+
+namespace {
+
+const int64_t kMaxElems = (int64_t(1) << 31) - 1;
+
+int validate_shape(int N, int C, int K, int H, int W, int R, int S) {
+  if (N <= 0 || C <= 0 || K <= 0 || H <= 0 || W <= 0 || R <= 0 || S <= 0) return CONV_EINVAL;
+  if (R > H || S > W) return CONV_EINVAL;
+  const int64_t P = H - R + 1, Q = W - S + 1;
+  if ((int64_t)N * C * H * W > kMaxElems) return CONV_ERANGE;
+  if ((int64_t)K * C * R * S > kMaxElems) return CONV_ERANGE;
+  if ((int64_t)N * K * P * Q > kMaxElems) return CONV_ERANGE;
+  return CONV_OK;
+}
+
+typedef std::tuple<int, int, int, int, int, int, int, int> Key;
+std::mutex g_mu;
+std::map<Key, conv_plan_t> g_cache;
+
+int cached_plan(const Shape& s, int dtype, conv_plan_t* out) {
+  const Key key{s.N, s.C, s.K, s.H, s.W, s.R, s.S, dtype};
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_cache.find(key);
+    if (it != g_cache.end()) {
+      *out = it->second;
+      return CONV_OK;
+    }
+  }
+  conv_plan_t p;
+  const int st = select_plan(s, dtype, &p);
+  if (st != CONV_OK) return st;
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_cache[key] = p;
+  }
+  *out = p;
+  return CONV_OK;
+}
+
+int run(const Shape& s, const void* In, const void* Ker, float* Out, const conv_plan_t& plan,
+        void* stream) {
+  const Variant* v = find_variant(plan.variant);
+  if (!v || v->dtype != plan.dtype) return CONV_EINVAL;
+  Geom g;
+  if (!resolve_geom(s, *v, plan, &g, nullptr)) return CONV_EINVAL;
+  return launch(*v, g, In, Ker, Out, stream);
+}
+
+// The selector assumes 16-byte aligned Ker for vector staging; for other
+// pointers pick the best plan among variants that stage Ker element-wise.
+int plan_for_pointer(const Shape& s, int dtype, const void* Ker, conv_plan_t* plan) {
+  int st = cached_plan(s, dtype, plan);
+  if (st != CONV_OK) return st;
+  const Variant* v = find_variant(plan->variant);
+  const int elem = dtype == CONV_DTYPE_BF16 ? 2 : 4;
+  if (v && v->ker_vec > 1 && (reinterpret_cast<uintptr_t>(Ker) % (elem * v->ker_vec)) != 0) {
+    conv_plan_t buf[512];
+    const int n = enumerate_plans(s, dtype, buf, 512);
+    for (int i = 0; i < n && i < 512; ++i) {
+      const Variant* w = find_variant(buf[i].variant);
+      if (w && w->ker_vec == 1) {
+        *plan = buf[i];
+        return CONV_OK;
+      }
+    }
+    return CONV_ENOPLAN;
+  }
+  return CONV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int conv_fwd(int N, int C, int K, int H, int W, int R, int S, const float* In, const float* Ker,
+             float* Out, void* stream) {
+  int st = validate_shape(N, C, K, H, W, R, S);
+  if (st != CONV_OK) return st;
+  if (!In || !Ker || !Out) return CONV_ENULL;
+  const Shape s{N, C, K, H, W, R, S};
+  conv_plan_t plan;
+  st = plan_for_pointer(s, CONV_DTYPE_F32, Ker, &plan);
+  if (st != CONV_OK) return st;
+  return run(s, In, Ker, Out, plan, stream);
+}
+
+int conv_fwd_bf16(int N, int C, int K, int H, int W, int R, int S, const uint16_t* In,
+                  const uint16_t* Ker, float* Out, void* stream) {
+  int st = validate_shape(N, C, K, H, W, R, S);
+  if (st != CONV_OK) return st;
+  if (!In || !Ker || !Out) return CONV_ENULL;
+  const Shape s{N, C, K, H, W, R, S};
+  conv_plan_t plan;
+  st = plan_for_pointer(s, CONV_DTYPE_BF16, Ker, &plan);
+  if (st != CONV_OK) return st;
+  return run(s, In, Ker, Out, plan, stream);
+}
+
+int conv_fwd_plan(int N, int C, int K, int H, int W, int R, int S, int dtype,
+                  conv_plan_t* plan_out) {
+  int st = validate_shape(N, C, K, H, W, R, S);
+  if (st != CONV_OK) return st;
+  if (!plan_out) return CONV_ENULL;
+  if (dtype != CONV_DTYPE_F32 && dtype != CONV_DTYPE_BF16) return CONV_EINVAL;
+  return cached_plan(Shape{N, C, K, H, W, R, S}, dtype, plan_out);
+}
+
+int conv_fwd_with_plan(int N, int C, int K, int H, int W, int R, int S, const void* In,
+                       const void* Ker, float* Out, const conv_plan_t* plan, void* stream) {
+  int st = validate_shape(N, C, K, H, W, R, S);
+  if (st != CONV_OK) return st;
+  if (!In || !Ker || !Out || !plan) return CONV_ENULL;
+  const Shape s{N, C, K, H, W, R, S};
+  conv_plan_t p = *plan;
+  st = score_plan(s, &p);
+  if (st != CONV_OK) return st;
+  return run(s, In, Ker, Out, p, stream);
+}
+
+int conv_fwd_candidates(int N, int C, int K, int H, int W, int R, int S, int dtype,
+                        conv_plan_t* plans, int cap) {
+  int st = validate_shape(N, C, K, H, W, R, S);
+  if (st != CONV_OK) return st;
+  if (cap < 0 || (cap > 0 && !plans)) return CONV_EINVAL;
+  if (dtype != CONV_DTYPE_F32 && dtype != CONV_DTYPE_BF16) return CONV_EINVAL;
+  const int n = enumerate_plans(Shape{N, C, K, H, W, R, S}, dtype, plans, cap);
+  return n > 0 ? n : CONV_ENOPLAN;
+}
+
+int conv_model_volume(const int perm[7], const int64_t N[7], const int64_t T[7], int out_factor,
+                      double dv[3]) {
+  if (!perm || !N || !T || !dv) return CONV_ENULL;
+  int seen = 0;
+  for (int i = 0; i < 7; ++i) {
+    if (perm[i] < 0 || perm[i] > 6 || (seen >> perm[i]) & 1) return CONV_EINVAL;
+    seen |= 1 << perm[i];
+    if (T[i] < 1 || T[i] > N[i]) return CONV_EINVAL;
+  }
+  if (out_factor < 0) return CONV_EINVAL;
+  model_volume(perm, N, T, out_factor, dv);
+  return CONV_OK;
+}
+
+int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S, const conv_plan_t* plan,
+                      int32_t* out, int cap) {
+  int st = validate_shape(N, C, K, H, W, R, S);
+  if (st != CONV_OK) return st;
+  if (!plan || (cap > 0 && !out)) return CONV_ENULL;
+  const Variant* v = find_variant(plan->variant);
+  if (!v) return CONV_EINVAL;
+  Geom g;
+  int lds = 0;
+  if (!resolve_geom(Shape{N, C, K, H, W, R, S}, *v, *plan, &g, &lds)) return CONV_EINVAL;
+  const int32_t f[CONV_GEOM_FIELDS] = {
+      g.N, g.C, g.K, g.H, g.W, g.R, g.S, g.P, g.Q,
+      g.tr, g.tw, g.tiles_rows, g.tiles_cols, g.tiles_k,
+      g.in_rows, g.in_wp, g.in_cstride, g.ker_rstride,
+      g.nwk, g.nwp, g.order, g.num_tiles,
+      g.lds_in_elems, g.lds_ker_elems, g.ni_in, g.ni_ker, g.nchunks,
+      v->wk, v->wp, v->tc, v->rc, v->sc, v->max_ni, v->max_nk, v->ker_vec, v->threads, lds,
+      0, 0, 0};
+  for (int i = 0; i < cap && i < CONV_GEOM_FIELDS; ++i) out[i] = f[i];
+  return CONV_GEOM_FIELDS;
+}
+
+const char* conv_fwd_strerror(int status) {
+  switch (status) {
+    case CONV_OK: return "ok";
+    case CONV_EINVAL: return "invalid argument (extent <= 0, R > H, S > W, or a bad plan)";
+    case CONV_ENULL: return "null pointer";
+    case CONV_ERANGE: return "tensor too large (2^31 elements or more)";
+    case CONV_ENOPLAN: return "no kernel configuration fits this shape";
+    case CONV_EHIP: return "HIP runtime error at launch";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,64 @@
+// Internal declarations shared by the selector, the dispatcher and the kernels.
+#pragma once
+
+#include <cstdint>
+
+#include "../../include/conv_fwd.h"
+
+namespace convfwd {
+
+// Problem extents of Eq. (1); P, Q are the output extents.
+struct Shape {
+  int N, C, K, H, W, R, S;
+  int P() const { return H - R + 1; }
+  int Q() const { return W - S + 1; }
+};
+
+// One compiled kernel instance (template parameters of the kernel family).
+struct Variant {
+  int id;
+  int dtype;      // CONV_DTYPE_*
+  int wk;         // 16-wide k blocks per wave (register tile along k)
+  int wp;         // 16-wide pixel blocks per wave (register tile along pixels)
+  int tc;         // input channels per pipeline step
+  int rc, sc;     // compile-time R, S (0 = runtime)
+  int max_ni;     // max In staging elements per thread
+  int max_nk;     // max Ker staging vectors per thread
+  int ker_vec;    // Ker global load width in elements (1 or 4 for fp32, 8 for bf16)
+  int threads;    // threads per workgroup the instance is built for
+};
+
+// Fully resolved launch geometry, passed by value to the kernels.
+struct Geom {
+  int N, C, K, H, W, R, S, P, Q;
+  int tr, tw;                            // workgroup tile: output rows (flattened n*P+h) x cols
+  int tiles_rows, tiles_cols, tiles_k;   // grid decomposition
+  int in_rows, in_wp, in_cstride;        // LDS In tile: rows, row pitch, per-channel stride
+  int ker_rstride;                       // LDS Ker tile: elements per k row
+  int nwk, nwp;                          // waves along k and along pixels
+  int order;                             // 0: k tiles innermost, 1: pixel tiles innermost
+  int num_tiles;                         // workgroups
+  int lds_in_elems, lds_ker_elems;       // LDS elements per pipeline buffer
+  int ni_in, ni_ker;                     // staging loads per thread (In elements, Ker vectors)
+  int nchunks;                           // pipeline steps = ceil(C / tc)
+};
+
+const Variant* variants(int* count);
+const Variant* find_variant(int id);
+
+// Resolve a plan's tile fields into a launch geometry; false if infeasible.
+bool resolve_geom(const Shape& s, const Variant& v, const conv_plan_t& plan, Geom* g, int* lds_bytes);
+
+// Launch the kernel of variant v (asynchronous).  Returns a conv_status_t.
+int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, float* Out, void* stream);
+
+// Selector entry points (host only, no HIP calls).
+int select_plan(const Shape& s, int dtype, conv_plan_t* out);
+int enumerate_plans(const Shape& s, int dtype, conv_plan_t* plans, int cap);
+int score_plan(const Shape& s, conv_plan_t* plan);  // fills the derived fields of a plan
+
+// Paper model, Sec. 3.2: per-array volumes for a permutation (codes n=0..w=6).
+void model_volume(const int perm[7], const int64_t N[7], const int64_t T[7], int out_factor,
+                  double dv[3]);
+
+}  // namespace convfwd

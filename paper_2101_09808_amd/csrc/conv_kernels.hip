@@ -1,0 +1,343 @@
+// Forward convolution kernels for gfx950 (CDNA4), Eq. (1):
+//   Out[n][k][h][w] = sum_{c,r,s} In[n][c][h+r][w+s] * Ker[k][c][r][s]
+//
+// Structure (one workgroup = one tile of the non-reduction loops, Sec. 7):
+//   * The grid enumerates workgroup tiles of (k, pixel) -- pixels are a range
+//     of rows of the flattened (n, h) output-row index times a range of
+//     columns.  The linear order of the tiles is the outer tile-loop order
+//     chosen by the selector (k tiles innermost or pixel tiles innermost), and
+//     consecutive tiles of that order are mapped to the same XCD so that they
+//     share its L2.
+//   * Per pipeline step the workgroup stages `TC` input channels of the In
+//     halo tile (rows h..h+tile+R-1, Eq. (4)'s (T_h + T_r - 1)(T_w + T_s - 1)
+//     footprint) and the matching Ker tile [tile_k][TC*R*S] in LDS, double
+//     buffered: the global loads of step i+1 are issued before the MFMAs of
+//     step i.
+//   * Each wave keeps a (16*WK) x (16*WP) tile of Out in accumulator
+//     registers for the whole reduction (the Out-stationary classes of Sec. 4,
+//     reduction loops c, r, s innermost) and issues one 16x16x4 fp32 MFMA per
+//     (k block, pixel block, 4 channels, tap).  This plays the part of the
+//     paper's outer-product microkernel (Sec. 6): an MFMA is an outer-product
+//     accumulation done by the matrix core, and WK*WP independent
+//     accumulators keep enough MFMAs in flight to cover their latency.
+//   * Epilogue: each accumulator element is stored once; 16 consecutive lanes
+//     hold 16 consecutive output pixels, so stores coalesce.
+#include <hip/hip_runtime.h>
+
+#include "conv_internal.h"
+
+namespace convfwd {
+namespace {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+template <int N>
+struct FVec {
+  typedef float type __attribute__((ext_vector_type(N)));
+};
+template <>
+struct FVec<1> {
+  typedef float type;
+};
+
+constexpr int kThreads = 256;
+
+// Hardware dispatches workgroup b to XCD b % 8.  Give XCD x the contiguous
+// range [x*G8/8, (x+1)*G8/8) of the logical tile order (tail left as is).
+__device__ __forceinline__ int xcd_remap(int b, int G) {
+  const int G8 = G & ~7;
+  return (b < G8) ? (b & 7) * (G8 >> 3) + (b >> 3) : b;
+}
+
+struct TileCoord {
+  int rho0, rho_end;  // output rows [rho0, rho_end) of the flattened n*P+h index
+  int q0, tw_eff;     // output columns [q0, q0 + tw_eff)
+  int k0;             // first output channel
+  int nu0, nrows;     // input rows [nu0, nu0 + nrows) of the flattened n*H+y index
+};
+
+__device__ __forceinline__ TileCoord tile_coord(const Geom& g, int BK) {
+  const int L = xcd_remap(blockIdx.x, g.num_tiles);
+  int kt, ct, rt;
+  if (g.order == 0) {
+    kt = L % g.tiles_k;
+    const int rest = L / g.tiles_k;
+    ct = rest % g.tiles_cols;
+    rt = rest / g.tiles_cols;
+  } else {
+    ct = L % g.tiles_cols;
+    const int rest = L / g.tiles_cols;
+    rt = rest % g.tiles_rows;
+    kt = rest / g.tiles_rows;
+  }
+  TileCoord t;
+  const int NP = g.N * g.P;
+  t.rho0 = rt * g.tr;
+  t.rho_end = min(t.rho0 + g.tr, NP);
+  t.q0 = ct * g.tw;
+  t.tw_eff = min(g.tw, g.Q - t.q0);
+  t.k0 = kt * BK;
+  const int nf = t.rho0 / g.P, pf = t.rho0 - nf * g.P;
+  t.nu0 = nf * g.H + pf;
+  const int nl = (t.rho_end - 1) / g.P, pl = (t.rho_end - 1) - nl * g.P;
+  t.nrows = nl * g.H + pl + g.R - t.nu0;
+  return t;
+}
+
+// ---------------------------------------------------------------------------
+// fp32 kernel.  WK x WP blocks of 16x16 per wave, TC channels per step,
+// compile-time taps RC x SC (0 = runtime), staging arrays of MAXNI In
+// elements and MAXNK Ker vectors of KV floats per thread.
+template <int WK, int WP, int TC, int RC, int SC, int MAXNI, int MAXNK, int KV>
+__global__ void __launch_bounds__(kThreads)
+conv_f32_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
+                float* __restrict__ Out, const Geom g) {
+  typedef typename FVec<KV>::type kvec_t;
+  extern __shared__ __align__(16) float lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int j = lane & 15, gq = lane >> 4;
+  const int wk = wave % g.nwk, wp = wave / g.nwk;
+  const int BK = 16 * WK * g.nwk;
+  const int R = RC ? RC : g.R, S = SC ? SC : g.S;
+  const int RS = R * S;
+  const int H = g.H, W = g.W, C = g.C, K = g.K;
+  const TileCoord t = tile_coord(g, BK);
+
+  // Per-thread staging list for the In halo tile: element idx = tid + 256*i
+  // of the [TC][in_rows][in_wp] LDS image.  in_goff is the global offset
+  // relative to channel c0 (-1: outside the tile, stage a zero); in_lc packs
+  // the LDS offset (low 20 bits) and the channel within the step.
+  int in_goff[MAXNI], in_lc[MAXNI];
+  {
+    const int E = g.in_rows * g.in_wp;
+    const int ncols = t.tw_eff + S - 1;
+#pragma unroll
+    for (int i = 0; i < MAXNI; ++i) {
+      const int idx = tid + kThreads * i;
+      in_lc[i] = -1;
+      in_goff[i] = -1;
+      if (i < g.ni_in && idx < TC * E) {
+        const int cl = idx / E, e = idx - cl * E;
+        const int row = e / g.in_wp, x = e - row * g.in_wp;
+        in_lc[i] = (cl * g.in_cstride + e) | (cl << 20);
+        if (row < t.nrows && x < ncols) {
+          const int nu = t.nu0 + row;
+          const int n = nu / H, y = nu - n * H;
+          in_goff[i] = ((n * C + cl) * H + y) * W + t.q0 + x;
+        }
+      }
+    }
+  }
+  // Per-thread staging list for the Ker tile [BK][TC*RS] (row pitch
+  // ker_rstride in LDS), in vectors of KV: packed (row << 16 | column), or -1.
+  const int TCRS = TC * RS;
+  int ker_km[MAXNK];
+  {
+    const int per_row = TCRS / KV;
+#pragma unroll
+    for (int i = 0; i < MAXNK; ++i) {
+      const int idx = tid + kThreads * i;
+      ker_km[i] = -1;
+      if (i < g.ni_ker && idx < BK * per_row) {
+        const int kl = idx / per_row, m = (idx - kl * per_row) * KV;
+        ker_km[i] = (kl << 16) | m;
+      }
+    }
+  }
+  // Per-lane LDS offsets of this lane's output pixel in each pixel block.
+  const int tpx = g.tr * g.tw;
+  int poff[WP];
+#pragma unroll
+  for (int pb = 0; pb < WP; ++pb) {
+    const int px = (wp * WP + pb) * 16 + j;
+    const int row_i = px / g.tw, col = px - row_i * g.tw;
+    const int rho = t.rho0 + row_i;
+    int off = 0;  // masked pixels read a valid, zero-filled LDS location
+    if (px < tpx && rho < t.rho_end && col < t.tw_eff) {
+      const int n = rho / g.P, p = rho - n * g.P;
+      off = (n * H + p - t.nu0) * g.in_wp + col;
+    }
+    poff[pb] = off;
+  }
+  int koff[WK];
+#pragma unroll
+  for (int kb = 0; kb < WK; ++kb) koff[kb] = ((wk * WK + kb) * 16 + j) * g.ker_rstride;
+
+  v4f acc[WK][WP];
+#pragma unroll
+  for (int kb = 0; kb < WK; ++kb)
+#pragma unroll
+    for (int pb = 0; pb < WP; ++pb) acc[kb][pb] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  float in_st[MAXNI];
+  kvec_t ker_st[MAXNK];
+  const int kcs = C * RS;
+
+  auto gload = [&](int c0) {
+    const float* inb = In + (size_t)c0 * H * W;
+#pragma unroll
+    for (int i = 0; i < MAXNI; ++i)
+      if (in_lc[i] >= 0)
+        in_st[i] = (in_goff[i] >= 0 && c0 + (in_lc[i] >> 20) < C) ? inb[in_goff[i]] : 0.f;
+    const float* kbp = Ker + (size_t)c0 * RS;
+    const int mlim = (C - c0) * RS;
+#pragma unroll
+    for (int i = 0; i < MAXNK; ++i) {
+      if (ker_km[i] >= 0) {
+        const int kl = ker_km[i] >> 16, m = ker_km[i] & 0xffff;
+        kvec_t v = (kvec_t)(0.f);
+        if (t.k0 + kl < K && m < mlim)
+          v = *reinterpret_cast<const kvec_t*>(kbp + (size_t)(t.k0 + kl) * kcs + m);
+        ker_st[i] = v;
+      }
+    }
+  };
+  auto lstore = [&](int buf) {
+    float* lin = lds + buf * g.lds_in_elems;
+    float* lk = lds + 2 * g.lds_in_elems + buf * g.lds_ker_elems;
+#pragma unroll
+    for (int i = 0; i < MAXNI; ++i)
+      if (in_lc[i] >= 0) lin[in_lc[i] & 0xfffff] = in_st[i];
+#pragma unroll
+    for (int i = 0; i < MAXNK; ++i)
+      if (ker_km[i] >= 0)
+        *reinterpret_cast<kvec_t*>(lk + (ker_km[i] >> 16) * g.ker_rstride + (ker_km[i] & 0xffff)) =
+            ker_st[i];
+  };
+  auto compute = [&](int buf) {
+    const float* lin = lds + buf * g.lds_in_elems;
+    const float* lk = lds + 2 * g.lds_in_elems + buf * g.lds_ker_elems;
+#pragma unroll
+    for (int cs = 0; cs < TC / 4; ++cs) {
+      // reduction slot gq of the MFMA <-> channel 4*cs + gq at tap (r, s)
+      const float* lin_c = lin + (cs * 4 + gq) * g.in_cstride;
+      const float* lk_c = lk + (cs * 4 + gq) * RS;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          const int tap = r * g.in_wp + s;
+          const int rs = r * S + s;
+          float a[WK], b[WP];
+#pragma unroll
+          for (int kb = 0; kb < WK; ++kb) a[kb] = lk_c[koff[kb] + rs];
+#pragma unroll
+          for (int pb = 0; pb < WP; ++pb) b[pb] = lin_c[poff[pb] + tap];
+#pragma unroll
+          for (int kb = 0; kb < WK; ++kb)
+#pragma unroll
+            for (int pb = 0; pb < WP; ++pb)
+              acc[kb][pb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[kb], b[pb], acc[kb][pb], 0, 0, 0);
+        }
+      }
+    }
+  };
+
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int ch = 0; ch < g.nchunks; ++ch) {
+    const int buf = ch & 1;
+    if (ch + 1 < g.nchunks) gload((ch + 1) * TC);
+    compute(buf);
+    if (ch + 1 < g.nchunks) lstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  // Epilogue: lane (j, gq) holds Out[k0 + block*16 + 4*gq + v][pixel j].
+  const size_t PQ = (size_t)g.P * g.Q;
+#pragma unroll
+  for (int pb = 0; pb < WP; ++pb) {
+    const int px = (wp * WP + pb) * 16 + j;
+    const int row_i = px / g.tw, col = px - row_i * g.tw;
+    const int rho = t.rho0 + row_i;
+    if (px < tpx && rho < t.rho_end && col < t.tw_eff) {
+      const int n = rho / g.P, p = rho - n * g.P;
+      float* ob = Out + ((size_t)n * K * g.P + p) * g.Q + t.q0 + col;
+#pragma unroll
+      for (int kb = 0; kb < WK; ++kb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int k = t.k0 + (wk * WK + kb) * 16 + 4 * gq + v;
+          if (k < K) ob[(size_t)k * PQ] = acc[kb][pb][v];
+        }
+    }
+  }
+}
+
+typedef void (*KernelF32)(const float*, const float*, float*, const Geom);
+
+struct Instance {
+  Variant v;
+  KernelF32 f32;
+};
+
+#define F32_INST(ID, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV)                               \
+  Instance{Variant{ID, CONV_DTYPE_F32, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV, kThreads}, \
+           &conv_f32_kernel<WK, WP, TC, RC, SC, MAXNI, MAXNK, KV>}
+
+const Instance kInstances[] = {
+    // 3x3 taps, Ker staged in float4
+    F32_INST(1, 4, 4, 8, 3, 3, 8, 12, 4),
+    F32_INST(2, 2, 4, 8, 3, 3, 8, 12, 4),
+    F32_INST(3, 4, 2, 8, 3, 3, 8, 12, 4),
+    F32_INST(4, 2, 2, 8, 3, 3, 8, 12, 4),
+    F32_INST(5, 1, 4, 8, 3, 3, 8, 12, 4),
+    F32_INST(6, 4, 1, 8, 3, 3, 8, 12, 4),
+    F32_INST(7, 2, 2, 4, 3, 3, 8, 12, 4),
+    // 1x1 taps
+    F32_INST(20, 4, 4, 16, 1, 1, 16, 4, 4),
+    F32_INST(21, 2, 4, 16, 1, 1, 16, 4, 4),
+    F32_INST(22, 4, 2, 16, 1, 1, 16, 4, 4),
+    F32_INST(23, 2, 2, 16, 1, 1, 16, 4, 4),
+    F32_INST(24, 4, 4, 8, 1, 1, 8, 4, 4),
+    // any taps (runtime R, S), scalar Ker staging: any C, any alignment
+    F32_INST(40, 2, 2, 4, 0, 0, 12, 16, 1),
+    F32_INST(41, 4, 4, 4, 0, 0, 12, 32, 1),
+};
+
+constexpr int kNumInstances = sizeof(kInstances) / sizeof(kInstances[0]);
+
+const Instance* find_instance(int id) {
+  for (int i = 0; i < kNumInstances; ++i)
+    if (kInstances[i].v.id == id) return &kInstances[i];
+  return nullptr;
+}
+
+}  // namespace
+
+const Variant* variants(int* count) {
+  static Variant table[kNumInstances];
+  static bool init = false;
+  if (!init) {
+    for (int i = 0; i < kNumInstances; ++i) table[i] = kInstances[i].v;
+    init = true;
+  }
+  *count = kNumInstances;
+  return table;
+}
+
+const Variant* find_variant(int id) {
+  const Instance* in = find_instance(id);
+  return in ? &in->v : nullptr;
+}
+
+int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, float* Out,
+           void* stream) {
+  const Instance* inst = find_instance(v.id);
+  if (!inst) return CONV_EINVAL;
+  const int lds_bytes = 2 * (g.lds_in_elems + g.lds_ker_elems) * (int)sizeof(float);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (v.ker_vec > 1 && (reinterpret_cast<uintptr_t>(Ker) % (4 * v.ker_vec)) != 0) return CONV_EINVAL;
+  if (lds_bytes > 65536) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(inst->f32),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes) != hipSuccess)
+      return CONV_EHIP;
+  }
+  hipLaunchKernelGGL(inst->f32, dim3(g.num_tiles), dim3(kThreads), lds_bytes, st,
+                     static_cast<const float*>(In), static_cast<const float*>(Ker), Out, g);
+  return hipGetLastError() == hipSuccess ? CONV_OK : CONV_EHIP;
+}
+
+}  // namespace convfwd

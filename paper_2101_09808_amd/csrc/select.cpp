@@ -1,0 +1,421 @@
+// Tile selector for the gfx950 convolution kernels (host only, no HIP calls).
+//
+// The paper's method (Sec. 3-5, Algorithm 1 of Sec. 8) chooses, for each
+// level of the memory hierarchy, a tile-loop permutation from the eight
+// pruned classes and tile sizes that minimise the bandwidth-scaled data
+// volume of the most constrained level: min over plans of max_l DV^l / BW^l.
+// Here the search runs over integer candidates that the kernels can execute
+// (tile sizes are multiples of the 16x16 MFMA block; the reduction loops are
+// innermost inside a workgroup, i.e. the Out-stationary classes), so the
+// max is evaluated directly instead of through region-constrained solves.
+//
+// Levels (innermost first), and how their volumes follow the paper's model:
+//   REG  LDS -> VGPR operand reads.  Inside a wave the accumulator tile is
+//        stationary and every operand is read once per (4 channels, tap), so
+//        the level behaves like the tiled matmul of Sec. 2.2 over the im2col
+//        view: bytes = MACs * (1/T_k + 1/T_px) * 4 (Eq. (3) form, Out moves 0).
+//   LDS  L2 -> LDS staging.  Class <{n,k,h,w},{c,r},s> with T_r = R, T_s = S:
+//        per workgroup tile, every channel step brings the In halo footprint
+//        (T_h + R - 1)(T_w + S - 1) and the Ker footprint T_k*T_c*R*S
+//        (Sec. 3.2, first case; Eq. (4) footprints).
+//   L2   MALL/HBM -> L2 per XCD: the outer tile-loop order of the grid (k
+//        tiles innermost: In stays, Ker re-read unless it fits the XCD's L2;
+//        pixel tiles innermost: Ker stays, In re-read per k tile).
+//   HBM  compulsory bytes: In + Ker read once, Out written once.
+// A compute "level" (MFMA time incl. padding and wave quantisation over the
+// 256 CUs) plays the part of the paper's load balancing step.
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <vector>
+
+#include "conv_internal.h"
+
+namespace convfwd {
+
+// ---------------------------------------------------------------------------
+// The paper's single-level model, Sec. 3.2.  Iterator codes n=0 k=1 c=2 r=3
+// s=4 h=5 w=6.  In is indexed by n, c, h+r, w+s; Ker by k, c, r, s; Out by
+// n, k, h, w.
+namespace {
+enum { IN = 0, KER = 1, OUT = 2 };
+const bool kPresent[3][7] = {
+    /* In  */ {true, false, true, true, true, true, true},
+    /* Ker */ {false, true, true, true, true, false, false},
+    /* Out */ {true, true, false, false, false, true, true},
+};
+}  // namespace
+
+void model_volume(const int perm[7], const int64_t N[7], const int64_t T[7], int out_factor,
+                  double dv[3]) {
+  // pos[x]: 1 for the innermost loop, 7 for the outermost.
+  int pos[7];
+  for (int i = 0; i < 7; ++i) pos[perm[i]] = 7 - i;
+  const double Tn = (double)T[0], Tk = (double)T[1], Tc = (double)T[2], Tr = (double)T[3],
+               Ts = (double)T[4], Th = (double)T[5], Tw = (double)T[6];
+  const double foot[3] = {
+      Tn * Tc * (Th + Tr - 1) * (Tw + Ts - 1),  // In
+      Tk * Tc * Tr * Ts,                        // Ker
+      Tn * Tk * Th * Tw,                        // Out
+  };
+  for (int a = 0; a < 3; ++a) {
+    int ra = 8, it = -1;
+    for (int x = 0; x < 7; ++x)
+      if (kPresent[a][x] && pos[x] < ra) {
+        ra = pos[x];
+        it = x;
+      }
+    const bool sliding = (a == IN) && (it == 3 || it == 4 || it == 5 || it == 6);
+    double ratio = 1.0;
+    for (int x = 0; x < 7; ++x)
+      if (sliding ? pos[x] > ra : pos[x] >= ra) ratio *= (double)N[x] / (double)T[x];
+    double v;
+    if (sliding) {
+      // Consecutive tiles along the sliding iterator share all but T_x of
+      // their extent in that data dimension: first tile in full, then the
+      // extent replaced by N_x - T_x.
+      double part;
+      if (it == 6) part = Tn * Tc * (Th + Tr - 1) * ((double)N[6] - Tw);
+      else if (it == 4) part = Tn * Tc * (Th + Tr - 1) * ((double)N[4] - Ts);
+      else if (it == 5) part = Tn * Tc * ((double)N[5] - Th) * (Tw + Ts - 1);
+      else part = Tn * Tc * ((double)N[3] - Tr) * (Tw + Ts - 1);
+      v = ratio * (foot[IN] + part);
+    } else {
+      v = ratio * foot[a];
+    }
+    dv[a] = (a == OUT) ? v * out_factor : v;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Hardware description of one MI355X (AMD public figures; the LDS and L2
+// figures are per-CU port widths times the clock).
+namespace {
+struct Hw {
+  double clock_hz = 2.4e9;
+  int cus = 256;
+  int xcds = 8;
+  int simds_per_cu = 4;
+  int lds_bytes = 163840;
+  double l2_bytes = 4.0 * 1024 * 1024;  // per XCD
+  double bw[CONV_NUM_LVLS] = {
+      256 * 128 * 2.4e9,  // REG: LDS read, 128 B/clk/CU
+      256 * 64 * 2.4e9,   // LDS: L2 -> CU, 64 B/clk/CU
+      17.0e12,            // L2: MALL/fabric -> L2 (aggregate)
+      8.0e12,             // HBM
+  };
+  int mfma_f32_cycles = 32;  // 16x16x4 f32 per SIMD
+};
+const Hw kHw;
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Bank-conflict degree of a wave's 64 4-byte LDS reads (addresses in
+// elements): the max over banks of the distinct addresses hitting it, for a
+// 64-bank view of the full wave plus a 32-bank view of each half wave.
+int conflict_cost(const int* addr) {
+  int worst64 = 0, worst32 = 0;
+  {
+    std::vector<int> seen;
+    for (int b = 0; b < 64; ++b) {
+      seen.clear();
+      for (int l = 0; l < 64; ++l)
+        if (((addr[l] % 64) + 64) % 64 == b &&
+            std::find(seen.begin(), seen.end(), addr[l]) == seen.end())
+          seen.push_back(addr[l]);
+      worst64 = std::max(worst64, (int)seen.size());
+    }
+  }
+  for (int h = 0; h < 2; ++h) {
+    std::vector<int> seen;
+    for (int b = 0; b < 32; ++b) {
+      seen.clear();
+      for (int l = 32 * h; l < 32 * h + 32; ++l)
+        if (((addr[l] % 32) + 32) % 32 == b &&
+            std::find(seen.begin(), seen.end(), addr[l]) == seen.end())
+          seen.push_back(addr[l]);
+      worst32 = std::max(worst32, (int)seen.size());
+    }
+  }
+  return worst64 + worst32;
+}
+
+// Row pitch of the Ker tile: >= need, a multiple of `mult`, with the least
+// conflicted A-operand reads (lane (i, g) reads row i, column g*RS).
+int pick_ker_rstride(int need, int mult, int rs) {
+  int best = -1, best_cost = 1 << 30;
+  for (int cand = ((need + mult - 1) / mult) * mult; cand < need + 64 + mult; cand += mult) {
+    int addr[64];
+    for (int l = 0; l < 64; ++l) addr[l] = (l & 15) * cand + (l >> 4) * rs;
+    const int c = conflict_cost(addr);
+    if (c < best_cost) {
+      best_cost = c;
+      best = cand;
+    }
+  }
+  return best;
+}
+
+// Channel stride of the In tile: >= need, a multiple of 4, least conflicted
+// B-operand reads (lane (j, g) reads channel g, pixel j).
+int pick_in_cstride(int need) {
+  int best = -1, best_cost = 1 << 30;
+  for (int cand = ((need + 3) / 4) * 4; cand < need + 68; cand += 4) {
+    int addr[64];
+    for (int l = 0; l < 64; ++l) addr[l] = (l >> 4) * cand + (l & 15);
+    const int c = conflict_cost(addr);
+    if (c < best_cost) {
+      best_cost = c;
+      best = cand;
+    }
+  }
+  return best;
+}
+
+// The problem as the kernels see it: a 1x1 correlation of an H x W plane is
+// the same computation on a 1 x (H*W) plane, which lets a workgroup tile span
+// whole image rows.
+Shape kernel_view(const Shape& s) {
+  Shape k = s;
+  if (s.R == 1 && s.S == 1) {
+    k.W = s.H * s.W;
+    k.H = 1;
+  }
+  return k;
+}
+}  // namespace
+
+bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Geom* g,
+                  int* lds_bytes) {
+  const Shape s = kernel_view(s0);
+  if (plan.dtype != v.dtype) return false;
+  if (v.rc && (s.R != v.rc || s.S != v.sc)) return false;
+  if (plan.tile_c != v.tc) return false;
+  const int nwk = plan.waves_k, nwp = plan.waves_px;
+  if (nwk < 1 || nwp < 1 || nwk * nwp * 64 != v.threads) return false;
+  const int BK = 16 * v.wk * nwk, BP = 16 * v.wp * nwp;
+  if (plan.tile_k != BK || plan.wave_k != 16 * v.wk || plan.wave_px != 16 * v.wp) return false;
+  if (plan.grid_order != 0 && plan.grid_order != 1) return false;
+  const int P = s.P(), Q = s.Q();
+  const int tr = plan.tile_rows, tw = plan.tile_cols;
+  if (tw < 1 || tw > Q || tr < 1 || (int64_t)tr * tw > BP) return false;
+  const int64_t NP = (int64_t)s.N * P;
+  const int64_t tiles_rows = cdiv(NP, tr), tiles_cols = cdiv(Q, tw), tiles_k = cdiv(s.K, BK);
+  const int64_t num_tiles = tiles_rows * tiles_cols * tiles_k;
+  if (num_tiles <= 0 || num_tiles >= (int64_t(1) << 31)) return false;
+  // Input rows (flattened n*H + y) spanned by the worst row tile.
+  int in_rows = 0;
+  for (int64_t rt = 0; rt < tiles_rows; ++rt) {
+    const int64_t r0 = rt * tr, r1 = std::min<int64_t>(r0 + tr, NP) - 1;
+    const int64_t nu0 = (r0 / P) * s.H + r0 % P, nu1 = (r1 / P) * s.H + r1 % P + s.R - 1;
+    in_rows = std::max<int>(in_rows, (int)(nu1 - nu0 + 1));
+  }
+  const int RS = s.R * s.S, TC = v.tc;
+  const int in_wp = tw + s.S - 1;
+  const int64_t E = (int64_t)in_rows * in_wp;
+  if (E * TC >= (1 << 20)) return false;
+  const int in_cstride = pick_in_cstride((int)E);
+  const int TCRS = TC * RS;
+  if (v.ker_vec > 1 && ((int64_t)s.C * RS % v.ker_vec != 0 || TCRS % v.ker_vec != 0)) return false;
+  if (TCRS >= (1 << 16) || BK >= (1 << 15)) return false;
+  const int ker_rstride = pick_ker_rstride(TCRS, std::max(4, v.ker_vec), RS);
+  const int64_t lds_in = (int64_t)TC * in_cstride;
+  const int64_t lds_ker = ((int64_t)BK * ker_rstride + 3) / 4 * 4;
+  const int64_t bytes = 2 * (lds_in + lds_ker) * 4;
+  if (bytes > kHw.lds_bytes) return false;
+  const int64_t ni_in = cdiv(TC * E, v.threads);
+  const int64_t ni_ker = cdiv((int64_t)BK * TCRS / v.ker_vec, v.threads);
+  if (ni_in > v.max_ni || ni_ker > v.max_nk) return false;
+  Geom q;
+  std::memset(&q, 0, sizeof(q));
+  q.N = s.N; q.C = s.C; q.K = s.K; q.H = s.H; q.W = s.W; q.R = s.R; q.S = s.S;
+  q.P = P; q.Q = Q;
+  q.tr = tr; q.tw = tw;
+  q.tiles_rows = (int)tiles_rows; q.tiles_cols = (int)tiles_cols; q.tiles_k = (int)tiles_k;
+  q.in_rows = in_rows; q.in_wp = in_wp; q.in_cstride = in_cstride;
+  q.ker_rstride = ker_rstride;
+  q.nwk = nwk; q.nwp = nwp;
+  q.order = plan.grid_order;
+  q.num_tiles = (int)num_tiles;
+  q.lds_in_elems = (int)lds_in; q.lds_ker_elems = (int)lds_ker;
+  q.ni_in = (int)ni_in; q.ni_ker = (int)ni_ker;
+  q.nchunks = (int)cdiv(s.C, TC);
+  if (g) *g = q;
+  if (lds_bytes) *lds_bytes = (int)bytes;
+  return true;
+}
+
+// Fill the model fields of a plan whose tile fields are set.  0 or an error.
+int score_plan(const Shape& s0, conv_plan_t* plan) {
+  const Variant* v = find_variant(plan->variant);
+  if (!v) return CONV_EINVAL;
+  Geom g;
+  int lds = 0;
+  if (!resolve_geom(s0, *v, *plan, &g, &lds)) return CONV_EINVAL;
+  const Shape s = kernel_view(s0);
+  const double e = (plan->dtype == CONV_DTYPE_BF16) ? 2.0 : 4.0;
+  const int RS = s.R * s.S;
+  const int64_t NP = (int64_t)s.N * g.P;
+  plan->lds_bytes = lds;
+  plan->num_wg = g.num_tiles;
+
+  // REG: per wave and per (4 channels, tap), WK + WP operand reads of 64 lanes.
+  const double waves = (double)g.num_tiles * (g.nwk * g.nwp);
+  const double steps = (double)g.nchunks * (v->tc / 4) * RS;
+  plan->pred_bytes[CONV_LVL_REG] = waves * steps * (v->wk + v->wp) * 64 * 4.0;
+
+  // LDS: per workgroup, every channel brings its In halo rows and Ker rows.
+  double in_tiles = 0;  // sum over pixel tiles of the halo footprint (elements per channel)
+  for (int64_t rt = 0; rt < g.tiles_rows; ++rt) {
+    const int64_t r0 = rt * g.tr, r1 = std::min<int64_t>(r0 + g.tr, NP) - 1;
+    const int64_t nu0 = (r0 / g.P) * s.H + r0 % g.P, nu1 = (r1 / g.P) * s.H + r1 % g.P + s.R - 1;
+    for (int64_t ct = 0; ct < g.tiles_cols; ++ct) {
+      const int64_t cols = std::min<int64_t>(g.tw, g.Q - ct * g.tw) + s.S - 1;
+      in_tiles += (double)(nu1 - nu0 + 1) * cols;
+    }
+  }
+  const double in_halo_bytes = in_tiles * s.C * e;     // one pass over all pixel tiles
+  const double ker_bytes = (double)s.K * s.C * RS * e;  // whole kernel tensor
+  const double pix_tiles = (double)g.tiles_rows * g.tiles_cols;
+  plan->pred_bytes[CONV_LVL_LDS] = in_halo_bytes * g.tiles_k + ker_bytes * pix_tiles;
+
+  // L2: outer tile-loop order of the grid, per XCD.
+  const double in_bytes = (double)s.N * s.C * s.H * s.W * e;
+  const double out_bytes = (double)s.N * s.K * g.P * g.Q * 4.0;
+  if (plan->grid_order == 0) {
+    // k tiles innermost: each pixel tile's halo is fetched once.  Every XCD
+    // needs the whole kernel tensor; it stays resident if it fits in half the
+    // XCD's L2, else it is re-fetched once per group of pixel tiles that are
+    // in flight together on the XCD.
+    double ker_l2;
+    if (ker_bytes <= 0.5 * kHw.l2_bytes) {
+      ker_l2 = std::min<double>(kHw.xcds, pix_tiles) * ker_bytes;
+    } else {
+      const double occ = std::max(1, std::min(2, kHw.lds_bytes / std::max(1, lds)));
+      const double resident = (double)kHw.cus / kHw.xcds * occ;
+      const double inflight = std::max(1.0, resident / g.tiles_k);
+      ker_l2 = pix_tiles / inflight * ker_bytes;
+    }
+    plan->pred_bytes[CONV_LVL_L2] = in_halo_bytes + ker_l2;
+    plan->class_lvl[CONV_LVL_L2] = 5;  // <{n,c,h,r,s}, w, k>: k innermost
+  } else {
+    // pixel tiles innermost: a k slice of Ker stays; In is re-read per k tile.
+    plan->pred_bytes[CONV_LVL_L2] = in_halo_bytes * g.tiles_k + ker_bytes;
+    plan->class_lvl[CONV_LVL_L2] = 1;  // <{k,c,r,s},{n,h},w>: pixels innermost
+  }
+  plan->pred_bytes[CONV_LVL_HBM] = in_bytes + ker_bytes + out_bytes;
+  plan->class_lvl[CONV_LVL_REG] = 3;  // <{n,k,h,w},{c,r},s>
+  plan->class_lvl[CONV_LVL_LDS] = 3;
+  plan->class_lvl[CONV_LVL_HBM] = 0;
+
+  double tmax = 0;
+  for (int l = 0; l < CONV_NUM_LVLS; ++l) {
+    plan->pred_us[l] = plan->pred_bytes[l] / kHw.bw[l] * 1e6;
+    tmax = std::max(tmax, plan->pred_us[l]);
+  }
+  // Compute: MFMA cycles of one wave; a CU runs ceil(num_wg / cus) workgroups
+  // whose waves share its SIMDs.
+  const double mfma_per_step = (double)v->wk * v->wp;
+  const double wave_cycles = steps * mfma_per_step * kHw.mfma_f32_cycles;
+  const double per_cu = std::ceil((double)g.num_tiles / kHw.cus);
+  const double waves_per_simd = per_cu * (g.nwk * g.nwp) / kHw.simds_per_cu;
+  plan->pred_mfma_us = waves_per_simd * wave_cycles / kHw.clock_hz * 1e6;
+  tmax = std::max(tmax, plan->pred_mfma_us);
+  plan->pred_total_us = tmax;
+  return CONV_OK;
+}
+
+namespace {
+void fill_plan_fields(conv_plan_t* p, const Variant& v, int nwk, int nwp, int tr, int tw,
+                      int order) {
+  std::memset(p, 0, sizeof(*p));
+  p->dtype = v.dtype;
+  p->variant = v.id;
+  p->tile_k = 16 * v.wk * nwk;
+  p->tile_rows = tr;
+  p->tile_cols = tw;
+  p->tile_c = v.tc;
+  p->wave_k = 16 * v.wk;
+  p->wave_px = 16 * v.wp;
+  p->waves_k = nwk;
+  p->waves_px = nwp;
+  p->grid_order = order;
+}
+
+// Deterministic preference among plans (tie-breaks: predicted time, total
+// predicted bytes, fewer workgroups, variant id, larger k tile).
+bool better(const conv_plan_t& a, const conv_plan_t& b) {
+  if (a.pred_total_us != b.pred_total_us) return a.pred_total_us < b.pred_total_us;
+  double ba = 0, bb = 0;
+  for (int l = 0; l < CONV_NUM_LVLS; ++l) {
+    ba += a.pred_bytes[l];
+    bb += b.pred_bytes[l];
+  }
+  if (ba != bb) return ba < bb;
+  if (a.num_wg != b.num_wg) return a.num_wg < b.num_wg;
+  if (a.variant != b.variant) return a.variant < b.variant;
+  if (a.tile_k != b.tile_k) return a.tile_k > b.tile_k;
+  if (a.tile_rows != b.tile_rows) return a.tile_rows > b.tile_rows;
+  if (a.tile_cols != b.tile_cols) return a.tile_cols > b.tile_cols;
+  return a.grid_order < b.grid_order;
+}
+}  // namespace
+
+int enumerate_plans(const Shape& s0, int dtype, conv_plan_t* plans, int cap) {
+  const Shape s = kernel_view(s0);
+  int nv = 0;
+  const Variant* vs = variants(&nv);
+  std::vector<conv_plan_t> all;
+  const int P = s.P(), Q = s.Q();
+  for (int vi = 0; vi < nv; ++vi) {
+    const Variant& v = vs[vi];
+    if (v.dtype != dtype) continue;
+    if (v.rc && (s.R != v.rc || s.S != v.sc)) continue;
+    const int nw = v.threads / 64;
+    for (int nwk = 1; nwk <= nw; ++nwk) {
+      if (nw % nwk) continue;
+      const int nwp = nw / nwk;
+      const int BP = 16 * v.wp * nwp;
+      // Column tiles: whole rows, or Q split into m near-equal parts.
+      std::vector<int> tws;
+      for (int m = 1; m <= 16; ++m) {
+        const int tw = (int)cdiv(Q, m);
+        if (tw <= BP && std::find(tws.begin(), tws.end(), tw) == tws.end()) tws.push_back(tw);
+      }
+      if (Q > BP) tws.push_back(BP);
+      for (int tw : tws) {
+        const int tr_max = BP / tw;
+        // Row tiles: as many rows as fit, or a divisor-friendly smaller count.
+        std::vector<int> trs = {tr_max};
+        if (tr_max > 1 && P % tr_max) {
+          for (int d = tr_max - 1; d >= 1; --d)
+            if (P % d == 0 || d % P == 0) {
+              trs.push_back(d);
+              break;
+            }
+        }
+        for (int tr : trs)
+          for (int order = 0; order < 2; ++order) {
+            conv_plan_t p;
+            fill_plan_fields(&p, v, nwk, nwp, tr, tw, order);
+            if (score_plan(s0, &p) == CONV_OK) all.push_back(p);
+          }
+      }
+    }
+  }
+  std::sort(all.begin(), all.end(), better);
+  const int n = (int)all.size();
+  for (int i = 0; i < n && i < cap; ++i) plans[i] = all[i];
+  return n;
+}
+
+int select_plan(const Shape& s, int dtype, conv_plan_t* out) {
+  std::vector<conv_plan_t> buf(4096);
+  const int n = enumerate_plans(s, dtype, buf.data(), (int)buf.size());
+  if (n <= 0) return CONV_ENOPLAN;
+  *out = buf[0];
+  return CONV_OK;
+}
+
+}  // namespace convfwd

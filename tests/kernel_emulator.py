@@ -1,0 +1,203 @@
+"""CPU emulation of the fp32 HIP kernel's addressing (tests only).
+
+Mirrors, step by step, the index arithmetic of ``conv_f32_kernel`` for a
+resolved launch geometry (``conv_fwd_geometry``): workgroup -> tile mapping
+(with the XCD remap), the per-thread staging lists, LDS writes and reads of
+each pipeline step, the MFMA operand lanes and the epilogue stores.  Every
+global and LDS access is checked against its buffer; LDS reads by unmasked
+lanes must hit data written in the same step; every output must be stored
+exactly once.  The arithmetic is done in float64 so the result can be
+compared with the oracle.  This lets a launch configuration be checked on the
+host before it ever runs on a GPU.
+"""
+import numpy as np
+
+
+class EmulationError(AssertionError):
+    pass
+
+
+def _chk(cond, msg):
+    if not np.all(cond):
+        raise EmulationError(msg)
+
+
+def tile_coord(g, b, BK):
+    G = g["num_tiles"]
+    G8 = G & ~7
+    L = (b & 7) * (G8 >> 3) + (b >> 3) if b < G8 else b
+    if g["order"] == 0:
+        kt = L % g["tiles_k"]
+        rest = L // g["tiles_k"]
+        ct = rest % g["tiles_cols"]
+        rt = rest // g["tiles_cols"]
+    else:
+        ct = L % g["tiles_cols"]
+        rest = L // g["tiles_cols"]
+        rt = rest % g["tiles_rows"]
+        kt = rest // g["tiles_rows"]
+    NP = g["N"] * g["P"]
+    rho0 = rt * g["tr"]
+    rho_end = min(rho0 + g["tr"], NP)
+    q0 = ct * g["tw"]
+    tw_eff = min(g["tw"], g["Q"] - q0)
+    k0 = kt * BK
+    nf, pf = divmod(rho0, g["P"])
+    nu0 = nf * g["H"] + pf
+    nl, pl = divmod(rho_end - 1, g["P"])
+    nrows = nl * g["H"] + pl + g["R"] - nu0
+    return L, dict(rho0=rho0, rho_end=rho_end, q0=q0, tw_eff=tw_eff, k0=k0, nu0=nu0, nrows=nrows)
+
+
+def emulate(g, In, Ker, wgs=None):
+    """Run the kernel's addressing for workgroups ``wgs`` (default: all).
+
+    In, Ker: flat float64 arrays of the problem (the kernel view, identical
+    memory).  Returns (out_flat, written) where written counts stores per
+    output element (NaN outputs where nothing was stored)."""
+    N, C, K, H, W, R, S, P, Q = (g[x] for x in "N C K H W R S P Q".split())
+    WK, WP, TC, KV, NT = g["wk"], g["wp"], g["tc"], g["ker_vec"], g["threads"]
+    _chk(NT == 256, "threads per workgroup")
+    nwk, nwp = g["nwk"], g["nwp"]
+    _chk(nwk * nwp * 64 == NT, "waves do not fill the workgroup")
+    BK = 16 * WK * nwk
+    RS = R * S
+    if g["rc"]:
+        _chk(g["rc"] == R and g["sc"] == S, "compile-time taps differ from the shape")
+    in_size, ker_size, out_size = N * C * H * W, K * C * R * S, N * K * P * Q
+    _chk(In.size == in_size and Ker.size == ker_size, "input sizes")
+    lin_n, lker_n = g["lds_in_elems"], g["lds_ker_elems"]
+    _chk(2 * (lin_n + lker_n) * 4 == g["lds_bytes"], "LDS byte count")
+    _chk(g["lds_bytes"] <= 160 * 1024, "LDS capacity")
+    out = np.full(out_size, np.nan)
+    written = np.zeros(out_size, np.int64)
+    tid = np.arange(NT)
+    lane = np.arange(64)
+    j, gq = lane & 15, lane >> 4
+    E = g["in_rows"] * g["in_wp"]
+    TCRS = TC * RS
+    _chk(TCRS % KV == 0, "Ker vector width")
+    per_row = TCRS // KV
+    _chk(g["ni_in"] <= g["max_ni"] and g["ni_ker"] <= g["max_nk"], "staging capacity")
+    _chk(g["ni_in"] * NT >= TC * E, "In staging does not cover the LDS tile")
+    _chk(g["ni_ker"] * NT >= BK * per_row, "Ker staging does not cover the LDS tile")
+    seen_L = set()
+    for b in (range(g["num_tiles"]) if wgs is None else wgs):
+        L, t = tile_coord(g, b, BK)
+        _chk(0 <= L < g["num_tiles"] and L not in seen_L, "workgroup remap is not a bijection")
+        seen_L.add(L)
+        ncols = t["tw_eff"] + S - 1
+        _chk(t["nrows"] <= g["in_rows"], "tile needs more LDS rows than allocated")
+        # In staging list
+        in_items = []
+        for i in range(g["max_ni"]):
+            idx = tid + NT * i
+            ok = (i < g["ni_in"]) & (idx < TC * E)
+            cl, e = idx // E, idx % E
+            row, x = e // g["in_wp"], e % g["in_wp"]
+            loff = cl * g["in_cstride"] + e
+            inside = ok & (row < t["nrows"]) & (x < ncols)
+            nu = t["nu0"] + row
+            n, y = nu // H, nu % H
+            goff = np.where(inside, ((n * C + cl) * H + y) * W + t["q0"] + x, -1)
+            _chk(~ok | (loff < (1 << 20)), "LDS offset does not fit its packing")
+            in_items.append((ok, cl, loff, goff))
+        ker_items = []
+        for i in range(g["max_nk"]):
+            idx = tid + NT * i
+            ok = (i < g["ni_ker"]) & (idx < BK * per_row)
+            kl, m = idx // per_row, (idx % per_row) * KV
+            ker_items.append((ok, kl, m))
+        # per-lane pixel offsets and Ker rows, per wave
+        tpx = g["tr"] * g["tw"]
+        waves = []
+        for wave in range(nwk * nwp):
+            wk, wp = wave % nwk, wave // nwk
+            poff, pvalid, pinfo = [], [], []
+            for pb in range(WP):
+                px = (wp * WP + pb) * 16 + j
+                row_i, col = px // g["tw"], px % g["tw"]
+                rho = t["rho0"] + row_i
+                valid = (px < tpx) & (rho < t["rho_end"]) & (col < t["tw_eff"])
+                n, p = rho // P, rho % P
+                off = np.where(valid, (n * H + p - t["nu0"]) * g["in_wp"] + col, 0)
+                poff.append(off)
+                pvalid.append(valid)
+                pinfo.append((n, p, col))
+            koff = [((wk * WK + kb) * 16 + j) * g["ker_rstride"] for kb in range(WK)]
+            waves.append(dict(wk=wk, wp=wp, poff=poff, pvalid=pvalid, pinfo=pinfo, koff=koff,
+                              acc=np.zeros((WK, WP, 16, 16))))
+        lin = [np.full(lin_n, np.nan), np.full(lin_n, np.nan)]
+        lker = [np.full(lker_n, np.nan), np.full(lker_n, np.nan)]
+
+        def stage(c0, buf):
+            fresh_in = np.full(lin_n, np.nan)
+            for ok, cl, loff, goff in in_items:
+                use = ok
+                src = np.where(use & (goff >= 0) & (c0 + cl < C), c0 * H * W + goff, -1)
+                _chk(src[src >= 0] < in_size, "In read out of bounds")
+                vals = np.where(src >= 0, In[np.clip(src, 0, in_size - 1)], 0.0)
+                _chk(loff[use] < lin_n, "LDS In write out of bounds")
+                _chk(np.isnan(fresh_in[loff[use]]), "two threads write one LDS In element")
+                fresh_in[loff[use]] = vals[use]
+            lin[buf][:] = fresh_in  # anything not rewritten this step counts as stale
+            fresh_k = np.full(lker_n, np.nan)
+            mlim = (C - c0) * RS
+            for ok, kl, m in ker_items:
+                valid = ok & (t["k0"] + kl < K) & (m < mlim)
+                base = c0 * RS + (t["k0"] + kl) * C * RS + m
+                for e in range(KV):
+                    src = np.where(valid, base + e, -1)
+                    _chk(src[valid] < ker_size, "Ker read out of bounds")
+                    vals = np.where(valid, Ker[np.clip(src, 0, ker_size - 1)], 0.0)
+                    dst = kl * g["ker_rstride"] + m + e
+                    _chk(dst[ok] < lker_n, "LDS Ker write out of bounds")
+                    _chk(np.isnan(fresh_k[dst[ok]]), "two threads write one LDS Ker element")
+                    fresh_k[dst[ok]] = vals[ok]
+            lker[buf][:] = fresh_k
+
+        def compute(buf):
+            for wv in waves:
+                for cs in range(TC // 4):
+                    for r in range(R):
+                        for s in range(S):
+                            tap = r * g["in_wp"] + s
+                            rs = r * S + s
+                            A = []
+                            for kb in range(WK):
+                                ai = (cs * 4 + gq) * RS + wv["koff"][kb] + rs
+                                _chk((ai >= 0) & (ai < lker_n), "LDS Ker read out of bounds")
+                                a = lker[buf][ai]
+                                _chk(~np.isnan(a), "LDS Ker read of an element not staged this step")
+                                A.append(a)
+                            for pb in range(WP):
+                                bi = (cs * 4 + gq) * g["in_cstride"] + wv["poff"][pb] + tap
+                                _chk((bi >= 0) & (bi < lin_n), "LDS In read out of bounds")
+                                bv = lin[buf][bi]
+                                _chk(~np.isnan(bv), "LDS In read of an element not staged this step")
+                                Bm = np.zeros((4, 16))
+                                Bm[gq, j] = bv
+                                for kb in range(WK):
+                                    Am = np.zeros((16, 4))
+                                    Am[j, gq] = A[kb]
+                                    wv["acc"][kb, pb] += Am @ Bm
+
+        stage(0, 0)
+        for ch in range(g["nchunks"]):
+            compute(ch & 1)
+            if ch + 1 < g["nchunks"]:
+                stage((ch + 1) * TC, (ch + 1) & 1)
+        for wv in waves:
+            for pb in range(WP):
+                valid = wv["pvalid"][pb]
+                n, p, col = wv["pinfo"][pb]
+                for kb in range(WK):
+                    for v in range(4):
+                        k = t["k0"] + (wv["wk"] * WK + kb) * 16 + 4 * gq + v
+                        st = valid & (k < K)
+                        dst = ((n * K + k) * P + p) * Q + t["q0"] + col
+                        _chk((dst[st] >= 0) & (dst[st] < out_size), "Out store out of bounds")
+                        vals = wv["acc"][kb, pb][4 * gq + v, j]
+                        out[dst[st]] = vals[st]
+                        np.add.at(written, dst[st], 1)
+    return out, written

@@ -1,0 +1,100 @@
+"""The C-ABI library loads, exports what the header declares, and rejects bad
+arguments before touching the GPU (CPU only: no compute call is made)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2101_09808_amd import conv as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "conv_fwd.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(conv_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    fns = declared_functions()
+    for name in ("conv_fwd", "conv_fwd_bf16", "conv_fwd_plan", "conv_fwd_strerror",
+                 "conv_fwd_with_plan", "conv_fwd_candidates", "conv_model_volume"):
+        assert name in fns
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), f"missing export {name}"
+    nm = subprocess.run(["nm", "-D", "--defined-only", B.LIB_PATH], capture_output=True, text=True)
+    if nm.returncode == 0:
+        for name in declared_functions():
+            assert re.search(rf"\bT {name}$", nm.stdout, flags=re.M), name
+
+
+def test_plan_struct_layout_matches_header():
+    # conv_plan_t: 12 ints, int64, 4 ints, 4+4+1+1 doubles
+    assert ctypes.sizeof(B.ConvPlan) == 12 * 4 + 8 + 4 * 4 + 10 * 8
+
+
+VALID = (1, 4, 8, 6, 6, 3, 3)
+
+
+@pytest.mark.parametrize("shape,status", [
+    ((0, 4, 8, 6, 6, 3, 3), B.CONV_EINVAL),
+    ((1, 0, 8, 6, 6, 3, 3), B.CONV_EINVAL),
+    ((1, 4, -1, 6, 6, 3, 3), B.CONV_EINVAL),
+    ((1, 4, 8, 2, 6, 3, 3), B.CONV_EINVAL),   # R > H
+    ((1, 4, 8, 6, 2, 3, 3), B.CONV_EINVAL),   # S > W
+    ((1, 4, 8, 6, 6, 0, 3), B.CONV_EINVAL),
+    ((4096, 4096, 8, 64, 64, 3, 3), B.CONV_ERANGE),   # In has 2^36 elements
+    ((1, 65536, 65536, 6, 6, 1, 1), B.CONV_ERANGE),   # Ker has 2^32 elements
+])
+def test_bad_shapes_rejected(shape, status):
+    L = B.lib()
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    assert L.conv_fwd(*shape, fake, fake, fake, None) == status
+    assert L.conv_fwd_bf16(*shape, fake, fake, fake, None) == status
+    p = B.ConvPlan()
+    assert L.conv_fwd_plan(*shape, 0, ctypes.byref(p)) == status
+
+
+@pytest.mark.parametrize("which", [0, 1, 2])
+def test_null_pointers_rejected(which):
+    L = B.lib()
+    ptrs = [ctypes.c_void_p(0x1000)] * 3
+    ptrs[which] = None
+    assert L.conv_fwd(*VALID, *ptrs, None) == B.CONV_ENULL
+    assert L.conv_fwd_bf16(*VALID, *ptrs, None) == B.CONV_ENULL
+    assert L.conv_fwd_with_plan(*VALID, *ptrs, ctypes.byref(B.ConvPlan()), None) == B.CONV_ENULL
+    assert L.conv_fwd_plan(*VALID, 0, None) == B.CONV_ENULL
+
+
+def test_bad_plan_rejected_without_launch():
+    L = B.lib()
+    fake = ctypes.c_void_p(0x1000)
+    p = B.ConvPlan.from_dict(B.conv_fwd_plan(*VALID))
+    p.tile_k = 48  # not 16 * wave blocks * waves
+    assert L.conv_fwd_with_plan(*VALID, fake, fake, fake, ctypes.byref(p), None) == B.CONV_EINVAL
+    p = B.ConvPlan.from_dict(B.conv_fwd_plan(*VALID))
+    p.variant = 999
+    assert L.conv_fwd_with_plan(*VALID, fake, fake, fake, ctypes.byref(p), None) == B.CONV_EINVAL
+    assert L.conv_fwd_plan(*VALID, 7, ctypes.byref(B.ConvPlan())) == B.CONV_EINVAL
+
+
+def test_strerror():
+    for st in (B.CONV_OK, B.CONV_EINVAL, B.CONV_ENULL, B.CONV_ERANGE, B.CONV_ENOPLAN, B.CONV_EHIP):
+        assert B.strerror(st)
+    assert "unknown" in B.strerror(12345)
+
+
+def test_python_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros(1, 2, 4, 4)
+    k = torch.zeros(3, 2, 3, 3)
+    with pytest.raises(ValueError):
+        B.conv_fwd(x, k)

@@ -1,0 +1,227 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle of Eq. (1).
+
+Bar: max|Out - ref| / max|ref| <= 1e-5 for fp32 inputs and <= 1e-2 for bf16
+inputs (products of bf16 values are exact in fp32, so the bf16 path is in
+practice as accurate as fp32); bitwise equality where every partial sum is an
+exact integer (integer-valued inputs, all-ones and one-hot kernels), since
+then the result does not depend on the summation order.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import conv as oconv
+from paper_2101_09808_amd import conv as B
+from paper_2101_09808_amd.workloads import CONFIGS, ConvShape, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 1e-2}
+DEV = "cuda:0"
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def gpu_conv(shape, In, Ker, plan=None, out=None):
+    In_d, Ker_d = In.to(DEV), Ker.to(DEV)
+    if plan is not None:
+        o = B.conv_fwd_with_plan(In_d, Ker_d, plan, out=out)
+    elif shape.dtype == "bf16":
+        o = B.conv_fwd_bf16(In_d, Ker_d, out=out)
+    else:
+        o = B.conv_fwd(In_d, Ker_d, out=out)
+    torch.cuda.synchronize()
+    return o
+
+
+def host(x):
+    return x.float().cpu().numpy()
+
+
+def rel_err(out, ref):
+    m = float(np.max(np.abs(ref)))
+    e = float(np.max(np.abs(out.astype(np.float64) - ref)))
+    return e / m if m > 0 else e
+
+
+def check_full(shape, kind="uniform", seed=None, plan=None):
+    In, Ker = make_inputs(shape, seed=seed, kind=kind)
+    say(f"[gpu] {shape.name} {shape.key()} {shape.dtype} kind={kind} plan={plan and plan.get('variant')}")
+    out = host(gpu_conv(shape, In, Ker, plan))
+    ref = oconv.conv_fwd(host(In), host(Ker))
+    assert out.shape == ref.shape
+    if kind == "int":
+        assert np.array_equal(out.astype(np.float64), ref), f"{shape.name}: integer result not exact"
+    else:
+        err = rel_err(out, ref)
+        assert err <= TOL[shape.dtype], f"{shape.name}: rel err {err:.3e}"
+    return out, ref
+
+
+def small_version(c, n=2):
+    return ConvShape(c.name + f"_n{min(c.N, n)}", min(c.N, n), c.C, c.K, c.H, c.W, c.R, c.S, c.dtype, c.seed)
+
+
+# ----------------------------------------------------------------- configs
+
+@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda c: c.name)
+def test_config_reduced_batch_full_compare(cfg):
+    """Each layer at batch <= 2: every output against the oracle."""
+    check_full(small_version(cfg, 1 if cfg.dtype == "bf16" else 2))
+
+
+@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda c: c.name)
+def test_config_full_size_sampled(cfg):
+    """Full layer size, the plan the benchmark times; sampled outputs (plus
+    every tile-boundary corner) against the oracle computed point by point."""
+    In, Ker = make_inputs(cfg)
+    say(f"[gpu] full {cfg.name} plan={B.conv_fwd_plan(*cfg.key(), dtype=int(cfg.dtype == 'bf16'))}")
+    out = host(gpu_conv(cfg, In, Ker)).reshape(-1)
+    P, Q = cfg.P, cfg.Q
+    total = cfg.N * cfg.K * P * Q
+    rng = np.random.default_rng(cfg.seed)
+    idx = rng.integers(0, total, 20000)
+    corners = []
+    for n in (0, cfg.N - 1):
+        for k in (0, cfg.K - 1):
+            for p in (0, P - 1):
+                for q in (0, Q - 1):
+                    corners.append(((n * cfg.K + k) * P + p) * Q + q)
+    idx = np.concatenate([idx, np.array(corners, np.int64)])
+    ref = oconv.conv_fwd_points(host(In), host(Ker), idx)
+    assert np.all(np.isfinite(out))
+    m = float(np.max(np.abs(ref)))
+    err = float(np.max(np.abs(out[idx].astype(np.float64) - ref))) / m
+    assert err <= TOL[cfg.dtype], f"{cfg.name}: rel err {err:.3e}"
+
+
+def test_smallest_config_full_size_full_compare():
+    check_full(CONFIGS[0])
+
+
+# ----------------------------------------------------------------- edges
+
+EDGE = [
+    ConvShape("primes_3x3", 2, 3, 5, 13, 13, 3, 3, "f32", 11),
+    ConvShape("rect_taps", 2, 7, 33, 11, 17, 2, 4, "f32", 12),
+    ConvShape("pointwise_odd", 3, 5, 17, 9, 7, 1, 1, "f32", 13),
+    ConvShape("one_pixel_out", 2, 9, 20, 3, 3, 3, 3, "f32", 14),
+    ConvShape("single_everything", 1, 1, 1, 1, 1, 1, 1, "f32", 15),
+    ConvShape("tall_thin", 1, 6, 16, 40, 3, 3, 3, "f32", 16),
+    ConvShape("wide_row", 1, 4, 16, 3, 300, 3, 3, "f32", 17),
+    ConvShape("k_tail_c_tail", 2, 13, 70, 10, 12, 3, 3, "f32", 18),
+    ConvShape("big_taps_5x5", 2, 6, 24, 14, 12, 5, 5, "f32", 19),
+    ConvShape("r_eq_h", 2, 8, 32, 3, 9, 3, 1, "f32", 20),
+    ConvShape("many_images_small", 37, 8, 16, 5, 5, 3, 3, "f32", 21),
+    ConvShape("pointwise_many_k", 2, 32, 200, 7, 7, 1, 1, "f32", 22),
+]
+
+
+@pytest.mark.parametrize("shape", EDGE, ids=lambda s: s.name)
+def test_edge_shapes(shape):
+    check_full(shape)
+
+
+@pytest.mark.parametrize("shape", [EDGE[0], EDGE[7], small_version(CONFIGS[2]), small_version(CONFIGS[3]),
+                                   small_version(CONFIGS[1])], ids=lambda s: s.name)
+def test_integer_inputs_bitwise(shape):
+    check_full(shape, kind="int", seed=shape.seed + 1)
+
+
+def test_closed_forms_bitwise():
+    s = ConvShape("ones", 2, 12, 40, 15, 11, 3, 3, "f32", 0)
+    say("[gpu] all-ones")
+    In = torch.ones(s.N, s.C, s.H, s.W)
+    Ker = torch.ones(s.K, s.C, s.R, s.S)
+    out = host(gpu_conv(s, In, Ker))
+    assert np.all(out == s.C * s.R * s.S)
+    say("[gpu] one-hot kernel")
+    g = torch.Generator().manual_seed(5)
+    In = torch.rand(s.N, s.C, s.H, s.W, generator=g) * 2 - 1
+    Ker = torch.zeros(s.K, s.C, s.R, s.S)
+    sel = [((3 * k + 1) % s.C, k % s.R, (k // s.R + 1) % s.S) for k in range(s.K)]
+    for k, (c0, r0, s0) in enumerate(sel):
+        Ker[k, c0, r0, s0] = 1.0
+    out = host(gpu_conv(s, In, Ker))
+    for k, (c0, r0, s0) in enumerate(sel):
+        assert np.array_equal(out[:, k], In[:, c0, r0:r0 + s.P, s0:s0 + s.Q].numpy())
+
+
+def test_deterministic_and_overwrites_poisoned_output_with_guards():
+    s = small_version(CONFIGS[2])
+    In, Ker = make_inputs(s)
+    In_d, Ker_d = In.to(DEV), Ker.to(DEV)
+    n_out = s.N * s.K * s.P * s.Q
+    guard = 4096
+    buf = torch.full((n_out + 2 * guard,), float("nan"), device=DEV)
+    buf[:guard] = 7.0
+    buf[-guard:] = 7.0
+    out = buf[guard:guard + n_out].view(s.N, s.K, s.P, s.Q)
+    say("[gpu] poisoned output run 1")
+    B.conv_fwd(In_d, Ker_d, out=out)
+    torch.cuda.synchronize()
+    first = out.clone()
+    assert torch.isfinite(first).all(), "some outputs were not written"
+    assert (buf[:guard] == 7.0).all() and (buf[-guard:] == 7.0).all(), "write outside Out"
+    say("[gpu] poisoned output run 2")
+    out.fill_(float("nan"))
+    B.conv_fwd(In_d, Ker_d, out=out)
+    torch.cuda.synchronize()
+    assert torch.equal(out, first), "two runs differ"
+
+
+def test_side_stream():
+    s = EDGE[7]
+    In, Ker = make_inputs(s)
+    ref = oconv.conv_fwd(host(In), host(Ker))
+    st = torch.cuda.Stream()
+    In_d, Ker_d = In.to(DEV), Ker.to(DEV)
+    torch.cuda.synchronize()
+    say("[gpu] side stream")
+    with torch.cuda.stream(st):
+        out = B.conv_fwd(In_d, Ker_d)
+    st.synchronize()
+    assert rel_err(host(out), ref) <= TOL["f32"]
+
+
+def test_error_leaves_output_untouched():
+    In = torch.zeros(1, 4, 2, 2, device=DEV)
+    Ker = torch.zeros(3, 4, 3, 3, device=DEV)
+    with pytest.raises(B.ConvError):
+        B.conv_fwd(In, Ker)
+
+
+# ----------------------------------------------------------------- every kernel variant
+
+def _plans_per_variant(dims, dtype=B.CONV_DTYPE_F32, per_variant=3):
+    cands = B.conv_fwd_candidates(*dims, dtype=dtype)
+    chosen = {}
+    for p in cands:
+        key = (p["variant"], p["waves_k"], p["grid_order"])
+        chosen.setdefault(key, p)
+    by_var = {}
+    for key, p in sorted(chosen.items()):
+        by_var.setdefault(key[0], [])
+        if len(by_var[key[0]]) < per_variant:
+            by_var[key[0]].append(p)
+    return [p for ps in by_var.values() for p in ps]
+
+
+@pytest.mark.parametrize("shape", [
+    ConvShape("var3x3", 3, 20, 72, 19, 23, 3, 3, "f32", 31),
+    ConvShape("var1x1", 3, 40, 72, 13, 11, 1, 1, "f32", 32),
+    ConvShape("var2x4", 2, 9, 40, 12, 13, 2, 4, "f32", 33),
+], ids=lambda s: s.name)
+def test_every_variant(shape):
+    In, Ker = make_inputs(shape)
+    ref = oconv.conv_fwd(host(In), host(Ker))
+    plans = _plans_per_variant(shape.key())
+    assert plans
+    for p in plans:
+        say(f"[gpu] {shape.name} variant={p['variant']} tile={p['tile_k']}x{p['tile_rows']}x{p['tile_cols']} "
+            f"waves={p['waves_k']}x{p['waves_px']} order={p['grid_order']}")
+        out = host(gpu_conv(shape, In, Ker, plan=p))
+        err = rel_err(out, ref)
+        assert err <= TOL["f32"], (p, err)

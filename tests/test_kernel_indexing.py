@@ -1,0 +1,62 @@
+"""Host-side emulation of the kernel's index arithmetic for the plans the
+library launches (CPU only): every access in bounds, every output stored
+exactly once, and the emulated result equal to the oracle."""
+import numpy as np
+import pytest
+
+from oracle import conv as oconv
+from paper_2101_09808_amd import conv as B
+from paper_2101_09808_amd.workloads import CONFIGS, ConvShape, make_inputs
+from tests.kernel_emulator import emulate
+from tests.test_gpu_parity import EDGE, _plans_per_variant, small_version
+
+
+def _run(shape, plan, wgs=None):
+    g = B.conv_fwd_geometry(*shape.key(), plan)
+    In, Ker = make_inputs(shape)
+    In = In.float().numpy().astype(np.float64)
+    Ker = Ker.float().numpy().astype(np.float64)
+    out, written = emulate(g, In.reshape(-1), Ker.reshape(-1), wgs)
+    return g, In, Ker, out, written
+
+
+def _check_all(shape, plan):
+    g, In, Ker, out, written = _run(shape, plan)
+    assert np.all(written == 1), "outputs not stored exactly once"
+    ref = oconv.conv_fwd(In.astype(np.float32), Ker.astype(np.float32)).reshape(-1)
+    assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
+
+
+SMALL = EDGE + [small_version(c, 1) for c in CONFIGS if c.dtype == "f32" and c.N * c.K * c.P * c.Q <= 400000]
+
+
+@pytest.mark.parametrize("shape", SMALL, ids=lambda s: s.name)
+def test_selected_plan_indexing(shape):
+    _check_all(shape, B.conv_fwd_plan(*shape.key()))
+
+
+@pytest.mark.parametrize("shape", [
+    ConvShape("var3x3", 3, 20, 72, 19, 23, 3, 3, "f32", 31),
+    ConvShape("var1x1", 3, 40, 72, 13, 11, 1, 1, "f32", 32),
+    ConvShape("var2x4", 2, 9, 40, 12, 13, 2, 4, "f32", 33),
+], ids=lambda s: s.name)
+def test_every_variant_indexing(shape):
+    for p in _plans_per_variant(shape.key()):
+        _check_all(shape, p)
+
+
+@pytest.mark.parametrize("cfg", [c for c in CONFIGS if c.dtype == "f32"], ids=lambda c: c.name)
+def test_full_config_sampled_workgroups(cfg):
+    """Full-size plans: emulate the first, last and some middle workgroups;
+    their outputs must equal the oracle at those points."""
+    plan = B.conv_fwd_plan(*cfg.key())
+    G = plan["num_wg"]
+    rng = np.random.default_rng(1)
+    wgs = sorted(set([0, 1, 7, 8, G // 2, G - 9, G - 8, G - 1] + list(rng.integers(0, G, 4))))
+    wgs = [w for w in wgs if 0 <= w < G]
+    g, In, Ker, out, written = _run(cfg, plan, wgs)
+    assert written.max() <= 1
+    idx = np.nonzero(written)[0]
+    assert idx.size > 0
+    ref = oconv.conv_fwd_points(In.astype(np.float32), Ker.astype(np.float32), idx)
+    assert np.max(np.abs(out[idx] - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))

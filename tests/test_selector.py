@@ -1,0 +1,101 @@
+"""The library's tile selector (host C++) against the cost-model oracle and its
+own invariants (CPU only)."""
+import itertools
+import random
+from fractions import Fraction
+
+import pytest
+
+from oracle import cost_model as cm
+from paper_2101_09808_amd import conv as B
+from paper_2101_09808_amd.workloads import CONFIGS
+
+
+def divisors(n):
+    return [d for d in range(1, n + 1) if n % d == 0]
+
+
+def test_model_volume_matches_oracle_exactly():
+    """The C++ rule of Sec. 3.2 equals the exact-rational oracle on random
+    permutations and divisible tile sizes (all values are integers < 2^53)."""
+    rng = random.Random(21)
+    allp = list(itertools.permutations(cm.ITERS))
+    for _ in range(400):
+        N = {j: rng.randint(1, 64) for j in cm.ITERS}
+        T = {j: rng.choice(divisors(N[j])) for j in cm.ITERS}
+        p = rng.choice(allp)
+        for of in (1, 2):
+            got = B.conv_model_volume(p, N, T, of)
+            ref = cm.volumes(p, N, T, of)
+            for a in cm.ARRAYS:
+                assert Fraction(got[a]) == ref[a], (a, p, N, T, of)
+
+
+def test_model_volume_non_divisible_tiles():
+    """Ratios N/T that are not integers are still the oracle's rationals (to
+    double rounding)."""
+    rng = random.Random(22)
+    allp = list(itertools.permutations(cm.ITERS))
+    for _ in range(300):
+        N = {j: rng.randint(1, 50) for j in cm.ITERS}
+        T = {j: rng.randint(1, N[j]) for j in cm.ITERS}
+        p = rng.choice(allp)
+        got = B.conv_model_volume(p, N, T, 2)
+        ref = cm.volumes(p, N, T, 2)
+        for a in cm.ARRAYS:
+            assert abs(got[a] - float(ref[a])) <= 1e-12 * float(ref[a])
+
+
+def test_model_volume_rejects_bad_input():
+    with pytest.raises(B.ConvError):
+        B.conv_model_volume("nkcrshh", dict(n=1, k=1, c=1, r=1, s=1, h=1, w=1),
+                            dict(n=1, k=1, c=1, r=1, s=1, h=1, w=1))
+    with pytest.raises(B.ConvError):
+        B.conv_model_volume("nkcrshw", dict(n=1, k=1, c=1, r=1, s=1, h=1, w=1),
+                            dict(n=2, k=1, c=1, r=1, s=1, h=1, w=1))
+
+
+SHAPES = [c.key() + ((B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32),) for c in CONFIGS] + [
+    (1, 3, 5, 13, 13, 3, 3, 0), (2, 7, 33, 11, 17, 2, 4, 0), (3, 16, 16, 9, 9, 1, 1, 0),
+    (1, 1, 1, 1, 1, 1, 1, 0), (1, 64, 64, 58, 58, 3, 3, 0),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=str)
+def test_plan_invariants(shape):
+    *dims, dtype = shape
+    N, C, K, H, W, R, S = dims
+    try:
+        plan = B.conv_fwd_plan(*dims, dtype=dtype)
+    except B.ConvError as e:
+        if dtype == B.CONV_DTYPE_BF16 and e.status == B.CONV_ENOPLAN:
+            pytest.skip("no bf16 kernel variant built")
+        raise
+    assert plan["dtype"] == dtype
+    assert 0 < plan["lds_bytes"] <= 160 * 1024
+    assert plan["tile_k"] == plan["wave_k"] * plan["waves_k"]
+    assert plan["wave_px"] % 16 == 0 and plan["wave_k"] % 16 == 0
+    assert plan["tile_rows"] * plan["tile_cols"] <= plan["wave_px"] * plan["waves_px"]
+    e = 2 if dtype == B.CONV_DTYPE_BF16 else 4
+    P, Q = H - R + 1, W - S + 1
+    compulsory = (N * C * H * W + K * C * R * S) * e + N * K * P * Q * 4
+    assert plan["pred_bytes"]["hbm"] >= compulsory * (1 - 1e-12)
+    # each level moves at least the bytes it must deliver once
+    assert plan["pred_bytes"]["lds"] >= (N * C * H * W + K * C * R * S) * e * (1 - 1e-12) or R * S == 1
+    assert plan["pred_total_us"] == max(list(plan["pred_us"].values()) + [plan["pred_mfma_us"]])
+    # deterministic and cached
+    assert B.conv_fwd_plan(*dims, dtype=dtype) == plan
+    cands = B.conv_fwd_candidates(*dims, dtype=dtype)
+    assert cands[0] == plan
+    tot = [c["pred_total_us"] for c in cands]
+    assert tot == sorted(tot)
+
+
+def test_selector_is_minimum_of_its_objective():
+    """The chosen plan has the smallest predicted max-level time of all the
+    candidates it scored (the min-max of Sec. 5)."""
+    for c in CONFIGS:
+        if c.dtype != "f32":
+            continue
+        cands = B.conv_fwd_candidates(*c.key())
+        assert cands[0]["pred_total_us"] == min(x["pred_total_us"] for x in cands)
