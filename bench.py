@@ -1,0 +1,209 @@
+"""Benchmark of the MI355X forward convolution (Eq. (1)).
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-layers] [--no-cpu]
+
+A step is one conv_fwd call (tile selection is cached, so the step is the
+kernel launch) on the pointwise layer N=32 C=256 K=64 56x56 1x1 fp32, the
+workload the headline metric is quoted on.  Inputs are seeded uniform[-1,1)
+synthetic tensors of that shape.  The timed steps cycle through enough
+independent In/Out buffer sets (more than twice the 256 MB last-level cache)
+that every step reads In from HBM and writes Out to HBM.
+
+Prints ONE JSON line with the metric, the roofline of the kernel (achieved
+rate from HIP events around every launch on the launch stream), the CPU oracle
+timed on this host (cpu_baseline), and a per-layer table for the other layer
+configurations.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"fp32_mfma_tflops": 157.3, "bf16_mfma_tflops": 2516.6, "hbm_gbs": 8000.0}
+HEADLINE = "conv1x1_n32_c256_k64_in56"
+MALL_BYTES = 256 * 2 ** 20
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_conv1x1_n32_c256_k64_in56.json")
+
+
+def flops(c):
+    return 2.0 * c.N * c.K * c.P * c.Q * c.C * c.R * c.S
+
+
+def alg_bytes(c):
+    e = 2 if c.dtype == "bf16" else 4
+    return (c.N * c.C * c.H * c.W + c.K * c.C * c.R * c.S) * e + c.N * c.K * c.P * c.Q * 4
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("conv_kernels.hip", "select.cpp"):
+        with open(os.path.join(ROOT, "paper_2101_09808_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def time_layer(c, steps, warmup):
+    """Mean per-launch kernel time (HIP events on the launch stream) and the
+    wall time of `steps` back-to-back launches over rotating buffer sets."""
+    import torch
+    from paper_2101_09808_amd import conv as B
+    from paper_2101_09808_amd.workloads import make_inputs
+
+    In0, Ker0 = make_inputs(c)
+    set_bytes = In0.numel() * In0.element_size() + c.N * c.K * c.P * c.Q * 4
+    nsets = max(2, -(-2 * MALL_BYTES // set_bytes) + 1)
+    dev = torch.device("cuda:0")
+    Ker = Ker0.to(dev)
+    ins = [In0.to(dev) for _ in range(nsets)]
+    outs = [torch.empty(c.N, c.K, c.P, c.Q, device=dev) for _ in range(nsets)]
+    bf16 = c.dtype == "bf16"
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    kp = Ker.data_ptr()
+    ips = [t.data_ptr() for t in ins]
+    ops = [t.data_ptr() for t in outs]
+
+    def fn(i):
+        st = B.conv_fwd_ptr(*c.key(), ips[i], kp, ops[i], sp, bf16)
+        if st != B.CONV_OK:
+            raise B.ConvError(st, "conv_fwd")
+
+    fn(0)  # checked call through the tensor API first
+    (B.conv_fwd_bf16 if bf16 else B.conv_fwd)(ins[0], Ker, out=outs[0])
+    for i in range(warmup):
+        fn(i % nsets)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ev[i][0].record(stream)
+        fn(i % nsets)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [a.elapsed_time(b) for a, b in ev]  # ms
+    per.sort()
+    mean_ms = sum(per) / len(per)
+    return dict(mean_kernel_ms=mean_ms, median_kernel_ms=per[len(per) // 2], min_kernel_ms=per[0],
+                wall_ms_per_step=wall * 1e3 / steps, buffer_sets=nsets)
+
+
+def cpu_baseline(c, budget_s=10.0):
+    """The fp64 oracle on this host's cores over a bounded batch sample."""
+    import numpy as np
+
+    from oracle import conv as oconv
+    from paper_2101_09808_amd.workloads import make_inputs
+
+    In, Ker = make_inputs(c)
+    In = In.float().numpy()
+    Ker = Ker.float().numpy()
+    n = 1
+    t0 = time.perf_counter()
+    oconv.conv_fwd(In[:1], Ker)
+    dt = time.perf_counter() - t0
+    if dt < budget_s and c.N > 1:
+        n = int(min(c.N, max(1, budget_s / max(dt, 1e-6))))
+        t0 = time.perf_counter()
+        oconv.conv_fwd(np.ascontiguousarray(In[:n]), Ker)
+        dt = time.perf_counter() - t0
+    f = flops(c) * n / c.N
+    return {"value": f / dt / 1e9, "unit": "GFLOP/s", "cores": oconv.num_threads(), "kind": "oracle",
+            "sample": f"{n} of {c.N} images of {c.name} (fp64 plain loops, OpenMP over n,k), {dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--no-layers", action="store_true", help="skip the per-layer table")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--layer", default=HEADLINE, help="workload of the timed step")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU (got --gpus {args.gpus}); "
+              "the convolution shards by batch or output channel without communication, "
+              "but no multi-GPU run is part of this benchmark.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2101_09808_amd import conv as B
+    from paper_2101_09808_amd.workloads import BY_NAME, CONFIGS
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    B.lib()  # fail loudly if the HIP library is missing
+    c = BY_NAME[args.layer]
+    dtype_code = B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32
+    plan = B.conv_fwd_plan(*c.key(), dtype=dtype_code)
+    r = time_layer(c, args.steps, args.warmup)
+    F, Bt = flops(c), alg_bytes(c)
+    ms = r["wall_ms_per_step"]
+    value = F / (ms * 1e-3) / 1e9
+    kern_s = r["mean_kernel_ms"] * 1e-3
+    peak_tf = PEAK["bf16_mfma_tflops"] if c.dtype == "bf16" else PEAK["fp32_mfma_tflops"]
+    t_mfma = F / (peak_tf * 1e12)
+    t_hbm = Bt / (PEAK["hbm_gbs"] * 1e9)
+    if t_mfma >= t_hbm:
+        roof = {"bound": "mfma", "achieved": F / kern_s / 1e12, "peak": peak_tf, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": Bt / kern_s / 1e9, "peak": PEAK["hbm_gbs"], "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    if c.name == HEADLINE and os.path.exists(TRAFFIC_FILE):
+        t = json.load(open(TRAFFIC_FILE))
+        if t.get("kernel_sha") == kernel_source_hash() and t.get("plan_variant") == plan["variant"]:
+            roof["traffic"] = t["hbm_bytes_per_launch"]
+    roof["kernel_ms"] = r["mean_kernel_ms"]
+    roof["alg_bytes"] = Bt
+    roof["alg_flop"] = F
+    roof["hbm_gbs_alg"] = Bt / kern_s / 1e9
+    roof["hbm_frac_alg"] = roof["hbm_gbs_alg"] / PEAK["hbm_gbs"]
+    out = {
+        "metric": "conv_fwd GFLOP/s per layer shape + % of MI355X MFMA peak (fp32) on 1 GPU",
+        "value": value, "unit": "GFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if c.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded uniform[-1,1), Table-1-style layer shape)",
+        "config": {"workload": c.name, "N": c.N, "C": c.C, "K": c.K, "H": c.H, "W": c.W, "R": c.R,
+                   "S": c.S, "layout": "NCHW/KCRS->NKPQ", "buffer_sets": r["buffer_sets"],
+                   "plan": {k: plan[k] for k in ("variant", "tile_k", "tile_rows", "tile_cols", "tile_c",
+                                                 "wave_k", "wave_px", "waves_k", "waves_px",
+                                                 "grid_order", "num_wg")}},
+        "pct_fp32_mfma_peak": 100.0 * F / kern_s / 1e12 / PEAK["fp32_mfma_tflops"],
+        "roofline": roof,
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(c)
+    if not args.no_layers:
+        layers = {}
+        for lc in CONFIGS:
+            try:
+                lr = time_layer(lc, 50, 5)
+            except B.ConvError as e:
+                layers[lc.name] = {"error": str(e)}
+                continue
+            lk = lr["mean_kernel_ms"] * 1e-3
+            lpeak = PEAK["bf16_mfma_tflops"] if lc.dtype == "bf16" else PEAK["fp32_mfma_tflops"]
+            layers[lc.name] = {
+                "dtype": lc.dtype, "kernel_us": lk * 1e6, "gflops": flops(lc) / lk / 1e9,
+                "pct_fp32_mfma_peak": 100 * flops(lc) / lk / 1e12 / PEAK["fp32_mfma_tflops"],
+                "pct_dtype_mfma_peak": 100 * flops(lc) / lk / 1e12 / lpeak,
+                "alg_hbm_gbs": alg_bytes(lc) / lk / 1e9,
+                "pct_hbm_peak": 100 * alg_bytes(lc) / lk / 1e9 / PEAK["hbm_gbs"],
+            }
+        out["per_layer"] = layers
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

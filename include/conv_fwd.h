@@ -161,11 +161,14 @@ int conv_model_volume(const int perm[7], const int64_t N[7], const int64_t T[7],
  *   LDS In / Ker elements per buffer; staging loads per thread (In, Ker);
  *   pipeline steps; then the kernel variant's k blocks per wave, pixel blocks
  *   per wave, channels per step, compile-time R, S (0 = runtime), staging
- *   capacity (In, Ker), Ker vector width, threads per workgroup; LDS bytes.
+ *   capacity (In, Ker), Ker vector width, threads per workgroup; LDS bytes;
+ *   kernel family (1 register-staged, 2 direct-to-LDS), In vector width,
+ *   pipeline stages, LDS elements per stage, In elements per stage (family
+ *   2), In and Ker bytes.
  * Writes min(cap, CONV_GEOM_FIELDS) values and returns CONV_GEOM_FIELDS, or
  * a negative conv_status_t (CONV_EINVAL for a plan the kernels cannot run).
  */
-#define CONV_GEOM_FIELDS 40
+#define CONV_GEOM_FIELDS 48
 int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S,
                       const conv_plan_t* plan, int32_t* out, int cap);
 

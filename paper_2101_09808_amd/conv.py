@@ -134,6 +134,13 @@ def conv_fwd(In, Ker, out=None, stream=None):
     return out
 
 
+def conv_fwd_ptr(N, C, K, H, W, R, S, in_ptr, ker_ptr, out_ptr, stream_ptr, bf16=False):
+    """Raw-pointer call for tight loops (device addresses as ints, stream as
+    an int hipStream_t); returns the status code instead of raising."""
+    f = lib().conv_fwd_bf16 if bf16 else lib().conv_fwd
+    return f(N, C, K, H, W, R, S, in_ptr, ker_ptr, out_ptr, stream_ptr)
+
+
 def conv_fwd_bf16(In, Ker, out=None, stream=None):
     """Eq. (1) for bf16 In and Ker, fp32 accumulation and fp32 Out."""
     shape = _check_inputs(In, Ker, torch.bfloat16)
@@ -197,6 +204,7 @@ GEOM_FIELDS = (
     "nwk", "nwp", "order", "num_tiles",
     "lds_in_elems", "lds_ker_elems", "ni_in", "ni_ker", "nchunks",
     "wk", "wp", "tc", "rc", "sc", "max_ni", "max_nk", "ker_vec", "threads", "lds_bytes",
+    "family", "in_vec", "stages", "stage_elems", "in_region", "in_bytes", "ker_bytes",
 )
 
 
@@ -204,8 +212,8 @@ def conv_fwd_geometry(N, C, K, H, W, R, S, plan):
     """The launch geometry a plan resolves to (host only), as a dict."""
     if isinstance(plan, dict):
         plan = ConvPlan.from_dict(plan)
-    buf = (_i32 * 40)()
-    st = lib().conv_fwd_geometry(N, C, K, H, W, R, S, ctypes.byref(plan), buf, 40)
+    buf = (_i32 * 48)()
+    st = lib().conv_fwd_geometry(N, C, K, H, W, R, S, ctypes.byref(plan), buf, 48)
     if st < 0:
         raise ConvError(st, "conv_fwd_geometry")
     return dict(zip(GEOM_FIELDS, list(buf)[:len(GEOM_FIELDS)]))

@@ -6,6 +6,7 @@
 #include <map>
 #include <mutex>
 #include <tuple>
+#include <vector>
 
 #include "conv_internal.h"
 
@@ -25,12 +26,46 @@ int validate_shape(int N, int C, int K, int H, int W, int R, int S) {
   return CONV_OK;
 }
 
-typedef std::tuple<int, int, int, int, int, int, int, int> Key;
+// Per (shape, dtype, Ker alignment) the selected plan and its resolved launch.
+struct Entry {
+  conv_plan_t plan;
+  const Variant* v;
+  Geom g;
+};
+typedef std::tuple<int, int, int, int, int, int, int, int, int> Key;
 std::mutex g_mu;
-std::map<Key, conv_plan_t> g_cache;
+std::map<Key, Entry> g_cache;
 
-int cached_plan(const Shape& s, int dtype, conv_plan_t* out) {
-  const Key key{s.N, s.C, s.K, s.H, s.W, s.R, s.S, dtype};
+int select_entry(const Shape& s, int dtype, bool ker_aligned, Entry* e) {
+  conv_plan_t p;
+  int st = select_plan(s, dtype, &p);
+  if (st != CONV_OK) return st;
+  const Variant* v = find_variant(p.variant);
+  const int elem = dtype == CONV_DTYPE_BF16 ? 2 : 4;
+  if (!ker_aligned && v && v->ker_vec * elem > elem) {
+    // Vector Ker loads need an aligned tensor: best plan of a variant that
+    // loads Ker element-wise.
+    std::vector<conv_plan_t> buf(4096);
+    const int n = enumerate_plans(s, dtype, buf.data(), (int)buf.size());
+    v = nullptr;
+    for (int i = 0; i < n && i < (int)buf.size(); ++i) {
+      const Variant* w = find_variant(buf[i].variant);
+      if (w && w->ker_vec == 1) {
+        p = buf[i];
+        v = w;
+        break;
+      }
+    }
+    if (!v) return CONV_ENOPLAN;
+  }
+  if (!v || !resolve_geom(s, *v, p, &e->g, nullptr)) return CONV_ENOPLAN;
+  e->plan = p;
+  e->v = v;
+  return CONV_OK;
+}
+
+int cached_entry(const Shape& s, int dtype, bool ker_aligned, Entry* out) {
+  const Key key{s.N, s.C, s.K, s.H, s.W, s.R, s.S, dtype, ker_aligned ? 1 : 0};
   {
     std::lock_guard<std::mutex> lk(g_mu);
     auto it = g_cache.find(key);
@@ -39,15 +74,22 @@ int cached_plan(const Shape& s, int dtype, conv_plan_t* out) {
       return CONV_OK;
     }
   }
-  conv_plan_t p;
-  const int st = select_plan(s, dtype, &p);
+  Entry e;
+  const int st = select_entry(s, dtype, ker_aligned, &e);
   if (st != CONV_OK) return st;
   {
     std::lock_guard<std::mutex> lk(g_mu);
-    g_cache[key] = p;
+    g_cache[key] = e;
   }
-  *out = p;
+  *out = e;
   return CONV_OK;
+}
+
+int cached_plan(const Shape& s, int dtype, conv_plan_t* out) {
+  Entry e;
+  const int st = cached_entry(s, dtype, true, &e);
+  if (st == CONV_OK) *out = e.plan;
+  return st;
 }
 
 int run(const Shape& s, const void* In, const void* Ker, float* Out, const conv_plan_t& plan,
@@ -59,26 +101,15 @@ int run(const Shape& s, const void* In, const void* Ker, float* Out, const conv_
   return launch(*v, g, In, Ker, Out, stream);
 }
 
-// The selector assumes 16-byte aligned Ker for vector staging; for other
-// pointers pick the best plan among variants that stage Ker element-wise.
-int plan_for_pointer(const Shape& s, int dtype, const void* Ker, conv_plan_t* plan) {
-  int st = cached_plan(s, dtype, plan);
+// Selected plan for a call: cached per shape; Ker vector loads need a
+// 16-byte aligned tensor.
+int run_selected(const Shape& s, int dtype, const void* In, const void* Ker, float* Out,
+                 void* stream) {
+  const bool aligned = (reinterpret_cast<uintptr_t>(Ker) & 15) == 0;
+  Entry e;
+  const int st = cached_entry(s, dtype, aligned, &e);
   if (st != CONV_OK) return st;
-  const Variant* v = find_variant(plan->variant);
-  const int elem = dtype == CONV_DTYPE_BF16 ? 2 : 4;
-  if (v && v->ker_vec > 1 && (reinterpret_cast<uintptr_t>(Ker) % (elem * v->ker_vec)) != 0) {
-    conv_plan_t buf[512];
-    const int n = enumerate_plans(s, dtype, buf, 512);
-    for (int i = 0; i < n && i < 512; ++i) {
-      const Variant* w = find_variant(buf[i].variant);
-      if (w && w->ker_vec == 1) {
-        *plan = buf[i];
-        return CONV_OK;
-      }
-    }
-    return CONV_ENOPLAN;
-  }
-  return CONV_OK;
+  return launch(*e.v, e.g, In, Ker, Out, stream);
 }
 
 }  // namespace
@@ -90,11 +121,7 @@ int conv_fwd(int N, int C, int K, int H, int W, int R, int S, const float* In, c
   int st = validate_shape(N, C, K, H, W, R, S);
   if (st != CONV_OK) return st;
   if (!In || !Ker || !Out) return CONV_ENULL;
-  const Shape s{N, C, K, H, W, R, S};
-  conv_plan_t plan;
-  st = plan_for_pointer(s, CONV_DTYPE_F32, Ker, &plan);
-  if (st != CONV_OK) return st;
-  return run(s, In, Ker, Out, plan, stream);
+  return run_selected(Shape{N, C, K, H, W, R, S}, CONV_DTYPE_F32, In, Ker, Out, stream);
 }
 
 int conv_fwd_bf16(int N, int C, int K, int H, int W, int R, int S, const uint16_t* In,
@@ -102,11 +129,7 @@ int conv_fwd_bf16(int N, int C, int K, int H, int W, int R, int S, const uint16_
   int st = validate_shape(N, C, K, H, W, R, S);
   if (st != CONV_OK) return st;
   if (!In || !Ker || !Out) return CONV_ENULL;
-  const Shape s{N, C, K, H, W, R, S};
-  conv_plan_t plan;
-  st = plan_for_pointer(s, CONV_DTYPE_BF16, Ker, &plan);
-  if (st != CONV_OK) return st;
-  return run(s, In, Ker, Out, plan, stream);
+  return run_selected(Shape{N, C, K, H, W, R, S}, CONV_DTYPE_BF16, In, Ker, Out, stream);
 }
 
 int conv_fwd_plan(int N, int C, int K, int H, int W, int R, int S, int dtype,
@@ -171,7 +194,8 @@ int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S, const con
       g.nwk, g.nwp, g.order, g.num_tiles,
       g.lds_in_elems, g.lds_ker_elems, g.ni_in, g.ni_ker, g.nchunks,
       v->wk, v->wp, v->tc, v->rc, v->sc, v->max_ni, v->max_nk, v->ker_vec, v->threads, lds,
-      0, 0, 0};
+      v->family, v->in_vec, v->stages, g.stage_elems, g.in_region, (int32_t)g.in_bytes,
+      (int32_t)g.ker_bytes, 0, 0, 0, 0};
   for (int i = 0; i < cap && i < CONV_GEOM_FIELDS; ++i) out[i] = f[i];
   return CONV_GEOM_FIELDS;
 }

@@ -14,18 +14,27 @@ struct Shape {
   int Q() const { return W - S + 1; }
 };
 
+// Kernel families.
+enum {
+  FAMILY_STAGED = 1,  // global -> VGPR -> LDS staging, double buffered (any size)
+  FAMILY_DMA = 2,     // global -> LDS direct buffer loads, NS-stage pipeline
+};
+
 // One compiled kernel instance (template parameters of the kernel family).
 struct Variant {
   int id;
   int dtype;      // CONV_DTYPE_*
+  int family;     // FAMILY_*
   int wk;         // 16-wide k blocks per wave (register tile along k)
   int wp;         // 16-wide pixel blocks per wave (register tile along pixels)
   int tc;         // input channels per pipeline step
   int rc, sc;     // compile-time R, S (0 = runtime)
-  int max_ni;     // max In staging elements per thread
-  int max_nk;     // max Ker staging vectors per thread
-  int ker_vec;    // Ker global load width in elements (1 or 4 for fp32, 8 for bf16)
-  int threads;    // threads per workgroup the instance is built for
+  int max_ni;     // STAGED: max In staging elements per thread; DMA: In loads per wave per step
+  int max_nk;     // STAGED: max Ker staging vectors per thread; DMA: Ker loads per wave per step
+  int ker_vec;    // Ker load width in elements
+  int in_vec;     // In load width in elements (DMA family; 1 for STAGED)
+  int threads;    // threads per workgroup
+  int stages;     // pipeline depth (LDS buffers)
 };
 
 // Fully resolved launch geometry, passed by value to the kernels.
@@ -41,6 +50,8 @@ struct Geom {
   int lds_in_elems, lds_ker_elems;       // LDS elements per pipeline buffer
   int ni_in, ni_ker;                     // staging loads per thread (In elements, Ker vectors)
   int nchunks;                           // pipeline steps = ceil(C / tc)
+  unsigned in_bytes, ker_bytes;          // tensor sizes (DMA family range checks)
+  int stage_elems, in_region;            // DMA family: LDS elements per stage / In part
 };
 
 const Variant* variants(int* count);

@@ -24,6 +24,8 @@
 //     hold 16 consecutive output pixels, so stores coalesce.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "conv_internal.h"
 
 namespace convfwd {
@@ -266,6 +268,227 @@ conv_f32_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
   }
 }
 
+// ---------------------------------------------------------------------------
+// Direct-to-LDS pipeline (gfx950 buffer loads with an LDS destination).
+//
+// Each buffer load writes its 64 lanes' data to LDS at M0 + lane * width, so
+// a wave instruction fills one contiguous 256 B (dword) or 1 KB (dwordx4)
+// block of the stage buffer; lanes whose element lies outside the tensor, the
+// tile or the channel range pass an offset past the buffer's range and the
+// hardware writes zeros.  No VGPRs are used for staging, so NS stages can be
+// in flight.  The loads are issued from inline assembly: the compiler then
+// does not treat them as LDS writes and does not force a full vmcnt wait
+// before every LDS read; instead each step waits for exactly the loads of
+// the step it is about to read (loads retire in order) and then barriers.
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) float lds_float;
+
+constexpr unsigned kOob = 0x80000000u;  // past every buffer's range (tensors < 2 GB)
+
+__device__ __forceinline__ v4i make_rsrc(const void* base, unsigned bytes) {
+  const unsigned long long p = reinterpret_cast<unsigned long long>(base);
+  v4i r;
+  r[0] = (int)(unsigned)p;
+  r[1] = (int)((unsigned)(p >> 32) & 0xffffu);  // stride 0: raw buffer
+  r[2] = (int)bytes;                            // range in bytes
+  r[3] = 0x00020000;                            // 32-bit data format
+  return r;
+}
+
+template <int KV>
+__device__ __forceinline__ void dma_load(v4i rsrc, unsigned m0, unsigned voff) {
+  if constexpr (KV == 1) {
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                 :: "s"(m0), "v"(voff), "s"(rsrc) : "memory", "m0");
+  } else {
+    static_assert(KV == 4, "dword or dwordx4");
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :: "s"(m0), "v"(voff), "s"(rsrc) : "memory", "m0");
+  }
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // s_waitcnt: vmcnt in bits [3:0] and [15:14]; expcnt and lgkmcnt left at max
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
+
+template <int WK, int WP, int NW, int TC, int RC, int SC, int NS, int NLI, int KVI, int NLK, int KVK>
+__global__ void __launch_bounds__(NW * 64)
+conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
+                    float* __restrict__ Out, const Geom g) {
+  static_assert(NS >= 2 && NS <= 4, "pipeline depth");
+  extern __shared__ __align__(16) float lds[];
+  constexpr int IN_REGION = NLI * NW * 64 * KVI;
+  constexpr int KER_REGION = NLK * NW * 64 * KVK;
+  constexpr int STAGE = IN_REGION + KER_REGION;
+  constexpr int L = NLI + NLK;  // loads per wave per step
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int j = lane & 15, gq = lane >> 4;
+  const int wk = wave % g.nwk, wp = wave / g.nwk;
+  const int BK = 16 * WK * g.nwk;
+  const int R = RC ? RC : g.R, S = SC ? SC : g.S;
+  const int RS = R * S;
+  const int H = g.H, W = g.W, C = g.C, K = g.K;
+  const TileCoord t = tile_coord(g, BK);
+  const v4i in_rsrc = make_rsrc(In, g.in_bytes);
+  const v4i ker_rsrc = make_rsrc(Ker, g.ker_bytes);
+  const unsigned lds_base = (unsigned)(size_t)(lds_float*)lds;
+
+  // In loads: instruction i of this wave fills LDS elements
+  // [(i*NW + wave)*64*KVI, +64*KVI) of the [TC][in_cstride] In image.
+  int in_goff[NLI], in_cl[NLI];
+  {
+    const int ncols = t.tw_eff + S - 1;
+#pragma unroll
+    for (int i = 0; i < NLI; ++i) {
+      const int e = ((i * NW + wave) * 64 + lane) * KVI;
+      in_goff[i] = -1;
+      in_cl[i] = 0;
+      if (e < TC * g.in_cstride) {
+        const int cl = e / g.in_cstride, pos = e - cl * g.in_cstride;
+        const int row = pos / g.in_wp, x = pos - row * g.in_wp;
+        if (row < t.nrows && x < ncols) {
+          const int nu = t.nu0 + row;
+          const int n = nu / H, y = nu - n * H;
+          in_goff[i] = ((n * C + cl) * H + y) * W + t.q0 + x;
+          in_cl[i] = cl;
+        }
+      }
+    }
+  }
+  // Ker loads: instruction i fills [(i*NW + wave)*64*KVK, +64*KVK) of the
+  // [BK][ker_rstride] Ker image.
+  const int TCRS = TC * RS;
+  int ker_goff[NLK], ker_m[NLK];
+#pragma unroll
+  for (int i = 0; i < NLK; ++i) {
+    const int e = ((i * NW + wave) * 64 + lane) * KVK;
+    const int kl = e / g.ker_rstride, m = e - kl * g.ker_rstride;
+    ker_goff[i] = -1;
+    ker_m[i] = 0;
+    if (kl < BK && m < TCRS && t.k0 + kl < K) {
+      ker_goff[i] = (t.k0 + kl) * C * RS + m;
+      ker_m[i] = m;
+    }
+  }
+  // Per-lane LDS offsets of this lane's output pixel in each pixel block.
+  const int tpx = g.tr * g.tw;
+  int poff[WP];
+#pragma unroll
+  for (int pb = 0; pb < WP; ++pb) {
+    const int px = (wp * WP + pb) * 16 + j;
+    const int row_i = px / g.tw, col = px - row_i * g.tw;
+    const int rho = t.rho0 + row_i;
+    int off = 0;
+    if (px < tpx && rho < t.rho_end && col < t.tw_eff) {
+      const int n = rho / g.P, p = rho - n * g.P;
+      off = (n * H + p - t.nu0) * g.in_wp + col;
+    }
+    poff[pb] = off;
+  }
+  int koff[WK];
+#pragma unroll
+  for (int kb = 0; kb < WK; ++kb) koff[kb] = ((wk * WK + kb) * 16 + j) * g.ker_rstride;
+
+  auto issue = [&](int ch) {
+    const int c0 = ch * TC;
+    const unsigned stage = lds_base + (unsigned)((ch % NS) * STAGE) * 4u;
+    const int coff = c0 * H * W;
+#pragma unroll
+    for (int i = 0; i < NLI; ++i) {
+      const unsigned voff =
+          (in_goff[i] >= 0 && c0 + in_cl[i] < C) ? (unsigned)(coff + in_goff[i]) * 4u : kOob;
+      dma_load<KVI>(in_rsrc, __builtin_amdgcn_readfirstlane(stage + (unsigned)((i * NW + wave) * 64 * KVI) * 4u),
+                    voff);
+    }
+    const int mlim = (C - c0) * RS, kc = c0 * RS;
+#pragma unroll
+    for (int i = 0; i < NLK; ++i) {
+      const unsigned voff =
+          (ker_goff[i] >= 0 && ker_m[i] < mlim) ? (unsigned)(kc + ker_goff[i]) * 4u : kOob;
+      dma_load<KVK>(ker_rsrc,
+                    __builtin_amdgcn_readfirstlane(stage + (unsigned)(IN_REGION + (i * NW + wave) * 64 * KVK) * 4u),
+                    voff);
+    }
+  };
+
+  v4f acc[WK][WP];
+#pragma unroll
+  for (int kb = 0; kb < WK; ++kb)
+#pragma unroll
+    for (int pb = 0; pb < WP; ++pb) acc[kb][pb] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  // One chunk: steps st = (channel quad cs, tap r, tap s).  The operands of
+  // step st+1 are read from LDS before the MFMAs of step st are issued, so
+  // LDS latency overlaps the matrix core instead of stalling it.
+  static_assert(RC > 0 && SC > 0, "compile-time taps");
+  constexpr int NSTEP = (TC / 4) * RC * SC;
+  auto compute = [&](int buf) {
+    const float* lin = lds + buf * STAGE;
+    const float* lk = lin + IN_REGION;
+    float a[2][WK], b[2][WP];
+    auto fetch = [&](int st, int slot) {
+      const int cs = st / (RC * SC), rs = st % (RC * SC);
+      const int r = rs / SC, s = rs % SC;
+      const float* lin_c = lin + (cs * 4 + gq) * g.in_cstride + r * g.in_wp + s;
+      const float* lk_c = lk + (cs * 4 + gq) * RS + rs;
+#pragma unroll
+      for (int kb = 0; kb < WK; ++kb) a[slot][kb] = lk_c[koff[kb]];
+#pragma unroll
+      for (int pb = 0; pb < WP; ++pb) b[slot][pb] = lin_c[poff[pb]];
+    };
+    fetch(0, 0);
+#pragma unroll
+    for (int st = 0; st < NSTEP; ++st) {
+      const int cur = st & 1;
+      if (st + 1 < NSTEP) fetch(st + 1, cur ^ 1);
+#pragma unroll
+      for (int kb = 0; kb < WK; ++kb)
+#pragma unroll
+        for (int pb = 0; pb < WP; ++pb)
+          acc[kb][pb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[cur][kb], b[cur][pb], acc[kb][pb], 0, 0, 0);
+    }
+  };
+
+  const int nch = g.nchunks;
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nch) issue(s);
+  for (int ch = 0; ch < nch; ++ch) {
+    // wait for this step's loads: the later steps already issued may stay in flight
+    const int ahead = min(NS - 2, nch - 1 - ch);
+    if (NS >= 4 && ahead >= 2) wait_vmcnt<(NS >= 4 ? 2 * L : 0)>();
+    else if (NS >= 3 && ahead >= 1) wait_vmcnt<(NS >= 3 ? L : 0)>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if (ch + NS - 1 < nch) issue(ch + NS - 1);
+    compute(ch % NS);
+  }
+
+  // Epilogue: lane (j, gq) holds Out[k0 + block*16 + 4*gq + v][pixel j].
+  const size_t PQ = (size_t)g.P * g.Q;
+#pragma unroll
+  for (int pb = 0; pb < WP; ++pb) {
+    const int px = (wp * WP + pb) * 16 + j;
+    const int row_i = px / g.tw, col = px - row_i * g.tw;
+    const int rho = t.rho0 + row_i;
+    if (px < tpx && rho < t.rho_end && col < t.tw_eff) {
+      const int n = rho / g.P, p = rho - n * g.P;
+      float* ob = Out + ((size_t)n * K * g.P + p) * g.Q + t.q0 + col;
+#pragma unroll
+      for (int kb = 0; kb < WK; ++kb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int k = t.k0 + (wk * WK + kb) * 16 + 4 * gq + v;
+          if (k < K) ob[(size_t)k * PQ] = acc[kb][pb][v];
+        }
+    }
+  }
+}
+
 typedef void (*KernelF32)(const float*, const float*, float*, const Geom);
 
 struct Instance {
@@ -273,11 +496,37 @@ struct Instance {
   KernelF32 f32;
 };
 
-#define F32_INST(ID, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV)                               \
-  Instance{Variant{ID, CONV_DTYPE_F32, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV, kThreads}, \
+#define F32_INST(ID, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV)                                  \
+  Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STAGED, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV, 1, \
+                   kThreads, 2},                                                             \
            &conv_f32_kernel<WK, WP, TC, RC, SC, MAXNI, MAXNK, KV>}
 
+#define F32_DMA(ID, WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK)                              \
+  Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_DMA, WK, WP, TC, RC, SC, NLI, NLK, KVK, KVI, NW * 64, \
+                   NS},                                                                          \
+           &conv_f32_dma_kernel<WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK>}
+
 const Instance kInstances[] = {
+    // ---- direct-to-LDS pipeline
+    // 3x3 taps
+    F32_DMA(101, 1, 13, 4, 8, 3, 3, 3, 9, 1, 5, 4),
+    F32_DMA(102, 4, 4, 4, 8, 3, 3, 3, 12, 1, 10, 4),
+    F32_DMA(103, 2, 2, 4, 8, 3, 3, 3, 8, 1, 5, 4),
+    F32_DMA(104, 1, 4, 4, 8, 3, 3, 3, 8, 1, 5, 4),
+    F32_DMA(105, 2, 4, 4, 8, 3, 3, 3, 12, 1, 5, 4),
+    F32_DMA(106, 1, 7, 8, 8, 3, 3, 3, 5, 1, 3, 4),
+    F32_DMA(107, 1, 4, 8, 8, 3, 3, 3, 4, 1, 3, 4),
+    F32_DMA(108, 2, 4, 8, 8, 3, 3, 3, 6, 1, 3, 4),
+    // 1x1 taps
+    F32_DMA(121, 1, 25, 4, 16, 1, 1, 4, 7, 4, 2, 4),
+    F32_DMA(126, 1, 13, 8, 16, 1, 1, 4, 4, 4, 1, 4),
+    F32_DMA(127, 1, 7, 8, 16, 1, 1, 4, 2, 4, 1, 4),
+    F32_DMA(128, 2, 7, 8, 16, 1, 1, 3, 4, 4, 1, 4),
+    F32_DMA(122, 1, 25, 4, 16, 1, 1, 3, 7, 4, 2, 4),
+    F32_DMA(123, 4, 4, 4, 16, 1, 1, 3, 4, 4, 2, 4),
+    F32_DMA(124, 2, 13, 4, 16, 1, 1, 3, 7, 4, 2, 4),
+    F32_DMA(125, 1, 13, 4, 16, 1, 1, 4, 4, 4, 2, 4),
+    // ---- register-staged, double buffered (any shape, any alignment)
     // 3x3 taps, Ker staged in float4
     F32_INST(1, 4, 4, 8, 3, 3, 8, 12, 4),
     F32_INST(2, 2, 4, 8, 3, 3, 8, 12, 4),
@@ -327,15 +576,25 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
            void* stream) {
   const Instance* inst = find_instance(v.id);
   if (!inst) return CONV_EINVAL;
-  const int lds_bytes = 2 * (g.lds_in_elems + g.lds_ker_elems) * (int)sizeof(float);
+  const int lds_bytes = (v.family == FAMILY_DMA)
+                            ? v.stages * g.stage_elems * (int)sizeof(float)
+                            : 2 * (g.lds_in_elems + g.lds_ker_elems) * (int)sizeof(float);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   if (v.ker_vec > 1 && (reinterpret_cast<uintptr_t>(Ker) % (4 * v.ker_vec)) != 0) return CONV_EINVAL;
   if (lds_bytes > 65536) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(inst->f32),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes) != hipSuccess)
-      return CONV_EHIP;
+    // Raise the kernel's dynamic LDS limit once (to the device maximum).
+    static std::mutex mu;
+    static bool done[kNumInstances] = {};
+    const int idx = (int)(inst - kInstances);
+    std::lock_guard<std::mutex> lk(mu);
+    if (!done[idx]) {
+      if (hipFuncSetAttribute(reinterpret_cast<const void*>(inst->f32),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, 163840) != hipSuccess)
+        return CONV_EHIP;
+      done[idx] = true;
+    }
   }
-  hipLaunchKernelGGL(inst->f32, dim3(g.num_tiles), dim3(kThreads), lds_bytes, st,
+  hipLaunchKernelGGL(inst->f32, dim3(g.num_tiles), dim3(v.threads), lds_bytes, st,
                      static_cast<const float*>(In), static_cast<const float*>(Ker), Out, g);
   return hipGetLastError() == hipSuccess ? CONV_OK : CONV_EHIP;
 }

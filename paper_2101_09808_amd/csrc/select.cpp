@@ -28,6 +28,9 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <map>
+#include <mutex>
+#include <tuple>
 #include <vector>
 
 #include "conv_internal.h"
@@ -143,7 +146,7 @@ int conflict_cost(const int* addr) {
 
 // Row pitch of the Ker tile: >= need, a multiple of `mult`, with the least
 // conflicted A-operand reads (lane (i, g) reads row i, column g*RS).
-int pick_ker_rstride(int need, int mult, int rs) {
+int pick_ker_rstride_uncached(int need, int mult, int rs) {
   int best = -1, best_cost = 1 << 30;
   for (int cand = ((need + mult - 1) / mult) * mult; cand < need + 64 + mult; cand += mult) {
     int addr[64];
@@ -159,7 +162,7 @@ int pick_ker_rstride(int need, int mult, int rs) {
 
 // Channel stride of the In tile: >= need, a multiple of 4, least conflicted
 // B-operand reads (lane (j, g) reads channel g, pixel j).
-int pick_in_cstride(int need) {
+int pick_in_cstride_uncached(int need) {
   int best = -1, best_cost = 1 << 30;
   for (int cand = ((need + 3) / 4) * 4; cand < need + 68; cand += 4) {
     int addr[64];
@@ -171,6 +174,36 @@ int pick_in_cstride(int need) {
     }
   }
   return best;
+}
+
+// Both searches depend on a few small integers; memoise them.
+std::mutex g_pad_mu;
+std::map<std::tuple<int, int, int>, int> g_pad_cache;
+
+int pick_ker_rstride(int need, int mult, int rs) {
+  const auto key = std::make_tuple(need, mult, rs);
+  {
+    std::lock_guard<std::mutex> lk(g_pad_mu);
+    auto it = g_pad_cache.find(key);
+    if (it != g_pad_cache.end()) return it->second;
+  }
+  const int v = pick_ker_rstride_uncached(need, mult, rs);
+  std::lock_guard<std::mutex> lk(g_pad_mu);
+  g_pad_cache[key] = v;
+  return v;
+}
+
+int pick_in_cstride(int need) {
+  const auto key = std::make_tuple(need, -1, -1);
+  {
+    std::lock_guard<std::mutex> lk(g_pad_mu);
+    auto it = g_pad_cache.find(key);
+    if (it != g_pad_cache.end()) return it->second;
+  }
+  const int v = pick_in_cstride_uncached(need);
+  std::lock_guard<std::mutex> lk(g_pad_mu);
+  g_pad_cache[key] = v;
+  return v;
 }
 
 // The problem as the kernels see it: a 1x1 correlation of an H x W plane is
@@ -220,13 +253,41 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
   if (v.ker_vec > 1 && ((int64_t)s.C * RS % v.ker_vec != 0 || TCRS % v.ker_vec != 0)) return false;
   if (TCRS >= (1 << 16) || BK >= (1 << 15)) return false;
   const int ker_rstride = pick_ker_rstride(TCRS, std::max(4, v.ker_vec), RS);
-  const int64_t lds_in = (int64_t)TC * in_cstride;
-  const int64_t lds_ker = ((int64_t)BK * ker_rstride + 3) / 4 * 4;
-  const int64_t bytes = 2 * (lds_in + lds_ker) * 4;
+  const int64_t in_elems_total = (int64_t)s.N * s.C * s.H * s.W;
+  const int64_t ker_elems_total = (int64_t)s.K * s.C * RS;
+  int64_t lds_in, lds_ker, bytes, ni_in, ni_ker, stage = 0, in_region = 0;
+  if (v.family == FAMILY_DMA) {
+    // Byte offsets of the buffer loads are 32-bit with an out-of-range
+    // marker at 2^31: both tensors must stay below 2 GB.
+    if (in_elems_total * 4 >= (int64_t(1) << 31) || ker_elems_total * 4 >= (int64_t(1) << 31))
+      return false;
+    if (v.in_vec == 4) {
+      // Vector In loads need whole, aligned 4-element groups that never
+      // straddle a row or the tile edge: pointwise taps, rows and tiles in
+      // multiples of 4 elements.
+      if (s.R != 1 || s.S != 1 || s.W % 4 || tw % 4 || Q % 4) return false;
+    } else if (v.in_vec != 1) {
+      return false;
+    }
+    const int64_t nw = v.threads / 64;
+    in_region = (int64_t)v.max_ni * nw * 64 * v.in_vec;
+    const int64_t ker_region = (int64_t)v.max_nk * nw * 64 * v.ker_vec;
+    lds_in = (int64_t)TC * in_cstride;
+    lds_ker = (int64_t)BK * ker_rstride;
+    if (in_cstride % v.in_vec || lds_in > in_region || lds_ker > ker_region) return false;
+    stage = in_region + ker_region;
+    bytes = (int64_t)v.stages * stage * 4;
+    ni_in = v.max_ni;
+    ni_ker = v.max_nk;
+  } else {
+    lds_in = (int64_t)TC * in_cstride;
+    lds_ker = ((int64_t)BK * ker_rstride + 3) / 4 * 4;
+    bytes = 2 * (lds_in + lds_ker) * 4;
+    ni_in = cdiv(TC * E, v.threads);
+    ni_ker = cdiv((int64_t)BK * TCRS / v.ker_vec, v.threads);
+    if (ni_in > v.max_ni || ni_ker > v.max_nk) return false;
+  }
   if (bytes > kHw.lds_bytes) return false;
-  const int64_t ni_in = cdiv(TC * E, v.threads);
-  const int64_t ni_ker = cdiv((int64_t)BK * TCRS / v.ker_vec, v.threads);
-  if (ni_in > v.max_ni || ni_ker > v.max_nk) return false;
   Geom q;
   std::memset(&q, 0, sizeof(q));
   q.N = s.N; q.C = s.C; q.K = s.K; q.H = s.H; q.W = s.W; q.R = s.R; q.S = s.S;
@@ -241,6 +302,10 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
   q.lds_in_elems = (int)lds_in; q.lds_ker_elems = (int)lds_ker;
   q.ni_in = (int)ni_in; q.ni_ker = (int)ni_ker;
   q.nchunks = (int)cdiv(s.C, TC);
+  q.in_bytes = (unsigned)std::min<int64_t>(in_elems_total * 4, 0xffffffffLL);
+  q.ker_bytes = (unsigned)std::min<int64_t>(ker_elems_total * 4, 0xffffffffLL);
+  q.stage_elems = (int)stage;
+  q.in_region = (int)in_region;
   if (g) *g = q;
   if (lds_bytes) *lds_bytes = (int)bytes;
   return true;
@@ -346,6 +411,10 @@ void fill_plan_fields(conv_plan_t* p, const Variant& v, int nwk, int nwp, int tr
 // Deterministic preference among plans (tie-breaks: predicted time, total
 // predicted bytes, fewer workgroups, variant id, larger k tile).
 bool better(const conv_plan_t& a, const conv_plan_t& b) {
+  // The direct-to-LDS pipeline keeps several steps of loads in flight; the
+  // register-staged family is the fallback for shapes it cannot take.
+  const int fa = find_variant(a.variant)->family, fb = find_variant(b.variant)->family;
+  if (fa != fb) return fa == FAMILY_DMA;
   if (a.pred_total_us != b.pred_total_us) return a.pred_total_us < b.pred_total_us;
   double ba = 0, bb = 0;
   for (int l = 0; l < CONV_NUM_LVLS; ++l) {

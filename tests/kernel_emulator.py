@@ -1,6 +1,8 @@
-"""CPU emulation of the fp32 HIP kernel's addressing (tests only).
+"""CPU emulation of the fp32 HIP kernels' addressing (tests only).
 
-Mirrors, step by step, the index arithmetic of ``conv_f32_kernel`` for a
+Mirrors, step by step, the index arithmetic of ``conv_f32_kernel`` (family 1,
+register-staged) and ``conv_f32_dma_kernel`` (family 2, direct-to-LDS loads)
+for a
 resolved launch geometry (``conv_fwd_geometry``): workgroup -> tile mapping
 (with the XCD remap), the per-thread staging lists, LDS writes and reads of
 each pipeline step, the MFMA operand lanes and the epilogue stores.  Every
@@ -57,7 +59,7 @@ def emulate(g, In, Ker, wgs=None):
     output element (NaN outputs where nothing was stored)."""
     N, C, K, H, W, R, S, P, Q = (g[x] for x in "N C K H W R S P Q".split())
     WK, WP, TC, KV, NT = g["wk"], g["wp"], g["tc"], g["ker_vec"], g["threads"]
-    _chk(NT == 256, "threads per workgroup")
+    _chk(NT == 256 or (g["family"] == 2 and NT in (256, 512)), "threads per workgroup")
     nwk, nwp = g["nwk"], g["nwp"]
     _chk(nwk * nwp * 64 == NT, "waves do not fill the workgroup")
     BK = 16 * WK * nwk
@@ -66,8 +68,22 @@ def emulate(g, In, Ker, wgs=None):
         _chk(g["rc"] == R and g["sc"] == S, "compile-time taps differ from the shape")
     in_size, ker_size, out_size = N * C * H * W, K * C * R * S, N * K * P * Q
     _chk(In.size == in_size and Ker.size == ker_size, "input sizes")
-    lin_n, lker_n = g["lds_in_elems"], g["lds_ker_elems"]
-    _chk(2 * (lin_n + lker_n) * 4 == g["lds_bytes"], "LDS byte count")
+    dma = g["family"] == 2
+    NW = NT // 64
+    if dma:
+        NLI, NLK, KVI, NS = g["max_ni"], g["max_nk"], g["in_vec"], g["stages"]
+        IN_REGION = NLI * NW * 64 * KVI
+        KER_REGION = NLK * NW * 64 * KV
+        _chk(g["in_region"] == IN_REGION and g["stage_elems"] == IN_REGION + KER_REGION, "DMA regions")
+        _chk(NS * g["stage_elems"] * 4 == g["lds_bytes"], "LDS byte count")
+        _chk(g["in_bytes"] == in_size * 4 and g["ker_bytes"] == ker_size * 4, "buffer ranges")
+        _chk(in_size * 4 < 2 ** 31 and ker_size * 4 < 2 ** 31, "tensors under 2 GB")
+        lin_n, lker_n = IN_REGION, KER_REGION
+        _chk(TC * g["in_cstride"] <= IN_REGION, "In tile exceeds its LDS region")
+        _chk(BK * g["ker_rstride"] <= KER_REGION, "Ker tile exceeds its LDS region")
+    else:
+        lin_n, lker_n = g["lds_in_elems"], g["lds_ker_elems"]
+        _chk(2 * (lin_n + lker_n) * 4 == g["lds_bytes"], "LDS byte count")
     _chk(g["lds_bytes"] <= 160 * 1024, "LDS capacity")
     out = np.full(out_size, np.nan)
     written = np.zeros(out_size, np.int64)
@@ -78,9 +94,10 @@ def emulate(g, In, Ker, wgs=None):
     TCRS = TC * RS
     _chk(TCRS % KV == 0, "Ker vector width")
     per_row = TCRS // KV
-    _chk(g["ni_in"] <= g["max_ni"] and g["ni_ker"] <= g["max_nk"], "staging capacity")
-    _chk(g["ni_in"] * NT >= TC * E, "In staging does not cover the LDS tile")
-    _chk(g["ni_ker"] * NT >= BK * per_row, "Ker staging does not cover the LDS tile")
+    if not dma:
+        _chk(g["ni_in"] <= g["max_ni"] and g["ni_ker"] <= g["max_nk"], "staging capacity")
+        _chk(g["ni_in"] * NT >= TC * E, "In staging does not cover the LDS tile")
+        _chk(g["ni_ker"] * NT >= BK * per_row, "Ker staging does not cover the LDS tile")
     seen_L = set()
     for b in (range(g["num_tiles"]) if wgs is None else wgs):
         L, t = tile_coord(g, b, BK)
@@ -130,7 +147,50 @@ def emulate(g, In, Ker, wgs=None):
         lin = [np.full(lin_n, np.nan), np.full(lin_n, np.nan)]
         lker = [np.full(lker_n, np.nan), np.full(lker_n, np.nan)]
 
+        def stage_dma(c0, buf):
+            wave = tid >> 6
+            lane_t = tid & 63
+            fresh_in = np.full(lin_n, np.nan)
+            for i in range(NLI):
+                e = ((i * NW + wave) * 64 + lane_t) * KVI
+                cl, pos = e // g["in_cstride"], e % g["in_cstride"]
+                row, x = pos // g["in_wp"], pos % g["in_wp"]
+                valid = (e < TC * g["in_cstride"]) & (row < t["nrows"]) & (x < ncols) & (c0 + cl < C)
+                nu = t["nu0"] + row
+                n, y = nu // H, nu % H
+                goff = ((n * C + cl) * H + y) * W + t["q0"] + x
+                for q in range(KVI):
+                    src = c0 * H * W + goff + q
+                    _chk((src[valid] >= 0) & (src[valid] < in_size), "In read out of bounds")
+                    _chk(~valid | (src * 4 < 2 ** 31), "In byte offset overflows")
+                    vals = np.where(valid, In[np.clip(src, 0, in_size - 1)], 0.0)
+                    dst = e + q
+                    _chk(dst < lin_n, "In DMA writes past its region")
+                    _chk(np.isnan(fresh_in[dst]), "two lanes write one LDS In element")
+                    fresh_in[dst] = vals
+            lin[buf][:] = fresh_in
+            fresh_k = np.full(lker_n, np.nan)
+            mlim = (C - c0) * RS
+            for i in range(NLK):
+                e = ((i * NW + wave) * 64 + lane_t) * KV
+                kl, m = e // g["ker_rstride"], e % g["ker_rstride"]
+                valid = (kl < BK) & (m < TCRS) & (t["k0"] + kl < K) & (m < mlim)
+                if KV > 1:
+                    _chk(~valid | (m + KV <= mlim), "Ker vector straddles the channel range")
+                    _chk(g["ker_rstride"] % KV == 0, "Ker vector straddles an LDS row")
+                for q in range(KV):
+                    src = (t["k0"] + kl) * C * RS + c0 * RS + m + q
+                    _chk((src[valid] >= 0) & (src[valid] < ker_size), "Ker read out of bounds")
+                    vals = np.where(valid, Ker[np.clip(src, 0, ker_size - 1)], 0.0)
+                    dst = e + q
+                    _chk(dst < lker_n, "Ker DMA writes past its region")
+                    _chk(np.isnan(fresh_k[dst]), "two lanes write one LDS Ker element")
+                    fresh_k[dst] = vals
+            lker[buf][:] = fresh_k
+
         def stage(c0, buf):
+            if dma:
+                return stage_dma(c0, buf)
             fresh_in = np.full(lin_n, np.nan)
             for ok, cl, loff, goff in in_items:
                 use = ok

@@ -87,15 +87,21 @@ def test_plan_invariants(shape):
     assert B.conv_fwd_plan(*dims, dtype=dtype) == plan
     cands = B.conv_fwd_candidates(*dims, dtype=dtype)
     assert cands[0] == plan
-    tot = [c["pred_total_us"] for c in cands]
-    assert tot == sorted(tot)
+    # direct-to-LDS plans first, each family ordered by predicted time
+    fam = [B.conv_fwd_geometry(*dims, c)["family"] for c in cands]
+    assert fam == sorted(fam, key=lambda f: 0 if f == 2 else 1)
+    for f in set(fam):
+        tot = [c["pred_total_us"] for c, ff in zip(cands, fam) if ff == f]
+        assert tot == sorted(tot)
 
 
 def test_selector_is_minimum_of_its_objective():
     """The chosen plan has the smallest predicted max-level time of all the
-    candidates it scored (the min-max of Sec. 5)."""
+    candidates of its kernel family (the min-max of Sec. 5)."""
     for c in CONFIGS:
         if c.dtype != "f32":
             continue
         cands = B.conv_fwd_candidates(*c.key())
-        assert cands[0]["pred_total_us"] == min(x["pred_total_us"] for x in cands)
+        fam0 = B.conv_fwd_geometry(*c.key(), cands[0])["family"]
+        same = [x for x in cands if B.conv_fwd_geometry(*c.key(), x)["family"] == fam0]
+        assert cands[0]["pred_total_us"] == min(x["pred_total_us"] for x in same)
