@@ -162,9 +162,9 @@ int conv_model_volume(const int perm[7], const int64_t N[7], const int64_t T[7],
  *   pipeline steps; then the kernel variant's k blocks per wave, pixel blocks
  *   per wave, channels per step, compile-time R, S (0 = runtime), staging
  *   capacity (In, Ker), Ker vector width, threads per workgroup; LDS bytes;
- *   kernel family (1 register-staged, 2 direct-to-LDS), In vector width,
- *   pipeline stages, LDS elements per stage, In elements per stage (family
- *   2), In and Ker bytes.
+ *   kernel family (1 register-staged, 2 direct-to-LDS, 3 bf16), In vector
+ *   width, pipeline stages, LDS elements per stage (family 3: LDS bytes), In
+ *   elements per stage (family 2), In and Ker bytes, workgroups launched.
  * Writes min(cap, CONV_GEOM_FIELDS) values and returns CONV_GEOM_FIELDS, or
  * a negative conv_status_t (CONV_EINVAL for a plan the kernels cannot run).
  */

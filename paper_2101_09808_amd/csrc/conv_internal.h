@@ -18,6 +18,7 @@ struct Shape {
 enum {
   FAMILY_STAGED = 1,  // global -> VGPR -> LDS staging, double buffered (any size)
   FAMILY_DMA = 2,     // global -> LDS direct buffer loads, NS-stage pipeline
+  FAMILY_BF16 = 3,    // bf16 inputs: persistent, channel-fastest transposed LDS tiles
 };
 
 // One compiled kernel instance (template parameters of the kernel family).
@@ -52,6 +53,8 @@ struct Geom {
   int nchunks;                           // pipeline steps = ceil(C / tc)
   unsigned in_bytes, ker_bytes;          // tensor sizes (DMA family range checks)
   int stage_elems, in_region;            // DMA family: LDS elements per stage / In part
+                                         // (bf16 family: stage_elems = LDS bytes)
+  int grid;                              // workgroups launched (persistent families)
 };
 
 const Variant* variants(int* count);

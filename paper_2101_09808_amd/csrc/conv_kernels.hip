@@ -489,22 +489,244 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 inputs, fp32 accumulation (16x16x32 bf16 MFMA).
+//
+// The MFMA's 32-deep reduction is one tap (r, s) of 32 input channels, so
+// both operands must hold 8 consecutive channels per lane.  In arrives as
+// NCHW; the staging step transposes a tile into a channel-fastest LDS image
+// [row][pixel][32 channels] (64 B per pixel, four 16 B chunks of 8 channels,
+// chunk index XOR-swizzled with pixel bits so that 16 lanes reading 16
+// neighbouring pixels touch every bank pair once).  Ker is held in LDS for the
+// whole kernel as [k][tap][32 channels] (same chunk swizzle by k).  Each
+// workgroup is persistent over a contiguous range of tiles; while it computes
+// one tile, the global loads of the next tile's In are in flight in
+// registers.  Per tile: stage, barrier, MFMAs, stores.
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef unsigned short v8u16 __attribute__((ext_vector_type(8)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ int chunk_swz(int chunk, int idx) { return chunk ^ ((idx >> 1) & 3); }
+
+template <int WK, int WP, int RC, int SC, int MAXIT>
+__global__ void __launch_bounds__(kThreads)
+conv_bf16_kernel(const unsigned short* __restrict__ In, const unsigned short* __restrict__ Ker,
+                 float* __restrict__ Out, const Geom g) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int TC = 32;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int j = lane & 15, gq = lane >> 4;
+  const int wk = wave % g.nwk, wp = wave / g.nwk;
+  const int BK = 16 * WK * g.nwk;
+  const int R = RC, S = SC, RS = RC * SC;
+  const int H = g.H, W = g.W, C = g.C, K = g.K, P = g.P, Q = g.Q;
+  // LDS: Ker [BK][kpitch taps][64 B], then In [in_rows][in_wp pixels][64 B]
+  const int kpitch = (RS & 1) ? RS : RS + 1;
+  unsigned char* lker = smem;
+  unsigned char* lin = smem + (size_t)BK * kpitch * 64;
+  const int tiles = g.tiles_rows * g.tiles_cols * g.tiles_k;
+  const int G = gridDim.x;
+  const int L = xcd_remap(blockIdx.x, G);
+  const int per = (tiles + G - 1) / G;
+  const int t_begin = L * per, t_end = min(tiles, t_begin + per);
+  if (t_begin >= t_end) return;
+  const int nchunks = (C + TC - 1) / TC;
+  const bool resident = (nchunks == 1) && (g.tiles_k == 1);
+
+  auto tile_of = [&](int T, int& kt, int& ct, int& rt) {
+    kt = T % g.tiles_k;
+    const int rest = T / g.tiles_k;
+    ct = rest % g.tiles_cols;
+    rt = rest / g.tiles_cols;
+  };
+
+  // Ker staging for channel chunk c0 and k tile k0: items (kl, tap, octet).
+  auto stage_ker = [&](int k0, int c0) {
+    const int items = BK * RS * 4;
+    for (int it = tid; it < items; it += kThreads) {
+      const int o = it & 3, rest = it >> 2;
+      const int rs = rest % RS, kl = rest / RS;
+      v8u16 v;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int c = c0 + 8 * o + e, k = k0 + kl;
+        v[e] = (c < C && k < K) ? Ker[((size_t)k * C + c) * RS + rs] : (unsigned short)0;
+      }
+      *reinterpret_cast<v8u16*>(lker + ((size_t)kl * kpitch + rs) * 64 + chunk_swz(o, kl) * 16) = v;
+    }
+  };
+
+  // In staging through registers: items (octet o, halo row, pixel pair).
+  const int in_wp = g.in_wp;             // halo columns, even
+  const int npair = in_wp >> 1;
+  const int in_items = 4 * g.in_rows * npair;
+  unsigned st_lo[MAXIT][8];              // per item: 8 channels x 2 pixels (packed pairs)
+  auto gload_in = [&](int T, int c0) {
+    int kt, ct, rt;
+    tile_of(T, kt, ct, rt);
+    const int NP = g.N * P;
+    const int rho0 = rt * g.tr, rho_end = min(rho0 + g.tr, NP);
+    const int q0 = ct * g.tw, ncols = min(g.tw, Q - q0) + S - 1;
+    const int nf = rho0 / P, nu0 = nf * H + (rho0 - nf * P);
+    const int nl = (rho_end - 1) / P, nrows = nl * H + (rho_end - 1 - nl * P) + R - nu0;
+    const bool even = ((W | q0) & 1) == 0 && (reinterpret_cast<uintptr_t>(In) & 3) == 0;
+#pragma unroll
+    for (int m = 0; m < MAXIT; ++m) {
+      const int it = tid + m * kThreads;
+      const int o = it / (g.in_rows * npair), rest = it - o * (g.in_rows * npair);
+      const int row = rest / npair, x = (rest - row * npair) * 2;
+      const bool ok = it < in_items && row < nrows;
+      const int nu = nu0 + row;
+      const int n = nu / H, y = nu - n * H;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int c = c0 + 8 * o + e;
+        unsigned v = 0;
+        if (ok && c < C && x < ncols) {
+          const size_t base = (((size_t)n * C + c) * H + y) * W + q0 + x;
+          if (even && x + 1 < ncols) {
+            v = *reinterpret_cast<const unsigned*>(In + base);
+          } else {
+            v = In[base];
+            if (x + 1 < ncols) v |= (unsigned)In[base + 1] << 16;
+          }
+        }
+        st_lo[m][e] = v;
+      }
+    }
+  };
+  auto lstore_in = [&]() {
+#pragma unroll
+    for (int m = 0; m < MAXIT; ++m) {
+      const int it = tid + m * kThreads;
+      if (it < in_items) {
+        const int o = it / (g.in_rows * npair), rest = it - o * (g.in_rows * npair);
+        const int row = rest / npair, x = (rest - row * npair) * 2;
+        v4u p0, p1;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const unsigned a = st_lo[m][2 * e], b = st_lo[m][2 * e + 1];
+          p0[e] = (a & 0xffffu) | (b << 16);          // pixel x: channels 2e, 2e+1
+          p1[e] = (a >> 16) | (b & 0xffff0000u);      // pixel x+1
+        }
+        const int px0 = row * in_wp + x, px1 = px0 + 1;
+        *reinterpret_cast<v4u*>(lin + (size_t)px0 * 64 + chunk_swz(o, px0) * 16) = p0;
+        *reinterpret_cast<v4u*>(lin + (size_t)px1 * 64 + chunk_swz(o, px1) * 16) = p1;
+      }
+    }
+  };
+
+  if (resident) {
+    stage_ker(0, 0);
+  }
+  if (resident) gload_in(t_begin, 0);
+  for (int T = t_begin; T < t_end; ++T) {
+    int kt, ct, rt;
+    tile_of(T, kt, ct, rt);
+    const int NP = g.N * P;
+    const int rho0 = rt * g.tr, rho_end = min(rho0 + g.tr, NP);
+    const int q0 = ct * g.tw, tw_eff = min(g.tw, Q - q0);
+    const int k0 = kt * BK;
+    const int nf = rho0 / P, nu0 = nf * H + (rho0 - nf * P);
+    const int tpx = g.tr * g.tw;
+    int poff[WP];
+#pragma unroll
+    for (int pb = 0; pb < WP; ++pb) {
+      const int px = (wp * WP + pb) * 16 + j;
+      const int row_i = px / g.tw, col = px - row_i * g.tw;
+      const int rho = rho0 + row_i;
+      int off = 0;
+      if (px < tpx && rho < rho_end && col < tw_eff) {
+        const int n = rho / P, p = rho - n * P;
+        off = (n * H + p - nu0) * in_wp + col;
+      }
+      poff[pb] = off;
+    }
+    v4f acc[WK][WP];
+#pragma unroll
+    for (int kb = 0; kb < WK; ++kb)
+#pragma unroll
+      for (int pb = 0; pb < WP; ++pb) acc[kb][pb] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    for (int ch = 0; ch < nchunks; ++ch) {
+      __syncthreads();  // previous users of the LDS buffers are done
+      if (!resident) {
+        stage_ker(k0, ch * TC);
+        gload_in(T, ch * TC);
+      }
+      lstore_in();
+      __syncthreads();
+      if (resident && T + 1 < t_end) gload_in(T + 1, 0);  // in flight during the MFMAs
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          v8bf a[WK], b[WP];
+#pragma unroll
+          for (int kb = 0; kb < WK; ++kb) {
+            const int kl = (wk * WK + kb) * 16 + j;
+            a[kb] = *reinterpret_cast<const v8bf*>(lker + ((size_t)kl * kpitch + r * S + s) * 64 +
+                                                  chunk_swz(gq, kl) * 16);
+          }
+#pragma unroll
+          for (int pb = 0; pb < WP; ++pb) {
+            const int pp = poff[pb] + r * in_wp + s;
+            b[pb] = *reinterpret_cast<const v8bf*>(lin + (size_t)pp * 64 + chunk_swz(gq, pp) * 16);
+          }
+#pragma unroll
+          for (int kb = 0; kb < WK; ++kb)
+#pragma unroll
+            for (int pb = 0; pb < WP; ++pb)
+              acc[kb][pb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[kb], b[pb], acc[kb][pb], 0, 0, 0);
+        }
+      }
+    }
+    // Epilogue: lane (j, gq) holds Out[k0 + block*16 + 4*gq + v][pixel j].
+    const size_t PQ = (size_t)P * Q;
+#pragma unroll
+    for (int pb = 0; pb < WP; ++pb) {
+      const int px = (wp * WP + pb) * 16 + j;
+      const int row_i = px / g.tw, col = px - row_i * g.tw;
+      const int rho = rho0 + row_i;
+      if (px < tpx && rho < rho_end && col < tw_eff) {
+        const int n = rho / P, p = rho - n * P;
+        float* ob = Out + ((size_t)n * K * P + p) * Q + q0 + col;
+#pragma unroll
+        for (int kb = 0; kb < WK; ++kb)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int k = k0 + (wk * WK + kb) * 16 + 4 * gq + v;
+            if (k < K) ob[(size_t)k * PQ] = acc[kb][pb][v];
+          }
+      }
+    }
+  }
+}
+
 typedef void (*KernelF32)(const float*, const float*, float*, const Geom);
+typedef void (*KernelBF16)(const unsigned short*, const unsigned short*, float*, const Geom);
 
 struct Instance {
   Variant v;
   KernelF32 f32;
+  KernelBF16 bf16;
 };
 
 #define F32_INST(ID, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV)                                  \
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STAGED, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV, 1, \
                    kThreads, 2},                                                             \
-           &conv_f32_kernel<WK, WP, TC, RC, SC, MAXNI, MAXNK, KV>}
+           &conv_f32_kernel<WK, WP, TC, RC, SC, MAXNI, MAXNK, KV>, nullptr}
 
 #define F32_DMA(ID, WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK)                              \
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_DMA, WK, WP, TC, RC, SC, NLI, NLK, KVK, KVI, NW * 64, \
                    NS},                                                                          \
-           &conv_f32_dma_kernel<WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK>}
+           &conv_f32_dma_kernel<WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK>, nullptr}
+
+#define BF16_INST(ID, WK, WP, RC, SC, MAXIT)                                                  \
+  Instance{Variant{ID, CONV_DTYPE_BF16, FAMILY_BF16, WK, WP, 32, RC, SC, MAXIT, 0, 8, 8, kThreads, \
+                   1},                                                                        \
+           nullptr, &conv_bf16_kernel<WK, WP, RC, SC, MAXIT>}
 
 const Instance kInstances[] = {
     // ---- direct-to-LDS pipeline
@@ -526,6 +748,12 @@ const Instance kInstances[] = {
     F32_DMA(123, 4, 4, 4, 16, 1, 1, 3, 4, 4, 2, 4),
     F32_DMA(124, 2, 13, 4, 16, 1, 1, 3, 7, 4, 2, 4),
     F32_DMA(125, 1, 13, 4, 16, 1, 1, 4, 4, 4, 2, 4),
+    // ---- bf16 inputs (persistent, transposed channel-fastest LDS tiles)
+    BF16_INST(201, 4, 4, 3, 3, 3),
+    BF16_INST(202, 2, 4, 3, 3, 3),
+    BF16_INST(203, 4, 2, 3, 3, 3),
+    BF16_INST(204, 4, 4, 1, 1, 3),
+    BF16_INST(205, 2, 2, 3, 3, 3),
     // ---- register-staged, double buffered (any shape, any alignment)
     // 3x3 taps, Ker staged in float4
     F32_INST(1, 4, 4, 8, 3, 3, 8, 12, 4),
@@ -576,11 +804,16 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
            void* stream) {
   const Instance* inst = find_instance(v.id);
   if (!inst) return CONV_EINVAL;
-  const int lds_bytes = (v.family == FAMILY_DMA)
-                            ? v.stages * g.stage_elems * (int)sizeof(float)
-                            : 2 * (g.lds_in_elems + g.lds_ker_elems) * (int)sizeof(float);
+  int lds_bytes;
+  if (v.family == FAMILY_DMA) lds_bytes = v.stages * g.stage_elems * (int)sizeof(float);
+  else if (v.family == FAMILY_BF16) lds_bytes = g.stage_elems;  // bytes
+  else lds_bytes = 2 * (g.lds_in_elems + g.lds_ker_elems) * (int)sizeof(float);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (v.ker_vec > 1 && (reinterpret_cast<uintptr_t>(Ker) % (4 * v.ker_vec)) != 0) return CONV_EINVAL;
+  if (v.family != FAMILY_BF16 && v.ker_vec > 1 &&
+      (reinterpret_cast<uintptr_t>(Ker) % (4 * v.ker_vec)) != 0)
+    return CONV_EINVAL;
+  const void* fn = inst->f32 ? reinterpret_cast<const void*>(inst->f32)
+                             : reinterpret_cast<const void*>(inst->bf16);
   if (lds_bytes > 65536) {
     // Raise the kernel's dynamic LDS limit once (to the device maximum).
     static std::mutex mu;
@@ -588,14 +821,19 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
     const int idx = (int)(inst - kInstances);
     std::lock_guard<std::mutex> lk(mu);
     if (!done[idx]) {
-      if (hipFuncSetAttribute(reinterpret_cast<const void*>(inst->f32),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, 163840) != hipSuccess)
+      if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, 163840) != hipSuccess)
         return CONV_EHIP;
       done[idx] = true;
     }
   }
-  hipLaunchKernelGGL(inst->f32, dim3(g.num_tiles), dim3(v.threads), lds_bytes, st,
-                     static_cast<const float*>(In), static_cast<const float*>(Ker), Out, g);
+  if (inst->f32) {
+    hipLaunchKernelGGL(inst->f32, dim3(g.num_tiles), dim3(v.threads), lds_bytes, st,
+                       static_cast<const float*>(In), static_cast<const float*>(Ker), Out, g);
+  } else {
+    hipLaunchKernelGGL(inst->bf16, dim3(g.grid), dim3(v.threads), lds_bytes, st,
+                       static_cast<const unsigned short*>(In),
+                       static_cast<const unsigned short*>(Ker), Out, g);
+  }
   return hipGetLastError() == hipSuccess ? CONV_OK : CONV_EHIP;
 }
 

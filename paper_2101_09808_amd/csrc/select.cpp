@@ -245,6 +245,34 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
     in_rows = std::max<int>(in_rows, (int)(nu1 - nu0 + 1));
   }
   const int RS = s.R * s.S, TC = v.tc;
+  if (v.family == FAMILY_BF16) {
+    // LDS: Ker [BK][RS or RS+1 taps][64 B] + In [in_rows][in_wp][64 B] (bytes)
+    const int in_wp_b = ((tw + s.S - 1) + 1) & ~1;
+    const int kpitch = (RS & 1) ? RS : RS + 1;
+    const int64_t bytes_b = (int64_t)BK * kpitch * 64 + (int64_t)in_rows * in_wp_b * 64;
+    if (bytes_b > kHw.lds_bytes) return false;
+    if ((int64_t)4 * in_rows * (in_wp_b / 2) > (int64_t)v.max_ni * v.threads) return false;
+    Geom q;
+    std::memset(&q, 0, sizeof(q));
+    q.N = s.N; q.C = s.C; q.K = s.K; q.H = s.H; q.W = s.W; q.R = s.R; q.S = s.S;
+    q.P = P; q.Q = Q;
+    q.tr = tr; q.tw = tw;
+    q.tiles_rows = (int)tiles_rows; q.tiles_cols = (int)tiles_cols; q.tiles_k = (int)tiles_k;
+    q.in_rows = in_rows; q.in_wp = in_wp_b; q.in_cstride = 0;
+    q.ker_rstride = kpitch;
+    q.nwk = nwk; q.nwp = nwp;
+    q.order = plan.grid_order;
+    q.num_tiles = (int)num_tiles;
+    q.nchunks = (int)cdiv(s.C, TC);
+    q.stage_elems = (int)bytes_b;
+    const int occ = std::max(1, std::min(2, (int)(kHw.lds_bytes / bytes_b)));
+    q.grid = (int)std::min<int64_t>(num_tiles, (int64_t)kHw.cus * occ);
+    q.in_bytes = (unsigned)std::min<int64_t>((int64_t)s.N * s.C * s.H * s.W * 2, 0xffffffffLL);
+    q.ker_bytes = (unsigned)std::min<int64_t>((int64_t)s.K * s.C * RS * 2, 0xffffffffLL);
+    if (g) *g = q;
+    if (lds_bytes) *lds_bytes = (int)bytes_b;
+    return true;
+  }
   const int in_wp = tw + s.S - 1;
   const int64_t E = (int64_t)in_rows * in_wp;
   if (E * TC >= (1 << 20)) return false;
@@ -306,6 +334,7 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
   q.ker_bytes = (unsigned)std::min<int64_t>(ker_elems_total * 4, 0xffffffffLL);
   q.stage_elems = (int)stage;
   q.in_region = (int)in_region;
+  q.grid = (int)num_tiles;
   if (g) *g = q;
   if (lds_bytes) *lds_bytes = (int)bytes;
   return true;
@@ -327,8 +356,10 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
 
   // REG: per wave and per (4 channels, tap), WK + WP operand reads of 64 lanes.
   const double waves = (double)g.num_tiles * (g.nwk * g.nwp);
-  const double steps = (double)g.nchunks * (v->tc / 4) * RS;
-  plan->pred_bytes[CONV_LVL_REG] = waves * steps * (v->wk + v->wp) * 64 * 4.0;
+  const int kdepth = (plan->dtype == CONV_DTYPE_BF16) ? 32 : 4;  // reduction per MFMA
+  const double steps = (double)g.nchunks * (v->tc / kdepth) * RS;
+  plan->pred_bytes[CONV_LVL_REG] =
+      waves * steps * (v->wk + v->wp) * 64 * ((plan->dtype == CONV_DTYPE_BF16) ? 16.0 : 4.0);
 
   // LDS: per workgroup, every channel brings its In halo rows and Ker rows.
   double in_tiles = 0;  // sum over pixel tiles of the halo footprint (elements per channel)
@@ -382,7 +413,8 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
   // Compute: MFMA cycles of one wave; a CU runs ceil(num_wg / cus) workgroups
   // whose waves share its SIMDs.
   const double mfma_per_step = (double)v->wk * v->wp;
-  const double wave_cycles = steps * mfma_per_step * kHw.mfma_f32_cycles;
+  const double mfma_cycles = (plan->dtype == CONV_DTYPE_BF16) ? 16.0 : kHw.mfma_f32_cycles;
+  const double wave_cycles = steps * mfma_per_step * mfma_cycles;
   const double per_cu = std::ceil((double)g.num_tiles / kHw.cus);
   const double waves_per_simd = per_cu * (g.nwk * g.nwp) / kHw.simds_per_cu;
   plan->pred_mfma_us = waves_per_simd * wave_cycles / kHw.clock_hz * 1e6;

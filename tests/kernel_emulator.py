@@ -261,3 +261,169 @@ def emulate(g, In, Ker, wgs=None):
                         out[dst[st]] = vals[st]
                         np.add.at(written, dst[st], 1)
     return out, written
+
+
+# ---------------------------------------------------------------------------
+# bf16 family (conv_bf16_kernel): persistent workgroups over tile ranges,
+# channel-fastest swizzled LDS images, 16x16x32 MFMA.
+
+def _swz(chunk, idx):
+    return chunk ^ ((idx >> 1) & 3)
+
+
+def emulate_bf16(g, In, Ker, wgs=None, in_aligned=True):
+    """In, Ker: flat float64 arrays holding the bf16 values.  Emulates the
+    workgroups ``wgs`` (default all) of the persistent grid."""
+    N, C, K, H, W, R, S, P, Q = (g[x] for x in "N C K H W R S P Q".split())
+    _chk(g["family"] == 3 and g["threads"] == 256, "bf16 family geometry")
+    WK, WP, MAXIT = g["wk"], g["wp"], g["max_ni"]
+    nwk, nwp = g["nwk"], g["nwp"]
+    _chk(nwk * nwp == 4, "waves")
+    BK = 16 * WK * nwk
+    RS = R * S
+    TC = 32
+    kpitch = RS if RS % 2 else RS + 1
+    _chk(g["ker_rstride"] == kpitch, "Ker pitch")
+    in_wp = g["in_wp"]
+    _chk(in_wp % 2 == 0, "halo pitch even")
+    lds_bytes = BK * kpitch * 64 + g["in_rows"] * in_wp * 64
+    _chk(lds_bytes == g["stage_elems"] == g["lds_bytes"] and lds_bytes <= 160 * 1024, "LDS bytes")
+    in_size, ker_size, out_size = N * C * H * W, K * C * RS, N * K * P * Q
+    _chk(In.size == in_size and Ker.size == ker_size, "input sizes")
+    out = np.full(out_size, np.nan)
+    written = np.zeros(out_size, np.int64)
+    tiles = g["tiles_rows"] * g["tiles_cols"] * g["tiles_k"]
+    G = g["grid"]
+    _chk(1 <= G <= tiles, "grid")
+    nchunks = -(-C // TC)
+    resident = nchunks == 1 and g["tiles_k"] == 1
+    npair = in_wp // 2
+    in_items = 4 * g["in_rows"] * npair
+    _chk(in_items <= MAXIT * 256, "In staging capacity")
+    tid = np.arange(256)
+    lane = np.arange(64)
+    j, gq = lane & 15, lane >> 4
+    seen = np.zeros(tiles, bool)
+    for b in (range(G) if wgs is None else wgs):
+        G8 = G & ~7
+        L = (b & 7) * (G8 >> 3) + (b >> 3) if b < G8 else b
+        per = -(-tiles // G)
+        t_begin, t_end = L * per, min(tiles, L * per + per)
+        lds = np.full(lds_bytes // 2, np.nan)  # bf16 slots
+
+        def stage_ker(k0, c0):
+            items = BK * RS * 4
+            for it in range(items):
+                o, rest = it & 3, it >> 2
+                rs, kl = rest % RS, rest // RS
+                for e in range(8):
+                    c, k = c0 + 8 * o + e, k0 + kl
+                    val = 0.0
+                    if c < C and k < K:
+                        src = (k * C + c) * RS + rs
+                        _chk(0 <= src < ker_size, "Ker read out of bounds")
+                        val = Ker[src]
+                    dst = ((kl * kpitch + rs) * 64 + _swz(o, kl) * 16) // 2 + e
+                    _chk(dst < BK * kpitch * 32, "LDS Ker write out of range")
+                    lds[dst] = val
+
+        def stage_in(T, c0):
+            kt, rest = T % g["tiles_k"], T // g["tiles_k"]
+            ct, rt = rest % g["tiles_cols"], rest // g["tiles_cols"]
+            NP = N * P
+            rho0, rho_end = rt * g["tr"], min(rt * g["tr"] + g["tr"], NP)
+            q0 = ct * g["tw"]
+            ncols = min(g["tw"], Q - q0) + S - 1
+            nf = rho0 // P
+            nu0 = nf * H + (rho0 - nf * P)
+            nl = (rho_end - 1) // P
+            nrows = nl * H + (rho_end - 1 - nl * P) + R - nu0
+            _chk(nrows <= g["in_rows"], "tile needs more halo rows than allocated")
+            ker_base = BK * kpitch * 32
+            for m in range(MAXIT):
+                it = tid + m * 256
+                o = it // (g["in_rows"] * npair)
+                rest = it - o * (g["in_rows"] * npair)
+                row, x = rest // npair, (rest - (rest // npair) * npair) * 2
+                for t in range(256):
+                    if it[t] >= in_items:
+                        continue
+                    ok = row[t] < nrows
+                    nu = nu0 + row[t]
+                    n, y = nu // H, nu % H
+                    for e in range(8):
+                        c = c0 + 8 * o[t] + e
+                        for d in range(2):
+                            xx = x[t] + d
+                            val = 0.0
+                            if ok and c < C and xx < ncols:
+                                src = ((n * C + c) * H + y) * W + q0 + xx
+                                _chk(0 <= src < in_size, "In read out of bounds")
+                                val = In[src]
+                            px = row[t] * in_wp + x[t] + d
+                            dst = ker_base + (px * 64 + _swz(o[t], px) * 16) // 2 + e
+                            _chk(dst < lds.size, "LDS In write out of range")
+                            lds[dst] = val
+            return rho0, rho_end, q0, kt, nu0
+
+        if resident:
+            stage_ker(0, 0)
+        for T in range(t_begin, t_end):
+            _chk(not seen[T], "tile processed twice")
+            seen[T] = True
+            acc = {}
+            for ch in range(nchunks):
+                if not resident:
+                    kt0 = T % g["tiles_k"]
+                    stage_ker(kt0 * BK, ch * TC)
+                rho0, rho_end, q0, kt, nu0 = stage_in(T, ch * TC)
+                k0 = kt * BK
+                tw_eff = min(g["tw"], Q - q0)
+                tpx = g["tr"] * g["tw"]
+                for wave in range(4):
+                    wk, wp = wave % nwk, wave // nwk
+                    for pb in range(WP):
+                        px = (wp * WP + pb) * 16 + j
+                        row_i, col = px // g["tw"], px % g["tw"]
+                        rho = rho0 + row_i
+                        valid = (px < tpx) & (rho < rho_end) & (col < tw_eff)
+                        n, p = rho // P, rho % P
+                        poff = np.where(valid, (n * H + p - nu0) * in_wp + col, 0)
+                        for kb in range(WK):
+                            kl = (wk * WK + kb) * 16 + j
+                            cmat = acc.setdefault((wave, kb, pb), np.zeros((16, 16)))
+                            for r in range(R):
+                                for s in range(S):
+                                    ai = ((kl * kpitch + r * S + s) * 64 + _swz(gq, kl) * 16) // 2
+                                    pp = poff + r * in_wp + s
+                                    bi = BK * kpitch * 32 + (pp * 64 + _swz(gq, pp) * 16) // 2
+                                    A = np.zeros((16, 32))
+                                    Bm = np.zeros((32, 16))
+                                    for e in range(8):
+                                        _chk((ai + e < BK * kpitch * 32).all(), "LDS Ker read range")
+                                        _chk((bi + e < lds.size).all(), "LDS In read range")
+                                        av = lds[ai + e]
+                                        bv = lds[bi + e]
+                                        _chk(~np.isnan(av), "Ker read of an unstaged slot")
+                                        _chk(~np.isnan(bv[valid]), "In read of an unstaged slot")
+                                        A[j, 8 * gq + e] = av
+                                        Bm[8 * gq + e, j] = np.nan_to_num(bv)
+                                    cmat += A @ Bm
+            # epilogue
+            for wave in range(4):
+                wk, wp = wave % nwk, wave // nwk
+                for pb in range(WP):
+                    px = (wp * WP + pb) * 16 + j
+                    row_i, col = px // g["tw"], px % g["tw"]
+                    rho = rho0 + row_i
+                    valid = (px < tpx) & (rho < rho_end) & (col < tw_eff)
+                    n, p = rho // P, rho % P
+                    for kb in range(WK):
+                        for v in range(4):
+                            k = k0 + (wk * WK + kb) * 16 + 4 * gq + v
+                            st = valid & (k < K)
+                            dst = ((n * K + k) * P + p) * Q + q0 + col
+                            _chk((dst[st] >= 0).all() and (dst[st] < out_size).all(), "Out store range")
+                            out[dst[st]] = acc[(wave, kb, pb)][4 * gq + v, j][st]
+                            np.add.at(written, dst[st], 1)
+    return out, written

@@ -124,6 +124,31 @@ def test_edge_shapes(shape):
     check_full(shape)
 
 
+EDGE_BF16 = [
+    ConvShape("bf16_multi_chunk_ktail", 2, 40, 72, 11, 13, 3, 3, "bf16", 41),
+    ConvShape("bf16_one_chunk", 1, 32, 64, 20, 22, 3, 3, "bf16", 42),
+    ConvShape("bf16_pointwise", 3, 16, 20, 7, 9, 1, 1, "bf16", 43),
+    ConvShape("bf16_odd_width", 1, 8, 16, 6, 9, 3, 3, "bf16", 44),
+    ConvShape("bf16_rect_taps_generic", 2, 12, 24, 9, 10, 2, 3, "bf16", 45),
+]
+
+
+@pytest.mark.parametrize("shape", EDGE_BF16, ids=lambda s: s.name)
+def test_bf16_edge_shapes(shape):
+    try:
+        B.conv_fwd_plan(*shape.key(), dtype=B.CONV_DTYPE_BF16)
+    except B.ConvError as e:
+        if e.status == B.CONV_ENOPLAN:
+            pytest.skip("no bf16 kernel variant for these taps")
+        raise
+    check_full(shape)
+
+
+@pytest.mark.parametrize("shape", EDGE_BF16[:2], ids=lambda s: s.name)
+def test_bf16_integer_inputs_bitwise(shape):
+    check_full(shape, kind="int", seed=shape.seed + 1)
+
+
 @pytest.mark.parametrize("shape", [EDGE[0], EDGE[7], small_version(CONFIGS[2]), small_version(CONFIGS[3]),
                                    small_version(CONFIGS[1])], ids=lambda s: s.name)
 def test_integer_inputs_bitwise(shape):

@@ -60,3 +60,40 @@ def test_full_config_sampled_workgroups(cfg):
     assert idx.size > 0
     ref = oconv.conv_fwd_points(In.astype(np.float32), Ker.astype(np.float32), idx)
     assert np.max(np.abs(out[idx] - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
+
+
+BF16_SHAPES = [
+    ConvShape("bf16_multi_chunk_ktail", 2, 40, 72, 11, 13, 3, 3, "bf16", 1),
+    ConvShape("bf16_one_chunk", 1, 32, 64, 20, 22, 3, 3, "bf16", 2),
+    ConvShape("bf16_pointwise", 3, 16, 20, 7, 9, 1, 1, "bf16", 3),
+    ConvShape("bf16_odd_width", 1, 8, 16, 6, 9, 3, 3, "bf16", 4),
+]
+
+
+@pytest.mark.parametrize("shape", BF16_SHAPES, ids=lambda s: s.name)
+def test_bf16_plans_indexing(shape):
+    from tests.kernel_emulator import emulate_bf16
+    In, Ker = make_inputs(shape)
+    In64 = In.float().numpy().astype(np.float64)
+    Ker64 = Ker.float().numpy().astype(np.float64)
+    ref = oconv.conv_fwd(In64.astype(np.float32), Ker64.astype(np.float32)).reshape(-1)
+    for p in B.conv_fwd_candidates(*shape.key(), dtype=B.CONV_DTYPE_BF16)[:2]:
+        g = B.conv_fwd_geometry(*shape.key(), p)
+        out, written = emulate_bf16(g, In64.reshape(-1), Ker64.reshape(-1))
+        assert np.all(written == 1)
+        assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
+
+
+def test_bf16_full_config_sampled_workgroups():
+    from tests.kernel_emulator import emulate_bf16
+    cfg = [c for c in CONFIGS if c.dtype == "bf16"][0]
+    plan = B.conv_fwd_plan(*cfg.key(), dtype=B.CONV_DTYPE_BF16)
+    g = B.conv_fwd_geometry(*cfg.key(), plan)
+    In, Ker = make_inputs(cfg)
+    In64 = In.float().numpy().astype(np.float64).reshape(-1)
+    Ker64 = Ker.float().numpy().astype(np.float64).reshape(-1)
+    out, written = emulate_bf16(g, In64, Ker64, [0, g["grid"] - 1])
+    assert written.max() == 1
+    idx = np.nonzero(written)[0]
+    ref = oconv.conv_fwd_points(In.float().numpy(), Ker.float().numpy(), idx)
+    assert np.max(np.abs(out[idx] - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
