@@ -19,6 +19,7 @@ enum {
   FAMILY_STAGED = 1,  // global -> VGPR -> LDS staging, double buffered (any size)
   FAMILY_DMA = 2,     // global -> LDS direct buffer loads, NS-stage pipeline
   FAMILY_BF16 = 3,    // bf16 inputs: persistent, channel-fastest transposed LDS tiles
+  FAMILY_STREAM1X1 = 4,  // pointwise: Ker resident in LDS, In streamed to registers
 };
 
 // One compiled kernel instance (template parameters of the kernel family).

@@ -25,6 +25,7 @@
 #include <hip/hip_runtime.h>
 
 #include <mutex>
+#include <type_traits>
 
 #include "conv_internal.h"
 
@@ -704,6 +705,180 @@ conv_bf16_kernel(const unsigned short* __restrict__ In, const unsigned short* __
   }
 }
 
+// ---------------------------------------------------------------------------
+// Pointwise (1x1) streaming kernel.
+//
+// With R = S = 1 the convolution is Out[n][k][px] = sum_c Ker[k][c] In[n][c][px]
+// over the flattened pixels px of each image.  Each workgroup keeps its
+// 64-wide slice of Ker resident in LDS as rows [k][c] with a pitch of one
+// float more than the (ring-padded) channel count: the fill is a coalesced
+// copy of whole Ker rows, and the A operands (lane (i, gq) reads row
+// kb*16 + i at channel 4q + gq) hit 16 distinct banks per 16-lane group.
+// Each wave owns a contiguous range of `wpx` pixels (NB1 + NB2 blocks of 16)
+// and streams its In columns straight from global memory into a ring of D
+// register slots (D channel quads ahead); no LDS traffic or barriers for In.
+// The pixel blocks are done in two phases (NB1, then NB2 blocks) so the first
+// phase's stores drain while the second phase computes.  Requires C % 4 == 0
+// (whole channel quads) and In below 1 GB (32-bit byte offsets).
+template <int NB1, int NB2, int D, int NQ>
+__global__ void __launch_bounds__(kThreads)
+conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
+                      float* __restrict__ Out, const Geom g) {
+  extern __shared__ __align__(16) float lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int j = lane & 15, gq = lane >> 4;
+  const int C = g.C, K = g.K;
+  const int HW = g.W;                   // kernel view: one row of H*W pixels per image
+  const int total_px = g.N * HW;
+  const int kt = blockIdx.x % g.tiles_k;
+  const int pg = blockIdx.x / g.tiles_k;
+  const int k0 = kt * 64;
+  const int wpx = g.tw;                 // pixels per wave
+  const int px_begin = (pg * 4 + wave) * wpx;
+  const int px_end = min(px_begin + wpx, total_px);
+  // Channel quads: NQ > 0 fixes the count at compile time so the channel loop
+  // unrolls completely and every wait on the register ring is exact.
+  const int nq = NQ > 0 ? NQ : (C + 3) / 4;
+  const int nq_pad = (nq + D - 1) / D * D;
+
+  // Ker slice -> LDS rows [k][c], zero-padded to whole ring groups of quads.
+  // Coalesced row reads, a whole batch of loads in flight at once (every
+  // workgroup reads the same slice at the same time, so round trips are long).
+  // With NQ > 0 the slice is one batch, issued before the In ring prologue and
+  // written to LDS after it, so the two latencies overlap.
+  const int cpad = nq_pad * 4, pitch = cpad + 1;
+  constexpr int FB = NQ > 0 ? ((NQ + D - 1) / D * D * 4 * 64) / kThreads : 16;  // loads per batch
+  float kv[FB];
+  auto fill_load = [&](int e0) {
+#pragma unroll
+    for (int i = 0; i < FB; ++i) {
+      const int e = e0 + tid + i * kThreads;
+      const int kl = e / cpad, c = e - kl * cpad;
+      const int k = k0 + kl;
+      kv[i] = (e < 64 * cpad && k < K && c < C) ? Ker[(size_t)k * C + c] : 0.f;
+    }
+  };
+  auto fill_store = [&](int e0) {
+#pragma unroll
+    for (int i = 0; i < FB; ++i) {
+      const int e = e0 + tid + i * kThreads;
+      const int kl = e / cpad, c = e - kl * cpad;
+      if (e < 64 * cpad) lds[kl * pitch + c] = kv[i];
+    }
+  };
+  if constexpr (NQ > 0) fill_load(0);
+  auto ker_ready = [&]() {
+    if constexpr (NQ > 0) {
+      fill_store(0);
+    } else {
+      for (int e0 = 0; e0 < 64 * cpad; e0 += kThreads * FB) {
+        fill_load(e0);
+        fill_store(e0);
+      }
+    }
+    __syncthreads();
+  };
+  // In through raw buffer loads: masked lanes and channels past C read zeros
+  // from the range check, so the loop has no branches.
+  __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(In), (short)0, (int)g.in_bytes, 0x00020000);
+  const unsigned qstride = 16u * (unsigned)HW;  // bytes between channel quads
+
+  auto phase = [&](auto nb_const, int blk0, auto first_const) {
+    constexpr int NB = decltype(nb_const)::value;
+    if constexpr (NB > 0) {
+      unsigned voff[NB];
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int px = px_begin + (blk0 + b) * 16 + j;
+        const int n = px / HW, hw = px - n * HW;
+        voff[b] = (px < px_end) ? (unsigned)((n * C + gq) * HW + hw) * 4u : kOob;
+      }
+      v4f acc[4][NB];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) acc[kb][b] = v4f{0.f, 0.f, 0.f, 0.f};
+      float ring[D][NB];
+      // Offsets: masked pixels start at 2^31; quads past the channel range
+      // add 2^30 (wave-uniform).  With In below 1 GB both land past the
+      // buffer's range without wrapping, so every load is unconditional.
+      auto load = [&](int q, int slot) {
+        const unsigned qoff = (unsigned)q * qstride + (q < nq ? 0u : 0x40000000u);
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          ring[slot][b] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, voff[b] + qoff, 0, 0));
+      };
+#pragma unroll
+      for (int d = 0; d < D; ++d) load(d, d);
+      if constexpr (decltype(first_const)::value) ker_ready();
+      // A operands (Ker[k0 + kb*16 + j][4q + gq], kb = 0..3) are read one
+      // quad ahead so the LDS latency hides behind the current quad's MFMAs.
+      const float* arow = lds + j * pitch + gq;
+      float a[2][4];
+      auto read_a = [&](int q, float* dst) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) dst[kb] = arow[kb * 16 * pitch + 4 * q];
+      };
+      auto step = [&](int q, int d) {
+        const float* ac = a[q & 1];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+            acc[kb][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(ac[kb], ring[d][b], acc[kb][b], 0, 0, 0);
+      };
+      read_a(0, a[0]);
+      if constexpr (NQ > 0) {
+        constexpr int NQP = (NQ + D - 1) / D * D;
+#pragma unroll
+        for (int q = 0; q < NQP; ++q) {
+          if (q + 1 < NQP) read_a(q + 1, a[(q + 1) & 1]);
+          __builtin_amdgcn_sched_barrier(0);  // issue the A reads first
+          step(q, q % D);
+          if (q + D < NQP) load(q + D, q % D);
+          // keep each refill right behind the MFMAs that free its slot: left
+          // alone, the scheduler sinks loads towards their uses and the ring
+          // degenerates to a few loads in flight
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      } else {
+        static_assert(D % 2 == 0, "the A double buffer alternates within a ring group");
+        for (int q0 = 0; q0 < nq_pad; q0 += D) {
+#pragma unroll
+          for (int d = 0; d < D; ++d) {
+            read_a(min(q0 + d + 1, nq_pad - 1), a[(d + 1) & 1]);  // last one unused
+            __builtin_amdgcn_sched_barrier(0);
+            step(q0 + d, d);
+            load(q0 + d + D, d);  // past the last quad this reads zeros
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+      }
+      // lane (j, gq) holds Out[k0 + kb*16 + 4*gq + v][pixel px_begin + (blk0+b)*16 + j]
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int px = px_begin + (blk0 + b) * 16 + j;
+        if (px < px_end) {
+          const int n = px / HW, hw = px - n * HW;
+          float* ob = Out + (size_t)n * K * HW + hw;
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const int k = k0 + kb * 16 + 4 * gq + v;
+              if (k < K) ob[(size_t)k * HW] = acc[kb][b][v];
+            }
+        }
+      }
+    }
+  };
+  static_assert(NB1 > 0, "the first phase makes the Ker slice ready");
+  phase(std::integral_constant<int, NB1>{}, 0, std::true_type{});
+  phase(std::integral_constant<int, NB2>{}, NB1, std::false_type{});
+}
+
 typedef void (*KernelF32)(const float*, const float*, float*, const Geom);
 typedef void (*KernelBF16)(const unsigned short*, const unsigned short*, float*, const Geom);
 
@@ -723,12 +898,33 @@ struct Instance {
                    NS},                                                                          \
            &conv_f32_dma_kernel<WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK>, nullptr}
 
+#define F32_STREAM1X1(ID, NB1, NB2, D, NQ)                                                   \
+  Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STREAM1X1, 4, NB1 + NB2, 4 * NQ, 1, 1, NB1, NB2, 1, \
+                   1, kThreads, D},                                                            \
+           &conv1x1_stream_kernel<NB1, NB2, D, NQ>, nullptr}
+
 #define BF16_INST(ID, WK, WP, RC, SC, MAXIT)                                                  \
   Instance{Variant{ID, CONV_DTYPE_BF16, FAMILY_BF16, WK, WP, 32, RC, SC, MAXIT, 0, 8, 8, kThreads, \
                    1},                                                                        \
            nullptr, &conv_bf16_kernel<WK, WP, RC, SC, MAXIT>}
 
 const Instance kInstances[] = {
+    // ---- pointwise streaming (Ker resident in LDS, In straight to registers)
+    // (tile_c = 4 * NQ: the channel count of the unrolled instances; 0 = any)
+    F32_STREAM1X1(301, 4, 3, 8, 64),
+    F32_STREAM1X1(302, 4, 4, 8, 64),
+    F32_STREAM1X1(303, 3, 3, 8, 64),
+    F32_STREAM1X1(304, 4, 0, 8, 64),
+    F32_STREAM1X1(308, 7, 0, 4, 64),
+    F32_STREAM1X1(309, 7, 0, 8, 64),
+    F32_STREAM1X1(310, 8, 0, 4, 64),
+    F32_STREAM1X1(305, 4, 3, 8, 32),
+    F32_STREAM1X1(306, 4, 3, 8, 128),
+    F32_STREAM1X1(307, 4, 3, 8, 16),
+    F32_STREAM1X1(311, 4, 3, 8, 0),
+    F32_STREAM1X1(312, 4, 0, 8, 0),
+    F32_STREAM1X1(313, 2, 2, 8, 0),
+    F32_STREAM1X1(314, 2, 0, 8, 0),
     // ---- direct-to-LDS pipeline
     // 3x3 taps
     F32_DMA(101, 1, 13, 4, 8, 3, 3, 3, 9, 1, 5, 4),
@@ -739,7 +935,20 @@ const Instance kInstances[] = {
     F32_DMA(106, 1, 7, 8, 8, 3, 3, 3, 5, 1, 3, 4),
     F32_DMA(107, 1, 4, 8, 8, 3, 3, 3, 4, 1, 3, 4),
     F32_DMA(108, 2, 4, 8, 8, 3, 3, 3, 6, 1, 3, 4),
+    // squat wave tiles (4 k blocks x 4..8 pixel blocks), Ker rows loaded
+    // element-wise so their LDS pitch can be conflict-free
+    F32_DMA(141, 4, 4, 4, 8, 3, 3, 3, 7, 1, 19, 1),
+    F32_DMA(142, 4, 4, 8, 8, 3, 3, 3, 4, 1, 10, 1),
+    F32_DMA(143, 2, 4, 8, 8, 3, 3, 3, 4, 1, 10, 1),
+    F32_DMA(144, 4, 2, 4, 8, 3, 3, 3, 4, 1, 19, 1),
+    F32_DMA(145, 2, 8, 8, 8, 3, 3, 3, 7, 1, 10, 1),
     // 1x1 taps
+    F32_DMA(131, 4, 7, 4, 16, 1, 1, 3, 7, 4, 5, 1),
+    F32_DMA(132, 4, 7, 4, 16, 1, 1, 4, 7, 4, 5, 1),
+    F32_DMA(133, 4, 4, 8, 16, 1, 1, 3, 4, 4, 3, 1),
+    F32_DMA(134, 4, 8, 4, 16, 1, 1, 3, 8, 4, 5, 1),
+    F32_DMA(135, 4, 6, 4, 16, 1, 1, 3, 6, 4, 5, 1),
+    F32_DMA(136, 4, 8, 8, 16, 1, 1, 3, 8, 4, 3, 1),
     F32_DMA(121, 1, 25, 4, 16, 1, 1, 4, 7, 4, 2, 4),
     F32_DMA(126, 1, 13, 8, 16, 1, 1, 4, 4, 4, 1, 4),
     F32_DMA(127, 1, 7, 8, 16, 1, 1, 4, 2, 4, 1, 4),
@@ -806,7 +1015,7 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
   if (!inst) return CONV_EINVAL;
   int lds_bytes;
   if (v.family == FAMILY_DMA) lds_bytes = v.stages * g.stage_elems * (int)sizeof(float);
-  else if (v.family == FAMILY_BF16) lds_bytes = g.stage_elems;  // bytes
+  else if (v.family == FAMILY_BF16 || v.family == FAMILY_STREAM1X1) lds_bytes = g.stage_elems;  // bytes
   else lds_bytes = 2 * (g.lds_in_elems + g.lds_ker_elems) * (int)sizeof(float);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   if (v.family != FAMILY_BF16 && v.ker_vec > 1 &&
@@ -827,7 +1036,7 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
     }
   }
   if (inst->f32) {
-    hipLaunchKernelGGL(inst->f32, dim3(g.num_tiles), dim3(v.threads), lds_bytes, st,
+    hipLaunchKernelGGL(inst->f32, dim3(g.grid), dim3(v.threads), lds_bytes, st,
                        static_cast<const float*>(In), static_cast<const float*>(Ker), Out, g);
   } else {
     hipLaunchKernelGGL(inst->bf16, dim3(g.grid), dim3(v.threads), lds_bytes, st,

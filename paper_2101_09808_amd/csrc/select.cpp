@@ -114,34 +114,28 @@ const Hw kHw;
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// Bank-conflict degree of a wave's 64 4-byte LDS reads (addresses in
-// elements): the max over banks of the distinct addresses hitting it, for a
-// 64-bank view of the full wave plus a 32-bank view of each half wave.
+// Bank-conflict cost of a wave's 64 4-byte LDS reads (addresses in
+// elements), for the gfx950 LDS as measured: 32 banks of 4 bytes, a wave's
+// ds_read_b32 served 16 lanes at a time; each 16-lane group takes as many
+// passes as the most distinct addresses that fall into one bank.  Returns the
+// sum of passes over the four groups (4 = conflict-free).
 int conflict_cost(const int* addr) {
-  int worst64 = 0, worst32 = 0;
-  {
-    std::vector<int> seen;
-    for (int b = 0; b < 64; ++b) {
-      seen.clear();
-      for (int l = 0; l < 64; ++l)
-        if (((addr[l] % 64) + 64) % 64 == b &&
-            std::find(seen.begin(), seen.end(), addr[l]) == seen.end())
-          seen.push_back(addr[l]);
-      worst64 = std::max(worst64, (int)seen.size());
-    }
-  }
-  for (int h = 0; h < 2; ++h) {
-    std::vector<int> seen;
+  int total = 0;
+  for (int grp = 0; grp < 4; ++grp) {
+    int worst = 0;
     for (int b = 0; b < 32; ++b) {
-      seen.clear();
-      for (int l = 32 * h; l < 32 * h + 32; ++l)
-        if (((addr[l] % 32) + 32) % 32 == b &&
-            std::find(seen.begin(), seen.end(), addr[l]) == seen.end())
-          seen.push_back(addr[l]);
-      worst32 = std::max(worst32, (int)seen.size());
+      int seen[16], n = 0;
+      for (int l = 16 * grp; l < 16 * grp + 16; ++l) {
+        if (((addr[l] % 32) + 32) % 32 != b) continue;
+        bool dup = false;
+        for (int q = 0; q < n; ++q) dup |= seen[q] == addr[l];
+        if (!dup) seen[n++] = addr[l];
+      }
+      worst = std::max(worst, n);
     }
+    total += std::max(1, worst);
   }
-  return worst64 + worst32;
+  return total;
 }
 
 // Row pitch of the Ker tile: >= need, a multiple of `mult`, with the least
@@ -223,6 +217,41 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
                   int* lds_bytes) {
   const Shape s = kernel_view(s0);
   if (plan.dtype != v.dtype) return false;
+  if (v.family == FAMILY_STREAM1X1) {
+    // Pointwise streaming: tile_cols = pixels per wave, 4 waves per workgroup,
+    // 64 output channels per workgroup, the whole channel range resident.
+    if (s0.R != 1 || s0.S != 1) return false;
+    if (plan.tile_k != 64 || plan.waves_k != 1 || plan.waves_px != 4 || plan.tile_rows != 1) return false;
+    if (plan.wave_k != 64 || plan.wave_px != 16 * v.wp || plan.tile_c != v.tc) return false;
+    const int nb = v.max_ni + v.max_nk;
+    const int wpx = plan.tile_cols;
+    if (wpx < 1 || wpx > 16 * nb) return false;
+    const int64_t total_px = (int64_t)s.N * s.W;
+    const int64_t groups = cdiv(total_px, 4 * (int64_t)wpx);
+    const int64_t tiles_k = cdiv(s.K, 64);
+    const int64_t nq_pad = cdiv(cdiv(s.C, 4), v.stages) * v.stages;  // stages = ring depth
+    const int64_t bytes = (nq_pad * 4 + 1) * 64 * 4;  // Ker rows [k][c] + 1 pad
+    if (bytes > kHw.lds_bytes || groups * tiles_k >= (int64_t(1) << 31)) return false;
+    if ((int64_t)s.N * s.C * s.W * 4 >= (int64_t(1) << 30)) return false;  // 32-bit byte offsets
+    if (s.C % 4) return false;  // whole channel quads
+    if (v.tc && v.tc != s.C) return false;  // unrolled instance for this channel count
+    Geom q;
+    std::memset(&q, 0, sizeof(q));
+    q.N = s.N; q.C = s.C; q.K = s.K; q.H = s.H; q.W = s.W; q.R = 1; q.S = 1;
+    q.P = s.P(); q.Q = s.Q();
+    q.tr = 1; q.tw = wpx;
+    q.tiles_rows = (int)groups; q.tiles_cols = 1; q.tiles_k = (int)tiles_k;
+    q.nwk = 1; q.nwp = 4;
+    q.num_tiles = (int)(groups * tiles_k);
+    q.grid = q.num_tiles;
+    q.nchunks = (int)cdiv(s.C, 4);
+    q.stage_elems = (int)bytes;
+    q.in_bytes = (unsigned)std::min<int64_t>((int64_t)s.N * s.C * s.H * s.W * 4, 0xffffffffLL);
+    q.ker_bytes = (unsigned)std::min<int64_t>((int64_t)s.K * s.C * 4, 0xffffffffLL);
+    if (g) *g = q;
+    if (lds_bytes) *lds_bytes = (int)bytes;
+    return true;
+  }
   if (v.rc && (s.R != v.rc || s.S != v.sc)) return false;
   if (plan.tile_c != v.tc) return false;
   const int nwk = plan.waves_k, nwp = plan.waves_px;
@@ -349,6 +378,35 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
   if (!resolve_geom(s0, *v, *plan, &g, &lds)) return CONV_EINVAL;
   const Shape s = kernel_view(s0);
   const double e = (plan->dtype == CONV_DTYPE_BF16) ? 2.0 : 4.0;
+  if (v->family == FAMILY_STREAM1X1) {
+    // In moves HBM -> VGPR once; Ker slices are staged into LDS once per
+    // workgroup; A operands are four 4 B LDS reads per lane per channel quad and phase.
+    plan->lds_bytes = lds;
+    plan->num_wg = g.grid;
+    const double in_b = (double)s.N * s.C * s.W * 4.0, ker_b = (double)s.K * s.C * 4.0;
+    const double out_b = (double)s.N * s.K * s.W * 4.0;
+    const double waves = (double)g.grid * 4;
+    const double nq = std::ceil(s.C / 4.0);
+    const double phases = v->max_nk > 0 ? 2.0 : 1.0;  // each phase re-reads the A operands
+    plan->pred_bytes[CONV_LVL_REG] = waves * phases * nq * 64 * 16.0;
+    plan->pred_bytes[CONV_LVL_LDS] = (double)g.grid * s.C * 64 * 4.0;
+    plan->pred_bytes[CONV_LVL_L2] = in_b * g.tiles_k + ker_b * std::min<double>(g.tiles_rows, kHw.xcds);
+    plan->pred_bytes[CONV_LVL_HBM] = in_b + ker_b + out_b;
+    plan->class_lvl[CONV_LVL_REG] = 3;
+    plan->class_lvl[CONV_LVL_LDS] = 3;
+    plan->class_lvl[CONV_LVL_L2] = 1;
+    plan->class_lvl[CONV_LVL_HBM] = 0;
+    double tmax = 0;
+    for (int l = 0; l < CONV_NUM_LVLS; ++l) {
+      plan->pred_us[l] = plan->pred_bytes[l] / kHw.bw[l] * 1e6;
+      tmax = std::max(tmax, plan->pred_us[l]);
+    }
+    const double nb = v->max_ni + v->max_nk;
+    const double rounds = std::ceil((double)g.grid / kHw.cus);
+    plan->pred_mfma_us = rounds * nb * 4 * nq * kHw.mfma_f32_cycles / kHw.clock_hz * 1e6;
+    plan->pred_total_us = std::max(tmax, plan->pred_mfma_us);
+    return CONV_OK;
+  }
   const int RS = s.R * s.S;
   const int64_t NP = (int64_t)s.N * g.P;
   plan->lds_bytes = lds;
@@ -445,8 +503,11 @@ void fill_plan_fields(conv_plan_t* p, const Variant& v, int nwk, int nwp, int tr
 bool better(const conv_plan_t& a, const conv_plan_t& b) {
   // The direct-to-LDS pipeline keeps several steps of loads in flight; the
   // register-staged family is the fallback for shapes it cannot take.
-  const int fa = find_variant(a.variant)->family, fb = find_variant(b.variant)->family;
-  if (fa != fb) return fa == FAMILY_DMA;
+  auto rank = [](int fam) {
+    return fam == FAMILY_STREAM1X1 ? 0 : fam == FAMILY_DMA ? 1 : fam == FAMILY_BF16 ? 1 : 2;
+  };
+  const int fa = rank(find_variant(a.variant)->family), fb = rank(find_variant(b.variant)->family);
+  if (fa != fb) return fa < fb;
   if (a.pred_total_us != b.pred_total_us) return a.pred_total_us < b.pred_total_us;
   double ba = 0, bb = 0;
   for (int l = 0; l < CONV_NUM_LVLS; ++l) {
@@ -473,6 +534,28 @@ int enumerate_plans(const Shape& s0, int dtype, conv_plan_t* plans, int cap) {
     const Variant& v = vs[vi];
     if (v.dtype != dtype) continue;
     if (v.rc && (s.R != v.rc || s.S != v.sc)) continue;
+    if (v.family == FAMILY_STREAM1X1) {
+      // pixels per wave so that the workgroup count lands near a multiple
+      // of the CU count; the instance's block count must match
+      const int nb = v.max_ni + v.max_nk;
+      const int64_t total_px = (int64_t)s.N * s.W;
+      std::vector<int> wpxs;
+      for (int64_t G = 1; G <= 4096; ++G) {
+        const int64_t wpx = cdiv(total_px, 4 * G);
+        if (wpx > 16 * (nb - 1) && wpx <= 16 * nb &&
+            std::find(wpxs.begin(), wpxs.end(), (int)wpx) == wpxs.end())
+          wpxs.push_back((int)wpx);
+      }
+      if (wpxs.empty() && 16 * nb >= cdiv(total_px, 4)) wpxs.push_back((int)cdiv(total_px, 4));
+      for (int wpx : wpxs) {
+        conv_plan_t p;
+        fill_plan_fields(&p, v, 1, 4, 1, wpx, 0);
+        p.tile_k = 64;
+        p.wave_k = 64;
+        if (score_plan(s0, &p) == CONV_OK) all.push_back(p);
+      }
+      continue;
+    }
     const int nw = v.threads / 64;
     for (int nwk = 1; nwk <= nw; ++nwk) {
       if (nw % nwk) continue;

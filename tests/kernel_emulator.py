@@ -57,6 +57,8 @@ def emulate(g, In, Ker, wgs=None):
     In, Ker: flat float64 arrays of the problem (the kernel view, identical
     memory).  Returns (out_flat, written) where written counts stores per
     output element (NaN outputs where nothing was stored)."""
+    if g["family"] == 4:
+        return emulate_stream1x1(g, In, Ker, wgs)
     N, C, K, H, W, R, S, P, Q = (g[x] for x in "N C K H W R S P Q".split())
     WK, WP, TC, KV, NT = g["wk"], g["wp"], g["tc"], g["ker_vec"], g["threads"]
     _chk(NT == 256 or (g["family"] == 2 and NT in (256, 512)), "threads per workgroup")
@@ -425,5 +427,83 @@ def emulate_bf16(g, In, Ker, wgs=None, in_aligned=True):
                             dst = ((n * K + k) * P + p) * Q + q0 + col
                             _chk((dst[st] >= 0).all() and (dst[st] < out_size).all(), "Out store range")
                             out[dst[st]] = acc[(wave, kb, pb)][4 * gq + v, j][st]
+                            np.add.at(written, dst[st], 1)
+    return out, written
+
+
+# ---------------------------------------------------------------------------
+# Pointwise streaming family (conv1x1_stream_kernel).
+
+def emulate_stream1x1(g, In, Ker, wgs=None):
+    """The pointwise streaming kernel: Ker rows [k][c] in LDS (pitch = padded
+    channel count + 1), In B operands from raw buffer loads whose 32-bit byte
+    offsets are emulated exactly (offsets at or past the buffer size read 0)."""
+    N, C, K, H, W = (g[x] for x in "N C K H W".split())
+    _chk(g["family"] == 4 and g["threads"] == 256 and g["R"] == 1 and g["S"] == 1, "stream geometry")
+    HW = W  # kernel view: one row per image
+    _chk(H == 1, "kernel view of a pointwise layer")
+    _chk(C % 4 == 0, "whole channel quads")
+    NB1, NB2, D = g["max_ni"], g["max_nk"], g["stages"]
+    _chk(g["tc"] in (0, C), "unrolled instance for another channel count")
+    wpx = g["tw"]
+    _chk(1 <= wpx <= 16 * (NB1 + NB2), "pixels per wave")
+    nq = C // 4
+    nq_pad = -(-nq // D) * D
+    cpad, pitch = 4 * nq_pad, 4 * nq_pad + 1
+    _chk(g["stage_elems"] == 64 * pitch * 4 == g["lds_bytes"] and g["lds_bytes"] <= 160 * 1024, "LDS bytes")
+    total_px = N * HW
+    in_size, ker_size, out_size = N * C * HW, K * C, N * K * HW
+    _chk(In.size == in_size and Ker.size == ker_size, "input sizes")
+    _chk(g["in_bytes"] == in_size * 4 and in_size * 4 < 2 ** 30, "In byte range below 1 GB")
+    out = np.full(out_size, np.nan)
+    written = np.zeros(out_size, np.int64)
+    lane = np.arange(64)
+    j, gq = lane & 15, lane >> 4
+    KOOB, QOOB, M32 = 0x80000000, 0x40000000, 0xFFFFFFFF
+    for b in (range(g["grid"]) if wgs is None else wgs):
+        kt, pg = b % g["tiles_k"], b // g["tiles_k"]
+        k0 = kt * 64
+        lds = np.full(64 * pitch, np.nan)  # the pad column is never read
+        for e in range(64 * cpad):
+            kl, c = divmod(e, cpad)
+            k = k0 + kl
+            _chk(kl * pitch + c < lds.size, "LDS Ker write out of range")
+            lds[kl * pitch + c] = Ker[k * C + c] if (k < K and c < C) else 0.0
+        for wave in range(4):
+            px_begin = (pg * 4 + wave) * wpx
+            px_end = min(px_begin + wpx, total_px)
+            for blk0, nb in ((0, NB1), (NB1, NB2)):
+                for bb in range(nb):
+                    px = px_begin + (blk0 + bb) * 16 + j
+                    valid = px < px_end
+                    n, hw = px // HW, px % HW
+                    voff = np.where(valid, ((n * C + gq) * HW + hw) * 4, KOOB)
+                    acc = np.zeros((4, 16, 16))
+                    for q in range(nq_pad):
+                        qoff = q * 16 * HW + (0 if q < nq else QOOB)
+                        off = (voff + qoff) & M32
+                        hit = off < g["in_bytes"]
+                        _chk((off[hit] % 4 == 0).all(), "misaligned In offset")
+                        bv = np.where(hit, In[np.where(hit, off // 4, 0)], 0.0)
+                        # the range check must drop exactly the masked lanes
+                        # and the padded quads
+                        _chk((hit == (valid & (q < nq))).all(), "range check does not match the mask")
+                        ai = (np.arange(4)[:, None] * 16 + j[None, :]) * pitch + 4 * q + gq[None, :]
+                        _chk((ai < lds.size).all(), "LDS Ker read out of range")
+                        av = lds[ai]
+                        _chk(not np.isnan(av).any(), "LDS Ker read of an unwritten element")
+                        for kb in range(4):
+                            Am = np.zeros((16, 4))
+                            Am[j, gq] = av[kb]
+                            Bm = np.zeros((4, 16))
+                            Bm[gq, j] = bv
+                            acc[kb] += Am @ Bm
+                    for kb in range(4):
+                        for v in range(4):
+                            k = k0 + kb * 16 + 4 * gq + v
+                            st = valid & (k < K)
+                            dst = (n * K + k) * HW + hw
+                            _chk((dst[st] >= 0).all() and (dst[st] < out_size).all(), "Out store range")
+                            out[dst[st]] = acc[kb][4 * gq + v, j][st]
                             np.add.at(written, dst[st], 1)
     return out, written

@@ -234,11 +234,19 @@ def _plans_per_variant(dims, dtype=B.CONV_DTYPE_F32, per_variant=3):
     return [p for ps in by_var.values() for p in ps]
 
 
-@pytest.mark.parametrize("shape", [
+VARIANT_SHAPES = [
     ConvShape("var3x3", 3, 20, 72, 19, 23, 3, 3, "f32", 31),
     ConvShape("var1x1", 3, 40, 72, 13, 11, 1, 1, "f32", 32),
     ConvShape("var2x4", 2, 9, 40, 12, 13, 2, 4, "f32", 33),
-], ids=lambda s: s.name)
+    # pointwise layers whose channel count has a fully unrolled streaming kernel
+    ConvShape("var1x1_c64", 2, 64, 72, 13, 11, 1, 1, "f32", 34),
+    ConvShape("var1x1_c128", 3, 128, 64, 7, 9, 1, 1, "f32", 35),
+    ConvShape("var1x1_c256", 2, 256, 80, 8, 10, 1, 1, "f32", 36),
+    ConvShape("var1x1_c512", 1, 512, 64, 7, 7, 1, 1, "f32", 37),
+]
+
+
+@pytest.mark.parametrize("shape", VARIANT_SHAPES, ids=lambda s: s.name)
 def test_every_variant(shape):
     In, Ker = make_inputs(shape)
     ref = oconv.conv_fwd(host(In), host(Ker))

@@ -8,7 +8,7 @@ from oracle import conv as oconv
 from paper_2101_09808_amd import conv as B
 from paper_2101_09808_amd.workloads import CONFIGS, ConvShape, make_inputs
 from tests.kernel_emulator import emulate
-from tests.test_gpu_parity import EDGE, _plans_per_variant, small_version
+from tests.test_gpu_parity import EDGE, VARIANT_SHAPES, _plans_per_variant, small_version
 
 
 def _run(shape, plan, wgs=None):
@@ -35,11 +35,7 @@ def test_selected_plan_indexing(shape):
     _check_all(shape, B.conv_fwd_plan(*shape.key()))
 
 
-@pytest.mark.parametrize("shape", [
-    ConvShape("var3x3", 3, 20, 72, 19, 23, 3, 3, "f32", 31),
-    ConvShape("var1x1", 3, 40, 72, 13, 11, 1, 1, "f32", 32),
-    ConvShape("var2x4", 2, 9, 40, 12, 13, 2, 4, "f32", 33),
-], ids=lambda s: s.name)
+@pytest.mark.parametrize("shape", VARIANT_SHAPES, ids=lambda s: s.name)
 def test_every_variant_indexing(shape):
     for p in _plans_per_variant(shape.key()):
         _check_all(shape, p)
