@@ -1,18 +1,21 @@
 """Benchmark of the MI355X forward convolution (Eq. (1)).
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-layers] [--no-cpu]
+    python bench.py --traffic-run              (under rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE)
+    python bench.py --traffic-parse FETCH_DIR WRITE_DIR
 
 A step is one conv_fwd call (tile selection is cached, so the step is the
-kernel launch) on the pointwise layer N=32 C=256 K=64 56x56 1x1 fp32, the
-workload the headline metric is quoted on.  Inputs are seeded uniform[-1,1)
-synthetic tensors of that shape.  The timed steps cycle through enough
-independent In/Out buffer sets (more than twice the 256 MB last-level cache)
-that every step reads In from HBM and writes Out to HBM.
+kernel launch) on the pointwise layer N=32 C=256 K=64 56x56 1x1 fp32.  Inputs
+are seeded uniform[-1,1) synthetic tensors of that shape.  The timed steps
+cycle through enough independent In/Out buffer sets (more than twice the
+256 MB last-level cache) that every step reads In from HBM and writes Out to
+HBM.
 
-Prints ONE JSON line with the metric, the roofline of the kernel (achieved
-rate from HIP events around every launch on the launch stream), the CPU oracle
-timed on this host (cpu_baseline), and a per-layer table for the other layer
-configurations.
+Prints ONE JSON line with the metric, the roofline of the kernel (average
+launch duration from HIP events recorded on the launch stream around the
+timed region), the HBM traffic measured by the counter passes when they match
+the current kernel sources, the CPU oracle timed on this host (cpu_baseline),
+and a per-layer table for the other layer configurations.
 """
 import argparse
 import hashlib
@@ -48,8 +51,9 @@ def kernel_source_hash():
 
 
 def time_layer(c, steps, warmup):
-    """Mean per-launch kernel time (HIP events on the launch stream) and the
-    wall time of `steps` back-to-back launches over rotating buffer sets."""
+    """Average launch duration from HIP events recorded on the launch stream
+    around the `steps` back-to-back launches of the timed region (rotating
+    buffer sets), and the host wall time of the same region."""
     import torch
     from paper_2101_09808_amd import conv as B
     from paper_2101_09808_amd.workloads import make_inputs
@@ -77,21 +81,103 @@ def time_layer(c, steps, warmup):
     (B.conv_fwd_bf16 if bf16 else B.conv_fwd)(ins[0], Ker, out=outs[0])
     for i in range(warmup):
         fn(i % nsets)
-    torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    start.record(stream)
     for i in range(steps):
-        ev[i][0].record(stream)
         fn(i % nsets)
-        ev[i][1].record(stream)
+    end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per = [a.elapsed_time(b) for a, b in ev]  # ms
-    per.sort()
-    mean_ms = sum(per) / len(per)
-    return dict(mean_kernel_ms=mean_ms, median_kernel_ms=per[len(per) // 2], min_kernel_ms=per[0],
-                wall_ms_per_step=wall * 1e3 / steps, buffer_sets=nsets)
+    ev_ms = start.elapsed_time(end)
+    return dict(mean_kernel_ms=ev_ms / steps, wall_ms_per_step=wall * 1e3 / steps, buffer_sets=nsets)
+
+
+COPY_BYTES = 256 * 2 ** 20  # plain device-to-device copy used to scale the HBM byte counters
+COPY_REPS = 3
+TRAFFIC_COMMANDS = [
+    "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/traffic_fetch -o f -- python -u bench.py --traffic-run",
+    "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/traffic_write -o w -- python -u bench.py --traffic-run",
+    "python bench.py --traffic-parse gpurun_out/traffic_fetch gpurun_out/traffic_write",
+]
+
+
+def traffic_run(c, launches=6):
+    """Workload for the two rocprofv3 --pmc passes (FETCH_SIZE, then WRITE_SIZE):
+    COPY_REPS plain copies of COPY_BYTES, then `launches` conv launches of the
+    timed plan on rotating buffer sets.  Inputs are generated on the device so
+    that no other copy kernel runs in this process."""
+    import torch
+    from paper_2101_09808_amd import conv as B
+
+    dev = torch.device("cuda:0")
+    src = torch.empty(COPY_BYTES // 4, device=dev).uniform_(-1, 1)
+    dst = torch.empty_like(src)
+    for _ in range(COPY_REPS):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    bf16 = c.dtype == "bf16"
+    edt = torch.bfloat16 if bf16 else torch.float32
+    set_bytes = c.N * c.C * c.H * c.W * (2 if bf16 else 4) + c.N * c.K * c.P * c.Q * 4
+    nsets = max(2, -(-2 * MALL_BYTES // set_bytes) + 1)
+    ins = [torch.empty(c.N, c.C, c.H, c.W, device=dev).uniform_(-1, 1).to(edt) for _ in range(nsets)]
+    Ker = torch.empty(c.K, c.C, c.R, c.S, device=dev).uniform_(-1, 1).to(edt)
+    outs = [torch.empty(c.N, c.K, c.P, c.Q, device=dev) for _ in range(nsets)]
+    torch.cuda.synchronize()
+    sp = torch.cuda.current_stream().cuda_stream
+    for i in range(launches):
+        st = B.conv_fwd_ptr(*c.key(), ins[i % nsets].data_ptr(), Ker.data_ptr(), outs[i % nsets].data_ptr(), sp, bf16)
+        if st != B.CONV_OK:
+            raise B.ConvError(st, "conv_fwd")
+    torch.cuda.synchronize()
+    print(f"traffic run: {COPY_REPS} copies of {COPY_BYTES} B, {launches} launches of {c.name}", flush=True)
+
+
+def traffic_parse(c, fetch_dir, write_dir, out_path):
+    """Scale the per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the conv kernel by
+    what the same counters read for the plain copy, and store the result."""
+    import csv
+    import glob
+
+    from paper_2101_09808_amd import conv as B
+
+    def per_dispatch(d, counter):
+        f = sorted(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True))
+        if not f:
+            raise SystemExit(f"no counter_collection.csv under {d}")
+        vals = {}
+        for r in csv.DictReader(open(f[0])):
+            if r["Counter_Name"] != counter:
+                continue
+            k = int(r["Dispatch_Id"])
+            name, v = vals.get(k, (r["Kernel_Name"], 0.0))
+            vals[k] = (name, v + float(r["Counter_Value"]))
+        return [vals[k] for k in sorted(vals)]
+
+    res = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = per_dispatch(d, counter)
+        conv = [v for n, v in rows if "convfwd::" in n]
+        copy = [v for n, v in rows if "convfwd::" not in n and "copy" in n.lower()]
+        if len(copy) != COPY_REPS or len(conv) < 2:
+            raise SystemExit(f"{counter}: expected {COPY_REPS} copy dispatches and >= 2 conv dispatches, "
+                             f"got {len(copy)} and {len(conv)}")
+        factor = COPY_BYTES * COPY_REPS / (sum(copy) * 1024.0)
+        conv = conv[1:]  # the first launch also faults in the buffers
+        res[counter] = {"kib_per_dispatch": sum(conv) / len(conv), "copy_kib_per_dispatch": sum(copy) / len(copy),
+                        "factor": factor, "bytes_per_launch": sum(conv) / len(conv) * 1024.0 * factor}
+    dtype_code = B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32
+    plan = B.conv_fwd_plan(*c.key(), dtype=dtype_code)
+    out = {"workload": c.name, "kernel_sha": kernel_source_hash(), "plan_variant": plan["variant"],
+           "copy_bytes": COPY_BYTES, "copy_reps": COPY_REPS,
+           "fetch": res["FETCH_SIZE"], "write": res["WRITE_SIZE"],
+           "hbm_bytes_per_launch": res["FETCH_SIZE"]["bytes_per_launch"] + res["WRITE_SIZE"]["bytes_per_launch"],
+           "alg_bytes_per_launch": alg_bytes(c), "commands": TRAFFIC_COMMANDS}
+    with open(out_path, "w") as fh:
+        json.dump(out, fh, indent=1)
+    print(json.dumps(out), flush=True)
 
 
 def cpu_baseline(c, budget_s=10.0):
@@ -113,9 +199,17 @@ def cpu_baseline(c, budget_s=10.0):
         t0 = time.perf_counter()
         oconv.conv_fwd(np.ascontiguousarray(In[:n]), Ker)
         dt = time.perf_counter() - t0
-    f = flops(c) * n / c.N
+    reps = 1
+    if n == c.N and dt < budget_s:  # the whole layer is cheap: repeat it for a stable rate
+        reps = max(1, int(budget_s / max(dt, 1e-6)))
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            oconv.conv_fwd(In, Ker)
+        dt = time.perf_counter() - t0
+    f = flops(c) * n / c.N * reps
     return {"value": f / dt / 1e9, "unit": "GFLOP/s", "cores": oconv.num_threads(), "kind": "oracle",
-            "sample": f"{n} of {c.N} images of {c.name} (fp64 plain loops, OpenMP over n,k), {dt:.2f} s"}
+            "sample": f"{n} of {c.N} images of {c.name}, {reps} pass(es) (fp64 plain loops, OpenMP over n,k), "
+                      f"{dt:.2f} s"}
 
 
 def main():
@@ -126,6 +220,10 @@ def main():
     ap.add_argument("--no-layers", action="store_true", help="skip the per-layer table")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--layer", default=HEADLINE, help="workload of the timed step")
+    ap.add_argument("--traffic-run", action="store_true",
+                    help="plain copies + a few launches, for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs")
+    ap.add_argument("--traffic-parse", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="turn the two counter runs into the HBM traffic record read by the benchmark")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU (got --gpus {args.gpus}); "
@@ -138,11 +236,18 @@ def main():
     from paper_2101_09808_amd import conv as B
     from paper_2101_09808_amd.workloads import BY_NAME, CONFIGS
 
+    if args.traffic_parse:  # host-only: reads the counter files of two earlier runs
+        traffic_parse(BY_NAME[args.layer], args.traffic_parse[0], args.traffic_parse[1], TRAFFIC_FILE)
+        return
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
     B.lib()  # fail loudly if the HIP library is missing
     c = BY_NAME[args.layer]
+    if args.traffic_run:
+        traffic_run(c)
+        return
+
     dtype_code = B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32
     plan = B.conv_fwd_plan(*c.key(), dtype=dtype_code)
     r = time_layer(c, args.steps, args.warmup)

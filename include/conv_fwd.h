@@ -10,7 +10,9 @@
  * padding), stride 1, with no kernel flip.  Out is overwritten (beta = 0).
  *
  * Layouts (Sec. 9, artifact appendix): In is NCHW, Ker is KCRS, Out is NKPQ;
- * all dense, contiguous, row-major.  Only element alignment is required.
+ * all dense, contiguous, row-major.  Only element alignment is required: the
+ * selected kernel depends on the shape and on whether In and Ker are 16-byte
+ * aligned (kernels with vector loads need it).
  *
  * Loop order and tile sizes are chosen per shape by a tile selector built on
  * the paper's data-movement model (Sec. 3-5, Algorithm 1 of Sec. 8),
@@ -124,7 +126,8 @@ int conv_fwd_plan(int N, int C, int K, int H, int W, int R, int S, int dtype,
  * plan is re-validated: only its dtype, variant, tile_* , wave_*, waves_* and
  * grid_order fields are read; the rest is recomputed.  `In`/`Ker` are fp32
  * or bf16 per plan->dtype.  Returns CONV_EINVAL for a plan the kernels cannot
- * run, else as conv_fwd.
+ * run -- including a plan whose vector loads need 16-byte aligned In or Ker
+ * when the tensors passed are not -- else as conv_fwd.
  */
 int conv_fwd_with_plan(int N, int C, int K, int H, int W, int R, int S,
                        const void* In, const void* Ker, float* Out,

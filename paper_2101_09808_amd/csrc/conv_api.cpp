@@ -26,7 +26,7 @@ int validate_shape(int N, int C, int K, int H, int W, int R, int S) {
   return CONV_OK;
 }
 
-// Per (shape, dtype, Ker alignment) the selected plan and its resolved launch.
+// Per (shape, dtype, tensor alignment) the selected plan and its resolved launch.
 struct Entry {
   conv_plan_t plan;
   const Variant* v;
@@ -36,21 +36,36 @@ typedef std::tuple<int, int, int, int, int, int, int, int, int> Key;
 std::mutex g_mu;
 std::map<Key, Entry> g_cache;
 
-int select_entry(const Shape& s, int dtype, bool ker_aligned, Entry* e) {
+// Alignment bits of a call: vector loads of In (4 fp32) or Ker need a
+// 16-byte aligned tensor.
+enum { ALIGN_KER = 1, ALIGN_IN = 2, ALIGN_ALL = 3 };
+
+int alignment_of(const void* In, const void* Ker) {
+  return ((reinterpret_cast<uintptr_t>(Ker) & 15) == 0 ? ALIGN_KER : 0) |
+         ((reinterpret_cast<uintptr_t>(In) & 15) == 0 ? ALIGN_IN : 0);
+}
+
+// Does variant v run with tensors of this alignment?
+bool variant_fits(const Variant& v, int dtype, int align) {
+  const int elem = dtype == CONV_DTYPE_BF16 ? 2 : 4;
+  if (v.ker_vec * elem > elem && v.family != FAMILY_BF16 && !(align & ALIGN_KER)) return false;
+  if (v.family == FAMILY_DMA && v.in_vec > 1 && !(align & ALIGN_IN)) return false;
+  return true;
+}
+
+int select_entry(const Shape& s, int dtype, int align, Entry* e) {
   conv_plan_t p;
   int st = select_plan(s, dtype, &p);
   if (st != CONV_OK) return st;
   const Variant* v = find_variant(p.variant);
-  const int elem = dtype == CONV_DTYPE_BF16 ? 2 : 4;
-  if (!ker_aligned && v && v->ker_vec * elem > elem) {
-    // Vector Ker loads need an aligned tensor: best plan of a variant that
-    // loads Ker element-wise.
+  if (v && !variant_fits(*v, dtype, align)) {
+    // best plan of a variant whose loads suit the tensors' alignment
     std::vector<conv_plan_t> buf(4096);
     const int n = enumerate_plans(s, dtype, buf.data(), (int)buf.size());
     v = nullptr;
     for (int i = 0; i < n && i < (int)buf.size(); ++i) {
       const Variant* w = find_variant(buf[i].variant);
-      if (w && w->ker_vec == 1) {
+      if (w && variant_fits(*w, dtype, align)) {
         p = buf[i];
         v = w;
         break;
@@ -64,8 +79,8 @@ int select_entry(const Shape& s, int dtype, bool ker_aligned, Entry* e) {
   return CONV_OK;
 }
 
-int cached_entry(const Shape& s, int dtype, bool ker_aligned, Entry* out) {
-  const Key key{s.N, s.C, s.K, s.H, s.W, s.R, s.S, dtype, ker_aligned ? 1 : 0};
+int cached_entry(const Shape& s, int dtype, int align, Entry* out) {
+  const Key key{s.N, s.C, s.K, s.H, s.W, s.R, s.S, dtype, align};
   {
     std::lock_guard<std::mutex> lk(g_mu);
     auto it = g_cache.find(key);
@@ -75,7 +90,7 @@ int cached_entry(const Shape& s, int dtype, bool ker_aligned, Entry* out) {
     }
   }
   Entry e;
-  const int st = select_entry(s, dtype, ker_aligned, &e);
+  const int st = select_entry(s, dtype, align, &e);
   if (st != CONV_OK) return st;
   {
     std::lock_guard<std::mutex> lk(g_mu);
@@ -87,7 +102,7 @@ int cached_entry(const Shape& s, int dtype, bool ker_aligned, Entry* out) {
 
 int cached_plan(const Shape& s, int dtype, conv_plan_t* out) {
   Entry e;
-  const int st = cached_entry(s, dtype, true, &e);
+  const int st = cached_entry(s, dtype, ALIGN_ALL, &e);
   if (st == CONV_OK) *out = e.plan;
   return st;
 }
@@ -96,18 +111,17 @@ int run(const Shape& s, const void* In, const void* Ker, float* Out, const conv_
         void* stream) {
   const Variant* v = find_variant(plan.variant);
   if (!v || v->dtype != plan.dtype) return CONV_EINVAL;
+  if (!variant_fits(*v, plan.dtype, alignment_of(In, Ker))) return CONV_EINVAL;
   Geom g;
   if (!resolve_geom(s, *v, plan, &g, nullptr)) return CONV_EINVAL;
   return launch(*v, g, In, Ker, Out, stream);
 }
 
-// Selected plan for a call: cached per shape; Ker vector loads need a
-// 16-byte aligned tensor.
+// Selected plan for a call: cached per shape and tensor alignment.
 int run_selected(const Shape& s, int dtype, const void* In, const void* Ker, float* Out,
                  void* stream) {
-  const bool aligned = (reinterpret_cast<uintptr_t>(Ker) & 15) == 0;
   Entry e;
-  const int st = cached_entry(s, dtype, aligned, &e);
+  const int st = cached_entry(s, dtype, alignment_of(In, Ker), &e);
   if (st != CONV_OK) return st;
   return launch(*e.v, e.g, In, Ker, Out, stream);
 }

@@ -258,3 +258,52 @@ def test_every_variant(shape):
         out = host(gpu_conv(shape, In, Ker, plan=p))
         err = rel_err(out, ref)
         assert err <= TOL["f32"], (p, err)
+
+
+@pytest.mark.parametrize("shape", [
+    ConvShape("bf16_var3x3", 2, 40, 72, 11, 13, 3, 3, "bf16", 51),
+    ConvShape("bf16_var1x1", 2, 64, 80, 10, 12, 1, 1, "bf16", 52),
+], ids=lambda s: s.name)
+def test_every_bf16_variant(shape):
+    In, Ker = make_inputs(shape)
+    ref = oconv.conv_fwd(host(In), host(Ker))
+    plans = _plans_per_variant(shape.key(), dtype=B.CONV_DTYPE_BF16)
+    assert plans
+    for p in plans:
+        say(f"[gpu] {shape.name} variant={p['variant']} tile={p['tile_k']}x{p['tile_rows']}x{p['tile_cols']} "
+            f"waves={p['waves_k']}x{p['waves_px']} order={p['grid_order']}")
+        out = host(gpu_conv(shape, In, Ker, plan=p))
+        err = rel_err(out, ref)
+        assert err <= TOL["bf16"], (p, err)
+
+
+@pytest.mark.parametrize("shape", [
+    ConvShape("misaligned_1x1_vec_in", 2, 30, 40, 8, 10, 1, 1, "f32", 61),
+    ConvShape("misaligned_3x3_vec_ker", 2, 24, 64, 14, 16, 3, 3, "f32", 62),
+], ids=lambda s: s.name)
+def test_misaligned_tensors(shape):
+    """In and Ker starting 4 bytes past a 16-byte boundary: the library picks
+    a kernel whose loads suit them, and an explicit plan with vector loads is
+    refused without a launch."""
+    In, Ker = make_inputs(shape)
+    ref = oconv.conv_fwd(host(In), host(Ker))
+    aligned_plan = B.conv_fwd_plan(*shape.key())
+    bi = torch.zeros(In.numel() + 4, device=DEV)
+    bk = torch.zeros(Ker.numel() + 4, device=DEV)
+    In_d = bi[1:1 + In.numel()].view(In.shape)
+    Ker_d = bk[1:1 + Ker.numel()].view(Ker.shape)
+    In_d.copy_(In.to(DEV))
+    Ker_d.copy_(Ker.to(DEV))
+    assert In_d.data_ptr() % 16 == 4 and Ker_d.data_ptr() % 16 == 4
+    say(f"[gpu] {shape.name} misaligned, aligned-case plan {aligned_plan['variant']}")
+    out = B.conv_fwd(In_d, Ker_d)
+    torch.cuda.synchronize()
+    assert rel_err(host(out), ref) <= TOL["f32"]
+    g = B.conv_fwd_geometry(*shape.key(), aligned_plan)
+    if g["in_vec"] > 1 or g["ker_vec"] > 1:
+        poison = torch.full_like(out, 7.0)
+        with pytest.raises(B.ConvError) as ei:
+            B.conv_fwd_with_plan(In_d, Ker_d, aligned_plan, out=poison)
+        assert ei.value.status == B.CONV_EINVAL
+        torch.cuda.synchronize()
+        assert (poison == 7.0).all()

@@ -93,3 +93,39 @@ def test_bf16_full_config_sampled_workgroups():
     idx = np.nonzero(written)[0]
     ref = oconv.conv_fwd_points(In.float().numpy(), Ker.float().numpy(), idx)
     assert np.max(np.abs(out[idx] - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
+
+
+@pytest.mark.parametrize("shape", [
+    ConvShape("bf16_var3x3", 2, 40, 72, 11, 13, 3, 3, "bf16", 51),
+    ConvShape("bf16_var1x1", 2, 64, 80, 10, 12, 1, 1, "bf16", 52),
+], ids=lambda s: s.name)
+def test_every_bf16_variant_indexing(shape):
+    """The plans the GPU test runs for every bf16 kernel variant."""
+    from tests.kernel_emulator import emulate_bf16
+    In, Ker = make_inputs(shape)
+    In64 = In.float().numpy().astype(np.float64)
+    Ker64 = Ker.float().numpy().astype(np.float64)
+    ref = oconv.conv_fwd(In64.astype(np.float32), Ker64.astype(np.float32)).reshape(-1)
+    plans = _plans_per_variant(shape.key(), dtype=B.CONV_DTYPE_BF16)
+    assert plans
+    for p in plans:
+        g = B.conv_fwd_geometry(*shape.key(), p)
+        out, written = emulate_bf16(g, In64.reshape(-1), Ker64.reshape(-1))
+        assert np.all(written == 1)
+        assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
+
+
+@pytest.mark.parametrize("shape", [
+    ConvShape("misaligned_1x1_vec_in", 2, 30, 40, 8, 10, 1, 1, "f32", 61),
+    ConvShape("misaligned_3x3_vec_ker", 2, 24, 64, 14, 16, 3, 3, "f32", 62),
+], ids=lambda s: s.name)
+def test_misaligned_fallback_plan_indexing(shape):
+    """The plan a call with In and Ker off 16-byte boundaries runs: the best
+    candidate without vector loads of In (direct-to-LDS family) or Ker."""
+    for p in B.conv_fwd_candidates(*shape.key()):
+        g = B.conv_fwd_geometry(*shape.key(), p)
+        if g["ker_vec"] == 1 and not (g["family"] == 2 and g["in_vec"] > 1):
+            break
+    else:
+        pytest.fail("no plan without vector loads")
+    _check_all(shape, p)
