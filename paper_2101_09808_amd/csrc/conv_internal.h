@@ -19,7 +19,8 @@ enum {
   FAMILY_STAGED = 1,  // global -> VGPR -> LDS staging, double buffered (any size)
   FAMILY_DMA = 2,     // global -> LDS direct buffer loads, NS-stage pipeline
   FAMILY_BF16 = 3,    // bf16 inputs: persistent, channel-fastest transposed LDS tiles
-  FAMILY_STREAM1X1 = 4,  // pointwise: Ker resident in LDS, In streamed to registers
+  FAMILY_STREAM1X1 = 4,  // pointwise: Ker resident in LDS, In streamed to registers (unrolled C)
+  FAMILY_STREAM1X1_LOOP = 5,  // the same for any C % 4 == 0, looped over channel quads
 };
 
 // One compiled kernel instance (template parameters of the kernel family).
@@ -28,11 +29,14 @@ struct Variant {
   int dtype;      // CONV_DTYPE_*
   int family;     // FAMILY_*
   int wk;         // 16-wide k blocks per wave (register tile along k)
-  int wp;         // 16-wide pixel blocks per wave (register tile along pixels)
+  int wp;         // 16-wide pixel blocks per wave (register tile along pixels; for the
+                  // unrolled streaming kernel in 16-pixel units: 2 * NB32 + NS16)
   int tc;         // input channels per pipeline step
   int rc, sc;     // compile-time R, S (0 = runtime)
-  int max_ni;     // STAGED: max In staging elements per thread; DMA: In loads per wave per step
-  int max_nk;     // STAGED: max Ker staging vectors per thread; DMA: Ker loads per wave per step
+  int max_ni;     // STAGED: max In staging elements per thread; DMA: In loads per wave per step;
+                  // STREAM: 32-pixel blocks (unrolled) / phase-one 16-pixel blocks (looped)
+  int max_nk;     // STAGED: max Ker staging vectors per thread; DMA: Ker loads per wave per step;
+                  // STREAM: 16-pixel blocks (unrolled, 0 or 1) / phase-two blocks (looped)
   int ker_vec;    // Ker load width in elements
   int in_vec;     // In load width in elements (DMA family; 1 for STAGED)
   int threads;    // threads per workgroup

@@ -26,6 +26,7 @@
 
 #include <mutex>
 #include <type_traits>
+#include <utility>
 
 #include "conv_internal.h"
 
@@ -33,6 +34,7 @@ namespace convfwd {
 namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 
 template <int N>
 struct FVec {
@@ -313,6 +315,15 @@ __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   // s_waitcnt: vmcnt in bits [3:0] and [15:14]; expcnt and lgkmcnt left at max
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
+
+// The same wait as opaque inline assembly: where compiler-issued loads are
+// also in flight, the compiler's wait bookkeeping (which cannot see loads
+// issued from inline assembly) might otherwise drop or relax it.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_opaque() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
 template <int WK, int WP, int NW, int TC, int RC, int SC, int NS, int NLI, int KVI, int NLK, int KVK>
@@ -706,28 +717,64 @@ conv_bf16_kernel(const unsigned short* __restrict__ In, const unsigned short* __
 }
 
 // ---------------------------------------------------------------------------
-// Pointwise (1x1) streaming kernel.
+// Pointwise (1x1) streaming kernels.
 //
 // With R = S = 1 the convolution is Out[n][k][px] = sum_c Ker[k][c] In[n][c][px]
 // over the flattened pixels px of each image.  Each workgroup keeps its
-// 64-wide slice of Ker resident in LDS as rows [k][c] with a pitch of one
-// float more than the (ring-padded) channel count: the fill is a coalesced
-// copy of whole Ker rows, and the A operands (lane (i, gq) reads row
-// kb*16 + i at channel 4q + gq) hit 16 distinct banks per 16-lane group.
-// Each wave owns a contiguous range of `wpx` pixels (NB1 + NB2 blocks of 16)
-// and streams its In columns straight from global memory into a ring of D
-// register slots (D channel quads ahead); no LDS traffic or barriers for In.
-// The pixel blocks are done in two phases (NB1, then NB2 blocks) so the first
-// phase's stores drain while the second phase computes.  Requires C % 4 == 0
-// (whole channel quads) and In below 1 GB (32-bit byte offsets).
-template <int NB1, int NB2, int D, int NQ>
+// 64-row slice of Ker resident in LDS as rows [k][c] with a pitch of one float
+// more than the stored channel count: lane (i, gq) reads row kb*16 + i at
+// channel 4q + gq for the A operands, 16 distinct banks per 16-lane group.
+// Each wave owns a contiguous range of `wpx` pixels (blocks of 16) and
+// streams its In columns straight from HBM into a ring of registers with
+// branch-free raw buffer loads: masked lanes start at 2^31, past the buffer's
+// range, and read zeros.  No LDS traffic or barriers for In.  Both kernels
+// require C % 4 == 0 and In below 1 GB (32-bit byte offsets).
+
+// Compile-time loop: f(std::integral_constant<int, i>) for i = 0..N-1, each
+// call inlined with its own constant (a plain unroll pragma gives up on long
+// bodies, and a rolled loop would index register arrays dynamically).
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Fully unrolled kernel for a compile-time channel count C = 4 * NQ.
+//
+// A wave's pixels are NB32 blocks of 32 done with v_mfma_f32_32x32x2f32 (two
+// 32-row k blocks, two channels per MFMA) plus NS16 (0 or 1) blocks of 16
+// done with v_mfma_f32_16x16x4f32 (four 16-row k blocks, four channels), so
+// the per-wave pixel count can be a multiple of 16 while most of the work
+// runs on the wider instruction: it reads half the operand registers per
+// flop, and its accumulators can be reused every few instructions without
+// stalls.  One step of the unrolled loop is one channel quad.  The Ker slice
+// arrives in chunks of 64 channels straight to LDS (buffer loads with the LDS
+// bit); chunk c+1 is requested during chunk c, so only the first chunk's
+// latency precedes the first MFMA.
+//
+// Lane layouts (l = lane): 32x32x2 A[i][k] = lane (i = l%32, k = l/32), B[k][j]
+// = lane (j = l%32, k = l/32), accumulator register v = (i = 8*(v/4) +
+// 4*(l/32) + v%4, j = l%32); 16x16x4 A (i = l%16, k = l/16), B (j = l%16,
+// k = l/16), register v = (i = 4*(l/16) + v, j = l%16).
+template <int NB32, int NS16, int D, int NQ>
 __global__ void __launch_bounds__(kThreads)
 conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
                       float* __restrict__ Out, const Geom g) {
+  static_assert(NQ % 16 == 0, "Ker arrives in chunks of 16 channel quads");
+  static_assert(NS16 == 0 || NS16 == 1, "at most one 16-pixel block");
+  constexpr int LPQ = 2 * NB32 + NS16;     // In loads per wave per channel quad
+  constexpr int PITCH = 4 * NQ + 1;        // LDS Ker row pitch, floats
+  constexpr int NCH = NQ / 16;             // Ker chunks of 64 channels
+  constexpr int LEAD = (48 / LPQ) < 16 ? (48 / LPQ) : 16;  // steps from a chunk's request to its wait
+  static_assert(D >= 1 && D * LPQ <= 48 && D <= NQ && LEAD >= 1, "loads in flight stay within vmcnt");
   extern __shared__ __align__(16) float lds[];
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int j = lane & 15, gq = lane >> 4;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, h32 = lane >> 5;  // 32x32x2 lane coordinates
+  const int l16 = lane & 15, h16 = lane >> 4;  // 16x16x4 lane coordinates
   const int C = g.C, K = g.K;
   const int HW = g.W;                   // kernel view: one row of H*W pixels per image
   const int total_px = g.N * HW;
@@ -737,55 +784,193 @@ conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ke
   const int wpx = g.tw;                 // pixels per wave
   const int px_begin = (pg * 4 + wave) * wpx;
   const int px_end = min(px_begin + wpx, total_px);
-  // Channel quads: NQ > 0 fixes the count at compile time so the channel loop
-  // unrolls completely and every wait on the register ring is exact.
-  const int nq = NQ > 0 ? NQ : (C + 3) / 4;
-  const int nq_pad = (nq + D - 1) / D * D;
 
-  // Ker slice -> LDS rows [k][c], zero-padded to whole ring groups of quads.
-  // Coalesced row reads, a whole batch of loads in flight at once (every
-  // workgroup reads the same slice at the same time, so round trips are long).
-  // With NQ > 0 the slice is one batch, issued before the In ring prologue and
-  // written to LDS after it, so the two latencies overlap.
-  const int cpad = nq_pad * 4, pitch = cpad + 1;
-  constexpr int FB = NQ > 0 ? ((NQ + D - 1) / D * D * 4 * 64) / kThreads : 16;  // loads per batch
-  float kv[FB];
-  auto fill_load = [&](int e0) {
+  // Ker chunk ch -> LDS: wave w copies rows 16w..16w+15, 64 channels per load
+  // (rows past K read zeros).
+  const v4i krsrc = make_rsrc(Ker, g.ker_bytes);
+  const unsigned lbase = (unsigned)(size_t)(lds_float*)lds;
+  auto ker_chunk = [&](int ch) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < FB; ++i) {
-      const int e = e0 + tid + i * kThreads;
-      const int kl = e / cpad, c = e - kl * cpad;
-      const int k = k0 + kl;
-      kv[i] = (e < 64 * cpad && k < K && c < C) ? Ker[(size_t)k * C + c] : 0.f;
+    for (int i = 0; i < 16; ++i) {
+      const int kl = wave * 16 + i, k = k0 + kl;
+      const unsigned voff = k < K ? (unsigned)(k * C + ch * 64 + lane) * 4u : kOob;
+      dma_load<1>(krsrc, __builtin_amdgcn_readfirstlane(lbase + (unsigned)(kl * PITCH + ch * 64) * 4u), voff);
     }
   };
-  auto fill_store = [&](int e0) {
-#pragma unroll
-    for (int i = 0; i < FB; ++i) {
-      const int e = e0 + tid + i * kThreads;
-      const int kl = e / cpad, c = e - kl * cpad;
-      if (e < 64 * cpad) lds[kl * pitch + c] = kv[i];
-    }
-  };
-  if constexpr (NQ > 0) fill_load(0);
-  auto ker_ready = [&]() {
-    if constexpr (NQ > 0) {
-      fill_store(0);
-    } else {
-      for (int e0 = 0; e0 < 64 * cpad; e0 += kThreads * FB) {
-        fill_load(e0);
-        fill_store(e0);
-      }
-    }
-    __syncthreads();
-  };
-  // In through raw buffer loads: masked lanes and channels past C read zeros
-  // from the range check, so the loop has no branches.
+
+  // In through raw buffer loads; masked lanes start at 2^31 and read zeros.
   __amdgpu_buffer_rsrc_t rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(In), (short)0, (int)g.in_bytes, 0x00020000);
-  const unsigned qstride = 16u * (unsigned)HW;  // bytes between channel quads
+  const unsigned cstride = 4u * (unsigned)HW;  // bytes between channels
+  auto in_off = [&](int px, int c) __attribute__((always_inline)) {
+    const int n = px / HW, hw = px - n * HW;
+    return (px < px_end) ? (unsigned)((n * C + c) * HW + hw) * 4u : kOob;
+  };
+  unsigned off32[NB32 > 0 ? NB32 : 1], off16 = 0;
+#pragma unroll
+  for (int b = 0; b < NB32; ++b) off32[b] = in_off(px_begin + 32 * b + l32, h32);
+  if constexpr (NS16 > 0) off16 = in_off(px_begin + 32 * NB32 + l16, h16);
+  float ring32[D][2][NB32 > 0 ? NB32 : 1], ring16[D];
+  auto load = [&](int q) __attribute__((always_inline)) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int b = 0; b < NB32; ++b)
+        ring32[q % D][e][b] = __builtin_bit_cast(
+            float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, off32[b] + (unsigned)(4 * q + 2 * e) * cstride, 0, 0));
+    if constexpr (NS16 > 0)
+      ring16[q % D] = __builtin_bit_cast(
+          float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, off16 + (unsigned)(4 * q) * cstride, 0, 0));
+  };
+  // A operands, read one quad ahead: a32[e][kb] = Ker[k0 + 32kb + l32][4q + 2e + h32],
+  // a16[kb] = Ker[k0 + 16kb + l16][4q + h16]
+  const float* arow32 = lds + l32 * PITCH + h32;
+  const float* arow16 = lds + l16 * PITCH + h16;
+  float a32[2][2][2], a16[2][4];
+  auto read_a = [&](int q, int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) a32[buf][e][kb] = arow32[kb * 32 * PITCH + 4 * q + 2 * e];
+    if constexpr (NS16 > 0) {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) a16[buf][kb] = arow16[kb * 16 * PITCH + 4 * q];
+    }
+  };
+  v16f acc32[NB32 > 0 ? NB32 : 1][2];
+  v4f acc16[4];
+#pragma unroll
+  for (int b = 0; b < NB32; ++b)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) acc32[b][kb] = v16f{};
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) acc16[kb] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  auto phase = [&](auto nb_const, int blk0, auto first_const) {
+  // prologue: first Ker chunk, then the ring, then wait for the chunk (the
+  // ring's D * LPQ loads are younger and may stay in flight)
+  ker_chunk(0);
+#pragma unroll
+  for (int q = 0; q < D; ++q) load(q);
+  wait_vmcnt_opaque<D * LPQ>();
+  __syncthreads();
+  read_a(0, 0);
+  static_for<NQ>([&](auto q_c) __attribute__((always_inline)) {
+    constexpr int q = decltype(q_c)::value;
+    constexpr int buf = q & 1;
+    constexpr bool chunk_end = q % 16 == 15 && q / 16 + 1 < NCH;
+    if constexpr (q + 1 < NQ && !chunk_end) read_a(q + 1, buf ^ 1);
+    __builtin_amdgcn_sched_barrier(0);  // issue the A reads first
+    if constexpr (q % 16 == 16 - LEAD && q / 16 + 1 < NCH) ker_chunk(q / 16 + 1);
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int b = 0; b < NB32; ++b)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+          acc32[b][kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a32[buf][e][kb], ring32[q % D][e][b],
+                                                              acc32[b][kb], 0, 0, 0);
+    if constexpr (NS16 > 0) {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+        acc16[kb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a16[buf][kb], ring16[q % D], acc16[kb], 0, 0, 0);
+    }
+    if constexpr (q + D < NQ) load(q + D);
+    if constexpr (chunk_end) {
+      // the next chunk was requested LEAD steps ago; LEAD * LPQ ring loads are younger
+      wait_vmcnt_opaque<LEAD * LPQ>();
+      __syncthreads();
+      read_a(q + 1, buf ^ 1);
+    }
+    // keep each refill right behind the MFMAs that free its slot: left alone,
+    // the scheduler sinks loads towards their uses and the ring degenerates
+    // to a few loads in flight
+    __builtin_amdgcn_sched_barrier(0);
+  });
+
+  // stores: 32 consecutive pixels (two rows of k) or 16 (four rows) per instruction
+#pragma unroll
+  for (int b = 0; b < NB32; ++b) {
+    const int px = px_begin + 32 * b + l32;
+    if (px < px_end) {
+      const int n = px / HW, hw = px - n * HW;
+      float* ob = Out + (size_t)n * K * HW + hw;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int k = k0 + 32 * kb + 8 * (v / 4) + 4 * h32 + v % 4;
+          if (k < K) ob[(size_t)k * HW] = acc32[b][kb][v];
+        }
+    }
+  }
+  if constexpr (NS16 > 0) {
+    const int px = px_begin + 32 * NB32 + l16;
+    if (px < px_end) {
+      const int n = px / HW, hw = px - n * HW;
+      float* ob = Out + (size_t)n * K * HW + hw;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int k = k0 + 16 * kb + 4 * h16 + v;
+          if (k < K) ob[(size_t)k * HW] = acc16[kb][v];
+        }
+    }
+  }
+}
+
+// Looped kernel for any channel count (C % 4 == 0): D quads per loop trip,
+// the Ker slice zero-padded to whole trips and copied to LDS up front; two
+// phases of NB1 and NB2 pixel blocks.
+template <int NB1, int NB2, int D>
+__global__ void __launch_bounds__(kThreads)
+conv1x1_stream_loop_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
+                           float* __restrict__ Out, const Geom g) {
+  static_assert(NB1 > 0 && D % 2 == 0, "phase one is not empty; the A double buffer alternates");
+  extern __shared__ __align__(16) float lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int j = lane & 15, gq = lane >> 4;
+  const int C = g.C, K = g.K;
+  const int HW = g.W;
+  const int total_px = g.N * HW;
+  const int kt = blockIdx.x % g.tiles_k;
+  const int pg = blockIdx.x / g.tiles_k;
+  const int k0 = kt * 64;
+  const int wpx = g.tw;
+  const int px_begin = (pg * 4 + wave) * wpx;
+  const int px_end = min(px_begin + wpx, total_px);
+  const int nq = C / 4;
+  const int nq_pad = (nq + D - 1) / D * D;
+  const int cpad = nq_pad * 4, pitch = cpad + 1;
+
+  // Ker slice -> LDS rows [k][c]: batches of coalesced loads, all in flight
+  // before any is waited on.
+  {
+    constexpr int FB = 16;
+    for (int e0 = 0; e0 < 64 * cpad; e0 += kThreads * FB) {
+      float kv[FB];
+#pragma unroll
+      for (int i = 0; i < FB; ++i) {
+        const int e = e0 + tid + i * kThreads;
+        const int kl = e / cpad, c = e - kl * cpad;
+        const int k = k0 + kl;
+        kv[i] = (e < 64 * cpad && k < K && c < C) ? Ker[(size_t)k * C + c] : 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < FB; ++i) {
+        const int e = e0 + tid + i * kThreads;
+        const int kl = e / cpad, c = e - kl * cpad;
+        if (e < 64 * cpad) lds[kl * pitch + c] = kv[i];
+      }
+    }
+  }
+  __syncthreads();
+  __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(In), (short)0, (int)g.in_bytes, 0x00020000);
+  const unsigned qstride = 16u * (unsigned)HW;
+
+  auto phase = [&](auto nb_const, int blk0) {
     constexpr int NB = decltype(nb_const)::value;
     if constexpr (NB > 0) {
       unsigned voff[NB];
@@ -801,9 +986,8 @@ conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ke
 #pragma unroll
         for (int b = 0; b < NB; ++b) acc[kb][b] = v4f{0.f, 0.f, 0.f, 0.f};
       float ring[D][NB];
-      // Offsets: masked pixels start at 2^31; quads past the channel range
-      // add 2^30 (wave-uniform).  With In below 1 GB both land past the
-      // buffer's range without wrapping, so every load is unconditional.
+      // quads past the channel range add 2^30 (wave-uniform): with In below
+      // 1 GB both sentinels land past the buffer's range without wrapping
       auto load = [&](int q, int slot) {
         const unsigned qoff = (unsigned)q * qstride + (q < nq ? 0u : 0x40000000u);
 #pragma unroll
@@ -812,51 +996,27 @@ conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ke
       };
 #pragma unroll
       for (int d = 0; d < D; ++d) load(d, d);
-      if constexpr (decltype(first_const)::value) ker_ready();
-      // A operands (Ker[k0 + kb*16 + j][4q + gq], kb = 0..3) are read one
-      // quad ahead so the LDS latency hides behind the current quad's MFMAs.
       const float* arow = lds + j * pitch + gq;
       float a[2][4];
       auto read_a = [&](int q, float* dst) {
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) dst[kb] = arow[kb * 16 * pitch + 4 * q];
       };
-      auto step = [&](int q, int d) {
-        const float* ac = a[q & 1];
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int b = 0; b < NB; ++b)
-            acc[kb][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(ac[kb], ring[d][b], acc[kb][b], 0, 0, 0);
-      };
       read_a(0, a[0]);
-      if constexpr (NQ > 0) {
-        constexpr int NQP = (NQ + D - 1) / D * D;
+      for (int q0 = 0; q0 < nq_pad; q0 += D) {
 #pragma unroll
-        for (int q = 0; q < NQP; ++q) {
-          if (q + 1 < NQP) read_a(q + 1, a[(q + 1) & 1]);
-          __builtin_amdgcn_sched_barrier(0);  // issue the A reads first
-          step(q, q % D);
-          if (q + D < NQP) load(q + D, q % D);
-          // keep each refill right behind the MFMAs that free its slot: left
-          // alone, the scheduler sinks loads towards their uses and the ring
-          // degenerates to a few loads in flight
+        for (int d = 0; d < D; ++d) {
+          read_a(min(q0 + d + 1, nq_pad - 1), a[(d + 1) & 1]);  // the last one is unused
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+              acc[kb][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[d & 1][kb], ring[d][b], acc[kb][b], 0, 0, 0);
+          load(q0 + d + D, d);  // past the last quad this reads zeros
           __builtin_amdgcn_sched_barrier(0);
         }
-      } else {
-        static_assert(D % 2 == 0, "the A double buffer alternates within a ring group");
-        for (int q0 = 0; q0 < nq_pad; q0 += D) {
-#pragma unroll
-          for (int d = 0; d < D; ++d) {
-            read_a(min(q0 + d + 1, nq_pad - 1), a[(d + 1) & 1]);  // last one unused
-            __builtin_amdgcn_sched_barrier(0);
-            step(q0 + d, d);
-            load(q0 + d + D, d);  // past the last quad this reads zeros
-            __builtin_amdgcn_sched_barrier(0);
-          }
-        }
       }
-      // lane (j, gq) holds Out[k0 + kb*16 + 4*gq + v][pixel px_begin + (blk0+b)*16 + j]
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
         const int px = px_begin + (blk0 + b) * 16 + j;
@@ -874,9 +1034,8 @@ conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ke
       }
     }
   };
-  static_assert(NB1 > 0, "the first phase makes the Ker slice ready");
-  phase(std::integral_constant<int, NB1>{}, 0, std::true_type{});
-  phase(std::integral_constant<int, NB2>{}, NB1, std::false_type{});
+  phase(std::integral_constant<int, NB1>{}, 0);
+  phase(std::integral_constant<int, NB2>{}, NB1);
 }
 
 typedef void (*KernelF32)(const float*, const float*, float*, const Geom);
@@ -898,10 +1057,15 @@ struct Instance {
                    NS},                                                                          \
            &conv_f32_dma_kernel<WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK>, nullptr}
 
-#define F32_STREAM1X1(ID, NB1, NB2, D, NQ)                                                   \
-  Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STREAM1X1, 4, NB1 + NB2, 4 * NQ, 1, 1, NB1, NB2, 1, \
-                   1, kThreads, D},                                                            \
-           &conv1x1_stream_kernel<NB1, NB2, D, NQ>, nullptr}
+#define F32_STREAM1X1(ID, NB32, NS16, D, NQ)                                               \
+  Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STREAM1X1, 4, 2 * NB32 + NS16, 4 * NQ, 1, 1, NB32, \
+                   NS16, 1, 1, kThreads, D},                                                 \
+           &conv1x1_stream_kernel<NB32, NS16, D, NQ>, nullptr}
+
+#define F32_STREAM1X1_LOOP(ID, NB1, NB2, D)                                                  \
+  Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STREAM1X1_LOOP, 4, NB1 + NB2, 0, 1, 1, NB1, NB2, \
+                   1, 1, kThreads, D},                                                       \
+           &conv1x1_stream_loop_kernel<NB1, NB2, D>, nullptr}
 
 #define BF16_INST(ID, WK, WP, RC, SC, MAXIT)                                                  \
   Instance{Variant{ID, CONV_DTYPE_BF16, FAMILY_BF16, WK, WP, 32, RC, SC, MAXIT, 0, 8, 8, kThreads, \
@@ -910,21 +1074,21 @@ struct Instance {
 
 const Instance kInstances[] = {
     // ---- pointwise streaming (Ker resident in LDS, In straight to registers)
-    // (tile_c = 4 * NQ: the channel count of the unrolled instances; 0 = any)
-    F32_STREAM1X1(301, 4, 3, 8, 64),
-    F32_STREAM1X1(302, 4, 4, 8, 64),
-    F32_STREAM1X1(303, 3, 3, 8, 64),
-    F32_STREAM1X1(304, 4, 0, 8, 64),
-    F32_STREAM1X1(308, 7, 0, 4, 64),
-    F32_STREAM1X1(309, 7, 0, 8, 64),
-    F32_STREAM1X1(310, 8, 0, 4, 64),
-    F32_STREAM1X1(305, 4, 3, 8, 32),
-    F32_STREAM1X1(306, 4, 3, 8, 128),
-    F32_STREAM1X1(307, 4, 3, 8, 16),
-    F32_STREAM1X1(311, 4, 3, 8, 0),
-    F32_STREAM1X1(312, 4, 0, 8, 0),
-    F32_STREAM1X1(313, 2, 2, 8, 0),
-    F32_STREAM1X1(314, 2, 0, 8, 0),
+    // unrolled for C = 4 * NQ: (32-pixel blocks, 16-pixel blocks, ring depth in quads)
+    F32_STREAM1X1(301, 3, 1, 6, 64),
+    F32_STREAM1X1(302, 3, 1, 4, 64),
+    F32_STREAM1X1(303, 4, 0, 5, 64),
+    F32_STREAM1X1(304, 3, 0, 8, 64),
+    F32_STREAM1X1(305, 2, 0, 12, 64),
+    F32_STREAM1X1(306, 2, 1, 8, 64),
+    F32_STREAM1X1(307, 3, 1, 6, 16),
+    F32_STREAM1X1(308, 3, 1, 6, 32),
+    F32_STREAM1X1(309, 3, 1, 6, 128),
+    // any C % 4 == 0: (phase-1 blocks, phase-2 blocks, quads per trip)
+    F32_STREAM1X1_LOOP(311, 4, 3, 8),
+    F32_STREAM1X1_LOOP(312, 4, 0, 8),
+    F32_STREAM1X1_LOOP(313, 2, 2, 8),
+    F32_STREAM1X1_LOOP(314, 2, 0, 8),
     // ---- direct-to-LDS pipeline
     // 3x3 taps
     F32_DMA(101, 1, 13, 4, 8, 3, 3, 3, 9, 1, 5, 4),
@@ -1015,7 +1179,8 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
   if (!inst) return CONV_EINVAL;
   int lds_bytes;
   if (v.family == FAMILY_DMA) lds_bytes = v.stages * g.stage_elems * (int)sizeof(float);
-  else if (v.family == FAMILY_BF16 || v.family == FAMILY_STREAM1X1) lds_bytes = g.stage_elems;  // bytes
+  else if (v.family == FAMILY_BF16 || v.family == FAMILY_STREAM1X1 || v.family == FAMILY_STREAM1X1_LOOP)
+    lds_bytes = g.stage_elems;  // bytes
   else lds_bytes = 2 * (g.lds_in_elems + g.lds_ker_elems) * (int)sizeof(float);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   if (v.family != FAMILY_BF16 && v.ker_vec > 1 &&

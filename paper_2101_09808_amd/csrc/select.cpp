@@ -217,24 +217,26 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
                   int* lds_bytes) {
   const Shape s = kernel_view(s0);
   if (plan.dtype != v.dtype) return false;
-  if (v.family == FAMILY_STREAM1X1) {
+  if (v.family == FAMILY_STREAM1X1 || v.family == FAMILY_STREAM1X1_LOOP) {
     // Pointwise streaming: tile_cols = pixels per wave, 4 waves per workgroup,
     // 64 output channels per workgroup, the whole channel range resident.
     if (s0.R != 1 || s0.S != 1) return false;
     if (plan.tile_k != 64 || plan.waves_k != 1 || plan.waves_px != 4 || plan.tile_rows != 1) return false;
     if (plan.wave_k != 64 || plan.wave_px != 16 * v.wp || plan.tile_c != v.tc) return false;
-    const int nb = v.max_ni + v.max_nk;
+    if (s.C % 4) return false;  // whole channel quads
+    const bool unrolled = v.family == FAMILY_STREAM1X1;
+    if (unrolled && v.tc != s.C) return false;  // compiled for this channel count
     const int wpx = plan.tile_cols;
-    if (wpx < 1 || wpx > 16 * nb) return false;
+    if (wpx < 1 || wpx > 16 * v.wp) return false;
     const int64_t total_px = (int64_t)s.N * s.W;
     const int64_t groups = cdiv(total_px, 4 * (int64_t)wpx);
     const int64_t tiles_k = cdiv(s.K, 64);
-    const int64_t nq_pad = cdiv(cdiv(s.C, 4), v.stages) * v.stages;  // stages = ring depth
-    const int64_t bytes = (nq_pad * 4 + 1) * 64 * 4;  // Ker rows [k][c] + 1 pad
+    // stored channels: exactly C (unrolled), or C padded to whole loop trips
+    const int64_t cst = unrolled ? s.C : cdiv(s.C / 4, v.stages) * v.stages * 4;
+    const int64_t bytes = (cst + 1) * 64 * 4;  // Ker rows [k][c] + 1 pad
     if (bytes > kHw.lds_bytes || groups * tiles_k >= (int64_t(1) << 31)) return false;
     if ((int64_t)s.N * s.C * s.W * 4 >= (int64_t(1) << 30)) return false;  // 32-bit byte offsets
-    if (s.C % 4) return false;  // whole channel quads
-    if (v.tc && v.tc != s.C) return false;  // unrolled instance for this channel count
+    if ((int64_t)s.K * s.C * 4 >= (int64_t(1) << 31)) return false;        // below the Ker sentinel
     Geom q;
     std::memset(&q, 0, sizeof(q));
     q.N = s.N; q.C = s.C; q.K = s.K; q.H = s.H; q.W = s.W; q.R = 1; q.S = 1;
@@ -378,17 +380,21 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
   if (!resolve_geom(s0, *v, *plan, &g, &lds)) return CONV_EINVAL;
   const Shape s = kernel_view(s0);
   const double e = (plan->dtype == CONV_DTYPE_BF16) ? 2.0 : 4.0;
-  if (v->family == FAMILY_STREAM1X1) {
+  if (v->family == FAMILY_STREAM1X1 || v->family == FAMILY_STREAM1X1_LOOP) {
     // In moves HBM -> VGPR once; Ker slices are staged into LDS once per
-    // workgroup; A operands are four 4 B LDS reads per lane per channel quad and phase.
+    // workgroup; A operands are 4 B LDS reads.
     plan->lds_bytes = lds;
     plan->num_wg = g.grid;
     const double in_b = (double)s.N * s.C * s.W * 4.0, ker_b = (double)s.K * s.C * 4.0;
     const double out_b = (double)s.N * s.K * s.W * 4.0;
     const double waves = (double)g.grid * 4;
     const double nq = std::ceil(s.C / 4.0);
-    const double phases = v->max_nk > 0 ? 2.0 : 1.0;  // each phase re-reads the A operands
-    plan->pred_bytes[CONV_LVL_REG] = waves * phases * nq * 64 * 16.0;
+    // A operands per lane and channel quad: 16 B per pass over the channels
+    // (the looped kernel makes one pass per phase); the unrolled kernel reads
+    // another 16 B for its 16-pixel block
+    const double a_bytes = v->family == FAMILY_STREAM1X1 ? 16.0 * (1 + v->max_nk)
+                                                         : 16.0 * (v->max_nk > 0 ? 2 : 1);
+    plan->pred_bytes[CONV_LVL_REG] = waves * nq * 64 * a_bytes;
     plan->pred_bytes[CONV_LVL_LDS] = (double)g.grid * s.C * 64 * 4.0;
     plan->pred_bytes[CONV_LVL_L2] = in_b * g.tiles_k + ker_b * std::min<double>(g.tiles_rows, kHw.xcds);
     plan->pred_bytes[CONV_LVL_HBM] = in_b + ker_b + out_b;
@@ -401,7 +407,7 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
       plan->pred_us[l] = plan->pred_bytes[l] / kHw.bw[l] * 1e6;
       tmax = std::max(tmax, plan->pred_us[l]);
     }
-    const double nb = v->max_ni + v->max_nk;
+    const double nb = v->wp;
     const double rounds = std::ceil((double)g.grid / kHw.cus);
     plan->pred_mfma_us = rounds * nb * 4 * nq * kHw.mfma_f32_cycles / kHw.clock_hz * 1e6;
     plan->pred_total_us = std::max(tmax, plan->pred_mfma_us);
@@ -501,10 +507,18 @@ void fill_plan_fields(conv_plan_t* p, const Variant& v, int nwk, int nwp, int tr
 // Deterministic preference among plans (tie-breaks: predicted time, total
 // predicted bytes, fewer workgroups, variant id, larger k tile).
 bool better(const conv_plan_t& a, const conv_plan_t& b) {
-  // The direct-to-LDS pipeline keeps several steps of loads in flight; the
-  // register-staged family is the fallback for shapes it cannot take.
+  // Family preference (measured, not modelled: the model does not capture
+  // latency hiding): the unrolled pointwise streaming kernel, then the
+  // direct-to-LDS pipeline (or the bf16 kernel), then the looped streaming
+  // kernel, then the register-staged fallback for shapes no other takes.
   auto rank = [](int fam) {
-    return fam == FAMILY_STREAM1X1 ? 0 : fam == FAMILY_DMA ? 1 : fam == FAMILY_BF16 ? 1 : 2;
+    switch (fam) {
+      case FAMILY_STREAM1X1: return 0;
+      case FAMILY_DMA:
+      case FAMILY_BF16: return 1;
+      case FAMILY_STREAM1X1_LOOP: return 2;
+      default: return 3;
+    }
   };
   const int fa = rank(find_variant(a.variant)->family), fb = rank(find_variant(b.variant)->family);
   if (fa != fb) return fa < fb;
@@ -534,10 +548,10 @@ int enumerate_plans(const Shape& s0, int dtype, conv_plan_t* plans, int cap) {
     const Variant& v = vs[vi];
     if (v.dtype != dtype) continue;
     if (v.rc && (s.R != v.rc || s.S != v.sc)) continue;
-    if (v.family == FAMILY_STREAM1X1) {
+    if (v.family == FAMILY_STREAM1X1 || v.family == FAMILY_STREAM1X1_LOOP) {
       // pixels per wave so that the workgroup count lands near a multiple
       // of the CU count; the instance's block count must match
-      const int nb = v.max_ni + v.max_nk;
+      const int nb = v.wp;
       const int64_t total_px = (int64_t)s.N * s.W;
       std::vector<int> wpxs;
       for (int64_t G = 1; G <= 4096; ++G) {

@@ -57,7 +57,7 @@ def emulate(g, In, Ker, wgs=None):
     In, Ker: flat float64 arrays of the problem (the kernel view, identical
     memory).  Returns (out_flat, written) where written counts stores per
     output element (NaN outputs where nothing was stored)."""
-    if g["family"] == 4:
+    if g["family"] in (4, 5):
         return emulate_stream1x1(g, In, Ker, wgs)
     N, C, K, H, W, R, S, P, Q = (g[x] for x in "N C K H W R S P Q".split())
     WK, WP, TC, KV, NT = g["wk"], g["wp"], g["tc"], g["ker_vec"], g["threads"]
@@ -435,75 +435,149 @@ def emulate_bf16(g, In, Ker, wgs=None, in_aligned=True):
 # Pointwise streaming family (conv1x1_stream_kernel).
 
 def emulate_stream1x1(g, In, Ker, wgs=None):
-    """The pointwise streaming kernel: Ker rows [k][c] in LDS (pitch = padded
-    channel count + 1), In B operands from raw buffer loads whose 32-bit byte
-    offsets are emulated exactly (offsets at or past the buffer size read 0)."""
+    """The pointwise streaming kernels.
+
+    Family 4 (unrolled for C = tc): per wave max_ni blocks of 32 pixels on
+    32x32x2 MFMAs (two 32-row k blocks, channel pairs) and max_nk (0/1) blocks
+    of 16 pixels on 16x16x4 MFMAs; Ker rows copied to LDS in 64-channel
+    chunks.  Family 5 (looped over trips of `stages` quads): max_ni then
+    max_nk blocks of 16 pixels, Ker zero-padded to whole trips.  Ker rows
+    [k][c] in LDS with a pitch of the stored channel count + 1; In operands
+    from raw buffer loads whose 32-bit byte offsets are emulated exactly
+    (offsets at or past the buffer size read 0)."""
     N, C, K, H, W = (g[x] for x in "N C K H W".split())
-    _chk(g["family"] == 4 and g["threads"] == 256 and g["R"] == 1 and g["S"] == 1, "stream geometry")
+    fam = g["family"]
+    _chk(fam in (4, 5) and g["threads"] == 256 and g["R"] == 1 and g["S"] == 1, "stream geometry")
     HW = W  # kernel view: one row per image
     _chk(H == 1, "kernel view of a pointwise layer")
     _chk(C % 4 == 0, "whole channel quads")
-    NB1, NB2, D = g["max_ni"], g["max_nk"], g["stages"]
-    _chk(g["tc"] in (0, C), "unrolled instance for another channel count")
-    wpx = g["tw"]
-    _chk(1 <= wpx <= 16 * (NB1 + NB2), "pixels per wave")
+    D = g["stages"]
     nq = C // 4
-    nq_pad = -(-nq // D) * D
-    cpad, pitch = 4 * nq_pad, 4 * nq_pad + 1
+    if fam == 4:
+        _chk(g["tc"] == C and nq % 16 == 0, "unrolled instance for this channel count")
+        NB32, NS16 = g["max_ni"], g["max_nk"]
+        _chk(NS16 in (0, 1), "at most one 16-pixel block")
+        NB = 2 * NB32 + NS16
+        nq_run, cst = nq, C
+    else:
+        _chk(g["tc"] == 0, "looped instance")
+        NB1, NB2 = g["max_ni"], g["max_nk"]
+        NB = NB1 + NB2
+        nq_run = -(-nq // D) * D
+        cst = 4 * nq_run
+    _chk(g["wp"] == NB, "pixel blocks per wave")
+    pitch = cst + 1
+    wpx = g["tw"]
+    _chk(1 <= wpx <= 16 * NB, "pixels per wave")
     _chk(g["stage_elems"] == 64 * pitch * 4 == g["lds_bytes"] and g["lds_bytes"] <= 160 * 1024, "LDS bytes")
     total_px = N * HW
     in_size, ker_size, out_size = N * C * HW, K * C, N * K * HW
     _chk(In.size == in_size and Ker.size == ker_size, "input sizes")
     _chk(g["in_bytes"] == in_size * 4 and in_size * 4 < 2 ** 30, "In byte range below 1 GB")
+    _chk(g["ker_bytes"] == ker_size * 4 and ker_size * 4 < 2 ** 31, "Ker byte range below the sentinel")
     out = np.full(out_size, np.nan)
     written = np.zeros(out_size, np.int64)
     lane = np.arange(64)
-    j, gq = lane & 15, lane >> 4
     KOOB, QOOB, M32 = 0x80000000, 0x40000000, 0xFFFFFFFF
+
+    def in_load(voff, byte_add, expect):
+        off = (voff + byte_add) & M32
+        hit = off < g["in_bytes"]
+        _chk((off[hit] % 4 == 0).all(), "misaligned In offset")
+        # the range check must drop exactly the masked lanes (and padded quads)
+        _chk((hit == expect).all(), "range check does not match the mask")
+        return np.where(hit, In[np.where(hit, off // 4, 0)], 0.0)
+
+    def lds_read(lds, idx):
+        _chk((idx >= 0).all() and (idx < lds.size).all(), "LDS Ker read out of range")
+        v = lds[idx]
+        _chk(not np.isnan(v).any(), "LDS Ker read of an unwritten element")
+        return v
+
+    def store(acc_rows, k, px, valid):
+        n, hw = px // HW, px % HW
+        st = valid & (k < K)
+        dst = (n * K + k) * HW + hw
+        _chk((dst[st] >= 0).all() and (dst[st] < out_size).all(), "Out store range")
+        out[dst[st]] = acc_rows[st]
+        np.add.at(written, dst[st], 1)
+
+    def block16(lds, k0, px_begin, px_end, blk_px0, quads):
+        """One 16-pixel block on 16x16x4 MFMAs (lane (j, gq))."""
+        j, gq = lane & 15, lane >> 4
+        px = blk_px0 + j
+        valid = px < px_end
+        n, hw = px // HW, px % HW
+        voff = np.where(valid, ((n * C + gq) * HW + hw) * 4, KOOB)
+        acc = np.zeros((4, 16, 16))
+        for q in range(quads):
+            bv = in_load(voff, q * 16 * HW + (0 if q < nq else QOOB), valid & (q < nq))
+            for kb in range(4):
+                av = lds_read(lds, (kb * 16 + j) * pitch + 4 * q + gq)
+                Am = np.zeros((16, 4))
+                Am[j, gq] = av
+                Bm = np.zeros((4, 16))
+                Bm[gq, j] = bv
+                acc[kb] += Am @ Bm
+        for kb in range(4):
+            for v in range(4):
+                store(acc[kb][4 * gq + v, j], k0 + kb * 16 + 4 * gq + v, px, valid)
+
+    def block32(lds, k0, px_end, blk_px0):
+        """One 32-pixel block on 32x32x2 MFMAs (lane (l32, h32))."""
+        l32, h32 = lane & 31, lane >> 5
+        px = blk_px0 + l32
+        valid = px < px_end
+        n, hw = px // HW, px % HW
+        voff = np.where(valid, ((n * C + h32) * HW + hw) * 4, KOOB)
+        acc = np.zeros((2, 32, 32))
+        for q in range(nq):
+            for e in range(2):
+                bv = in_load(voff, (4 * q + 2 * e) * 4 * HW, valid)
+                for kb in range(2):
+                    av = lds_read(lds, (kb * 32 + l32) * pitch + 4 * q + 2 * e + h32)
+                    Am = np.zeros((32, 2))
+                    Am[l32, h32] = av
+                    Bm = np.zeros((2, 32))
+                    Bm[h32, l32] = bv
+                    acc[kb] += Am @ Bm
+        for kb in range(2):
+            for v in range(16):
+                i = 8 * (v // 4) + 4 * h32 + v % 4
+                store(acc[kb][i, l32], k0 + 32 * kb + i, px, valid)
+
     for b in (range(g["grid"]) if wgs is None else wgs):
         kt, pg = b % g["tiles_k"], b // g["tiles_k"]
         k0 = kt * 64
         lds = np.full(64 * pitch, np.nan)  # the pad column is never read
-        for e in range(64 * cpad):
-            kl, c = divmod(e, cpad)
-            k = k0 + kl
-            _chk(kl * pitch + c < lds.size, "LDS Ker write out of range")
-            lds[kl * pitch + c] = Ker[k * C + c] if (k < K and c < C) else 0.0
+        if fam == 4:
+            # wave w copies rows 16w..16w+15, 64 channels per load: LDS
+            # destination M0 + 4 * lane, source offset or the sentinel
+            for w in range(4):
+                for ch in range(C // 64):
+                    for i in range(16):
+                        kl = w * 16 + i
+                        k = k0 + kl
+                        dst = kl * pitch + ch * 64 + lane
+                        _chk(dst.max() < lds.size, "LDS Ker chunk out of range")
+                        off = (k * C + ch * 64 + lane) * 4 if k < K else np.full(64, KOOB)
+                        hit = off < g["ker_bytes"]
+                        _chk(hit.all() == (k < K), "Ker range check does not match the row mask")
+                        lds[dst] = np.where(hit, Ker[np.where(hit, off // 4, 0)], 0.0)
+        else:
+            for e in range(64 * cst):
+                kl, c = divmod(e, cst)
+                k = k0 + kl
+                lds[kl * pitch + c] = Ker[k * C + c] if (k < K and c < C) else 0.0
         for wave in range(4):
             px_begin = (pg * 4 + wave) * wpx
             px_end = min(px_begin + wpx, total_px)
-            for blk0, nb in ((0, NB1), (NB1, NB2)):
-                for bb in range(nb):
-                    px = px_begin + (blk0 + bb) * 16 + j
-                    valid = px < px_end
-                    n, hw = px // HW, px % HW
-                    voff = np.where(valid, ((n * C + gq) * HW + hw) * 4, KOOB)
-                    acc = np.zeros((4, 16, 16))
-                    for q in range(nq_pad):
-                        qoff = q * 16 * HW + (0 if q < nq else QOOB)
-                        off = (voff + qoff) & M32
-                        hit = off < g["in_bytes"]
-                        _chk((off[hit] % 4 == 0).all(), "misaligned In offset")
-                        bv = np.where(hit, In[np.where(hit, off // 4, 0)], 0.0)
-                        # the range check must drop exactly the masked lanes
-                        # and the padded quads
-                        _chk((hit == (valid & (q < nq))).all(), "range check does not match the mask")
-                        ai = (np.arange(4)[:, None] * 16 + j[None, :]) * pitch + 4 * q + gq[None, :]
-                        _chk((ai < lds.size).all(), "LDS Ker read out of range")
-                        av = lds[ai]
-                        _chk(not np.isnan(av).any(), "LDS Ker read of an unwritten element")
-                        for kb in range(4):
-                            Am = np.zeros((16, 4))
-                            Am[j, gq] = av[kb]
-                            Bm = np.zeros((4, 16))
-                            Bm[gq, j] = bv
-                            acc[kb] += Am @ Bm
-                    for kb in range(4):
-                        for v in range(4):
-                            k = k0 + kb * 16 + 4 * gq + v
-                            st = valid & (k < K)
-                            dst = (n * K + k) * HW + hw
-                            _chk((dst[st] >= 0).all() and (dst[st] < out_size).all(), "Out store range")
-                            out[dst[st]] = acc[kb][4 * gq + v, j][st]
-                            np.add.at(written, dst[st], 1)
+            if fam == 4:
+                for bb in range(NB32):
+                    block32(lds, k0, px_end, px_begin + 32 * bb)
+                if NS16:
+                    block16(lds, k0, px_begin, px_end, px_begin + 32 * NB32, nq)
+            else:
+                for bb in range(NB):
+                    block16(lds, k0, px_begin, px_end, px_begin + 16 * bb, nq_run)
     return out, written

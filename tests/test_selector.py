@@ -87,9 +87,10 @@ def test_plan_invariants(shape):
     assert B.conv_fwd_plan(*dims, dtype=dtype) == plan
     cands = B.conv_fwd_candidates(*dims, dtype=dtype)
     assert cands[0] == plan
-    # families in the library's order of preference (pointwise streaming,
-    # then direct-to-LDS / bf16, then register-staged), each by predicted time
-    rank = {4: 0, 2: 1, 3: 1, 1: 2}
+    # families in the library's order of preference (unrolled pointwise
+    # streaming, then direct-to-LDS / bf16, then looped streaming, then
+    # register-staged), each by predicted time
+    rank = {4: 0, 2: 1, 3: 1, 5: 2, 1: 3}
     fam = [B.conv_fwd_geometry(*dims, c)["family"] for c in cands]
     assert fam == sorted(fam, key=lambda f: rank[f])
     for f in set(fam):
