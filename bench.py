@@ -3,6 +3,8 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-layers] [--no-cpu]
     python bench.py --traffic-run              (under rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE)
     python bench.py --traffic-parse FETCH_DIR WRITE_DIR
+    python bench.py --traffic-run --layer all  (under rocprofv3 --pmc, one counter per run)
+    python bench.py --model-check FETCH_DIR WRITE_DIR TCP_TCC_DIR LDS_DIR
 
 A step is one conv_fwd call (tile selection is cached, so the step is the
 kernel launch) on the pointwise layer N=32 C=256 K=64 56x56 1x1 fp32.  Inputs
@@ -96,6 +98,11 @@ def time_layer(c, steps, warmup):
 
 COPY_BYTES = 256 * 2 ** 20  # plain device-to-device copy used to scale the HBM byte counters
 COPY_REPS = 3
+MODEL_CHECK_COMMANDS = [
+    f"rocprofv3 --pmc {cnt} --output-format csv -d gpurun_out/model_check_{i} -o m -- python -u bench.py --traffic-run --layer all"
+    for i, cnt in enumerate(["FETCH_SIZE", "WRITE_SIZE", "TCP_TCC_READ_REQ_sum", "SQ_INSTS_LDS"])
+] + ["python bench.py --model-check gpurun_out/model_check_0 gpurun_out/model_check_1 "
+     "gpurun_out/model_check_2 gpurun_out/model_check_3"]
 TRAFFIC_COMMANDS = [
     "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/traffic_fetch -o f -- python -u bench.py --traffic-run",
     "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/traffic_write -o w -- python -u bench.py --traffic-run",
@@ -103,11 +110,12 @@ TRAFFIC_COMMANDS = [
 ]
 
 
-def traffic_run(c, launches=6):
-    """Workload for the two rocprofv3 --pmc passes (FETCH_SIZE, then WRITE_SIZE):
-    COPY_REPS plain copies of COPY_BYTES, then `launches` conv launches of the
-    timed plan on rotating buffer sets.  Inputs are generated on the device so
-    that no other copy kernel runs in this process."""
+def traffic_run(layers, launches=6):
+    """Workload for the rocprofv3 --pmc counter passes (one counter set per
+    run): COPY_REPS plain copies of COPY_BYTES, then `launches` launches of
+    each layer's selected plan on rotating buffer sets, layer after layer.
+    Inputs are generated on the device so that no other copy kernel runs in
+    this process."""
     import torch
     from paper_2101_09808_amd import conv as B
 
@@ -118,65 +126,168 @@ def traffic_run(c, launches=6):
         dst.copy_(src)
     torch.cuda.synchronize()
     del src, dst
-    bf16 = c.dtype == "bf16"
-    edt = torch.bfloat16 if bf16 else torch.float32
-    set_bytes = c.N * c.C * c.H * c.W * (2 if bf16 else 4) + c.N * c.K * c.P * c.Q * 4
-    nsets = max(2, -(-2 * MALL_BYTES // set_bytes) + 1)
-    ins = [torch.empty(c.N, c.C, c.H, c.W, device=dev).uniform_(-1, 1).to(edt) for _ in range(nsets)]
-    Ker = torch.empty(c.K, c.C, c.R, c.S, device=dev).uniform_(-1, 1).to(edt)
-    outs = [torch.empty(c.N, c.K, c.P, c.Q, device=dev) for _ in range(nsets)]
-    torch.cuda.synchronize()
-    sp = torch.cuda.current_stream().cuda_stream
-    for i in range(launches):
-        st = B.conv_fwd_ptr(*c.key(), ins[i % nsets].data_ptr(), Ker.data_ptr(), outs[i % nsets].data_ptr(), sp, bf16)
-        if st != B.CONV_OK:
-            raise B.ConvError(st, "conv_fwd")
-    torch.cuda.synchronize()
-    print(f"traffic run: {COPY_REPS} copies of {COPY_BYTES} B, {launches} launches of {c.name}", flush=True)
+    for c in layers:
+        bf16 = c.dtype == "bf16"
+        edt = torch.bfloat16 if bf16 else torch.float32
+        set_bytes = c.N * c.C * c.H * c.W * (2 if bf16 else 4) + c.N * c.K * c.P * c.Q * 4
+        nsets = max(2, -(-2 * MALL_BYTES // set_bytes) + 1)
+        ins = [torch.empty(c.N, c.C, c.H, c.W, device=dev).uniform_(-1, 1).to(edt) for _ in range(nsets)]
+        Ker = torch.empty(c.K, c.C, c.R, c.S, device=dev).uniform_(-1, 1).to(edt)
+        outs = [torch.empty(c.N, c.K, c.P, c.Q, device=dev) for _ in range(nsets)]
+        torch.cuda.synchronize()
+        sp = torch.cuda.current_stream().cuda_stream
+        for i in range(launches):
+            st = B.conv_fwd_ptr(*c.key(), ins[i % nsets].data_ptr(), Ker.data_ptr(), outs[i % nsets].data_ptr(),
+                                sp, bf16)
+            if st != B.CONV_OK:
+                raise B.ConvError(st, "conv_fwd")
+        torch.cuda.synchronize()
+        del ins, outs, Ker
+        print(f"traffic run: {launches} launches of {c.name}", flush=True)
+    print(f"traffic run: {COPY_REPS} copies of {COPY_BYTES} B first", flush=True)
 
 
-def traffic_parse(c, fetch_dir, write_dir, out_path):
-    """Scale the per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the conv kernel by
-    what the same counters read for the plain copy, and store the result."""
+def counter_per_dispatch(d, counter):
+    """[(kernel name, counter value summed over instances)] in dispatch order
+    from the counter_collection.csv of one rocprofv3 --pmc run."""
     import csv
     import glob
 
+    f = sorted(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True))
+    if not f:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    vals = {}
+    for r in csv.DictReader(open(f[0])):
+        if r["Counter_Name"] != counter:
+            continue
+        k = int(r["Dispatch_Id"])
+        name, v = vals.get(k, (r["Kernel_Name"], 0.0))
+        vals[k] = (name, v + float(r["Counter_Value"]))
+    return [vals[k] for k in sorted(vals)]
+
+
+def calibrated(d, counter, unit_bytes, layers, launches):
+    """Per layer: bytes per launch implied by `counter` (in units of
+    `unit_bytes`), scaled by copy bytes / what the counter reads for the
+    plain copies.  The first launch of each layer (which also faults in the
+    buffers) is left out."""
+    rows = counter_per_dispatch(d, counter)
+    conv = [v for n, v in rows if "convfwd::" in n]
+    # the calibration copies are the process's first copy kernels (later ones,
+    # e.g. dtype conversions of the inputs, are not of known size)
+    first_conv = next((i for i, (n, _) in enumerate(rows) if "convfwd::" in n), len(rows))
+    copy = [v for n, v in rows[:first_conv] if "copy" in n.lower()][:COPY_REPS]
+    if len(copy) != COPY_REPS or len(conv) != launches * len(layers):
+        raise SystemExit(f"{counter}: expected {COPY_REPS} copy and {launches * len(layers)} conv dispatches, "
+                         f"got {len(copy)} and {len(conv)}")
+    # counters a plain copy does not move (instruction counts) are not scaled
+    factor = COPY_BYTES * COPY_REPS / (sum(copy) * unit_bytes) if sum(copy) > 0 else 1.0
+    out = {}
+    for i, c in enumerate(layers):
+        mine = conv[i * launches + 1:(i + 1) * launches]
+        per = sum(mine) / len(mine)
+        out[c.name] = {"per_dispatch": per, "bytes_per_launch": per * unit_bytes * factor}
+    return factor, sum(copy) / len(copy), out
+
+
+def traffic_parse(c, fetch_dir, write_dir, out_path, launches=6):
+    """HBM bytes per launch of the timed layer from the FETCH_SIZE and
+    WRITE_SIZE runs (KiB per dispatch, scaled by the plain copy), stored with
+    a hash of the kernel sources."""
     from paper_2101_09808_amd import conv as B
 
-    def per_dispatch(d, counter):
-        f = sorted(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True))
-        if not f:
-            raise SystemExit(f"no counter_collection.csv under {d}")
-        vals = {}
-        for r in csv.DictReader(open(f[0])):
-            if r["Counter_Name"] != counter:
-                continue
-            k = int(r["Dispatch_Id"])
-            name, v = vals.get(k, (r["Kernel_Name"], 0.0))
-            vals[k] = (name, v + float(r["Counter_Value"]))
-        return [vals[k] for k in sorted(vals)]
-
     res = {}
-    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
-        rows = per_dispatch(d, counter)
-        conv = [v for n, v in rows if "convfwd::" in n]
-        copy = [v for n, v in rows if "convfwd::" not in n and "copy" in n.lower()]
-        if len(copy) != COPY_REPS or len(conv) < 2:
-            raise SystemExit(f"{counter}: expected {COPY_REPS} copy dispatches and >= 2 conv dispatches, "
-                             f"got {len(copy)} and {len(conv)}")
-        factor = COPY_BYTES * COPY_REPS / (sum(copy) * 1024.0)
-        conv = conv[1:]  # the first launch also faults in the buffers
-        res[counter] = {"kib_per_dispatch": sum(conv) / len(conv), "copy_kib_per_dispatch": sum(copy) / len(copy),
-                        "factor": factor, "bytes_per_launch": sum(conv) / len(conv) * 1024.0 * factor}
+    for key, counter, d in (("fetch", "FETCH_SIZE", fetch_dir), ("write", "WRITE_SIZE", write_dir)):
+        factor, copy_per, per_layer = calibrated(d, counter, 1024.0, [c], launches)
+        res[key] = {"kib_per_dispatch": per_layer[c.name]["per_dispatch"], "copy_kib_per_dispatch": copy_per,
+                    "factor": factor, "bytes_per_launch": per_layer[c.name]["bytes_per_launch"]}
     dtype_code = B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32
     plan = B.conv_fwd_plan(*c.key(), dtype=dtype_code)
     out = {"workload": c.name, "kernel_sha": kernel_source_hash(), "plan_variant": plan["variant"],
            "copy_bytes": COPY_BYTES, "copy_reps": COPY_REPS,
-           "fetch": res["FETCH_SIZE"], "write": res["WRITE_SIZE"],
-           "hbm_bytes_per_launch": res["FETCH_SIZE"]["bytes_per_launch"] + res["WRITE_SIZE"]["bytes_per_launch"],
+           "fetch": res["fetch"], "write": res["write"],
+           "hbm_bytes_per_launch": res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"],
            "alg_bytes_per_launch": alg_bytes(c), "commands": TRAFFIC_COMMANDS}
     with open(out_path, "w") as fh:
         json.dump(out, fh, indent=1)
+    print(json.dumps(out), flush=True)
+
+
+MODEL_CHECK_COUNTERS = [("FETCH_SIZE", 1024.0), ("WRITE_SIZE", 1024.0), ("TCP_TCC_READ_REQ_sum", 1.0),
+                        ("SQ_INSTS_LDS", 1.0)]
+MODEL_CHECK_FILE = os.path.join(ROOT, "profiles", "model_vs_counters")
+
+
+def model_check_parse(layers, dirs, launches=6):
+    """The selector's predicted bytes per level against counters, per layer
+    (one counter run per directory, in MODEL_CHECK_COUNTERS order).
+
+    * HBM level (compulsory In + Ker + Out): FETCH_SIZE + WRITE_SIZE, both
+      scaled by the plain copy.  MALL hits count as fetches, so this is the
+      traffic out of the L2s, an upper bound of the HBM traffic.
+    * L2 -> CU traffic: TCP_TCC_READ_REQ (L1 -> L2 read requests), scaled by
+      the copy's bytes per request.  Predicted: the LDS level of the model
+      (In and Ker tiles staged per workgroup), plus In itself for the
+      pointwise streaming kernels, whose In loads go to registers.
+    * Operand (REG) level: LDS instructions (SQ_INSTS_LDS, per wave), shown
+      beside the predicted operand bytes; the byte figure per instruction
+      depends on each kernel's read widths, so only the count is measured.
+    """
+    from paper_2101_09808_amd import conv as B
+
+    meas = {}
+    cal = {}
+    for (counter, unit), d in zip(MODEL_CHECK_COUNTERS, dirs):
+        factor, copy_per, per_layer = calibrated(d, counter, unit, layers, launches)
+        cal[counter] = {"factor": factor, "copy_per_dispatch": copy_per}
+        for name, v in per_layer.items():
+            meas.setdefault(name, {})[counter] = v
+    rows = []
+    for c in layers:
+        dtype_code = B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32
+        plan = B.conv_fwd_plan(*c.key(), dtype=dtype_code)
+        fam = B.conv_fwd_geometry(*c.key(), plan)["family"]
+        m = meas[c.name]
+        pb = plan["pred_bytes"]
+        e = 2 if c.dtype == "bf16" else 4
+        in_bytes = c.N * c.C * c.H * c.W * e
+        pred_l2cu = pb["lds"] + (in_bytes if fam in (4, 5) else 0)
+        out_bytes = c.N * c.K * c.P * c.Q * 4
+        hbm = m["FETCH_SIZE"]["bytes_per_launch"] + m["WRITE_SIZE"]["bytes_per_launch"]
+        l2cu = m["TCP_TCC_READ_REQ_sum"]["bytes_per_launch"]
+        rows.append({"workload": c.name, "plan_variant": plan["variant"], "family": fam,
+                     "hbm_pred": pb["hbm"], "hbm_meas": hbm, "hbm_ratio": hbm / pb["hbm"],
+                     "l2_pred": pb["l2"] + out_bytes, "l2_ratio": hbm / (pb["l2"] + out_bytes),
+                     "l2cu_pred": pred_l2cu, "l2cu_meas": l2cu, "l2cu_ratio": l2cu / pred_l2cu,
+                     "reg_pred_bytes": pb["reg"], "lds_instructions": m["SQ_INSTS_LDS"]["per_dispatch"],
+                     "fetch_bytes": m["FETCH_SIZE"]["bytes_per_launch"],
+                     "write_bytes": m["WRITE_SIZE"]["bytes_per_launch"]})
+    out = {"kernel_sha": kernel_source_hash(), "calibration": cal, "copy_bytes": COPY_BYTES,
+           "copy_reps": COPY_REPS, "launches_per_layer": launches, "layers": rows,
+           "commands": MODEL_CHECK_COMMANDS}
+    with open(MODEL_CHECK_FILE + ".json", "w") as fh:
+        json.dump(out, fh, indent=1)
+    lines = ["# Predicted vs measured bytes per level (selected plan of each layer)", "",
+             "Commands (MI355X, one GPU, from the repository root), one counter per run:", ""]
+    lines += ["    " + x for x in MODEL_CHECK_COMMANDS]
+    lines += ["", "Scale factors (plain 256 MiB copy: copy bytes / counter reading): " +
+              ", ".join(f"{k} {v['factor']:.4g}" for k, v in cal.items() if k != "SQ_INSTS_LDS"), "",
+              "| layer | variant | fabric meas MB | compulsory MB | ratio | L2 level + Out pred MB | ratio |"
+              " L2->CU pred MB | L2->CU meas MB | ratio | REG pred MB | LDS instr |",
+              "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| {r['workload']} | {r['plan_variant']} | {r['hbm_meas'] / 1e6:.2f} | {r['hbm_pred'] / 1e6:.2f} | "
+                     f"{r['hbm_ratio']:.3f} | {r['l2_pred'] / 1e6:.2f} | {r['l2_ratio']:.3f} | "
+                     f"{r['l2cu_pred'] / 1e6:.2f} | {r['l2cu_meas'] / 1e6:.2f} | "
+                     f"{r['l2cu_ratio']:.3f} | {r['reg_pred_bytes'] / 1e6:.1f} | {r['lds_instructions']:.4g} |")
+    lines += ["", "Fabric: FETCH_SIZE + WRITE_SIZE, the traffic between the XCDs' L2s and the fabric (MALL hits",
+              "count as fetches), against the compulsory In + Ker + Out (the model's HBM level) and against the",
+              "model's L2 level (per-XCD re-fetches of In and Ker) plus Out.  L2->CU: TCP_TCC_READ_REQ against",
+              "the model's LDS level (plus In for the pointwise streaming kernels, which load In into",
+              "registers).  REG: predicted operand bytes beside the measured LDS instruction count",
+              "(SQ_INSTS_LDS).", ""]
+    with open(MODEL_CHECK_FILE + ".md", "w") as fh:
+        fh.write("\n".join(lines))
     print(json.dumps(out), flush=True)
 
 
@@ -219,11 +330,15 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-layers", action="store_true", help="skip the per-layer table")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--layer", default=HEADLINE, help="workload of the timed step")
+    ap.add_argument("--layer", default=HEADLINE, help="workload of the timed step ('all': every layer, "
+                    "for --traffic-run)")
     ap.add_argument("--traffic-run", action="store_true",
                     help="plain copies + a few launches, for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs")
     ap.add_argument("--traffic-parse", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="turn the two counter runs into the HBM traffic record read by the benchmark")
+    ap.add_argument("--model-check", nargs=4, metavar=("FETCH", "WRITE", "TCP_TCC", "LDS"),
+                    help="predicted vs measured bytes per level for every layer, from four counter runs "
+                         "of --traffic-run --layer all")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU (got --gpus {args.gpus}); "
@@ -239,14 +354,17 @@ def main():
     if args.traffic_parse:  # host-only: reads the counter files of two earlier runs
         traffic_parse(BY_NAME[args.layer], args.traffic_parse[0], args.traffic_parse[1], TRAFFIC_FILE)
         return
+    if args.model_check:  # host-only: reads the counter files of four earlier runs
+        model_check_parse(list(CONFIGS), args.model_check)
+        return
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
     B.lib()  # fail loudly if the HIP library is missing
-    c = BY_NAME[args.layer]
     if args.traffic_run:
-        traffic_run(c)
+        traffic_run(list(CONFIGS) if args.layer == "all" else [BY_NAME[args.layer]])
         return
+    c = BY_NAME[args.layer]
 
     dtype_code = B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32
     plan = B.conv_fwd_plan(*c.key(), dtype=dtype_code)
