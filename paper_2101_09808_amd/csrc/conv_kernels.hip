@@ -744,35 +744,42 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 // Fully unrolled kernel for a compile-time channel count C = 4 * NQ.
 //
-// A wave's pixels are NB32 blocks of 32 done with v_mfma_f32_32x32x2f32 (two
-// 32-row k blocks, two channels per MFMA) plus NS16 (0 or 1) blocks of 16
-// done with v_mfma_f32_16x16x4f32 (four 16-row k blocks, four channels), so
-// the per-wave pixel count can be a multiple of 16 while most of the work
-// runs on the wider instruction: it reads half the operand registers per
-// flop, and its accumulators can be reused every few instructions without
-// stalls.  One step of the unrolled loop is one channel quad.  The Ker slice
-// arrives in chunks of 64 channels straight to LDS (buffer loads with the LDS
-// bit); chunk c+1 is requested during chunk c, so only the first chunk's
-// latency precedes the first MFMA.
+// Pixels go in units of 16: a wave with U units does U/2 blocks of 32 on
+// v_mfma_f32_32x32x2f32 (two 32-row k blocks, two channels per MFMA) and,
+// for odd U, one block of 16 on v_mfma_f32_16x16x4f32 (four 16-row k blocks,
+// four channels).  Most of the work thus runs on the wider instruction: it
+// reads half the operand registers per flop, and its accumulators can be
+// reused every few instructions without stalls, while the pixel count per
+// wave stays a multiple of 16.
+//
+// Each SIMD owns a contiguous range of `wpx` pixels.  With UB == 0 one wave
+// per SIMD takes it (UA units).  With UB > 0 two waves share the SIMD: wave
+// s takes the first 16 * UA pixels and wave s + 4 the next 16 * UB.  The two
+// interleave their MFMAs, and when UB < UA the narrower wave ends first, so
+// its stores drain while the other still computes.
+//
+// One step of the unrolled loop is one channel quad.  The Ker slice arrives
+// in chunks of 64 channels straight to LDS (buffer loads with the LDS bit);
+// chunk c+1 is requested during chunk c, so only the first chunk's latency
+// precedes the first MFMA.
 //
 // Lane layouts (l = lane): 32x32x2 A[i][k] = lane (i = l%32, k = l/32), B[k][j]
 // = lane (j = l%32, k = l/32), accumulator register v = (i = 8*(v/4) +
 // 4*(l/32) + v%4, j = l%32); 16x16x4 A (i = l%16, k = l/16), B (j = l%16,
 // k = l/16), register v = (i = 4*(l/16) + v, j = l%16).
-template <int NB32, int NS16, int D, int NQ>
-__global__ void __launch_bounds__(kThreads)
+template <int UA, int UB, int D, int NQ>
+__global__ void __launch_bounds__(UB > 0 ? 512 : 256)
 conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
                       float* __restrict__ Out, const Geom g) {
   static_assert(NQ % 16 == 0, "Ker arrives in chunks of 16 channel quads");
-  static_assert(NS16 == 0 || NS16 == 1, "at most one 16-pixel block");
-  constexpr int LPQ = 2 * NB32 + NS16;     // In loads per wave per channel quad
+  static_assert(UA >= 1 && UB >= 0, "pixel units per wave");
+  constexpr int NW = UB > 0 ? 8 : 4;       // waves per workgroup
   constexpr int PITCH = 4 * NQ + 1;        // LDS Ker row pitch, floats
   constexpr int NCH = NQ / 16;             // Ker chunks of 64 channels
-  constexpr int LEAD = (48 / LPQ) < 16 ? (48 / LPQ) : 16;  // steps from a chunk's request to its wait
-  static_assert(D >= 1 && D * LPQ <= 48 && D <= NQ && LEAD >= 1, "loads in flight stay within vmcnt");
   extern __shared__ __align__(16) float lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int simd = wave & 3;
   const int l32 = lane & 31, h32 = lane >> 5;  // 32x32x2 lane coordinates
   const int l16 = lane & 15, h16 = lane >> 4;  // 16x16x4 lane coordinates
   const int C = g.C, K = g.K;
@@ -781,142 +788,159 @@ conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ke
   const int kt = blockIdx.x % g.tiles_k;
   const int pg = blockIdx.x / g.tiles_k;
   const int k0 = kt * 64;
-  const int wpx = g.tw;                 // pixels per wave
-  const int px_begin = (pg * 4 + wave) * wpx;
-  const int px_end = min(px_begin + wpx, total_px);
+  const int wpx = g.tw;                 // pixels per SIMD
+  const int simd_begin = (pg * 4 + simd) * wpx;
+  const int simd_end = min(simd_begin + wpx, total_px);
 
-  // Ker chunk ch -> LDS: wave w copies rows 16w..16w+15, 64 channels per load
-  // (rows past K read zeros).
+  // Ker chunk ch -> LDS: the NW waves copy 64 / NW rows each, 64 channels per
+  // load (rows past K read zeros).
   const v4i krsrc = make_rsrc(Ker, g.ker_bytes);
   const unsigned lbase = (unsigned)(size_t)(lds_float*)lds;
   auto ker_chunk = [&](int ch) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int kl = wave * 16 + i, k = k0 + kl;
+    for (int i = 0; i < 64 / NW; ++i) {
+      const int kl = wave * (64 / NW) + i, k = k0 + kl;
       const unsigned voff = k < K ? (unsigned)(k * C + ch * 64 + lane) * 4u : kOob;
       dma_load<1>(krsrc, __builtin_amdgcn_readfirstlane(lbase + (unsigned)(kl * PITCH + ch * 64) * 4u), voff);
     }
   };
-
-  // In through raw buffer loads; masked lanes start at 2^31 and read zeros.
   __amdgpu_buffer_rsrc_t rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(In), (short)0, (int)g.in_bytes, 0x00020000);
   const unsigned cstride = 4u * (unsigned)HW;  // bytes between channels
-  auto in_off = [&](int px, int c) __attribute__((always_inline)) {
-    const int n = px / HW, hw = px - n * HW;
-    return (px < px_end) ? (unsigned)((n * C + c) * HW + hw) * 4u : kOob;
-  };
-  unsigned off32[NB32 > 0 ? NB32 : 1], off16 = 0;
-#pragma unroll
-  for (int b = 0; b < NB32; ++b) off32[b] = in_off(px_begin + 32 * b + l32, h32);
-  if constexpr (NS16 > 0) off16 = in_off(px_begin + 32 * NB32 + l16, h16);
-  float ring32[D][2][NB32 > 0 ? NB32 : 1], ring16[D];
-  auto load = [&](int q) __attribute__((always_inline)) {
-#pragma unroll
-    for (int e = 0; e < 2; ++e)
-#pragma unroll
-      for (int b = 0; b < NB32; ++b)
-        ring32[q % D][e][b] = __builtin_bit_cast(
-            float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, off32[b] + (unsigned)(4 * q + 2 * e) * cstride, 0, 0));
-    if constexpr (NS16 > 0)
-      ring16[q % D] = __builtin_bit_cast(
-          float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, off16 + (unsigned)(4 * q) * cstride, 0, 0));
-  };
-  // A operands, read one quad ahead: a32[e][kb] = Ker[k0 + 32kb + l32][4q + 2e + h32],
-  // a16[kb] = Ker[k0 + 16kb + l16][4q + h16]
-  const float* arow32 = lds + l32 * PITCH + h32;
-  const float* arow16 = lds + l16 * PITCH + h16;
-  float a32[2][2][2], a16[2][4];
-  auto read_a = [&](int q, int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int e = 0; e < 2; ++e)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) a32[buf][e][kb] = arow32[kb * 32 * PITCH + 4 * q + 2 * e];
-    if constexpr (NS16 > 0) {
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) a16[buf][kb] = arow16[kb * 16 * PITCH + 4 * q];
-    }
-  };
-  v16f acc32[NB32 > 0 ? NB32 : 1][2];
-  v4f acc16[4];
-#pragma unroll
-  for (int b = 0; b < NB32; ++b)
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) acc32[b][kb] = v16f{};
-#pragma unroll
-  for (int kb = 0; kb < 4; ++kb) acc16[kb] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  // prologue: first Ker chunk, then the ring, then wait for the chunk (the
-  // ring's D * LPQ loads are younger and may stay in flight)
-  ker_chunk(0);
+  // The work of one wave: U units of 16 pixels from px_begin (masked at px_end).
+  auto body = [&](auto u_c, int px_begin, int px_end) __attribute__((always_inline)) {
+    constexpr int U = decltype(u_c)::value;
+    constexpr int NB32 = U / 2, NS16 = U % 2;
+    constexpr int LPQ = 2 * NB32 + NS16;   // In loads per channel quad
+    constexpr int LEAD = (48 / LPQ) < 16 ? (48 / LPQ) : 16;  // steps from a chunk's request to its wait
+    static_assert(D >= 1 && D * LPQ <= 48 && D <= NQ && LEAD >= 1, "loads in flight stay within vmcnt");
+    // In through raw buffer loads; masked lanes start at 2^31 and read zeros.
+    auto in_off = [&](int px, int c) __attribute__((always_inline)) {
+      const int n = px / HW, hw = px - n * HW;
+      return (px < px_end) ? (unsigned)((n * C + c) * HW + hw) * 4u : kOob;
+    };
+    unsigned off32[NB32 > 0 ? NB32 : 1], off16 = 0;
 #pragma unroll
-  for (int q = 0; q < D; ++q) load(q);
-  wait_vmcnt_opaque<D * LPQ>();
-  __syncthreads();
-  read_a(0, 0);
-  static_for<NQ>([&](auto q_c) __attribute__((always_inline)) {
-    constexpr int q = decltype(q_c)::value;
-    constexpr int buf = q & 1;
-    constexpr bool chunk_end = q % 16 == 15 && q / 16 + 1 < NCH;
-    if constexpr (q + 1 < NQ && !chunk_end) read_a(q + 1, buf ^ 1);
-    __builtin_amdgcn_sched_barrier(0);  // issue the A reads first
-    if constexpr (q % 16 == 16 - LEAD && q / 16 + 1 < NCH) ker_chunk(q / 16 + 1);
+    for (int b = 0; b < NB32; ++b) off32[b] = in_off(px_begin + 32 * b + l32, h32);
+    if constexpr (NS16 > 0) off16 = in_off(px_begin + 32 * NB32 + l16, h16);
+    float ring32[D][2][NB32 > 0 ? NB32 : 1], ring16[D];
+    auto load = [&](int q) __attribute__((always_inline)) {
 #pragma unroll
-    for (int e = 0; e < 2; ++e)
+      for (int e = 0; e < 2; ++e)
 #pragma unroll
-      for (int b = 0; b < NB32; ++b)
+        for (int b = 0; b < NB32; ++b)
+          ring32[q % D][e][b] = __builtin_bit_cast(
+              float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, off32[b] + (unsigned)(4 * q + 2 * e) * cstride, 0, 0));
+      if constexpr (NS16 > 0)
+        ring16[q % D] = __builtin_bit_cast(
+            float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, off16 + (unsigned)(4 * q) * cstride, 0, 0));
+    };
+    // A operands, read one quad ahead: a32[e][kb] = Ker[k0 + 32kb + l32][4q + 2e + h32],
+    // a16[kb] = Ker[k0 + 16kb + l16][4q + h16]
+    const float* arow32 = lds + l32 * PITCH + h32;
+    const float* arow16 = lds + l16 * PITCH + h16;
+    float a32[2][2][2], a16[2][4];
+    auto read_a = [&](int q, int buf) __attribute__((always_inline)) {
+      if constexpr (NB32 > 0) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb) a32[buf][e][kb] = arow32[kb * 32 * PITCH + 4 * q + 2 * e];
+      }
+      if constexpr (NS16 > 0) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) a16[buf][kb] = arow16[kb * 16 * PITCH + 4 * q];
+      }
+    };
+    v16f acc32[NB32 > 0 ? NB32 : 1][2];
+    v4f acc16[4];
+#pragma unroll
+    for (int b = 0; b < NB32; ++b)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) acc32[b][kb] = v16f{};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) acc16[kb] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    // prologue: first Ker chunk, then the ring, then wait for the chunk (the
+    // ring's D * LPQ loads are younger and may stay in flight)
+    ker_chunk(0);
+#pragma unroll
+    for (int q = 0; q < D; ++q) load(q);
+    wait_vmcnt_opaque<D * LPQ>();
+    __syncthreads();
+    read_a(0, 0);
+    static_for<NQ>([&](auto q_c) __attribute__((always_inline)) {
+      constexpr int q = decltype(q_c)::value;
+      constexpr int buf = q & 1;
+      constexpr bool chunk_end = q % 16 == 15 && q / 16 + 1 < NCH;
+      if constexpr (q + 1 < NQ && !chunk_end) read_a(q + 1, buf ^ 1);
+      __builtin_amdgcn_sched_barrier(0);  // issue the A reads first
+      if constexpr (q % 16 == 16 - LEAD && q / 16 + 1 < NCH) ker_chunk(q / 16 + 1);
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int b = 0; b < NB32; ++b)
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+            acc32[b][kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a32[buf][e][kb], ring32[q % D][e][b],
+                                                                acc32[b][kb], 0, 0, 0);
+      if constexpr (NS16 > 0) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+          acc16[kb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a16[buf][kb], ring16[q % D], acc16[kb], 0, 0, 0);
+      }
+      if constexpr (q + D < NQ) load(q + D);
+      if constexpr (chunk_end) {
+        // the next chunk was requested LEAD steps ago; LEAD * LPQ ring loads are younger
+        wait_vmcnt_opaque<LEAD * LPQ>();
+        __syncthreads();
+        read_a(q + 1, buf ^ 1);
+      }
+      // keep each refill right behind the MFMAs that free its slot: left
+      // alone, the scheduler sinks loads towards their uses and the ring
+      // degenerates to a few loads in flight
+      __builtin_amdgcn_sched_barrier(0);
+    });
+
+    // stores: 32 consecutive pixels (two rows of k) or 16 (four rows) per instruction
+#pragma unroll
+    for (int b = 0; b < NB32; ++b) {
+      const int px = px_begin + 32 * b + l32;
+      if (px < px_end) {
+        const int n = px / HW, hw = px - n * HW;
+        float* ob = Out + (size_t)n * K * HW + hw;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
-          acc32[b][kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a32[buf][e][kb], ring32[q % D][e][b],
-                                                              acc32[b][kb], 0, 0, 0);
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int k = k0 + 32 * kb + 8 * (v / 4) + 4 * h32 + v % 4;
+            if (k < K) ob[(size_t)k * HW] = acc32[b][kb][v];
+          }
+      }
+    }
     if constexpr (NS16 > 0) {
+      const int px = px_begin + 32 * NB32 + l16;
+      if (px < px_end) {
+        const int n = px / HW, hw = px - n * HW;
+        float* ob = Out + (size_t)n * K * HW + hw;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-        acc16[kb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a16[buf][kb], ring16[q % D], acc16[kb], 0, 0, 0);
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int k = k0 + 16 * kb + 4 * h16 + v;
+            if (k < K) ob[(size_t)k * HW] = acc16[kb][v];
+          }
+      }
     }
-    if constexpr (q + D < NQ) load(q + D);
-    if constexpr (chunk_end) {
-      // the next chunk was requested LEAD steps ago; LEAD * LPQ ring loads are younger
-      wait_vmcnt_opaque<LEAD * LPQ>();
-      __syncthreads();
-      read_a(q + 1, buf ^ 1);
-    }
-    // keep each refill right behind the MFMAs that free its slot: left alone,
-    // the scheduler sinks loads towards their uses and the ring degenerates
-    // to a few loads in flight
-    __builtin_amdgcn_sched_barrier(0);
-  });
-
-  // stores: 32 consecutive pixels (two rows of k) or 16 (four rows) per instruction
-#pragma unroll
-  for (int b = 0; b < NB32; ++b) {
-    const int px = px_begin + 32 * b + l32;
-    if (px < px_end) {
-      const int n = px / HW, hw = px - n * HW;
-      float* ob = Out + (size_t)n * K * HW + hw;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int k = k0 + 32 * kb + 8 * (v / 4) + 4 * h32 + v % 4;
-          if (k < K) ob[(size_t)k * HW] = acc32[b][kb][v];
-        }
+  };
+  if constexpr (UB > 0) {
+    if (wave >= 4) {
+      body(std::integral_constant<int, UB>{}, simd_begin + 16 * UA, simd_end);
+      return;
     }
   }
-  if constexpr (NS16 > 0) {
-    const int px = px_begin + 32 * NB32 + l16;
-    if (px < px_end) {
-      const int n = px / HW, hw = px - n * HW;
-      float* ob = Out + (size_t)n * K * HW + hw;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int k = k0 + 16 * kb + 4 * h16 + v;
-          if (k < K) ob[(size_t)k * HW] = acc16[kb][v];
-        }
-    }
-  }
+  body(std::integral_constant<int, UA>{}, simd_begin, min(simd_begin + 16 * UA, simd_end));
 }
 
 // Looped kernel for any channel count (C % 4 == 0): D quads per loop trip,
@@ -1057,10 +1081,10 @@ struct Instance {
                    NS},                                                                          \
            &conv_f32_dma_kernel<WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK>, nullptr}
 
-#define F32_STREAM1X1(ID, NB32, NS16, D, NQ)                                               \
-  Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STREAM1X1, 4, 2 * NB32 + NS16, 4 * NQ, 1, 1, NB32, \
-                   NS16, 1, 1, kThreads, D},                                                 \
-           &conv1x1_stream_kernel<NB32, NS16, D, NQ>, nullptr}
+#define F32_STREAM1X1(ID, UA, UB, D, NQ)                                                   \
+  Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STREAM1X1, 4, UA + UB, 4 * NQ, 1, 1, UA, UB, 1, 1, \
+                   (UB > 0 ? 512 : 256), D},                                                 \
+           &conv1x1_stream_kernel<UA, UB, D, NQ>, nullptr}
 
 #define F32_STREAM1X1_LOOP(ID, NB1, NB2, D)                                                  \
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STREAM1X1_LOOP, 4, NB1 + NB2, 0, 1, 1, NB1, NB2, \
@@ -1074,16 +1098,17 @@ struct Instance {
 
 const Instance kInstances[] = {
     // ---- pointwise streaming (Ker resident in LDS, In straight to registers)
-    // unrolled for C = 4 * NQ: (32-pixel blocks, 16-pixel blocks, ring depth in quads)
-    F32_STREAM1X1(301, 3, 1, 6, 64),
-    F32_STREAM1X1(302, 3, 1, 4, 64),
-    F32_STREAM1X1(303, 4, 0, 5, 64),
-    F32_STREAM1X1(304, 3, 0, 8, 64),
-    F32_STREAM1X1(305, 2, 0, 12, 64),
-    F32_STREAM1X1(306, 2, 1, 8, 64),
-    F32_STREAM1X1(307, 3, 1, 6, 16),
-    F32_STREAM1X1(308, 3, 1, 6, 32),
-    F32_STREAM1X1(309, 3, 1, 6, 128),
+    // unrolled for C = 4 * NQ: (16-pixel units of the first wave per SIMD,
+    // of the second, ring depth in channel quads)
+    F32_STREAM1X1(301, 4, 3, 6, 64),
+    F32_STREAM1X1(302, 4, 3, 4, 64),
+    F32_STREAM1X1(303, 7, 0, 4, 64),
+    F32_STREAM1X1(304, 7, 0, 6, 64),
+    F32_STREAM1X1(305, 4, 4, 6, 64),
+    F32_STREAM1X1(306, 5, 2, 5, 64),
+    F32_STREAM1X1(307, 4, 3, 6, 16),
+    F32_STREAM1X1(308, 4, 3, 6, 32),
+    F32_STREAM1X1(309, 4, 3, 6, 128),
     // any C % 4 == 0: (phase-1 blocks, phase-2 blocks, quads per trip)
     F32_STREAM1X1_LOOP(311, 4, 3, 8),
     F32_STREAM1X1_LOOP(312, 4, 0, 8),

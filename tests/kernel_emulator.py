@@ -437,17 +437,18 @@ def emulate_bf16(g, In, Ker, wgs=None, in_aligned=True):
 def emulate_stream1x1(g, In, Ker, wgs=None):
     """The pointwise streaming kernels.
 
-    Family 4 (unrolled for C = tc): per wave max_ni blocks of 32 pixels on
-    32x32x2 MFMAs (two 32-row k blocks, channel pairs) and max_nk (0/1) blocks
-    of 16 pixels on 16x16x4 MFMAs; Ker rows copied to LDS in 64-channel
-    chunks.  Family 5 (looped over trips of `stages` quads): max_ni then
+    Family 4 (unrolled for C = tc): per SIMD a wave of max_ni and (if
+    max_nk > 0) a second wave of max_nk units of 16 pixels; a wave with U
+    units does U//2 blocks of 32 pixels on 32x32x2 MFMAs (two 32-row k
+    blocks, channel pairs) and U%2 blocks of 16 on 16x16x4 MFMAs; Ker rows
+    copied to LDS in 64-channel chunks.  Family 5 (looped over trips of `stages` quads): max_ni then
     max_nk blocks of 16 pixels, Ker zero-padded to whole trips.  Ker rows
     [k][c] in LDS with a pitch of the stored channel count + 1; In operands
     from raw buffer loads whose 32-bit byte offsets are emulated exactly
     (offsets at or past the buffer size read 0)."""
     N, C, K, H, W = (g[x] for x in "N C K H W".split())
     fam = g["family"]
-    _chk(fam in (4, 5) and g["threads"] == 256 and g["R"] == 1 and g["S"] == 1, "stream geometry")
+    _chk(fam in (4, 5) and g["R"] == 1 and g["S"] == 1, "stream geometry")
     HW = W  # kernel view: one row per image
     _chk(H == 1, "kernel view of a pointwise layer")
     _chk(C % 4 == 0, "whole channel quads")
@@ -455,12 +456,13 @@ def emulate_stream1x1(g, In, Ker, wgs=None):
     nq = C // 4
     if fam == 4:
         _chk(g["tc"] == C and nq % 16 == 0, "unrolled instance for this channel count")
-        NB32, NS16 = g["max_ni"], g["max_nk"]
-        _chk(NS16 in (0, 1), "at most one 16-pixel block")
-        NB = 2 * NB32 + NS16
+        UA, UB = g["max_ni"], g["max_nk"]
+        NW = 8 if UB > 0 else 4
+        _chk(g["threads"] == 64 * NW, "threads per workgroup")
+        NB = UA + UB
         nq_run, cst = nq, C
     else:
-        _chk(g["tc"] == 0, "looped instance")
+        _chk(g["tc"] == 0 and g["threads"] == 256, "looped instance")
         NB1, NB2 = g["max_ni"], g["max_nk"]
         NB = NB1 + NB2
         nq_run = -(-nq // D) * D
@@ -551,12 +553,12 @@ def emulate_stream1x1(g, In, Ker, wgs=None):
         k0 = kt * 64
         lds = np.full(64 * pitch, np.nan)  # the pad column is never read
         if fam == 4:
-            # wave w copies rows 16w..16w+15, 64 channels per load: LDS
-            # destination M0 + 4 * lane, source offset or the sentinel
-            for w in range(4):
+            # wave w copies rows (64/NW)w .. (64/NW)(w+1)-1, 64 channels per
+            # load: LDS destination M0 + 4 * lane, source offset or the sentinel
+            for w in range(NW):
                 for ch in range(C // 64):
-                    for i in range(16):
-                        kl = w * 16 + i
+                    for i in range(64 // NW):
+                        kl = w * (64 // NW) + i
                         k = k0 + kl
                         dst = kl * pitch + ch * 64 + lane
                         _chk(dst.max() < lds.size, "LDS Ker chunk out of range")
@@ -569,14 +571,17 @@ def emulate_stream1x1(g, In, Ker, wgs=None):
                 kl, c = divmod(e, cst)
                 k = k0 + kl
                 lds[kl * pitch + c] = Ker[k * C + c] if (k < K and c < C) else 0.0
-        for wave in range(4):
-            px_begin = (pg * 4 + wave) * wpx
+        for simd in range(4):
+            px_begin = (pg * 4 + simd) * wpx
             px_end = min(px_begin + wpx, total_px)
             if fam == 4:
-                for bb in range(NB32):
-                    block32(lds, k0, px_end, px_begin + 32 * bb)
-                if NS16:
-                    block16(lds, k0, px_begin, px_end, px_begin + 32 * NB32, nq)
+                # first wave: UA units from the SIMD's start; second: UB units after them
+                for u, w_begin, w_end in ((UA, px_begin, min(px_begin + 16 * UA, px_end)),
+                                          (UB, px_begin + 16 * UA, px_end)):
+                    for bb in range(u // 2):
+                        block32(lds, k0, w_end, w_begin + 32 * bb)
+                    if u % 2:
+                        block16(lds, k0, w_begin, w_end, w_begin + 32 * (u // 2), nq)
             else:
                 for bb in range(NB):
                     block16(lds, k0, px_begin, px_end, px_begin + 16 * bb, nq_run)
