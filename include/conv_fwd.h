@@ -19,8 +19,11 @@
  * re-derived for the gfx950 memory hierarchy; see conv_fwd_plan.
  *
  * Ownership: every tensor pointer is DEVICE memory allocated and freed by
- * the caller.  The library keeps a host-side plan cache only and makes no
- * device allocation.  In, Ker and Out must not overlap.
+ * the caller.  The library keeps a host-side plan cache only; its one device
+ * allocation is the temporary workspace of plans that split the channel
+ * reduction (split_c > 1), taken from and returned to the device's default
+ * memory pool in stream order within the call.  In, Ker and Out must not
+ * overlap.
  *
  * Asynchrony: the compute calls enqueue kernels on `stream` (a hipStream_t;
  * NULL = the default stream) and return without synchronising.  A return of
@@ -85,6 +88,14 @@ typedef struct {
   int waves_px;       /* waves along pixels in a workgroup                   */
   int grid_order;     /* 0: k tiles innermost in the workgroup order (In reuse
                          in L2); 1: pixel tiles innermost (Ker reuse)        */
+  int split_c;        /* input-channel ranges the reduction is split into
+                         (0 or 1 = none).  Above 1 (direct-to-LDS plans only),
+                         each range's partial Out goes to a stream-ordered
+                         temporary workspace of split_c x |Out| floats
+                         (hipMallocAsync / hipFreeAsync on the call's
+                         stream) and a second kernel adds the ranges in
+                         fixed order, so results stay deterministic.       */
+  int reserved;       /* 0                                                   */
   int lds_bytes;      /* dynamic LDS per workgroup                           */
   int64_t num_wg;     /* workgroups launched                                 */
   int class_lvl[CONV_NUM_LVLS]; /* paper class 1..8 (Sec. 4) per level, 0 = n/a */
@@ -165,13 +176,16 @@ int conv_model_volume(const int perm[7], const int64_t N[7], const int64_t T[7],
  *   pipeline steps; then the kernel variant's k blocks per wave, pixel blocks
  *   per wave, channels per step, compile-time R, S (0 = runtime), staging
  *   capacity (In, Ker), Ker vector width, threads per workgroup; LDS bytes;
- *   kernel family (1 register-staged, 2 direct-to-LDS, 3 bf16), In vector
+ *   kernel family (1 register-staged, 2 direct-to-LDS, 3 bf16, 4 / 5
+ *   pointwise streaming unrolled / looped), In vector
  *   width, pipeline stages, LDS elements per stage (family 3: LDS bytes), In
- *   elements per stage (family 2), In and Ker bytes, workgroups launched.
+ *   elements per stage (family 2), In and Ker bytes, workgroups launched;
+ *   three reserved zeros; channel ranges of the reduction, pipeline steps
+ *   per range.
  * Writes min(cap, CONV_GEOM_FIELDS) values and returns CONV_GEOM_FIELDS, or
  * a negative conv_status_t (CONV_EINVAL for a plan the kernels cannot run).
  */
-#define CONV_GEOM_FIELDS 48
+#define CONV_GEOM_FIELDS 50
 int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S,
                       const conv_plan_t* plan, int32_t* out, int cap);
 

@@ -26,13 +26,13 @@ class ConvPlan(ctypes.Structure):
     _fields_ = [
         ("dtype", _i32), ("variant", _i32), ("tile_k", _i32), ("tile_rows", _i32),
         ("tile_cols", _i32), ("tile_c", _i32), ("wave_k", _i32), ("wave_px", _i32),
-        ("waves_k", _i32), ("waves_px", _i32), ("grid_order", _i32), ("lds_bytes", _i32),
-        ("num_wg", _i64), ("class_lvl", _i32 * 4), ("pred_bytes", _dbl * 4),
+        ("waves_k", _i32), ("waves_px", _i32), ("grid_order", _i32), ("split_c", _i32),
+        ("reserved", _i32), ("lds_bytes", _i32), ("num_wg", _i64), ("class_lvl", _i32 * 4), ("pred_bytes", _dbl * 4),
         ("pred_us", _dbl * 4), ("pred_mfma_us", _dbl), ("pred_total_us", _dbl),
     ]
 
     def to_dict(self):
-        d = {f: getattr(self, f) for f, _ in self._fields_[:13]}
+        d = {f: getattr(self, f) for f, _ in self._fields_[:15] if f != "reserved"}
         d["class_lvl"] = dict(zip(LEVELS, list(self.class_lvl)))
         d["pred_bytes"] = dict(zip(LEVELS, list(self.pred_bytes)))
         d["pred_us"] = dict(zip(LEVELS, list(self.pred_us)))
@@ -43,7 +43,7 @@ class ConvPlan(ctypes.Structure):
     @classmethod
     def from_dict(cls, d):
         p = cls()
-        for f, _ in cls._fields_[:13]:
+        for f, _ in cls._fields_[:15]:
             if f in d:
                 setattr(p, f, d[f])
         return p
@@ -205,6 +205,7 @@ GEOM_FIELDS = (
     "lds_in_elems", "lds_ker_elems", "ni_in", "ni_ker", "nchunks",
     "wk", "wp", "tc", "rc", "sc", "max_ni", "max_nk", "ker_vec", "threads", "lds_bytes",
     "family", "in_vec", "stages", "stage_elems", "in_region", "in_bytes", "ker_bytes", "grid",
+    "reserved0", "reserved1", "reserved2", "split", "cps",
 )
 
 
@@ -212,8 +213,8 @@ def conv_fwd_geometry(N, C, K, H, W, R, S, plan):
     """The launch geometry a plan resolves to (host only), as a dict."""
     if isinstance(plan, dict):
         plan = ConvPlan.from_dict(plan)
-    buf = (_i32 * 48)()
-    st = lib().conv_fwd_geometry(N, C, K, H, W, R, S, ctypes.byref(plan), buf, 48)
+    buf = (_i32 * len(GEOM_FIELDS))()
+    st = lib().conv_fwd_geometry(N, C, K, H, W, R, S, ctypes.byref(plan), buf, len(GEOM_FIELDS))
     if st < 0:
         raise ConvError(st, "conv_fwd_geometry")
     return dict(zip(GEOM_FIELDS, list(buf)[:len(GEOM_FIELDS)]))

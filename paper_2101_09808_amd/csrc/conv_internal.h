@@ -59,7 +59,8 @@ struct Geom {
   unsigned in_bytes, ker_bytes;          // tensor sizes (DMA family range checks)
   int stage_elems, in_region;            // DMA family: LDS elements per stage / In part
                                          // (bf16 family: stage_elems = LDS bytes)
-  int grid;                              // workgroups launched (persistent families)
+  int grid;                              // workgroups launched
+  int split, cps;                        // channel ranges of the reduction; pipeline steps per range
 };
 
 const Variant* variants(int* count);

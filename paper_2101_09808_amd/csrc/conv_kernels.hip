@@ -24,6 +24,7 @@
 //     hold 16 consecutive output pixels, so stores coalesce.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <mutex>
 #include <type_traits>
 #include <utility>
@@ -61,8 +62,9 @@ struct TileCoord {
   int nu0, nrows;     // input rows [nu0, nu0 + nrows) of the flattened n*H+y index
 };
 
-__device__ __forceinline__ TileCoord tile_coord(const Geom& g, int BK) {
-  const int L = xcd_remap(blockIdx.x, g.num_tiles);
+// Output tile of workgroup b (0 <= b < num_tiles), in the grid order.
+__device__ __forceinline__ TileCoord tile_coord(const Geom& g, int BK, int b) {
+  const int L = xcd_remap(b, g.num_tiles);
   int kt, ct, rt;
   if (g.order == 0) {
     kt = L % g.tiles_k;
@@ -107,7 +109,7 @@ conv_f32_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
   const int R = RC ? RC : g.R, S = SC ? SC : g.S;
   const int RS = R * S;
   const int H = g.H, W = g.W, C = g.C, K = g.K;
-  const TileCoord t = tile_coord(g, BK);
+  const TileCoord t = tile_coord(g, BK, (int)blockIdx.x);
 
   // Per-thread staging list for the In halo tile: element idx = tid + 256*i
   // of the [TC][in_rows][in_wp] LDS image.  in_goff is the global offset
@@ -344,7 +346,9 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
   const int R = RC ? RC : g.R, S = SC ? SC : g.S;
   const int RS = R * S;
   const int H = g.H, W = g.W, C = g.C, K = g.K;
-  const TileCoord t = tile_coord(g, BK);
+  // Workgroups of channel range r follow those of range r - 1.
+  const int split_r = (int)blockIdx.x / g.num_tiles;
+  const TileCoord t = tile_coord(g, BK, (int)blockIdx.x - split_r * g.num_tiles);
   const v4i in_rsrc = make_rsrc(In, g.in_bytes);
   const v4i ker_rsrc = make_rsrc(Ker, g.ker_bytes);
   const unsigned lds_base = (unsigned)(size_t)(lds_float*)lds;
@@ -405,9 +409,9 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
 #pragma unroll
   for (int kb = 0; kb < WK; ++kb) koff[kb] = ((wk * WK + kb) * 16 + j) * g.ker_rstride;
 
-  auto issue = [&](int ch) {
+  auto issue = [&](int ch, int slot) {  // pipeline step ch into stage buffer slot % NS
     const int c0 = ch * TC;
-    const unsigned stage = lds_base + (unsigned)((ch % NS) * STAGE) * 4u;
+    const unsigned stage = lds_base + (unsigned)((slot % NS) * STAGE) * 4u;
     const int coff = c0 * H * W;
 #pragma unroll
     for (int i = 0; i < NLI; ++i) {
@@ -465,10 +469,12 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
     }
   };
 
-  const int nch = g.nchunks;
+  // This workgroup's channel range: pipeline steps [ch0, ch0 + nch).
+  const int ch0 = split_r * g.cps;
+  const int nch = min(g.cps, g.nchunks - ch0);
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
-    if (s < nch) issue(s);
+    if (s < nch) issue(ch0 + s, s);
   for (int ch = 0; ch < nch; ++ch) {
     // wait for this step's loads: the later steps already issued may stay in flight
     const int ahead = min(NS - 2, nch - 1 - ch);
@@ -476,11 +482,13 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
     else if (NS >= 3 && ahead >= 1) wait_vmcnt<(NS >= 3 ? L : 0)>();
     else wait_vmcnt<0>();
     __syncthreads();
-    if (ch + NS - 1 < nch) issue(ch + NS - 1);
+    if (ch + NS - 1 < nch) issue(ch0 + ch + NS - 1, ch + NS - 1);
     compute(ch % NS);
   }
 
-  // Epilogue: lane (j, gq) holds Out[k0 + block*16 + 4*gq + v][pixel j].
+  // Epilogue: lane (j, gq) holds Out[k0 + block*16 + 4*gq + v][pixel j]; a
+  // split plan writes range split_r's partial sums to slice split_r of the
+  // workspace passed as Out.
   const size_t PQ = (size_t)g.P * g.Q;
 #pragma unroll
   for (int pb = 0; pb < WP; ++pb) {
@@ -489,7 +497,7 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
     const int rho = t.rho0 + row_i;
     if (px < tpx && rho < t.rho_end && col < t.tw_eff) {
       const int n = rho / g.P, p = rho - n * g.P;
-      float* ob = Out + ((size_t)n * K * g.P + p) * g.Q + t.q0 + col;
+      float* ob = Out + (size_t)split_r * g.N * K * PQ + ((size_t)n * K * g.P + p) * g.Q + t.q0 + col;
 #pragma unroll
       for (int kb = 0; kb < WK; ++kb)
 #pragma unroll
@@ -1071,6 +1079,32 @@ struct Instance {
   KernelBF16 bf16;
 };
 
+// ---------------------------------------------------------------------------
+// Second pass of a split reduction: Out[i] = W[0][i] + W[1][i] + ... over the
+// split channel ranges' partial outputs, always in range order, so the result
+// does not depend on which workgroup finished first.  VEC4: n % 4 == 0 and a
+// 16-byte aligned Out (the workspace always is).
+template <bool VEC4>
+__global__ void __launch_bounds__(256)
+splitk_reduce_kernel(const float* __restrict__ W, float* __restrict__ Out, int64_t n, int split) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  if constexpr (VEC4) {
+    const int64_t n4 = n / 4;
+    const v4f* W4 = reinterpret_cast<const v4f*>(W);
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += stride) {
+      v4f acc = W4[i];
+      for (int r = 1; r < split; ++r) acc += W4[(size_t)r * n4 + i];
+      reinterpret_cast<v4f*>(Out)[i] = acc;
+    }
+  } else {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += stride) {
+      float acc = W[i];
+      for (int r = 1; r < split; ++r) acc += W[(size_t)r * n + i];
+      Out[i] = acc;
+    }
+  }
+}
+
 #define F32_INST(ID, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV)                                  \
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STAGED, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV, 1, \
                    kThreads, 2},                                                             \
@@ -1213,6 +1247,7 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
     return CONV_EINVAL;
   const void* fn = inst->f32 ? reinterpret_cast<const void*>(inst->f32)
                              : reinterpret_cast<const void*>(inst->bf16);
+  if (g.split > 1 && v.family != FAMILY_DMA) return CONV_EINVAL;
   if (lds_bytes > 65536) {
     // Raise the kernel's dynamic LDS limit once (to the device maximum).
     static std::mutex mu;
@@ -1224,6 +1259,24 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
         return CONV_EHIP;
       done[idx] = true;
     }
+  }
+  if (inst->f32 && g.split > 1) {
+    // Split reduction: partial outputs of the channel ranges into a
+    // stream-ordered workspace, then the fixed-order sum into Out.
+    const int64_t n = (int64_t)g.N * g.K * g.P * g.Q;
+    float* ws = nullptr;
+    if (hipMallocAsync(reinterpret_cast<void**>(&ws), (size_t)g.split * n * sizeof(float), st) != hipSuccess)
+      return CONV_EHIP;
+    hipLaunchKernelGGL(inst->f32, dim3(g.grid), dim3(v.threads), lds_bytes, st,
+                       static_cast<const float*>(In), static_cast<const float*>(Ker), ws, g);
+    const bool vec4 = (n % 4 == 0) && (reinterpret_cast<uintptr_t>(Out) % 16 == 0);
+    const int64_t items = vec4 ? n / 4 : n;
+    const int blocks = (int)std::min<int64_t>((items + 255) / 256, 4096);
+    if (vec4) hipLaunchKernelGGL(splitk_reduce_kernel<true>, dim3(blocks), dim3(256), 0, st, ws, Out, n, g.split);
+    else hipLaunchKernelGGL(splitk_reduce_kernel<false>, dim3(blocks), dim3(256), 0, st, ws, Out, n, g.split);
+    const hipError_t launched = hipGetLastError();
+    const hipError_t freed = hipFreeAsync(ws, st);
+    return (launched == hipSuccess && freed == hipSuccess) ? CONV_OK : CONV_EHIP;
   }
   if (inst->f32) {
     hipLaunchKernelGGL(inst->f32, dim3(g.grid), dim3(v.threads), lds_bytes, st,

@@ -109,6 +109,7 @@ struct Hw {
       8.0e12,             // HBM
   };
   int mfma_f32_cycles = 32;  // 16x16x4 f32 per SIMD
+  double launch_us = 3.0;    // one more kernel launch in the stream (measured gap, order of)
 };
 const Hw kHw;
 
@@ -217,6 +218,8 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
                   int* lds_bytes) {
   const Shape s = kernel_view(s0);
   if (plan.dtype != v.dtype) return false;
+  const int split = std::max(1, plan.split_c);
+  if (split > 1 && v.family != FAMILY_DMA) return false;  // only that kernel splits the reduction
   if (v.family == FAMILY_STREAM1X1 || v.family == FAMILY_STREAM1X1_LOOP) {
     // Pointwise streaming: tile_cols = pixels per wave, 4 waves per workgroup,
     // 64 output channels per workgroup, the whole channel range resident.
@@ -247,6 +250,8 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
     q.num_tiles = (int)(groups * tiles_k);
     q.grid = q.num_tiles;
     q.nchunks = (int)cdiv(s.C, 4);
+    q.split = 1;
+    q.cps = q.nchunks;
     q.stage_elems = (int)bytes;
     q.in_bytes = (unsigned)std::min<int64_t>((int64_t)s.N * s.C * s.H * s.W * 4, 0xffffffffLL);
     q.ker_bytes = (unsigned)std::min<int64_t>((int64_t)s.K * s.C * 4, 0xffffffffLL);
@@ -295,6 +300,8 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
     q.order = plan.grid_order;
     q.num_tiles = (int)num_tiles;
     q.nchunks = (int)cdiv(s.C, TC);
+    q.split = 1;
+    q.cps = q.nchunks;
     q.stage_elems = (int)bytes_b;
     const int occ = std::max(1, std::min(2, (int)(kHw.lds_bytes / bytes_b)));
     q.grid = (int)std::min<int64_t>(num_tiles, (int64_t)kHw.cus * occ);
@@ -361,11 +368,18 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
   q.lds_in_elems = (int)lds_in; q.lds_ker_elems = (int)lds_ker;
   q.ni_in = (int)ni_in; q.ni_ker = (int)ni_ker;
   q.nchunks = (int)cdiv(s.C, TC);
+  // Channel ranges: split ranges of cps pipeline steps each, none empty; the
+  // workgroups of range r follow those of range r-1.
+  q.split = split;
+  q.cps = (int)cdiv(q.nchunks, split);
+  if ((int64_t)(split - 1) * q.cps >= q.nchunks) return false;
+  if (num_tiles * split >= (int64_t(1) << 31)) return false;
+  if (split > 1 && (int64_t)split * s.N * s.K * P * Q >= (int64_t(1) << 31)) return false;  // workspace
   q.in_bytes = (unsigned)std::min<int64_t>(in_elems_total * 4, 0xffffffffLL);
   q.ker_bytes = (unsigned)std::min<int64_t>(ker_elems_total * 4, 0xffffffffLL);
   q.stage_elems = (int)stage;
   q.in_region = (int)in_region;
-  q.grid = (int)num_tiles;
+  q.grid = (int)(num_tiles * split);
   if (g) *g = q;
   if (lds_bytes) *lds_bytes = (int)bytes;
   return true;
@@ -423,7 +437,8 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
   const int RS = s.R * s.S;
   const int64_t NP = (int64_t)s.N * g.P;
   plan->lds_bytes = lds;
-  plan->num_wg = g.num_tiles;
+  plan->num_wg = g.grid;
+  plan->split_c = g.split;
 
   // REG: per wave and per (4 channels, tap), WK + WP operand reads of 64 lanes.
   const double waves = (double)g.num_tiles * (g.nwk * g.nwp);
@@ -471,7 +486,10 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
     plan->pred_bytes[CONV_LVL_L2] = in_halo_bytes * g.tiles_k + ker_bytes;
     plan->class_lvl[CONV_LVL_L2] = 1;  // <{k,c,r,s},{n,h},w>: pixels innermost
   }
-  plan->pred_bytes[CONV_LVL_HBM] = in_bytes + ker_bytes + out_bytes;
+  // split reduction: every range writes its partial Out to the workspace and
+  // the second pass reads them all back
+  const double ws_bytes = g.split > 1 ? 2.0 * g.split * out_bytes : 0.0;
+  plan->pred_bytes[CONV_LVL_HBM] = in_bytes + ker_bytes + out_bytes + ws_bytes;
   plan->class_lvl[CONV_LVL_REG] = 3;  // <{n,k,h,w},{c,r},s>
   plan->class_lvl[CONV_LVL_LDS] = 3;
   plan->class_lvl[CONV_LVL_HBM] = 0;
@@ -481,16 +499,32 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
     plan->pred_us[l] = plan->pred_bytes[l] / kHw.bw[l] * 1e6;
     tmax = std::max(tmax, plan->pred_us[l]);
   }
-  // Compute: MFMA cycles of one wave; a CU runs ceil(num_wg / cus) workgroups
-  // whose waves share its SIMDs.
+  // Compute: MFMA cycles of one wave (its channel range); a CU runs
+  // ceil(workgroups / cus) workgroups whose waves share its SIMDs.
   const double mfma_per_step = (double)v->wk * v->wp;
   const double mfma_cycles = (plan->dtype == CONV_DTYPE_BF16) ? 16.0 : kHw.mfma_f32_cycles;
-  const double wave_cycles = steps * mfma_per_step * mfma_cycles;
-  const double per_cu = std::ceil((double)g.num_tiles / kHw.cus);
+  const double wave_cycles = steps * ((double)g.cps / g.nchunks) * mfma_per_step * mfma_cycles;
+  const double per_cu = std::ceil((double)g.grid / kHw.cus);
   const double waves_per_simd = per_cu * (g.nwk * g.nwp) / kHw.simds_per_cu;
   plan->pred_mfma_us = waves_per_simd * wave_cycles / kHw.clock_hz * 1e6;
+  if (plan->dtype == CONV_DTYPE_F32) {
+    // Issue efficiency of the fp32 inner loop.  Each step of a WK x WP wave
+    // tile reads WK + WP operands from LDS for WK * WP MFMAs; measured
+    // (inner-loop probes and layer sweeps on MI355X) the loop sustains about
+    // c / (reads per MFMA) of the MFMA rate, capped: c = 0.53, cap 0.78 with
+    // one wave per SIMD; c = 0.70, cap 0.82 when two or more waves share a
+    // SIMD and cover each other's operand waits.
+    const double reads_per_mfma = (double)(v->wk + v->wp) / ((double)v->wk * v->wp);
+    const bool shared = (g.nwk * g.nwp) > kHw.simds_per_cu;
+    const double eff = std::min(shared ? 0.82 : 0.78, (shared ? 0.70 : 0.53) / reads_per_mfma);
+    plan->pred_mfma_us /= eff;
+  }
   tmax = std::max(tmax, plan->pred_mfma_us);
-  plan->pred_total_us = tmax;
+  // The reduction pass of a split plan runs after the main kernel: a launch
+  // plus reading the ranges and writing Out.
+  const double reduce_us =
+      g.split > 1 ? kHw.launch_us + (g.split + 1.0) * out_bytes / kHw.bw[CONV_LVL_HBM] * 1e6 : 0.0;
+  plan->pred_total_us = tmax + reduce_us;
   return CONV_OK;
 }
 
@@ -509,10 +543,11 @@ void fill_plan_fields(conv_plan_t* p, const Variant& v, int nwk, int nwp, int tr
   p->waves_k = nwk;
   p->waves_px = nwp;
   p->grid_order = order;
+  p->split_c = 1;
 }
 
 // Deterministic preference among plans (tie-breaks: predicted time, total
-// predicted bytes, fewer workgroups, variant id, larger k tile).
+// predicted bytes, fewer workgroups, variant id, larger k tile, no split).
 bool better(const conv_plan_t& a, const conv_plan_t& b) {
   // Family preference (measured, not modelled: the model does not capture
   // latency hiding): the unrolled pointwise streaming kernel, then the
@@ -541,7 +576,8 @@ bool better(const conv_plan_t& a, const conv_plan_t& b) {
   if (a.tile_k != b.tile_k) return a.tile_k > b.tile_k;
   if (a.tile_rows != b.tile_rows) return a.tile_rows > b.tile_rows;
   if (a.tile_cols != b.tile_cols) return a.tile_cols > b.tile_cols;
-  return a.grid_order < b.grid_order;
+  if (a.grid_order != b.grid_order) return a.grid_order < b.grid_order;
+  return a.split_c < b.split_c;
 }
 }  // namespace
 
@@ -604,7 +640,18 @@ int enumerate_plans(const Shape& s0, int dtype, conv_plan_t* plans, int cap) {
           for (int order = 0; order < 2; ++order) {
             conv_plan_t p;
             fill_plan_fields(&p, v, nwk, nwp, tr, tw, order);
-            if (score_plan(s0, &p) == CONV_OK) all.push_back(p);
+            if (score_plan(s0, &p) != CONV_OK) continue;
+            all.push_back(p);
+            // Too few workgroups to fill the CUs: also split the channel
+            // reduction into ranges (direct-to-LDS kernel only).
+            if (v.family == FAMILY_DMA && p.num_wg < kHw.cus) {
+              for (int split : {2, 3, 4, 6, 8, 12, 16}) {
+                if (p.num_wg * split > 2 * kHw.cus) break;
+                conv_plan_t q = p;
+                q.split_c = split;
+                if (score_plan(s0, &q) == CONV_OK) all.push_back(q);
+              }
+            }
           }
       }
     }

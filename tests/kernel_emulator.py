@@ -100,11 +100,21 @@ def emulate(g, In, Ker, wgs=None):
         _chk(g["ni_in"] <= g["max_ni"] and g["ni_ker"] <= g["max_nk"], "staging capacity")
         _chk(g["ni_in"] * NT >= TC * E, "In staging does not cover the LDS tile")
         _chk(g["ni_ker"] * NT >= BK * per_row, "Ker staging does not cover the LDS tile")
+    split, cps = g["split"], g["cps"]
+    _chk(split >= 1 and (split == 1 or dma), "only the direct-to-LDS kernel splits the reduction")
+    _chk(g["grid"] == g["num_tiles"] * split, "workgroups = tiles x channel ranges")
+    _chk(split * cps >= g["nchunks"] and (split - 1) * cps < g["nchunks"], "channel ranges cover the steps")
+    # a split plan writes range r's partial sums to workspace slice r; the
+    # second pass adds the slices in range order
+    ws = np.full(split * out_size, np.nan) if split > 1 else None
+    ws_written = np.zeros(split * out_size, np.int64) if split > 1 else None
     seen_L = set()
-    for b in (range(g["num_tiles"]) if wgs is None else wgs):
-        L, t = tile_coord(g, b, BK)
-        _chk(0 <= L < g["num_tiles"] and L not in seen_L, "workgroup remap is not a bijection")
-        seen_L.add(L)
+    tiles = range(g["num_tiles"]) if wgs is None else wgs
+    for b in [r * g["num_tiles"] + tb for tb in tiles for r in range(split)]:
+        split_r, tb = divmod(b, g["num_tiles"])
+        L, t = tile_coord(g, tb, BK)
+        _chk(0 <= L < g["num_tiles"] and (L, split_r) not in seen_L, "workgroup remap is not a bijection")
+        seen_L.add((L, split_r))
         ncols = t["tw_eff"] + S - 1
         _chk(t["nrows"] <= g["in_rows"], "tile needs more LDS rows than allocated")
         # In staging list
@@ -244,11 +254,14 @@ def emulate(g, In, Ker, wgs=None):
                                     Am[j, gq] = A[kb]
                                     wv["acc"][kb, pb] += Am @ Bm
 
-        stage(0, 0)
-        for ch in range(g["nchunks"]):
+        ch0 = split_r * cps
+        nch = min(cps, g["nchunks"] - ch0)
+        _chk(nch >= 1, "empty channel range")
+        stage(ch0 * TC, 0)
+        for ch in range(nch):
             compute(ch & 1)
-            if ch + 1 < g["nchunks"]:
-                stage((ch + 1) * TC, (ch + 1) & 1)
+            if ch + 1 < nch:
+                stage((ch0 + ch + 1) * TC, (ch + 1) & 1)
         for wv in waves:
             for pb in range(WP):
                 valid = wv["pvalid"][pb]
@@ -260,8 +273,24 @@ def emulate(g, In, Ker, wgs=None):
                         dst = ((n * K + k) * P + p) * Q + t["q0"] + col
                         _chk((dst[st] >= 0) & (dst[st] < out_size), "Out store out of bounds")
                         vals = wv["acc"][kb, pb][4 * gq + v, j]
-                        out[dst[st]] = vals[st]
-                        np.add.at(written, dst[st], 1)
+                        if split > 1:
+                            wdst = split_r * out_size + dst
+                            ws[wdst[st]] = vals[st]
+                            np.add.at(ws_written, wdst[st], 1)
+                        else:
+                            out[dst[st]] = vals[st]
+                            np.add.at(written, dst[st], 1)
+    if split > 1:
+        per = ws_written.reshape(split, out_size)
+        touched = per.max(axis=0) > 0
+        # every slice of every touched output written exactly once
+        _chk((per[:, touched] == 1).all(), "a channel range stored an output twice or not at all")
+        sl = ws.reshape(split, out_size)
+        acc = sl[0].copy()
+        for r in range(1, split):
+            acc = acc + sl[r]
+        out = np.where(touched, acc, np.nan)
+        written = touched.astype(np.int64)
     return out, written
 
 

@@ -37,8 +37,9 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_plan_struct_layout_matches_header():
-    # conv_plan_t: 12 ints, int64, 4 ints, 4+4+1+1 doubles
-    assert ctypes.sizeof(B.ConvPlan) == 12 * 4 + 8 + 4 * 4 + 10 * 8
+    # conv_plan_t: 14 ints, int64, 4 ints, 4+4+1+1 doubles (no padding)
+    assert ctypes.sizeof(B.ConvPlan) == 14 * 4 + 8 + 4 * 4 + 10 * 8
+    assert B.ConvPlan.num_wg.offset == 14 * 4
 
 
 VALID = (1, 4, 8, 6, 6, 3, 3)

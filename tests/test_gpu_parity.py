@@ -224,7 +224,7 @@ def _plans_per_variant(dims, dtype=B.CONV_DTYPE_F32, per_variant=3):
     cands = B.conv_fwd_candidates(*dims, dtype=dtype)
     chosen = {}
     for p in cands:
-        key = (p["variant"], p["waves_k"], p["grid_order"])
+        key = (p["variant"], p["waves_k"], p["grid_order"], p.get("split_c", 1) > 1)
         chosen.setdefault(key, p)
     by_var = {}
     for key, p in sorted(chosen.items()):
@@ -254,7 +254,7 @@ def test_every_variant(shape):
     assert plans
     for p in plans:
         say(f"[gpu] {shape.name} variant={p['variant']} tile={p['tile_k']}x{p['tile_rows']}x{p['tile_cols']} "
-            f"waves={p['waves_k']}x{p['waves_px']} order={p['grid_order']}")
+            f"waves={p['waves_k']}x{p['waves_px']} order={p['grid_order']} split={p['split_c']}")
         out = host(gpu_conv(shape, In, Ker, plan=p))
         err = rel_err(out, ref)
         assert err <= TOL["f32"], (p, err)
@@ -307,3 +307,36 @@ def test_misaligned_tensors(shape):
         assert ei.value.status == B.CONV_EINVAL
         torch.cuda.synchronize()
         assert (poison == 7.0).all()
+
+
+SPLIT_SHAPE = ConvShape("split_ranges", 1, 40, 64, 12, 12, 3, 3, "f32", 71)
+
+
+def split_plans(shape):
+    """Every split factor the selector offers for the shape, one plan each."""
+    plans = {}
+    for p in B.conv_fwd_candidates(*shape.key()):
+        if p["split_c"] > 1:
+            plans.setdefault(p["split_c"], p)
+    return [plans[k] for k in sorted(plans)]
+
+
+def test_split_reduction_parity_and_determinism():
+    """Channel ranges reduced by the second pass (uneven ranges included):
+    parity with the oracle, bitwise equality of two runs, and exact sums on
+    integer inputs."""
+    s = SPLIT_SHAPE
+    plans = split_plans(s)
+    assert len(plans) >= 2
+    In, Ker = make_inputs(s)
+    ref = oconv.conv_fwd(host(In), host(Ker))
+    In_i, Ker_i = make_inputs(s, seed=s.seed + 1, kind="int")
+    ref_i = oconv.conv_fwd(host(In_i), host(Ker_i))
+    for p in plans:
+        g = B.conv_fwd_geometry(*s.key(), p)
+        say(f"[gpu] split={p['split_c']} steps={g['nchunks']} per range={g['cps']} variant={p['variant']}")
+        a = gpu_conv(s, In, Ker, plan=p)
+        b = gpu_conv(s, In, Ker, plan=p)
+        assert torch.equal(a, b), "two runs differ"
+        assert rel_err(host(a), ref) <= TOL["f32"]
+        assert np.array_equal(host(gpu_conv(s, In_i, Ker_i, plan=p)).astype(np.float64), ref_i)

@@ -46,7 +46,7 @@ def test_full_config_sampled_workgroups(cfg):
     """Full-size plans: emulate the first, last and some middle workgroups;
     their outputs must equal the oracle at those points."""
     plan = B.conv_fwd_plan(*cfg.key())
-    G = plan["num_wg"]
+    G = B.conv_fwd_geometry(*cfg.key(), plan)["num_tiles"]  # output tiles (all channel ranges of each)
     rng = np.random.default_rng(1)
     wgs = sorted(set([0, 1, 7, 8, G // 2, G - 9, G - 8, G - 1] + list(rng.integers(0, G, 4))))
     wgs = [w for w in wgs if 0 <= w < G]
@@ -129,3 +129,13 @@ def test_misaligned_fallback_plan_indexing(shape):
     else:
         pytest.fail("no plan without vector loads")
     _check_all(shape, p)
+
+
+def test_split_plans_indexing():
+    """The split plans the GPU test runs: every range's partial output stored
+    once into its workspace slice, and the fixed-order sum equal to the oracle."""
+    from tests.test_gpu_parity import SPLIT_SHAPE, split_plans
+    plans = split_plans(SPLIT_SHAPE)
+    assert len(plans) >= 2
+    for p in plans:
+        _check_all(SPLIT_SHAPE, p)

@@ -82,7 +82,11 @@ def test_plan_invariants(shape):
     assert plan["pred_bytes"]["hbm"] >= compulsory * (1 - 1e-12)
     # each level moves at least the bytes it must deliver once
     assert plan["pred_bytes"]["lds"] >= (N * C * H * W + K * C * R * S) * e * (1 - 1e-12) or R * S == 1
-    assert plan["pred_total_us"] == max(list(plan["pred_us"].values()) + [plan["pred_mfma_us"]])
+    slowest = max(list(plan["pred_us"].values()) + [plan["pred_mfma_us"]])
+    if plan["split_c"] > 1:  # plus the second pass that adds the channel ranges
+        assert plan["pred_total_us"] > slowest
+    else:
+        assert plan["pred_total_us"] == slowest
     # deterministic and cached
     assert B.conv_fwd_plan(*dims, dtype=dtype) == plan
     cands = B.conv_fwd_candidates(*dims, dtype=dtype)
