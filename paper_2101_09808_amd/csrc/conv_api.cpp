@@ -37,12 +37,13 @@ std::mutex g_mu;
 std::map<Key, Entry> g_cache;
 
 // Alignment bits of a call: vector loads of In (4 fp32) or Ker need a
-// 16-byte aligned tensor.
-enum { ALIGN_KER = 1, ALIGN_IN = 2, ALIGN_ALL = 3 };
+// 16-byte aligned tensor; the transposing bf16 kernel loads In in dwords.
+enum { ALIGN_KER = 1, ALIGN_IN = 2, ALIGN_IN4 = 4, ALIGN_ALL = 7 };
 
 int alignment_of(const void* In, const void* Ker) {
   return ((reinterpret_cast<uintptr_t>(Ker) & 15) == 0 ? ALIGN_KER : 0) |
-         ((reinterpret_cast<uintptr_t>(In) & 15) == 0 ? ALIGN_IN : 0);
+         ((reinterpret_cast<uintptr_t>(In) & 15) == 0 ? ALIGN_IN : 0) |
+         ((reinterpret_cast<uintptr_t>(In) & 3) == 0 ? ALIGN_IN4 : 0);
 }
 
 // Does variant v run with tensors of this alignment?
@@ -50,6 +51,7 @@ bool variant_fits(const Variant& v, int dtype, int align) {
   const int elem = dtype == CONV_DTYPE_BF16 ? 2 : 4;
   if (v.ker_vec * elem > elem && v.family != FAMILY_BF16 && !(align & ALIGN_KER)) return false;
   if (v.family == FAMILY_DMA && v.in_vec > 1 && !(align & ALIGN_IN)) return false;
+  if (v.family == FAMILY_BF16_TR && !(align & ALIGN_IN4)) return false;
   return true;
 }
 
@@ -209,7 +211,7 @@ int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S, const con
       g.lds_in_elems, g.lds_ker_elems, g.ni_in, g.ni_ker, g.nchunks,
       v->wk, v->wp, v->tc, v->rc, v->sc, v->max_ni, v->max_nk, v->ker_vec, v->threads, lds,
       v->family, v->in_vec, v->stages, g.stage_elems, g.in_region, (int32_t)g.in_bytes,
-      (int32_t)g.ker_bytes, g.grid, 0, 0, 0, g.split, g.cps};
+      (int32_t)g.ker_bytes, g.grid, 0, 0, 0, g.split, g.cps, v->mfma32};
   for (int i = 0; i < cap && i < CONV_GEOM_FIELDS; ++i) out[i] = f[i];
   return CONV_GEOM_FIELDS;
 }

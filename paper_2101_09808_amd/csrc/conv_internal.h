@@ -21,6 +21,7 @@ enum {
   FAMILY_BF16 = 3,    // bf16 inputs: persistent, channel-fastest transposed LDS tiles
   FAMILY_STREAM1X1 = 4,  // pointwise: Ker resident in LDS, In streamed to registers (unrolled C)
   FAMILY_STREAM1X1_LOOP = 5,  // the same for any C % 4 == 0, looped over channel quads
+  FAMILY_BF16_TR = 6,  // bf16 inputs, C = 32: shifted pixel-fastest LDS copies, transposing reads
 };
 
 // One compiled kernel instance (template parameters of the kernel family).
@@ -41,6 +42,7 @@ struct Variant {
   int in_vec;     // In load width in elements (DMA family; 1 for STAGED)
   int threads;    // threads per workgroup
   int stages;     // pipeline depth (LDS buffers)
+  int mfma32;     // DMA: 1 = 32x32x2 inner loop (64-row k tile, 32-pixel blocks)
 };
 
 // Fully resolved launch geometry, passed by value to the kernels.

@@ -328,7 +328,13 @@ __device__ __forceinline__ void wait_vmcnt_opaque() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <int WK, int WP, int NW, int TC, int RC, int SC, int NS, int NLI, int KVI, int NLK, int KVK>
+// MF32 selects the inner loop: false, WK x WP blocks of 16x16 on
+// v_mfma_f32_16x16x4f32 (four channels per step); true, a 64-row k tile
+// (WK = 4) times WP/2 blocks of 32 pixels on v_mfma_f32_32x32x2f32 (two
+// channels per step), whose accumulators need no dependency padding and
+// which reads half the operand registers per flop.
+template <int WK, int WP, int NW, int TC, int RC, int SC, int NS, int NLI, int KVI, int NLK, int KVK,
+          bool MF32 = false>
 __global__ void __launch_bounds__(NW * 64)
 conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
                     float* __restrict__ Out, const Geom g) {
@@ -390,12 +396,17 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
       ker_m[i] = m;
     }
   }
+  static_assert(!MF32 || (WK == 4 && WP % 2 == 0), "32x32 blocks: 64 k rows, pixel blocks in pairs of 16");
+  constexpr int NPB = MF32 ? WP / 2 : WP;  // pixel blocks of this wave (32 or 16 wide)
+  constexpr int BW = MF32 ? 32 : 16;       // block width
+  const int l32 = lane & 31, h32 = lane >> 5;
+  const int jl = MF32 ? l32 : j;           // this lane's column within a pixel block
   // Per-lane LDS offsets of this lane's output pixel in each pixel block.
   const int tpx = g.tr * g.tw;
-  int poff[WP];
+  int poff[NPB];
 #pragma unroll
-  for (int pb = 0; pb < WP; ++pb) {
-    const int px = (wp * WP + pb) * 16 + j;
+  for (int pb = 0; pb < NPB; ++pb) {
+    const int px = wp * WP * 16 + pb * BW + jl;
     const int row_i = px / g.tw, col = px - row_i * g.tw;
     const int rho = t.rho0 + row_i;
     int off = 0;
@@ -405,9 +416,11 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
     }
     poff[pb] = off;
   }
-  int koff[WK];
+  constexpr int NKB = MF32 ? 2 : WK;  // k blocks of this wave (32 or 16 rows)
+  int koff[NKB];
 #pragma unroll
-  for (int kb = 0; kb < WK; ++kb) koff[kb] = ((wk * WK + kb) * 16 + j) * g.ker_rstride;
+  for (int kb = 0; kb < NKB; ++kb)
+    koff[kb] = (MF32 ? wk * 64 + kb * 32 + l32 : (wk * WK + kb) * 16 + j) * g.ker_rstride;
 
   auto issue = [&](int ch, int slot) {  // pipeline step ch into stage buffer slot % NS
     const int c0 = ch * TC;
@@ -431,30 +444,34 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
     }
   };
 
-  v4f acc[WK][WP];
+  typedef typename std::conditional<MF32, v16f, v4f>::type acc_t;
+  acc_t acc[NKB][NPB];
 #pragma unroll
-  for (int kb = 0; kb < WK; ++kb)
+  for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-    for (int pb = 0; pb < WP; ++pb) acc[kb][pb] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int pb = 0; pb < NPB; ++pb) acc[kb][pb] = acc_t{};
 
-  // One chunk: steps st = (channel quad cs, tap r, tap s).  The operands of
-  // step st+1 are read from LDS before the MFMAs of step st are issued, so
-  // LDS latency overlaps the matrix core instead of stalling it.
+  // One chunk: steps st = (channel group cs, tap r, tap s), a group being four
+  // channels (16x16x4) or two (32x32x2).  The operands of step st+1 are read
+  // from LDS before the MFMAs of step st are issued, so LDS latency overlaps
+  // the matrix core instead of stalling it.
   static_assert(RC > 0 && SC > 0, "compile-time taps");
-  constexpr int NSTEP = (TC / 4) * RC * SC;
+  constexpr int CG = MF32 ? 2 : 4;  // channels per step
+  constexpr int NSTEP = (TC / CG) * RC * SC;
+  const int cl = MF32 ? h32 : gq;   // this lane's channel within a group
   auto compute = [&](int buf) {
     const float* lin = lds + buf * STAGE;
     const float* lk = lin + IN_REGION;
-    float a[2][WK], b[2][WP];
+    float a[2][NKB], b[2][NPB];
     auto fetch = [&](int st, int slot) {
       const int cs = st / (RC * SC), rs = st % (RC * SC);
       const int r = rs / SC, s = rs % SC;
-      const float* lin_c = lin + (cs * 4 + gq) * g.in_cstride + r * g.in_wp + s;
-      const float* lk_c = lk + (cs * 4 + gq) * RS + rs;
+      const float* lin_c = lin + (cs * CG + cl) * g.in_cstride + r * g.in_wp + s;
+      const float* lk_c = lk + (cs * CG + cl) * RS + rs;
 #pragma unroll
-      for (int kb = 0; kb < WK; ++kb) a[slot][kb] = lk_c[koff[kb]];
+      for (int kb = 0; kb < NKB; ++kb) a[slot][kb] = lk_c[koff[kb]];
 #pragma unroll
-      for (int pb = 0; pb < WP; ++pb) b[slot][pb] = lin_c[poff[pb]];
+      for (int pb = 0; pb < NPB; ++pb) b[slot][pb] = lin_c[poff[pb]];
     };
     fetch(0, 0);
 #pragma unroll
@@ -462,10 +479,14 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
       const int cur = st & 1;
       if (st + 1 < NSTEP) fetch(st + 1, cur ^ 1);
 #pragma unroll
-      for (int kb = 0; kb < WK; ++kb)
+      for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-        for (int pb = 0; pb < WP; ++pb)
-          acc[kb][pb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[cur][kb], b[cur][pb], acc[kb][pb], 0, 0, 0);
+        for (int pb = 0; pb < NPB; ++pb) {
+          if constexpr (MF32)
+            acc[kb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cur][kb], b[cur][pb], acc[kb][pb], 0, 0, 0);
+          else
+            acc[kb][pb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[cur][kb], b[cur][pb], acc[kb][pb], 0, 0, 0);
+        }
     }
   };
 
@@ -486,25 +507,36 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
     compute(ch % NS);
   }
 
-  // Epilogue: lane (j, gq) holds Out[k0 + block*16 + 4*gq + v][pixel j]; a
-  // split plan writes range split_r's partial sums to slice split_r of the
-  // workspace passed as Out.
+  // Epilogue: lane (j, gq) holds Out[k0 + block*16 + 4*gq + v][pixel j]
+  // (16x16x4), lane (l32, h32) rows 8*(v/4) + 4*h32 + v%4 of pixel l32
+  // (32x32x2); a split plan writes range split_r's partial sums to slice
+  // split_r of the workspace passed as Out.
   const size_t PQ = (size_t)g.P * g.Q;
 #pragma unroll
-  for (int pb = 0; pb < WP; ++pb) {
-    const int px = (wp * WP + pb) * 16 + j;
+  for (int pb = 0; pb < NPB; ++pb) {
+    const int px = wp * WP * 16 + pb * BW + jl;
     const int row_i = px / g.tw, col = px - row_i * g.tw;
     const int rho = t.rho0 + row_i;
     if (px < tpx && rho < t.rho_end && col < t.tw_eff) {
       const int n = rho / g.P, p = rho - n * g.P;
       float* ob = Out + (size_t)split_r * g.N * K * PQ + ((size_t)n * K * g.P + p) * g.Q + t.q0 + col;
 #pragma unroll
-      for (int kb = 0; kb < WK; ++kb)
+      for (int kb = 0; kb < NKB; ++kb) {
+        if constexpr (MF32) {
+          // register v holds row 8*(v/4) + 4*h32 + v%4 of the 32-row block
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int k = t.k0 + (wk * WK + kb) * 16 + 4 * gq + v;
-          if (k < K) ob[(size_t)k * PQ] = acc[kb][pb][v];
+          for (int v = 0; v < 16; ++v) {
+            const int k = t.k0 + wk * 64 + kb * 32 + 8 * (v / 4) + 4 * h32 + v % 4;
+            if (k < K) ob[(size_t)k * PQ] = acc[kb][pb][v];
+          }
+        } else {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int k = t.k0 + (wk * WK + kb) * 16 + 4 * gq + v;
+            if (k < K) ob[(size_t)k * PQ] = acc[kb][pb][v];
+          }
         }
+      }
     }
   }
 }
@@ -718,6 +750,185 @@ conv_bf16_kernel(const unsigned short* __restrict__ In, const unsigned short* __
           for (int v = 0; v < 4; ++v) {
             const int k = k0 + (wk * WK + kb) * 16 + 4 * gq + v;
             if (k < K) ob[(size_t)k * PQ] = acc[kb][pb][v];
+          }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 kernel for C = 32 (one 16x16x32 MFMA covers the whole channel range),
+// K <= 64, taps RC x SC (SC <= 3), W even, tile columns a multiple of 16.
+//
+// The MFMA B operand wants eight consecutive channels of one pixel per lane,
+// while In is NCHW.  Rather than transposing In into a channel-fastest tile,
+// the tile stays pixel-fastest in LDS ([copy][c][row][x], row-major as in
+// memory) and the transposing LDS read of gfx950 (ds_read_b64_tr_b16)
+// produces the operand: within each 16-lane group, source lane s reads four
+// consecutive pixels 4*(s%4).. of channel 4h + s/4 (plus the group's channel
+// octet), and lane i receives pixel i of channels 4h..4h+3.  Those reads must
+// be 8-byte aligned, so each tap column s has its own copy of the tile,
+// shifted by s pixels (copy s at x holds pixel x + s); every channel plane is
+// padded so the four channels of one read fall on distinct banks.
+//
+// The Ker slice (64 k rows) stays in LDS for the whole kernel.  Workgroups
+// are persistent over contiguous tile ranges; each tile's In rows are loaded
+// into registers while the previous tile computes, then written as the SC
+// shifted copies (copy 1 is the funnel shift of neighbouring dwords).
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef short v8s __attribute__((ext_vector_type(8)));
+
+template <int TR, int TW, int RC, int SC>
+__global__ void __launch_bounds__(kThreads)
+conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short* __restrict__ Ker,
+                    float* __restrict__ Out, const Geom g) {
+  static_assert(SC >= 1 && SC <= 3, "copies from two neighbouring dwords");
+  static_assert(TW % 16 == 0 && (TR * (TW / 16)) % 4 == 0, "whole blocks of 16 for four waves");
+  extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int RS = RC * SC;
+  constexpr int KPITCH = (RS & 1) ? RS : RS + 1;  // Ker taps per row (odd: conflict-free rows)
+  constexpr int KER_BYTES = 64 * KPITCH * 64;
+  constexpr int IN_ROWS = TR + RC - 1;            // tiles never straddle images (P % TR == 0)
+  constexpr int CP = IN_ROWS * TW + (16 - (IN_ROWS * TW) % 64 + 64) % 64;  // plane: 16 (mod 64) elements
+  static_assert(CP % 64 == 16 && CP >= IN_ROWS * TW, "channel plane padding");
+  constexpr int HALF = TW / 2;                    // dwords per tile row
+  constexpr int GPR = HALF / 4;                   // groups of four dwords per tile row
+  constexpr int NITEMS = 32 * IN_ROWS * GPR;
+  constexpr int NIT = (NITEMS + kThreads - 1) / kThreads;
+  constexpr int CBR = TW / 16;                    // blocks per tile row
+  constexpr int WP = TR * CBR / 4;                // blocks per wave
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int j = lane & 15, gq = lane >> 4;
+  const int H = g.H, W = g.W, K = g.K, P = g.P, Q = g.Q;
+  unsigned char* lker = smem;
+  unsigned short* lin = reinterpret_cast<unsigned short*>(smem + KER_BYTES);
+  const int tiles = g.tiles_rows * g.tiles_cols;
+  const int G = gridDim.x;
+  const int L = xcd_remap(blockIdx.x, G);
+  const int per = (tiles + G - 1) / G;
+  const int t_begin = L * per, t_end = min(tiles, t_begin + per);
+  if (t_begin >= t_end) return;
+
+  // Ker -> LDS once: [k][tap][8 octets of channels, swizzled], rows past K zero
+  for (int it = tid; it < 64 * RS * 4; it += kThreads) {
+    const int o = it & 3, rest = it >> 2;
+    const int rs = rest % RS, kl = rest / RS;
+    v8u16 v;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = kl < K ? Ker[((size_t)kl * 32 + 8 * o + e) * RS + rs] : (unsigned short)0;
+    *reinterpret_cast<v8u16*>(lker + ((size_t)kl * KPITCH + rs) * 64 + chunk_swz(o, kl) * 16) = v;
+  }
+
+  // Tile T: output rows [rho0, rho0 + TR) of the flattened n*P + p index (one
+  // image), columns [q0, q0 + TW).
+  auto tile_start = [&](int T, int& n, int& p0, int& q0) __attribute__((always_inline)) {
+    const int ct = T % g.tiles_cols, rt = T / g.tiles_cols;
+    const int rho0 = rt * TR;
+    n = rho0 / P;
+    p0 = rho0 - n * P;
+    q0 = ct * TW;
+  };
+
+  // In rows of a tile -> registers: item it = (channel c, row, group gr of
+  // four dwords); it holds pixels q0+8gr .. q0+8gr+9 (dwords 4gr .. 4gr+4,
+  // the last one for the shifted copies).
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned short*>(In), (short)0, (int)g.in_bytes, 0x00020000);
+  unsigned dw[NIT][5];
+  auto gload = [&](int T) __attribute__((always_inline)) {
+    int n, p0, q0;
+    tile_start(T, n, p0, q0);
+#pragma unroll
+    for (int i = 0; i < NIT; ++i) {
+      const int it = tid + i * kThreads;
+      const int gr = it % GPR, cr = it / GPR;
+      const int c = cr / IN_ROWS, row = cr - c * IN_ROWS;
+      const int x = q0 + 8 * gr;
+      const bool ok = it < NITEMS;
+      const unsigned base = (unsigned)((((n * 32 + c) * H + p0 + row) * W + x) * 2);
+#pragma unroll
+      for (int e = 0; e < 5; ++e)  // pixel pair x + 2e, x + 2e + 1 (W even: both in or both out)
+        dw[i][e] = __builtin_amdgcn_raw_buffer_load_b32(rsrc, ok && x + 2 * e < W ? base + 4u * e : kOob, 0, 0);
+    }
+  };
+  auto lstore = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NIT; ++i) {
+      const int it = tid + i * kThreads;
+      if (it < NITEMS) {
+        const int gr = it % GPR, cr = it / GPR;
+        const int c = cr / IN_ROWS, row = cr - c * IN_ROWS;
+        v4u* dst = reinterpret_cast<v4u*>(lin + c * CP + row * TW + 8 * gr);  // 16-byte aligned
+        dst[0] = v4u{dw[i][0], dw[i][1], dw[i][2], dw[i][3]};  // copy 0: pixel x
+        if constexpr (SC > 1) {                                 // copy 1: x + 1
+          v4u v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = (dw[i][e] >> 16) | (dw[i][e + 1] << 16);
+          dst[32 * CP / 8] = v;
+        }
+        if constexpr (SC > 2) dst[32 * CP / 4] = v4u{dw[i][1], dw[i][2], dw[i][3], dw[i][4]};  // copy 2: x + 2
+      }
+    }
+  };
+
+  // transposing-read source of this lane: channel 8*gq + 4h + s/4, pixels
+  // 4*(s%4).. of the block (s = lane % 16)
+  const int src_c = 8 * gq + j / 4, src_x = 4 * (j % 4);
+  gload(t_begin);
+  for (int T = t_begin; T < t_end; ++T) {
+    __syncthreads();  // every wave is done with the previous tile's copies
+    lstore();
+    __syncthreads();
+    if (T + 1 < t_end) gload(T + 1);  // in flight during this tile's MFMAs
+    int n, p0, q0;
+    tile_start(T, n, p0, q0);
+    v4f acc[WP][4];
+#pragma unroll
+    for (int bi = 0; bi < WP; ++bi)
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) acc[bi][kb] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < RC; ++r) {
+#pragma unroll
+      for (int sx = 0; sx < SC; ++sx) {
+        const int rs = r * SC + sx;
+        v8bf a[4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+          const int kl = kb * 16 + j;
+          a[kb] = *reinterpret_cast<const v8bf*>(lker + ((size_t)kl * KPITCH + rs) * 64 + chunk_swz(gq, kl) * 16);
+        }
+#pragma unroll
+        for (int bi = 0; bi < WP; ++bi) {
+          // block b = wave * WP + bi: tile row b / CBR, columns 16 * (b % CBR) ..
+          const int b = wave * WP + bi;
+          const unsigned short* src =
+              lin + sx * 32 * CP + src_c * CP + (b / CBR + r) * TW + 16 * (b % CBR) + src_x;
+          const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(src));
+          const v4s hi =
+              __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(src + 4 * CP));
+          const v8bf bop = __builtin_bit_cast(v8bf, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+            acc[bi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[kb], bop, acc[bi][kb], 0, 0, 0);
+        }
+      }
+    }
+    // lane (j, gq) holds Out[k = 16*kb + 4*gq + v][pixel j of block bi]
+    const size_t PQ = (size_t)P * Q;
+#pragma unroll
+    for (int bi = 0; bi < WP; ++bi) {
+      const int b = wave * WP + bi;
+      const int col = q0 + 16 * (b % CBR) + j;
+      if (col < Q) {
+        float* ob = Out + ((size_t)n * K * P + p0 + b / CBR) * Q + col;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int k = kb * 16 + 4 * gq + v;
+            if (k < K) ob[(size_t)k * PQ] = acc[bi][kb][v];
           }
       }
     }
@@ -1112,8 +1323,14 @@ splitk_reduce_kernel(const float* __restrict__ W, float* __restrict__ Out, int64
 
 #define F32_DMA(ID, WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK)                              \
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_DMA, WK, WP, TC, RC, SC, NLI, NLK, KVK, KVI, NW * 64, \
-                   NS},                                                                          \
+                   NS, 0},                                                                       \
            &conv_f32_dma_kernel<WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK>, nullptr}
+
+// the same pipeline with the 32x32x2 inner loop (WK = 4, WP even)
+#define F32_DMA32(ID, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK)                                \
+  Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_DMA, 4, WP, TC, RC, SC, NLI, NLK, KVK, KVI, NW * 64, \
+                   NS, 1},                                                                       \
+           &conv_f32_dma_kernel<4, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK, true>, nullptr}
 
 #define F32_STREAM1X1(ID, UA, UB, D, NQ)                                                   \
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STREAM1X1, 4, UA + UB, 4 * NQ, 1, 1, UA, UB, 1, 1, \
@@ -1124,6 +1341,11 @@ splitk_reduce_kernel(const float* __restrict__ W, float* __restrict__ Out, int64
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STREAM1X1_LOOP, 4, NB1 + NB2, 0, 1, 1, NB1, NB2, \
                    1, 1, kThreads, D},                                                       \
            &conv1x1_stream_loop_kernel<NB1, NB2, D>, nullptr}
+
+#define BF16_TR_INST(ID, TR, TW, RC, SC)                                                       \
+  Instance{Variant{ID, CONV_DTYPE_BF16, FAMILY_BF16_TR, 4, TR * TW / 64, 32, RC, SC, TR, TW, 1, 1, \
+                   kThreads, 1},                                                                  \
+           nullptr, &conv_bf16_tr_kernel<TR, TW, RC, SC>}
 
 #define BF16_INST(ID, WK, WP, RC, SC, MAXIT)                                                  \
   Instance{Variant{ID, CONV_DTYPE_BF16, FAMILY_BF16, WK, WP, 32, RC, SC, MAXIT, 0, 8, 8, kThreads, \
@@ -1165,6 +1387,11 @@ const Instance kInstances[] = {
     F32_DMA(143, 2, 4, 8, 8, 3, 3, 3, 4, 1, 10, 1),
     F32_DMA(144, 4, 2, 4, 8, 3, 3, 3, 4, 1, 19, 1),
     F32_DMA(145, 2, 8, 8, 8, 3, 3, 3, 7, 1, 10, 1),
+    // 32x32x2 inner loop, 3x3 taps: (pixel units of 16 per wave, waves, ...)
+    F32_DMA32(151, 4, 4, 8, 3, 3, 3, 12, 1, 10, 4),
+    F32_DMA32(152, 4, 4, 8, 3, 3, 3, 7, 1, 19, 1),
+    F32_DMA32(153, 4, 8, 8, 3, 3, 3, 4, 1, 10, 1),
+    F32_DMA32(154, 2, 8, 8, 3, 3, 3, 5, 1, 19, 1),
     // 1x1 taps
     F32_DMA(131, 4, 7, 4, 16, 1, 1, 3, 7, 4, 5, 1),
     F32_DMA(132, 4, 7, 4, 16, 1, 1, 4, 7, 4, 5, 1),
@@ -1180,6 +1407,12 @@ const Instance kInstances[] = {
     F32_DMA(123, 4, 4, 4, 16, 1, 1, 3, 4, 4, 2, 4),
     F32_DMA(124, 2, 13, 4, 16, 1, 1, 3, 7, 4, 2, 4),
     F32_DMA(125, 1, 13, 4, 16, 1, 1, 4, 4, 4, 2, 4),
+    // ---- bf16 inputs, C = 32: pixel-fastest shifted LDS copies, transposing reads
+    // (tile rows, tile columns, taps)
+    BF16_TR_INST(211, 7, 64, 3, 3),
+    BF16_TR_INST(212, 4, 64, 3, 3),
+    BF16_TR_INST(213, 8, 64, 3, 3),
+    BF16_TR_INST(214, 8, 32, 3, 3),
     // ---- bf16 inputs (persistent, transposed channel-fastest LDS tiles)
     BF16_INST(201, 4, 4, 3, 3, 3),
     BF16_INST(202, 2, 4, 3, 3, 3),
@@ -1238,7 +1471,8 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
   if (!inst) return CONV_EINVAL;
   int lds_bytes;
   if (v.family == FAMILY_DMA) lds_bytes = v.stages * g.stage_elems * (int)sizeof(float);
-  else if (v.family == FAMILY_BF16 || v.family == FAMILY_STREAM1X1 || v.family == FAMILY_STREAM1X1_LOOP)
+  else if (v.family == FAMILY_BF16 || v.family == FAMILY_BF16_TR || v.family == FAMILY_STREAM1X1 ||
+           v.family == FAMILY_STREAM1X1_LOOP)
     lds_bytes = g.stage_elems;  // bytes
   else lds_bytes = 2 * (g.lds_in_elems + g.lds_ker_elems) * (int)sizeof(float);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);

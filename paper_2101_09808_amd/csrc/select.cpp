@@ -281,6 +281,45 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
     in_rows = std::max<int>(in_rows, (int)(nu1 - nu0 + 1));
   }
   const int RS = s.R * s.S, TC = v.tc;
+  if (v.family == FAMILY_BF16_TR) {
+    // C = 32 and K <= 64 (one channel chunk, one k tile), W even (dword
+    // loads of pixel pairs), columns in blocks of 16, every block of the
+    // tile owned by a wave.  LDS: Ker [64][taps][64 B] + S shifted copies of
+    // the In tile [32 c][in_rows][tw] bf16, channel planes padded to
+    // 16 (mod 64) elements so a transposing read's four channels hit
+    // distinct banks.
+    // Compile-time tile: max_ni rows x max_nk columns, P a multiple of the
+    // rows (a tile never straddles two images).
+    if (s.C != 32 || s.K > 64 || s.W % 2 || nwk != 1 || plan.grid_order != 1) return false;
+    if (tr != v.max_ni || tw != v.max_nk || P % tr) return false;
+    const int kpitch = (RS & 1) ? RS : RS + 1;
+    int64_t cp = (int64_t)in_rows * tw;
+    cp += (16 - cp % 64 + 64) % 64;
+    const int64_t bytes_t = (int64_t)64 * kpitch * 64 + (int64_t)s.S * 32 * cp * 2;
+    if (bytes_t > kHw.lds_bytes || in_rows != tr + s.R - 1) return false;
+    if ((int64_t)s.N * 32 * s.H * s.W * 2 >= (int64_t(1) << 31)) return false;  // below the sentinel
+    Geom q;
+    std::memset(&q, 0, sizeof(q));
+    q.N = s.N; q.C = s.C; q.K = s.K; q.H = s.H; q.W = s.W; q.R = s.R; q.S = s.S;
+    q.P = P; q.Q = Q;
+    q.tr = tr; q.tw = tw;
+    q.tiles_rows = (int)tiles_rows; q.tiles_cols = (int)tiles_cols; q.tiles_k = (int)tiles_k;
+    q.in_rows = in_rows; q.in_wp = tw; q.in_cstride = (int)cp;
+    q.ker_rstride = kpitch;
+    q.nwk = nwk; q.nwp = nwp;
+    q.order = 1;
+    q.num_tiles = (int)num_tiles;
+    q.nchunks = 1;
+    q.split = 1;
+    q.cps = 1;
+    q.stage_elems = (int)bytes_t;
+    q.grid = (int)std::min<int64_t>(num_tiles, (int64_t)kHw.cus);
+    q.in_bytes = (unsigned)((int64_t)s.N * s.C * s.H * s.W * 2);
+    q.ker_bytes = (unsigned)std::min<int64_t>((int64_t)s.K * s.C * RS * 2, 0xffffffffLL);
+    if (g) *g = q;
+    if (lds_bytes) *lds_bytes = (int)bytes_t;
+    return true;
+  }
   if (v.family == FAMILY_BF16) {
     // LDS: Ker [BK][RS or RS+1 taps][64 B] + In [in_rows][in_wp][64 B] (bytes)
     const int in_wp_b = ((tw + s.S - 1) + 1) & ~1;
@@ -440,12 +479,15 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
   plan->num_wg = g.grid;
   plan->split_c = g.split;
 
-  // REG: per wave and per (4 channels, tap), WK + WP operand reads of 64 lanes.
+  // REG: per wave and per (4 channels, tap), WK + WP operand reads of 64
+  // lanes; the 32x32x2 loop reads 2 + WP/2 operands per (2 channels, tap).
   const double waves = (double)g.num_tiles * (g.nwk * g.nwp);
   const int kdepth = (plan->dtype == CONV_DTYPE_BF16) ? 32 : 4;  // reduction per MFMA
   const double steps = (double)g.nchunks * (v->tc / kdepth) * RS;
+  // (per 4 channels: the 32x32x2 loop takes two steps of 2 + WP/2 reads)
+  const double reads_per_step = v->mfma32 ? 2.0 * (2 + v->wp / 2) : (double)(v->wk + v->wp);
   plan->pred_bytes[CONV_LVL_REG] =
-      waves * steps * (v->wk + v->wp) * 64 * ((plan->dtype == CONV_DTYPE_BF16) ? 16.0 : 4.0);
+      waves * steps * reads_per_step * 64 * ((plan->dtype == CONV_DTYPE_BF16) ? 16.0 : 4.0);
 
   // LDS: per workgroup, every channel brings its In halo rows and Ker rows.
   double in_tiles = 0;  // sum over pixel tiles of the halo footprint (elements per channel)
@@ -504,7 +546,8 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
   const double mfma_per_step = (double)v->wk * v->wp;
   const double mfma_cycles = (plan->dtype == CONV_DTYPE_BF16) ? 16.0 : kHw.mfma_f32_cycles;
   const double wave_cycles = steps * ((double)g.cps / g.nchunks) * mfma_per_step * mfma_cycles;
-  const double per_cu = std::ceil((double)g.grid / kHw.cus);
+  // tile executions: grid = tiles x ranges, or fewer persistent workgroups
+  const double per_cu = std::ceil((double)g.num_tiles * g.split / kHw.cus);
   const double waves_per_simd = per_cu * (g.nwk * g.nwp) / kHw.simds_per_cu;
   plan->pred_mfma_us = waves_per_simd * wave_cycles / kHw.clock_hz * 1e6;
   if (plan->dtype == CONV_DTYPE_F32) {
@@ -516,7 +559,10 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
     // SIMD and cover each other's operand waits.
     const double reads_per_mfma = (double)(v->wk + v->wp) / ((double)v->wk * v->wp);
     const bool shared = (g.nwk * g.nwp) > kHw.simds_per_cu;
-    const double eff = std::min(shared ? 0.82 : 0.78, (shared ? 0.70 : 0.53) / reads_per_mfma);
+    double eff = std::min(shared ? 0.82 : 0.78, (shared ? 0.70 : 0.53) / reads_per_mfma);
+    // 32x32x2 loop: full-rate MFMAs from 4 accumulators on, about 2 / (2 + WP/2)
+    // operand reads per 64-cycle MFMA (calibrated on the 3x3 layers)
+    if (v->mfma32) eff = shared ? 0.90 : 0.86;
     plan->pred_mfma_us /= eff;
   }
   tmax = std::max(tmax, plan->pred_mfma_us);
@@ -555,7 +601,8 @@ bool better(const conv_plan_t& a, const conv_plan_t& b) {
   // kernel, then the register-staged fallback for shapes no other takes.
   auto rank = [](int fam) {
     switch (fam) {
-      case FAMILY_STREAM1X1: return 0;
+      case FAMILY_STREAM1X1:
+      case FAMILY_BF16_TR: return 0;
       case FAMILY_DMA:
       case FAMILY_BF16: return 1;
       case FAMILY_STREAM1X1_LOOP: return 2;
@@ -618,15 +665,20 @@ int enumerate_plans(const Shape& s0, int dtype, conv_plan_t* plans, int cap) {
       if (nw % nwk) continue;
       const int nwp = nw / nwk;
       const int BP = 16 * v.wp * nwp;
-      // Column tiles: whole rows, or Q split into m near-equal parts.
+      // Column tiles: whole rows, or Q split into m near-equal parts (the
+      // transposing bf16 kernel: multiples of 16, rows filling the blocks).
       std::vector<int> tws;
-      for (int m = 1; m <= 16; ++m) {
-        const int tw = (int)cdiv(Q, m);
-        if (tw <= BP && std::find(tws.begin(), tws.end(), tw) == tws.end()) tws.push_back(tw);
+      if (v.family == FAMILY_BF16_TR) {
+        tws.push_back(v.max_nk);  // compile-time tile
+      } else {
+        for (int m = 1; m <= 16; ++m) {
+          const int tw = (int)cdiv(Q, m);
+          if (tw <= BP && std::find(tws.begin(), tws.end(), tw) == tws.end()) tws.push_back(tw);
+        }
+        if (Q > BP) tws.push_back(BP);
       }
-      if (Q > BP) tws.push_back(BP);
       for (int tw : tws) {
-        const int tr_max = BP / tw;
+        const int tr_max = v.family == FAMILY_BF16_TR ? v.max_ni : BP / tw;
         // Row tiles: as many rows as fit, or a divisor-friendly smaller count.
         std::vector<int> trs = {tr_max};
         if (tr_max > 1 && P % tr_max) {

@@ -71,6 +71,12 @@ def emulate(g, In, Ker, wgs=None):
     in_size, ker_size, out_size = N * C * H * W, K * C * R * S, N * K * P * Q
     _chk(In.size == in_size and Ker.size == ker_size, "input sizes")
     dma = g["family"] == 2
+    MF32 = bool(g.get("mfma32", 0))
+    _chk(not MF32 or (dma and WK == 4 and WP % 2 == 0), "32x32x2 loop: 64-row k tile, pairs of 16-pixel units")
+    NPB, BW, NKB, CG = (WP // 2, 32, 2, 2) if MF32 else (WP, 16, WK, 4)
+    l32, h32 = np.arange(64) & 31, np.arange(64) >> 5
+    jl = l32 if MF32 else (np.arange(64) & 15)
+    chl = h32 if MF32 else (np.arange(64) >> 4)  # this lane's channel within a step's group
     NW = NT // 64
     if dma:
         NLI, NLK, KVI, NS = g["max_ni"], g["max_nk"], g["in_vec"], g["stages"]
@@ -137,14 +143,15 @@ def emulate(g, In, Ker, wgs=None):
             ok = (i < g["ni_ker"]) & (idx < BK * per_row)
             kl, m = idx // per_row, (idx % per_row) * KV
             ker_items.append((ok, kl, m))
-        # per-lane pixel offsets and Ker rows, per wave
+        # per-lane pixel offsets and Ker rows, per wave (32x32x2 loop: 32-pixel
+        # blocks and 32-row k blocks, lane (l32, h32))
         tpx = g["tr"] * g["tw"]
         waves = []
         for wave in range(nwk * nwp):
             wk, wp = wave % nwk, wave // nwk
             poff, pvalid, pinfo = [], [], []
-            for pb in range(WP):
-                px = (wp * WP + pb) * 16 + j
+            for pb in range(NPB):
+                px = wp * WP * 16 + pb * BW + jl
                 row_i, col = px // g["tw"], px % g["tw"]
                 rho = t["rho0"] + row_i
                 valid = (px < tpx) & (rho < t["rho_end"]) & (col < t["tw_eff"])
@@ -153,9 +160,12 @@ def emulate(g, In, Ker, wgs=None):
                 poff.append(off)
                 pvalid.append(valid)
                 pinfo.append((n, p, col))
-            koff = [((wk * WK + kb) * 16 + j) * g["ker_rstride"] for kb in range(WK)]
+            if MF32:
+                koff = [(wk * 64 + kb * 32 + l32) * g["ker_rstride"] for kb in range(NKB)]
+            else:
+                koff = [((wk * WK + kb) * 16 + j) * g["ker_rstride"] for kb in range(NKB)]
             waves.append(dict(wk=wk, wp=wp, poff=poff, pvalid=pvalid, pinfo=pinfo, koff=koff,
-                              acc=np.zeros((WK, WP, 16, 16))))
+                              acc=np.zeros((NKB, NPB, BW, BW))))
         lin = [np.full(lin_n, np.nan), np.full(lin_n, np.nan)]
         lker = [np.full(lker_n, np.nan), np.full(lker_n, np.nan)]
 
@@ -230,28 +240,28 @@ def emulate(g, In, Ker, wgs=None):
 
         def compute(buf):
             for wv in waves:
-                for cs in range(TC // 4):
+                for cs in range(TC // CG):
                     for r in range(R):
                         for s in range(S):
                             tap = r * g["in_wp"] + s
                             rs = r * S + s
                             A = []
-                            for kb in range(WK):
-                                ai = (cs * 4 + gq) * RS + wv["koff"][kb] + rs
+                            for kb in range(NKB):
+                                ai = (cs * CG + chl) * RS + wv["koff"][kb] + rs
                                 _chk((ai >= 0) & (ai < lker_n), "LDS Ker read out of bounds")
                                 a = lker[buf][ai]
                                 _chk(~np.isnan(a), "LDS Ker read of an element not staged this step")
                                 A.append(a)
-                            for pb in range(WP):
-                                bi = (cs * 4 + gq) * g["in_cstride"] + wv["poff"][pb] + tap
+                            for pb in range(NPB):
+                                bi = (cs * CG + chl) * g["in_cstride"] + wv["poff"][pb] + tap
                                 _chk((bi >= 0) & (bi < lin_n), "LDS In read out of bounds")
                                 bv = lin[buf][bi]
                                 _chk(~np.isnan(bv), "LDS In read of an element not staged this step")
-                                Bm = np.zeros((4, 16))
-                                Bm[gq, j] = bv
-                                for kb in range(WK):
-                                    Am = np.zeros((16, 4))
-                                    Am[j, gq] = A[kb]
+                                Bm = np.zeros((CG, BW))
+                                Bm[chl, jl] = bv
+                                for kb in range(NKB):
+                                    Am = np.zeros((BW, CG))
+                                    Am[jl, chl] = A[kb]
                                     wv["acc"][kb, pb] += Am @ Bm
 
         ch0 = split_r * cps
@@ -263,16 +273,21 @@ def emulate(g, In, Ker, wgs=None):
             if ch + 1 < nch:
                 stage((ch0 + ch + 1) * TC, (ch + 1) & 1)
         for wv in waves:
-            for pb in range(WP):
+            for pb in range(NPB):
                 valid = wv["pvalid"][pb]
                 n, p, col = wv["pinfo"][pb]
-                for kb in range(WK):
-                    for v in range(4):
-                        k = t["k0"] + (wv["wk"] * WK + kb) * 16 + 4 * gq + v
+                for kb in range(NKB):
+                    for v in range(16 if MF32 else 4):
+                        if MF32:
+                            i = 8 * (v // 4) + 4 * h32 + v % 4
+                            k = t["k0"] + wv["wk"] * 64 + kb * 32 + i
+                        else:
+                            i = 4 * gq + v
+                            k = t["k0"] + (wv["wk"] * WK + kb) * 16 + i
                         st = valid & (k < K)
                         dst = ((n * K + k) * P + p) * Q + t["q0"] + col
                         _chk((dst[st] >= 0) & (dst[st] < out_size), "Out store out of bounds")
-                        vals = wv["acc"][kb, pb][4 * gq + v, j]
+                        vals = wv["acc"][kb, pb][i, jl]
                         if split > 1:
                             wdst = split_r * out_size + dst
                             ws[wdst[st]] = vals[st]
@@ -305,6 +320,8 @@ def _swz(chunk, idx):
 def emulate_bf16(g, In, Ker, wgs=None, in_aligned=True):
     """In, Ker: flat float64 arrays holding the bf16 values.  Emulates the
     workgroups ``wgs`` (default all) of the persistent grid."""
+    if g["family"] == 6:
+        return emulate_bf16_tr(g, In, Ker, wgs)
     N, C, K, H, W, R, S, P, Q = (g[x] for x in "N C K H W R S P Q".split())
     _chk(g["family"] == 3 and g["threads"] == 256, "bf16 family geometry")
     WK, WP, MAXIT = g["wk"], g["wp"], g["max_ni"]
@@ -614,4 +631,125 @@ def emulate_stream1x1(g, In, Ker, wgs=None):
             else:
                 for bb in range(NB):
                     block16(lds, k0, px_begin, px_end, px_begin + 16 * bb, nq_run)
+    return out, written
+
+
+# ---------------------------------------------------------------------------
+# bf16 kernel for C = 32 with shifted pixel-fastest LDS copies and
+# transposing reads (conv_bf16_tr_kernel, family 6).
+
+def tr16_b64(M):
+    """ds_read_b64_tr_b16 within one 16-lane group, as measured on gfx950:
+    source lane s supplies four 16-bit values M[s][0..3]; lane i receives
+    R[i][e] = M[4e + i // 4][i % 4]."""
+    R = np.empty((16, 4), dtype=M.dtype)
+    for i in range(16):
+        for e in range(4):
+            R[i, e] = M[4 * e + i // 4, i % 4]
+    return R
+
+
+def emulate_bf16_tr(g, In, Ker, wgs=None):
+    N, C, K, H, W, R, S, P, Q = (g[x] for x in "N C K H W R S P Q".split())
+    _chk(g["family"] == 6 and g["threads"] == 256, "transposing bf16 geometry")
+    TR, TW = g["max_ni"], g["max_nk"]
+    _chk(g["tr"] == TR and g["tw"] == TW and C == 32 and K <= 64 and W % 2 == 0 and P % TR == 0, "tile")
+    RS = R * S
+    IN_ROWS = TR + R - 1
+    CP = g["in_cstride"]
+    _chk(g["in_rows"] == IN_ROWS and CP >= IN_ROWS * TW and CP % 64 == 16, "LDS In planes")
+    kpitch = g["ker_rstride"]
+    _chk(kpitch == (RS if RS % 2 else RS + 1), "Ker pitch")
+    lds_bytes = 64 * kpitch * 64 + S * 32 * CP * 2
+    _chk(lds_bytes == g["stage_elems"] == g["lds_bytes"] and lds_bytes <= 160 * 1024, "LDS bytes")
+    CBR = TW // 16
+    WP = TR * CBR // 4
+    _chk(g["wp"] == WP and TR * CBR == 4 * WP, "blocks per wave")
+    GPR = TW // 8
+    NITEMS = 32 * IN_ROWS * GPR
+    in_size, out_size = N * C * H * W, N * K * P * Q
+    _chk(In.size == in_size and Ker.size == K * C * RS and g["in_bytes"] == in_size * 2, "sizes")
+    out = np.full(out_size, np.nan)
+    written = np.zeros(out_size, np.int64)
+    tiles = g["tiles_rows"] * g["tiles_cols"]
+    G = g["grid"]
+    per = -(-tiles // G)
+    lane = np.arange(64)
+    j, gq = lane & 15, lane >> 4
+    # Ker in LDS: [kl][tap][octet swizzled]; emulate the writes, read them back
+    lker = {}
+    for kl in range(64):
+        for rs in range(RS):
+            for o in range(4):
+                vals = [Ker[(kl * 32 + 8 * o + e) * RS + rs] if kl < K else 0.0 for e in range(8)]
+                lker[(kl, rs, o ^ ((kl >> 1) & 3))] = vals
+    for b in (range(G) if wgs is None else wgs):
+        G8 = G & ~7
+        L = (b & 7) * (G8 >> 3) + (b >> 3) if b < G8 else b
+        for T in range(L * per, min(tiles, (L + 1) * per)):
+            ct, rt = T % g["tiles_cols"], T // g["tiles_cols"]
+            rho0 = rt * TR
+            n, p0 = divmod(rho0, P)
+            q0 = ct * TW
+            lin = np.full(S * 32 * CP, np.nan)
+            for it in range(NITEMS):
+                gr, cr = it % GPR, it // GPR
+                c, row = divmod(cr, IN_ROWS)
+                x = q0 + 8 * gr
+                dw = []
+                for e in range(5):
+                    xe = x + 2 * e
+                    off = ((((n * 32 + c) * H + p0 + row) * W + x) * 2 + 4 * e) if xe < W else 0x80000000
+                    hit = off < g["in_bytes"]
+                    _chk(not hit or xe < W, "dword past the row end")
+                    dw.append((In[off // 2], In[off // 2 + 1]) if hit else (0.0, 0.0))
+                base = c * CP + row * TW + 8 * gr
+                _chk(base % 8 == 0 and base + 8 <= 32 * CP, "LDS copy write")
+                px = [v for pair in dw for v in pair]  # pixels x .. x+9
+                for sx in range(S):
+                    lin[sx * 32 * CP + base: sx * 32 * CP + base + 8] = px[sx:sx + 8]
+            acc = {}
+            for wave in range(4):
+                for bi in range(WP):
+                    bb = wave * WP + bi
+                    brow, bcol = bb // CBR, 16 * (bb % CBR)
+                    a_acc = np.zeros((4, 16, 16))
+                    for r in range(R):
+                        for sx in range(S):
+                            rs = r * S + sx
+                            # A: lane (j, gq) reads octet gq of row kl = 16kb + j
+                            A = np.zeros((4, 16, 32))
+                            for kb in range(4):
+                                for jj in range(16):
+                                    for q in range(4):
+                                        kl = kb * 16 + jj
+                                        A[kb, jj, 8 * q:8 * q + 8] = lker[(kl, rs, q ^ ((kl >> 1) & 3))]
+                            Bm = np.zeros((32, 16))
+                            for grp in range(4):
+                                for h in range(2):
+                                    M = np.zeros((16, 4))
+                                    for s_l in range(16):
+                                        src = (sx * 32 * CP + (8 * grp + s_l // 4 + 4 * h) * CP
+                                               + (brow + r) * TW + bcol + 4 * (s_l % 4))
+                                        _chk(src % 4 == 0 and 0 <= src and src + 4 <= lin.size,
+                                             "transposing read alignment / bounds")
+                                        M[s_l] = lin[src:src + 4]
+                                    Rr = tr16_b64(M)  # lane i: channels 8*grp + 4h + e of pixel i
+                                    for e in range(4):
+                                        Bm[8 * grp + 4 * h + e, :] = Rr[:, e]
+                            _chk(not np.isnan(Bm).any(), "transposing read of an unwritten element")
+                            for kb in range(4):
+                                a_acc[kb] += A[kb] @ Bm
+                    for kb in range(4):
+                        for jj in range(16):
+                            col = q0 + bcol + jj
+                            if col >= Q:
+                                continue
+                            for kk in range(16):
+                                k = kb * 16 + kk
+                                if k >= K:
+                                    continue
+                                dst = ((n * K + k) * P + p0 + brow) * Q + col
+                                out[dst] = a_acc[kb, kk, jj]
+                                written[dst] += 1
     return out, written

@@ -8,7 +8,7 @@ from oracle import conv as oconv
 from paper_2101_09808_amd import conv as B
 from paper_2101_09808_amd.workloads import CONFIGS, ConvShape, make_inputs
 from tests.kernel_emulator import emulate
-from tests.test_gpu_parity import EDGE, VARIANT_SHAPES, _plans_per_variant, small_version
+from tests.test_gpu_parity import BF16_VARIANT_SHAPES, EDGE, bf16_variant_plans, VARIANT_SHAPES, _plans_per_variant, small_version
 
 
 def _run(shape, plan, wgs=None):
@@ -35,9 +35,20 @@ def test_selected_plan_indexing(shape):
     _check_all(shape, B.conv_fwd_plan(*shape.key()))
 
 
-@pytest.mark.parametrize("shape", VARIANT_SHAPES, ids=lambda s: s.name)
-def test_every_variant_indexing(shape):
-    for p in _plans_per_variant(shape.key()):
+def _variant_cases():
+    cases = []
+    for shape in VARIANT_SHAPES:
+        for v in sorted({p["variant"] for p in _plans_per_variant(shape.key())}):
+            cases.append(pytest.param(shape, v, id=f"{shape.name}-v{v}"))
+    return cases
+
+
+@pytest.mark.parametrize("shape,variant", _variant_cases())
+def test_every_variant_indexing(shape, variant):
+    """The plans the GPU test runs for every kernel variant."""
+    plans = [p for p in _plans_per_variant(shape.key()) if p["variant"] == variant]
+    assert plans
+    for p in plans:
         _check_all(shape, p)
 
 
@@ -95,18 +106,23 @@ def test_bf16_full_config_sampled_workgroups():
     assert np.max(np.abs(out[idx] - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
 
 
-@pytest.mark.parametrize("shape", [
-    ConvShape("bf16_var3x3", 2, 40, 72, 11, 13, 3, 3, "bf16", 51),
-    ConvShape("bf16_var1x1", 2, 64, 80, 10, 12, 1, 1, "bf16", 52),
-], ids=lambda s: s.name)
-def test_every_bf16_variant_indexing(shape):
+def _bf16_variant_cases():
+    cases = []
+    for shape in BF16_VARIANT_SHAPES:
+        for v in sorted({p["variant"] for p in bf16_variant_plans(shape)}):
+            cases.append(pytest.param(shape, v, id=f"{shape.name}-v{v}"))
+    return cases
+
+
+@pytest.mark.parametrize("shape,variant", _bf16_variant_cases())
+def test_every_bf16_variant_indexing(shape, variant):
     """The plans the GPU test runs for every bf16 kernel variant."""
     from tests.kernel_emulator import emulate_bf16
     In, Ker = make_inputs(shape)
     In64 = In.float().numpy().astype(np.float64)
     Ker64 = Ker.float().numpy().astype(np.float64)
     ref = oconv.conv_fwd(In64.astype(np.float32), Ker64.astype(np.float32)).reshape(-1)
-    plans = _plans_per_variant(shape.key(), dtype=B.CONV_DTYPE_BF16)
+    plans = [p for p in bf16_variant_plans(shape) if p["variant"] == variant]
     assert plans
     for p in plans:
         g = B.conv_fwd_geometry(*shape.key(), p)
