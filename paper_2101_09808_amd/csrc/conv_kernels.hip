@@ -541,6 +541,18 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
   }
 }
 
+// Compile-time loop: f(std::integral_constant<int, i>) for i = 0..N-1, each
+// call inlined with its own constant (a plain unroll pragma gives up on long
+// bodies, and a rolled loop would index register arrays dynamically).
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
 // ---------------------------------------------------------------------------
 // bf16 inputs, fp32 accumulation (16x16x32 bf16 MFMA).
 //
@@ -760,21 +772,36 @@ conv_bf16_kernel(const unsigned short* __restrict__ In, const unsigned short* __
 // bf16 kernel for C = 32 (one 16x16x32 MFMA covers the whole channel range),
 // K <= 64, taps RC x SC (SC <= 3), W even, tile columns a multiple of 16.
 //
-// The MFMA B operand wants eight consecutive channels of one pixel per lane,
-// while In is NCHW.  Rather than transposing In into a channel-fastest tile,
-// the tile stays pixel-fastest in LDS ([copy][c][row][x], row-major as in
-// memory) and the transposing LDS read of gfx950 (ds_read_b64_tr_b16)
-// produces the operand: within each 16-lane group, source lane s reads four
-// consecutive pixels 4*(s%4).. of channel 4h + s/4 (plus the group's channel
-// octet), and lane i receives pixel i of channels 4h..4h+3.  Those reads must
-// be 8-byte aligned, so each tap column s has its own copy of the tile,
-// shifted by s pixels (copy s at x holds pixel x + s); every channel plane is
-// padded so the four channels of one read fall on distinct banks.
+// The MFMA operand that carries In wants eight consecutive channels of one
+// pixel per lane, while In is NCHW.  Rather than transposing In into a
+// channel-fastest tile, the tile stays pixel-fastest in LDS
+// ([copy][c][row][x], row-major as in memory) and the transposing LDS read of
+// gfx950 (ds_read_b64_tr_b16) produces the operand: within each 16-lane
+// group, source lane s reads four consecutive pixels 4*(s%4).. of channel
+// 4h + s/4 (plus the group's channel octet), and lane i receives pixel i of
+// channels 4h..4h+3.  Those reads must be 8-byte aligned, so each tap column
+// s has its own copy of the tile, shifted by s pixels (copy s at x holds pixel
+// x + s); every channel plane is padded so the four channels of one read fall
+// on distinct banks.
 //
-// The Ker slice (64 k rows) stays in LDS for the whole kernel.  Workgroups
-// are persistent over contiguous tile ranges; each tile's In rows are loaded
-// into registers while the previous tile computes, then written as the SC
-// shifted copies (copy 1 is the funnel shift of neighbouring dwords).
+// The In operand is the MFMA's A side (rows = pixels) and Ker its B side
+// (columns = k), so each lane ends with four consecutive pixels of one k and
+// stores them as one 16-byte vector.
+//
+// The Ker slice (64 k rows) stays in LDS for the whole kernel: it is read
+// once with 16-byte loads in its natural [k][c][r][s] order and scattered
+// into [k][tap][8 octets of channels, swizzled] while the first tile's In
+// loads are in flight.  Workgroups are persistent over contiguous tile ranges.
+// Each tile's In rows are loaded into registers while the previous tile
+// computes (16-byte loads away from the right image edge), then written as
+// the SC shifted copies (copy 1 is the funnel shift of neighbouring dwords).
+//
+// Every workgroup does the same work per tile, so if a tile's results were
+// stored in one burst after its last MFMA, all CUs would store at once and
+// leave HBM idle while they compute.  Instead each wave computes its tile in
+// NPART parts (groups of pixel blocks); the stores of one part are spread
+// over the MFMAs of the next part (the last part's over the first part of the
+// next tile), which keeps writes flowing during the whole kernel.
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef short v8s __attribute__((ext_vector_type(8)));
 
@@ -791,12 +818,19 @@ conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short*
   constexpr int IN_ROWS = TR + RC - 1;            // tiles never straddle images (P % TR == 0)
   constexpr int CP = IN_ROWS * TW + (16 - (IN_ROWS * TW) % 64 + 64) % 64;  // plane: 16 (mod 64) elements
   static_assert(CP % 64 == 16 && CP >= IN_ROWS * TW, "channel plane padding");
-  constexpr int HALF = TW / 2;                    // dwords per tile row
-  constexpr int GPR = HALF / 4;                   // groups of four dwords per tile row
-  constexpr int NITEMS = 32 * IN_ROWS * GPR;
-  constexpr int NIT = (NITEMS + kThreads - 1) / kThreads;
+  constexpr int GPR = TW / 8;                     // groups of four dwords (8 pixels) per tile row
+  constexpr int TPR = 32 * GPR;                   // threads covering one row of all 32 channels
+  static_assert(kThreads % TPR == 0, "whole rows per pass");
+  constexpr int RPT = kThreads / TPR;             // rows per pass
+  constexpr int NIT = (IN_ROWS + RPT - 1) / RPT;  // items per thread
   constexpr int CBR = TW / 16;                    // blocks per tile row
   constexpr int WP = TR * CBR / 4;                // blocks per wave
+  constexpr int NPART = WP % 2 == 0 ? 2 : 1;      // parts per tile
+  constexpr int PB = WP / NPART;                  // blocks per part
+  constexpr int NST = PB * 4;                     // (block, k block) stores per part
+  constexpr int KV = 64 * 32 * RS / 8;            // 16-byte vectors of a 64-row Ker slice
+  constexpr int NKV = KV / kThreads;
+  static_assert(KV % kThreads == 0, "whole Ker vectors per thread");
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int j = lane & 15, gq = lane >> 4;
@@ -809,19 +843,21 @@ conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short*
   const int per = (tiles + G - 1) / G;
   const int t_begin = L * per, t_end = min(tiles, t_begin + per);
   if (t_begin >= t_end) return;
+  // 16-byte output stores need Q % 4 == 0 and a 16-byte aligned Out
+  const bool vec_out = (Q & 3) == 0 && (reinterpret_cast<uintptr_t>(Out) & 15) == 0;
 
-  // Ker -> LDS once: [k][tap][8 octets of channels, swizzled], rows past K zero
-  for (int it = tid; it < 64 * RS * 4; it += kThreads) {
-    const int o = it & 3, rest = it >> 2;
-    const int rs = rest % RS, kl = rest / RS;
-    v8u16 v;
+  // Ker loads first (rows past K read zeros: past the buffer's range)
+  const __amdgpu_buffer_rsrc_t krsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned short*>(Ker), (short)0, (int)g.ker_bytes, 0x00020000);
+  v4u kv[NKV];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = kl < K ? Ker[((size_t)kl * 32 + 8 * o + e) * RS + rs] : (unsigned short)0;
-    *reinterpret_cast<v8u16*>(lker + ((size_t)kl * KPITCH + rs) * 64 + chunk_swz(o, kl) * 16) = v;
+  for (int i = 0; i < NKV; ++i) {
+    const int v = tid + i * kThreads;
+    kv[i] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(krsrc, 16u * v, 0, 0));
   }
+  __builtin_amdgcn_sched_barrier(0);  // all Ker loads ahead of the first tile's
 
-  // Tile T: output rows [rho0, rho0 + TR) of the flattened n*P + p index (one
-  // image), columns [q0, q0 + TW).
+  // Tile T: output rows [p0, p0 + TR) of image n, columns [q0, q0 + TW).
   auto tile_start = [&](int T, int& n, int& p0, int& q0) __attribute__((always_inline)) {
     const int ct = T % g.tiles_cols, rt = T / g.tiles_cols;
     const int rho0 = rt * TR;
@@ -830,109 +866,162 @@ conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short*
     q0 = ct * TW;
   };
 
-  // In rows of a tile -> registers: item it = (channel c, row, group gr of
-  // four dwords); it holds pixels q0+8gr .. q0+8gr+9 (dwords 4gr .. 4gr+4,
-  // the last one for the shifted copies).
+  // In rows of a tile -> registers.  Thread tid loads channel ic, group gr
+  // of four dwords (pixels x = q0+8gr .. x+9: dwords 4gr .. 4gr+4, the last
+  // one for the shifted copies) of rows irow0, irow0 + RPT, ...: per row one
+  // 16-byte load of pixels x .. x+7 and one 4-byte load of x+8, x+9.  A
+  // thread whose group crosses the right edge of the row (x < W < x + 8)
+  // loads the last 8 pixels of the row instead and keeps the number of dwords
+  // it moved back (sh = (x + 8 - W) / 2); the LDS write moves them forward
+  // again, with zeros past the row.  Groups wholly past the row read zeros.
+  // (W >= 8 keeps that load inside the row.)
   const __amdgpu_buffer_rsrc_t rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned short*>(In), (short)0, (int)g.in_bytes, 0x00020000);
-  unsigned dw[NIT][5];
+  const int gr = tid % GPR, ic = (tid / GPR) % 32, irow0 = tid / TPR;
+  v4u q[NIT];
+  unsigned d4[NIT];
+  unsigned sh = 0;
   auto gload = [&](int T) __attribute__((always_inline)) {
     int n, p0, q0;
     tile_start(T, n, p0, q0);
+    const int x = q0 + 8 * gr;
+    const int over = max(0, x + 8 - W);  // pixels past the row end (even; < 8 when x < W)
+    sh = (unsigned)over >> 1;
+    // element offset of (n, ic, p0 + irow0, x)
+    const unsigned base = (unsigned)(((n * 32 + ic) * H + p0 + irow0) * W + x) * 2u;
 #pragma unroll
     for (int i = 0; i < NIT; ++i) {
-      const int it = tid + i * kThreads;
-      const int gr = it % GPR, cr = it / GPR;
-      const int c = cr / IN_ROWS, row = cr - c * IN_ROWS;
-      const int x = q0 + 8 * gr;
-      const bool ok = it < NITEMS;
-      const unsigned base = (unsigned)((((n * 32 + c) * H + p0 + row) * W + x) * 2);
-#pragma unroll
-      for (int e = 0; e < 5; ++e)  // pixel pair x + 2e, x + 2e + 1 (W even: both in or both out)
-        dw[i][e] = __builtin_amdgcn_raw_buffer_load_b32(rsrc, ok && x + 2 * e < W ? base + 4u * e : kOob, 0, 0);
+      const bool ok = irow0 + RPT * i < IN_ROWS && x < W;
+      const unsigned off = base + (unsigned)(RPT * i * W) * 2u;
+      q[i] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsrc, ok ? off - 2u * over : kOob, 0, 0));
+      d4[i] = __builtin_amdgcn_raw_buffer_load_b32(rsrc, ok && x + 8 < W ? off + 16u : kOob, 0, 0);
     }
   };
   auto lstore = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < NIT; ++i) {
-      const int it = tid + i * kThreads;
-      if (it < NITEMS) {
-        const int gr = it % GPR, cr = it / GPR;
-        const int c = cr / IN_ROWS, row = cr - c * IN_ROWS;
-        v4u* dst = reinterpret_cast<v4u*>(lin + c * CP + row * TW + 8 * gr);  // 16-byte aligned
-        dst[0] = v4u{dw[i][0], dw[i][1], dw[i][2], dw[i][3]};  // copy 0: pixel x
-        if constexpr (SC > 1) {                                 // copy 1: x + 1
+      const int row = irow0 + RPT * i;
+      if (row < IN_ROWS) {
+        unsigned dw[5];
+        dw[0] = sh == 0 ? q[i][0] : sh == 1 ? q[i][1] : sh == 2 ? q[i][2] : q[i][3];
+        dw[1] = sh == 0 ? q[i][1] : sh == 1 ? q[i][2] : sh == 2 ? q[i][3] : 0u;
+        dw[2] = sh == 0 ? q[i][2] : sh == 1 ? q[i][3] : 0u;
+        dw[3] = sh == 0 ? q[i][3] : 0u;
+        dw[4] = d4[i];
+        v4u* dst = reinterpret_cast<v4u*>(lin + ic * CP + row * TW + 8 * gr);  // 16-byte aligned
+        dst[0] = v4u{dw[0], dw[1], dw[2], dw[3]};  // copy 0: pixel x
+        if constexpr (SC > 1) {                    // copy 1: x + 1
           v4u v;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = (dw[i][e] >> 16) | (dw[i][e + 1] << 16);
+          for (int e = 0; e < 4; ++e) v[e] = (dw[e] >> 16) | (dw[e + 1] << 16);
           dst[32 * CP / 8] = v;
         }
-        if constexpr (SC > 2) dst[32 * CP / 4] = v4u{dw[i][1], dw[i][2], dw[i][3], dw[i][4]};  // copy 2: x + 2
+        if constexpr (SC > 2) dst[32 * CP / 4] = v4u{dw[1], dw[2], dw[3], dw[4]};  // copy 2: x + 2
       }
+    }
+  };
+
+  gload(t_begin);
+  __builtin_amdgcn_sched_barrier(0);  // both sets of loads in flight before the Ker scatter waits
+  // Ker -> LDS [k][tap][octet of channels, swizzled][8]: element m of the
+  // natural order is (k, c, tap) = (m / (32 RS), (m / RS) % 32, m % RS).
+#pragma unroll
+  for (int i = 0; i < NKV; ++i) {
+    const int v = tid + i * kThreads;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const int m = 8 * v + t;
+      const int kl = m / (32 * RS), rem = m - kl * (32 * RS);
+      const int c = rem / RS, rs = rem - c * RS;
+      const unsigned short val = (unsigned short)(kv[i][t / 2] >> (16 * (t & 1)));
+      *reinterpret_cast<unsigned short*>(lker + ((size_t)kl * KPITCH + rs) * 64 + chunk_swz(c >> 3, kl) * 16 +
+                                         (c & 7) * 2) = val;
+    }
+  }
+
+  // Results of the previous part, stored while the current part computes.
+  // Lane (j, gq) holds Out[k = 16*kb + j][pixels 4*gq .. 4*gq+3 of block bi].
+  // Buffer stores with 32-bit offsets (Out < 2 GB); a masked lane's offset is
+  // past the buffer's range, where the store is dropped.
+  const __amdgpu_buffer_rsrc_t orsrc = __builtin_amdgcn_make_buffer_rsrc(
+      Out, (short)0, (int)((unsigned)g.N * K * P * Q * 4u), 0x00020000);
+  v4f pend[PB][4];
+  bool have_pend = false;
+  int pbase = 0, pcol = 0, ppart = 0;  // element offset of (n, k = j, row p0, column q0 + 4 gq)
+  auto store_pend = [&](auto si) __attribute__((always_inline)) {
+    constexpr int bi = decltype(si)::value / 4, kb = decltype(si)::value % 4;
+    const int b = wave * WP + ppart * PB + bi;
+    const int col = pcol + 16 * (b % CBR);
+    const bool ok = have_pend && kb * 16 + j < K;
+    const unsigned off = (unsigned)(pbase + kb * 16 * P * Q + (b / CBR) * Q + 16 * (b % CBR)) * 4u;
+    if (vec_out) {
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, pend[bi][kb]), orsrc,
+                                             ok && col < Q ? off : kOob, 0, 0);
+    } else {
+      // (the whole vector is reinterpreted: a bit cast of one element
+      // lvalue of a vector compiles to element 0 for every v)
+      const v4u pv = __builtin_bit_cast(v4u, pend[bi][kb]);
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        __builtin_amdgcn_raw_buffer_store_b32(pv[v], orsrc, ok && col + v < Q ? off + 4u * v : kOob, 0, 0);
     }
   };
 
   // transposing-read source of this lane: channel 8*gq + 4h + s/4, pixels
   // 4*(s%4).. of the block (s = lane % 16)
   const int src_c = 8 * gq + j / 4, src_x = 4 * (j % 4);
-  gload(t_begin);
   for (int T = t_begin; T < t_end; ++T) {
-    __syncthreads();  // every wave is done with the previous tile's copies
+    __syncthreads();  // every wave is done with the previous tile's copies (and the Ker writes)
     lstore();
     __syncthreads();
     if (T + 1 < t_end) gload(T + 1);  // in flight during this tile's MFMAs
     int n, p0, q0;
     tile_start(T, n, p0, q0);
-    v4f acc[WP][4];
+    static_for<NPART>([&](auto part) __attribute__((always_inline)) {
+      v4f acc[PB][4];
 #pragma unroll
-    for (int bi = 0; bi < WP; ++bi)
+      for (int bi = 0; bi < PB; ++bi)
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) acc[bi][kb] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int r = 0; r < RC; ++r) {
-#pragma unroll
-      for (int sx = 0; sx < SC; ++sx) {
-        const int rs = r * SC + sx;
-        v8bf a[4];
+        for (int kb = 0; kb < 4; ++kb) acc[bi][kb] = v4f{0.f, 0.f, 0.f, 0.f};
+      static_for<RS>([&](auto rsc) __attribute__((always_inline)) {
+        constexpr int rs = decltype(rsc)::value, r = rs / SC, sx = rs % SC;
+        v8bf kop[4];
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
           const int kl = kb * 16 + j;
-          a[kb] = *reinterpret_cast<const v8bf*>(lker + ((size_t)kl * KPITCH + rs) * 64 + chunk_swz(gq, kl) * 16);
+          kop[kb] = *reinterpret_cast<const v8bf*>(lker + ((size_t)kl * KPITCH + rs) * 64 + chunk_swz(gq, kl) * 16);
         }
 #pragma unroll
-        for (int bi = 0; bi < WP; ++bi) {
-          // block b = wave * WP + bi: tile row b / CBR, columns 16 * (b % CBR) ..
-          const int b = wave * WP + bi;
+        for (int bi = 0; bi < PB; ++bi) {
+          // block b: tile row b / CBR, columns 16 * (b % CBR) ..
+          const int b = wave * WP + decltype(part)::value * PB + bi;
           const unsigned short* src =
               lin + sx * 32 * CP + src_c * CP + (b / CBR + r) * TW + 16 * (b % CBR) + src_x;
           const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(src));
           const v4s hi =
               __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(src + 4 * CP));
-          const v8bf bop = __builtin_bit_cast(v8bf, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+          const v8bf iop = __builtin_bit_cast(v8bf, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
           for (int kb = 0; kb < 4; ++kb)
-            acc[bi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[kb], bop, acc[bi][kb], 0, 0, 0);
+            acc[bi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(iop, kop[kb], acc[bi][kb], 0, 0, 0);
         }
-      }
-    }
-    // lane (j, gq) holds Out[k = 16*kb + 4*gq + v][pixel j of block bi]
-    const size_t PQ = (size_t)P * Q;
+        // this tap's share of the previous part's stores
+        constexpr int s0 = rs * NST / RS, s1 = (rs + 1) * NST / RS;
+        static_for<s1 - s0>([&](auto si) __attribute__((always_inline)) {
+          store_pend(std::integral_constant<int, s0 + decltype(si)::value>{});
+        });
+      });
 #pragma unroll
-    for (int bi = 0; bi < WP; ++bi) {
-      const int b = wave * WP + bi;
-      const int col = q0 + 16 * (b % CBR) + j;
-      if (col < Q) {
-        float* ob = Out + ((size_t)n * K * P + p0 + b / CBR) * Q + col;
+      for (int bi = 0; bi < PB; ++bi)
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int k = kb * 16 + 4 * gq + v;
-            if (k < K) ob[(size_t)k * PQ] = acc[bi][kb][v];
-          }
-      }
-    }
+        for (int kb = 0; kb < 4; ++kb) pend[bi][kb] = acc[bi][kb];
+      have_pend = true;
+      pbase = ((n * K + j) * P + p0) * Q + q0 + 4 * gq;
+      pcol = q0 + 4 * gq;
+      ppart = decltype(part)::value;
+    });
   }
+  static_for<NST>([&](auto si) __attribute__((always_inline)) { store_pend(si); });
 }
 
 // ---------------------------------------------------------------------------
@@ -948,18 +1037,6 @@ conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short*
 // branch-free raw buffer loads: masked lanes start at 2^31, past the buffer's
 // range, and read zeros.  No LDS traffic or barriers for In.  Both kernels
 // require C % 4 == 0 and In below 1 GB (32-bit byte offsets).
-
-// Compile-time loop: f(std::integral_constant<int, i>) for i = 0..N-1, each
-// call inlined with its own constant (a plain unroll pragma gives up on long
-// bodies, and a rolled loop would index register arrays dynamically).
-template <typename F, int... I>
-__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
-  (f(std::integral_constant<int, I>{}), ...);
-}
-template <int N, typename F>
-__device__ __forceinline__ void static_for(F&& f) {
-  static_for_impl(f, std::make_integer_sequence<int, N>{});
-}
 
 // Fully unrolled kernel for a compile-time channel count C = 4 * NQ.
 //
@@ -1343,7 +1420,7 @@ splitk_reduce_kernel(const float* __restrict__ W, float* __restrict__ Out, int64
            &conv1x1_stream_loop_kernel<NB1, NB2, D>, nullptr}
 
 #define BF16_TR_INST(ID, TR, TW, RC, SC)                                                       \
-  Instance{Variant{ID, CONV_DTYPE_BF16, FAMILY_BF16_TR, 4, TR * TW / 64, 32, RC, SC, TR, TW, 1, 1, \
+  Instance{Variant{ID, CONV_DTYPE_BF16, FAMILY_BF16_TR, 4, TR * TW / 64, 32, RC, SC, TR, TW, 8, 1, \
                    kThreads, 1},                                                                  \
            nullptr, &conv_bf16_tr_kernel<TR, TW, RC, SC>}
 

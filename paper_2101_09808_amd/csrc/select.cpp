@@ -283,14 +283,15 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
   const int RS = s.R * s.S, TC = v.tc;
   if (v.family == FAMILY_BF16_TR) {
     // C = 32 and K <= 64 (one channel chunk, one k tile), W even (dword
-    // loads of pixel pairs), columns in blocks of 16, every block of the
-    // tile owned by a wave.  LDS: Ker [64][taps][64 B] + S shifted copies of
+    // loads of pixel pairs) and at least 8 (a row's last 8 pixels are one
+    // 16-byte load), columns in blocks of 16, every block of the tile owned
+    // by a wave.  In and Out below 2 GB (32-bit buffer offsets).  LDS: Ker [64][taps][64 B] + S shifted copies of
     // the In tile [32 c][in_rows][tw] bf16, channel planes padded to
     // 16 (mod 64) elements so a transposing read's four channels hit
     // distinct banks.
     // Compile-time tile: max_ni rows x max_nk columns, P a multiple of the
     // rows (a tile never straddles two images).
-    if (s.C != 32 || s.K > 64 || s.W % 2 || nwk != 1 || plan.grid_order != 1) return false;
+    if (s.C != 32 || s.K > 64 || s.W % 2 || s.W < 8 || nwk != 1 || plan.grid_order != 1) return false;
     if (tr != v.max_ni || tw != v.max_nk || P % tr) return false;
     const int kpitch = (RS & 1) ? RS : RS + 1;
     int64_t cp = (int64_t)in_rows * tw;
@@ -298,6 +299,7 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
     const int64_t bytes_t = (int64_t)64 * kpitch * 64 + (int64_t)s.S * 32 * cp * 2;
     if (bytes_t > kHw.lds_bytes || in_rows != tr + s.R - 1) return false;
     if ((int64_t)s.N * 32 * s.H * s.W * 2 >= (int64_t(1) << 31)) return false;  // below the sentinel
+    if ((int64_t)s.N * s.K * P * Q * 4 >= (int64_t(1) << 31)) return false;
     Geom q;
     std::memset(&q, 0, sizeof(q));
     q.N = s.N; q.C = s.C; q.K = s.K; q.H = s.H; q.W = s.W; q.R = s.R; q.S = s.S;

@@ -317,11 +317,11 @@ def _swz(chunk, idx):
     return chunk ^ ((idx >> 1) & 3)
 
 
-def emulate_bf16(g, In, Ker, wgs=None, in_aligned=True):
+def emulate_bf16(g, In, Ker, wgs=None, in_aligned=True, out_aligned=True):
     """In, Ker: flat float64 arrays holding the bf16 values.  Emulates the
     workgroups ``wgs`` (default all) of the persistent grid."""
     if g["family"] == 6:
-        return emulate_bf16_tr(g, In, Ker, wgs)
+        return emulate_bf16_tr(g, In, Ker, wgs, out_aligned)
     N, C, K, H, W, R, S, P, Q = (g[x] for x in "N C K H W R S P Q".split())
     _chk(g["family"] == 3 and g["threads"] == 256, "bf16 family geometry")
     WK, WP, MAXIT = g["wk"], g["wp"], g["max_ni"]
@@ -649,40 +649,70 @@ def tr16_b64(M):
     return R
 
 
-def emulate_bf16_tr(g, In, Ker, wgs=None):
+def emulate_bf16_tr(g, In, Ker, wgs=None, out_aligned=True):
+    """Transposing-read bf16 kernel (family 6): Ker read in 16-byte vectors of
+    its natural order and scattered into the LDS image; per thread one In
+    group (channel, 8 pixels) on every RPT-th tile row, shifted back at the
+    right edge of the image row; operands In x Ker on the MFMA (rows =
+    pixels); each wave's tile in NPART parts whose 16-byte (or, for Q % 4 != 0
+    or an unaligned Out, 4-byte) stores are checked lane by lane."""
     N, C, K, H, W, R, S, P, Q = (g[x] for x in "N C K H W R S P Q".split())
     _chk(g["family"] == 6 and g["threads"] == 256, "transposing bf16 geometry")
     TR, TW = g["max_ni"], g["max_nk"]
-    _chk(g["tr"] == TR and g["tw"] == TW and C == 32 and K <= 64 and W % 2 == 0 and P % TR == 0, "tile")
+    _chk(g["tr"] == TR and g["tw"] == TW and C == 32 and K <= 64 and W % 2 == 0 and W >= 8
+         and P % TR == 0, "tile")
     RS = R * S
     IN_ROWS = TR + R - 1
     CP = g["in_cstride"]
     _chk(g["in_rows"] == IN_ROWS and CP >= IN_ROWS * TW and CP % 64 == 16, "LDS In planes")
     kpitch = g["ker_rstride"]
     _chk(kpitch == (RS if RS % 2 else RS + 1), "Ker pitch")
-    lds_bytes = 64 * kpitch * 64 + S * 32 * CP * 2
+    ker_bytes_lds = 64 * kpitch * 64
+    lds_bytes = ker_bytes_lds + S * 32 * CP * 2
     _chk(lds_bytes == g["stage_elems"] == g["lds_bytes"] and lds_bytes <= 160 * 1024, "LDS bytes")
     CBR = TW // 16
     WP = TR * CBR // 4
     _chk(g["wp"] == WP and TR * CBR == 4 * WP, "blocks per wave")
+    NPART = 2 if WP % 2 == 0 else 1
+    PB = WP // NPART
     GPR = TW // 8
-    NITEMS = 32 * IN_ROWS * GPR
+    TPR = 32 * GPR
+    _chk(256 % TPR == 0, "whole rows per pass")
+    RPT = 256 // TPR
+    NIT = -(-IN_ROWS // RPT)
     in_size, out_size = N * C * H * W, N * K * P * Q
-    _chk(In.size == in_size and Ker.size == K * C * RS and g["in_bytes"] == in_size * 2, "sizes")
+    _chk(In.size == in_size and Ker.size == K * C * RS and g["in_bytes"] == in_size * 2
+         and g["ker_bytes"] == K * C * RS * 2, "sizes")
+    _chk(out_size * 4 < 2 ** 31 and in_size * 2 < 2 ** 31, "32-bit buffer offsets")
+    OOB = 0x80000000
+    vec_out = Q % 4 == 0 and out_aligned
     out = np.full(out_size, np.nan)
     written = np.zeros(out_size, np.int64)
     tiles = g["tiles_rows"] * g["tiles_cols"]
     G = g["grid"]
     per = -(-tiles // G)
-    lane = np.arange(64)
-    j, gq = lane & 15, lane >> 4
-    # Ker in LDS: [kl][tap][octet swizzled]; emulate the writes, read them back
+    # Ker: thread t, vector i covers elements 8v .. 8v+7 (v = t + 256 i) of
+    # the natural order; rows past K lie past the buffer and read zeros.
+    KV = 64 * 32 * RS // 8
+    _chk(KV % 256 == 0, "whole Ker vectors per thread")
     lker = {}
-    for kl in range(64):
-        for rs in range(RS):
-            for o in range(4):
-                vals = [Ker[(kl * 32 + 8 * o + e) * RS + rs] if kl < K else 0.0 for e in range(8)]
-                lker[(kl, rs, o ^ ((kl >> 1) & 3))] = vals
+    for v in range(KV):
+        off = 16 * v
+        for t in range(8):
+            m = 8 * v + t
+            val = Ker[m] if off + 16 <= g["ker_bytes"] else 0.0
+            _chk(off + 16 <= g["ker_bytes"] or off >= g["ker_bytes"], "Ker vector straddles the end")
+            kl, rem = divmod(m, 32 * RS)
+            c, rs = divmod(rem, RS)
+            addr = (kl * kpitch + rs) * 64 + ((c >> 3) ^ ((kl >> 1) & 3)) * 16 + (c & 7) * 2
+            _chk(0 <= addr and addr + 2 <= ker_bytes_lds, "Ker scatter bounds")
+            _chk(addr not in lker, "Ker element written twice")
+            lker[addr] = val
+    _chk(len(lker) == 64 * RS * 32, "Ker image complete")
+
+    def kval(kl, rs, c):
+        return lker[(kl * kpitch + rs) * 64 + ((c >> 3) ^ ((kl >> 1) & 3)) * 16 + (c & 7) * 2]
+
     for b in (range(G) if wgs is None else wgs):
         G8 = G & ~7
         L = (b & 7) * (G8 >> 3) + (b >> 3) if b < G8 else b
@@ -692,64 +722,85 @@ def emulate_bf16_tr(g, In, Ker, wgs=None):
             n, p0 = divmod(rho0, P)
             q0 = ct * TW
             lin = np.full(S * 32 * CP, np.nan)
-            for it in range(NITEMS):
-                gr, cr = it % GPR, it // GPR
-                c, row = divmod(cr, IN_ROWS)
+            for tid in range(256):
+                gr, ic, irow0 = tid % GPR, (tid // GPR) % 32, tid // TPR
                 x = q0 + 8 * gr
-                dw = []
-                for e in range(5):
-                    xe = x + 2 * e
-                    off = ((((n * 32 + c) * H + p0 + row) * W + x) * 2 + 4 * e) if xe < W else 0x80000000
-                    hit = off < g["in_bytes"]
-                    _chk(not hit or xe < W, "dword past the row end")
-                    dw.append((In[off // 2], In[off // 2 + 1]) if hit else (0.0, 0.0))
-                base = c * CP + row * TW + 8 * gr
-                _chk(base % 8 == 0 and base + 8 <= 32 * CP, "LDS copy write")
-                px = [v for pair in dw for v in pair]  # pixels x .. x+9
-                for sx in range(S):
-                    lin[sx * 32 * CP + base: sx * 32 * CP + base + 8] = px[sx:sx + 8]
-            acc = {}
+                over = max(0, x + 8 - W)
+                sh = over >> 1
+                base = (((n * 32 + ic) * H + p0 + irow0) * W + x) * 2
+                for i in range(NIT):
+                    row = irow0 + RPT * i
+                    ok = row < IN_ROWS and x < W
+                    off = base + RPT * i * W * 2
+                    o16 = off - 2 * over if ok else OOB
+                    o4 = off + 16 if ok and x + 8 < W else OOB
+                    if ok:
+                        rstart = ((n * 32 + ic) * H + p0 + row) * W * 2
+                        _chk(over < 8 and rstart <= o16 and o16 + 16 <= rstart + 2 * W, "16-byte load inside the row")
+                    if o4 != OOB:
+                        _chk(o4 + 4 <= rstart + 2 * W, "4-byte load inside the row")
+                    qv = In[o16 // 2: o16 // 2 + 8] if o16 < g["in_bytes"] else np.zeros(8)
+                    d4 = In[o4 // 2: o4 // 2 + 2] if o4 < g["in_bytes"] else np.zeros(2)
+                    if row >= IN_ROWS:
+                        continue
+                    qd = [qv[2 * e: 2 * e + 2] for e in range(4)]
+                    dw = [qd[e + sh] if e + sh < 4 else np.zeros(2) for e in range(4)] + [d4]
+                    px = np.concatenate(dw)  # pixels x .. x+9 (zeros past the row)
+                    if ok:
+                        for e in range(10):
+                            if x + e < W:
+                                _chk(px[e] == In[(((n * 32 + ic) * H + p0 + row) * W) + x + e], "edge shift")
+                    dst = ic * CP + row * TW + 8 * gr
+                    _chk(dst % 8 == 0 and dst + 8 <= 32 * CP, "LDS copy write")
+                    for sx in range(S):
+                        lin[sx * 32 * CP + dst: sx * 32 * CP + dst + 8] = px[sx:sx + 8]
             for wave in range(4):
-                for bi in range(WP):
-                    bb = wave * WP + bi
-                    brow, bcol = bb // CBR, 16 * (bb % CBR)
-                    a_acc = np.zeros((4, 16, 16))
-                    for r in range(R):
-                        for sx in range(S):
-                            rs = r * S + sx
-                            # A: lane (j, gq) reads octet gq of row kl = 16kb + j
-                            A = np.zeros((4, 16, 32))
-                            for kb in range(4):
-                                for jj in range(16):
-                                    for q in range(4):
-                                        kl = kb * 16 + jj
-                                        A[kb, jj, 8 * q:8 * q + 8] = lker[(kl, rs, q ^ ((kl >> 1) & 3))]
-                            Bm = np.zeros((32, 16))
-                            for grp in range(4):
-                                for h in range(2):
-                                    M = np.zeros((16, 4))
-                                    for s_l in range(16):
-                                        src = (sx * 32 * CP + (8 * grp + s_l // 4 + 4 * h) * CP
-                                               + (brow + r) * TW + bcol + 4 * (s_l % 4))
-                                        _chk(src % 4 == 0 and 0 <= src and src + 4 <= lin.size,
-                                             "transposing read alignment / bounds")
-                                        M[s_l] = lin[src:src + 4]
-                                    Rr = tr16_b64(M)  # lane i: channels 8*grp + 4h + e of pixel i
-                                    for e in range(4):
-                                        Bm[8 * grp + 4 * h + e, :] = Rr[:, e]
-                            _chk(not np.isnan(Bm).any(), "transposing read of an unwritten element")
-                            for kb in range(4):
-                                a_acc[kb] += A[kb] @ Bm
-                    for kb in range(4):
+                for part in range(NPART):
+                    for bi in range(PB):
+                        bb = wave * WP + part * PB + bi
+                        brow, bcol = bb // CBR, 16 * (bb % CBR)
+                        acc = np.zeros((4, 16, 16))  # [kb][pixel][k]
+                        for r in range(R):
+                            for sx in range(S):
+                                rs = r * S + sx
+                                Am = np.zeros((16, 32))  # pixels x channels (transposing reads)
+                                for grp in range(4):
+                                    for h in range(2):
+                                        M = np.zeros((16, 4))
+                                        for s_l in range(16):
+                                            src = (sx * 32 * CP + (8 * grp + s_l // 4 + 4 * h) * CP
+                                                   + (brow + r) * TW + bcol + 4 * (s_l % 4))
+                                            _chk(src % 4 == 0 and 0 <= src and src + 4 <= lin.size,
+                                                 "transposing read alignment / bounds")
+                                            M[s_l] = lin[src:src + 4]
+                                        Rr = tr16_b64(M)  # lane i: channels 8*grp + 4h + e of pixel i
+                                        for e in range(4):
+                                            Am[:, 8 * grp + 4 * h + e] = Rr[:, e]
+                                _chk(not np.isnan(Am).any(), "transposing read of an unwritten element")
+                                for kb in range(4):
+                                    Bm = np.array([[kval(kb * 16 + jj, rs, c) for jj in range(16)] for c in range(32)])
+                                    acc[kb] += Am @ Bm
+                        # stores: lane (j, gq) holds k = 16 kb + j, pixels 4 gq .. 4 gq + 3
                         for jj in range(16):
-                            col = q0 + bcol + jj
-                            if col >= Q:
-                                continue
-                            for kk in range(16):
-                                k = kb * 16 + kk
-                                if k >= K:
-                                    continue
-                                dst = ((n * K + k) * P + p0 + brow) * Q + col
-                                out[dst] = a_acc[kb, kk, jj]
-                                written[dst] += 1
+                            for gq in range(4):
+                                pbase = ((n * K + jj) * P + p0) * Q + q0 + 4 * gq
+                                col = q0 + bcol + 4 * gq
+                                for kb in range(4):
+                                    k = kb * 16 + jj
+                                    off = pbase + kb * 16 * P * Q + brow * Q + bcol
+                                    vals = acc[kb, 4 * gq: 4 * gq + 4, jj]
+                                    if k >= K:
+                                        continue
+                                    if vec_out:
+                                        if col >= Q:
+                                            continue
+                                        _chk(off % 4 == 0 and (off + 4) * 4 <= out_size * 4, "16-byte store")
+                                        lanes = range(4)
+                                    else:
+                                        lanes = [v for v in range(4) if col + v < Q]
+                                    for v in lanes:
+                                        dst = ((n * K + k) * P + p0 + brow) * Q + col + v
+                                        _chk(off + v == dst and col + v < Q, "store offset")
+                                        out[dst] = vals[v]
+                                        written[dst] += 1
     return out, written

@@ -266,9 +266,11 @@ BF16_VARIANT_SHAPES = [
     # C = 32: the transposing-read kernel (tiles of 8 x 32, 4 x 64, 7 x 64)
     ConvShape("bf16_var_c32", 2, 32, 48, 18, 42, 3, 3, "bf16", 53),
     ConvShape("bf16_c32_k64", 1, 32, 64, 58, 66, 3, 3, "bf16", 54),
+    # Q % 4 != 0: 4-byte stores; K < 64
+    ConvShape("bf16_c32_q42", 1, 32, 40, 10, 44, 3, 3, "bf16", 55),
 ]
 # kernel families each shape is there for (others are covered by the shapes before)
-BF16_SHAPE_FAMILIES = {"bf16_c32_k64": {6}}
+BF16_SHAPE_FAMILIES = {"bf16_c32_k64": {6}, "bf16_c32_q42": {6}}
 
 
 def bf16_variant_plans(shape):
@@ -277,6 +279,26 @@ def bf16_variant_plans(shape):
     if fams:
         plans = [p for p in plans if B.conv_fwd_geometry(*shape.key(), p)["family"] in fams]
     return plans
+
+
+def test_bf16_transposing_kernel_unaligned_out():
+    """Out 4 bytes past a 16-byte boundary: the transposing-read kernel falls
+    back from 16-byte to 4-byte stores."""
+    shape = BF16_VARIANT_SHAPES[2]
+    In, Ker = make_inputs(shape)
+    ref = oconv.conv_fwd(host(In), host(Ker))
+    plans = [p for p in bf16_variant_plans(shape) if B.conv_fwd_geometry(*shape.key(), p)["family"] == 6]
+    assert plans
+    buf = torch.full((shape.N * shape.K * shape.P * shape.Q + 4,), 7.0, device=DEV)
+    out = buf[1:1 + shape.N * shape.K * shape.P * shape.Q].view(shape.N, shape.K, shape.P, shape.Q)
+    assert out.data_ptr() % 16 == 4
+    for p in plans:
+        say(f"[gpu] {shape.name} unaligned Out variant={p['variant']}")
+        buf.fill_(7.0)
+        B.conv_fwd_with_plan(In.to(DEV), Ker.to(DEV), p, out=out)
+        torch.cuda.synchronize()
+        assert rel_err(host(out), ref) <= TOL["bf16"], p
+        assert buf[0].item() == 7.0 and (buf[-3:] == 7.0).all()
 
 
 @pytest.mark.parametrize("shape", BF16_VARIANT_SHAPES, ids=lambda s: s.name)

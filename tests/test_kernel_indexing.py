@@ -131,6 +131,24 @@ def test_every_bf16_variant_indexing(shape, variant):
         assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
 
 
+@pytest.mark.parametrize("shape_index", [2, 4])
+def test_bf16_transposing_unaligned_out_indexing(shape_index):
+    """Family 6 with Out off a 16-byte boundary: 4-byte stores, each output
+    once."""
+    from tests.kernel_emulator import emulate_bf16
+    shape = BF16_VARIANT_SHAPES[shape_index]
+    In, Ker = make_inputs(shape)
+    In64 = In.float().numpy().astype(np.float64)
+    Ker64 = Ker.float().numpy().astype(np.float64)
+    ref = oconv.conv_fwd(In64.astype(np.float32), Ker64.astype(np.float32)).reshape(-1)
+    plans = [p for p in bf16_variant_plans(shape) if B.conv_fwd_geometry(*shape.key(), p)["family"] == 6]
+    assert plans
+    g = B.conv_fwd_geometry(*shape.key(), plans[0])
+    out, written = emulate_bf16(g, In64.reshape(-1), Ker64.reshape(-1), out_aligned=False)
+    assert np.all(written == 1)
+    assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
+
+
 @pytest.mark.parametrize("shape", [
     ConvShape("misaligned_1x1_vec_in", 2, 30, 40, 8, 10, 1, 1, "f32", 61),
     ConvShape("misaligned_3x3_vec_ker", 2, 24, 64, 14, 16, 3, 3, "f32", 62),
