@@ -5,6 +5,7 @@
     python bench.py --traffic-parse FETCH_DIR WRITE_DIR
     python bench.py --traffic-run --layer all  (under rocprofv3 --pmc, one counter per run)
     python bench.py --model-check FETCH_DIR WRITE_DIR TCP_TCC_DIR LDS_DIR
+    python bench.py --rank-sweep [N]           (model rank vs measured time, every layer)
 
 A step is one conv_fwd call (tile selection is cached, so the step is the
 kernel launch) on the pointwise layer N=32 C=256 K=64 56x56 1x1 fp32.  Inputs
@@ -52,10 +53,13 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def time_layer(c, steps, warmup):
+def time_layer(c, steps, warmup, queued=False):
     """Average launch duration from HIP events recorded on the launch stream
     around the `steps` back-to-back launches of the timed region (rotating
-    buffer sets), and the host wall time of the same region."""
+    buffer sets), and the host wall time of the same region.  queued: the
+    launches first queue up behind a bounded spin kernel, so that for layers
+    shorter than the host's per-call time the events still see back-to-back
+    kernels (the wall time then includes the spin)."""
     import torch
     from paper_2101_09808_amd import conv as B
     from paper_2101_09808_amd.workloads import make_inputs
@@ -86,6 +90,8 @@ def time_layer(c, steps, warmup):
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    if queued:
+        torch.cuda._sleep(int(sleep_cycles_per_us() * 60 * steps))
     start.record(stream)
     for i in range(steps):
         fn(i % nsets)
@@ -291,6 +297,171 @@ def model_check_parse(layers, dirs, launches=6):
     print(json.dumps(out), flush=True)
 
 
+RANK_JSON = os.path.join(ROOT, "profiles", "model_rank_sweep.json")
+RANK_MD = os.path.join(ROOT, "profiles", "model_rank_sweep.md")
+
+
+def rank_sample(cands, n=100, top=5, seed=0):
+    """Indices (model order) of the plans a rank sweep times: the model's
+    `top` best plans plus a uniform sample without replacement of the rest,
+    `n` in all (Sec. 9 samples about 100 configurations per operator)."""
+    import random
+    head = list(range(min(top, len(cands))))
+    rest = list(range(len(head), len(cands)))
+    return sorted(head + random.Random(seed).sample(rest, max(0, min(n - len(head), len(rest)))))
+
+
+def ranks(x):
+    """Ranks 1..n of the values x, ties sharing their average rank."""
+    order = sorted(range(len(x)), key=lambda i: x[i])
+    r = [0.0] * len(x)
+    i = 0
+    while i < len(order):
+        j = i
+        while j + 1 < len(order) and x[order[j + 1]] == x[order[i]]:
+            j += 1
+        for t in range(i, j + 1):
+            r[order[t]] = (i + j) / 2.0 + 1.0
+        i = j + 1
+    return r
+
+
+def spearman(x, y):
+    """Spearman rank correlation: Pearson correlation of the tie-averaged ranks."""
+    rx, ry = ranks(x), ranks(y)
+    n = len(x)
+    mx, my = sum(rx) / n, sum(ry) / n
+    sxy = sum((a - mx) * (b - my) for a, b in zip(rx, ry))
+    sxx = sum((a - mx) ** 2 for a in rx)
+    syy = sum((b - my) ** 2 for b in ry)
+    return sxy / (sxx * syy) ** 0.5 if sxx > 0 and syy > 0 else float("nan")
+
+
+def topk_loss(times_in_model_order, k):
+    """Loss of performance of the best of the model's top k plans against the
+    best plan measured (Sec. 9): time ratio minus one."""
+    return min(times_in_model_order[:k]) / min(times_in_model_order) - 1.0
+
+
+_SLEEP_RATE = []
+
+
+def sleep_cycles_per_us():
+    """Rate of torch.cuda._sleep (a bounded spin kernel) on this device."""
+    import torch
+    if not _SLEEP_RATE:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(1000)
+        e0.record()
+        torch.cuda._sleep(2_000_000)
+        e1.record()
+        torch.cuda.synchronize()
+        _SLEEP_RATE.append(2_000_000 / max(1.0, e0.elapsed_time(e1) * 1e3))
+    return _SLEEP_RATE[0]
+
+
+def time_plan(c, plan, ins, outs, Ker, reps=10):
+    """Median launch duration of an explicit plan over `reps` launches on
+    rotating buffer sets (after two untimed launches), each bracketed by its
+    own pair of HIP events on the launch stream.  The launches queue up
+    behind a bounded spin kernel and then run back to back, so host time
+    between them does not count (a split plan's launch is its two kernels)."""
+    import ctypes
+    import torch
+    from paper_2101_09808_amd import conv as B
+    L = B.lib()
+    p = B.ConvPlan.from_dict(plan)
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    kp = Ker.data_ptr()
+    n = len(ins)
+
+    def fn(i):
+        st = L.conv_fwd_with_plan(*c.key(), ins[i % n].data_ptr(), kp, outs[i % n].data_ptr(), ctypes.byref(p), sp)
+        if st != B.CONV_OK:
+            raise B.ConvError(st, "conv_fwd_with_plan")
+
+    fn(0)
+    fn(1)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    torch.cuda._sleep(int(sleep_cycles_per_us() * 300 * reps))  # launches below queue up behind it
+    for i, (e0, e1) in enumerate(ev):
+        e0.record(stream)
+        fn(i + 2)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    t = sorted(e0.elapsed_time(e1) * 1e3 for e0, e1 in ev)
+    return t[len(t) // 2]
+
+
+def rank_sweep(configs, n=100, reps=10):
+    """Model validation on the GPU (Sec. 9): per layer, time the model's top
+    5 plans and a uniform sample of the other candidates; report the rank
+    correlation of predicted and measured time and the top-1/2/5 loss, plus
+    the empirical pick among the top 5 (Sec. 10, MOpt-5)."""
+    import torch
+    from paper_2101_09808_amd import conv as B
+    from paper_2101_09808_amd.workloads import make_inputs
+    res = {}
+    for c in configs:
+        dt = B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32
+        cands = B.conv_fwd_candidates(*c.key(), dtype=dt)
+        idx = rank_sample(cands, n=n, seed=c.seed)
+        In0, Ker0 = make_inputs(c)
+        set_bytes = In0.numel() * In0.element_size() + c.N * c.K * c.P * c.Q * 4
+        nsets = max(2, -(-2 * MALL_BYTES // set_bytes) + 1)
+        ins = [In0.cuda() for _ in range(nsets)]
+        outs = [torch.empty(c.N, c.K, c.P, c.Q, device="cuda") for _ in range(nsets)]
+        Ker = Ker0.cuda()
+        for i in range(30):  # clocks up before the first timed plan
+            B.conv_fwd_with_plan(ins[i % nsets], Ker, cands[0], out=outs[i % nsets])
+        rows = []
+        for i in idx:
+            p = cands[i]
+            us = time_plan(c, p, ins, outs, Ker, reps)
+            rows.append({"model_rank": i, "variant": p["variant"], "split_c": p["split_c"],
+                         "tile": [p["tile_k"], p["tile_rows"], p["tile_cols"], p["tile_c"]],
+                         "grid_order": p["grid_order"], "pred_us": p["pred_total_us"], "measured_us": us})
+            print(f"[rank] {c.name} rank {i} v{p['variant']} split {p['split_c']} pred {p['pred_total_us']:.1f} "
+                  f"measured {us:.1f} us", flush=True)
+        t = [r["measured_us"] for r in rows]  # model order
+        best = min(t)
+        res[c.name] = {
+            "candidates": len(cands), "sampled": len(rows),
+            "spearman_rank_vs_measured": spearman([r["model_rank"] for r in rows], t),
+            "spearman_pred_us_vs_measured": spearman([r["pred_us"] for r in rows], t),
+            "top1_loss": topk_loss(t, 1), "top2_loss": topk_loss(t, 2), "top5_loss": topk_loss(t, 5),
+            "mopt1_us": t[0], "mopt5_us": min(t[:5]), "best_sampled_us": best,
+            "best_sampled": min(rows, key=lambda r: r["measured_us"]),
+            "plans": rows,
+        }
+        del ins, outs
+        torch.cuda.empty_cache()
+    return res
+
+
+def rank_report(res):
+    lines = ["# Model-predicted rank vs measured time (Sec. 9), MI355X", "",
+             "Per layer: the model's 5 best plans plus a uniform sample of the other candidates "
+             "(about 100 in all), each the median of 10 launches on rotating buffer sets, every launch "
+             "between its own pair of HIP events, queued behind a spin kernel so that they run back "
+             "to back (no host time).  Spearman "
+             "correlation of the model's order (and of its predicted time) with the measured time; "
+             "top-k loss = best of the model's first k sampled plans over the best sampled plan, "
+             "minus 1; MOpt-1 = the selector's plan, MOpt-5 = best of its top 5 (Sec. 10).", "",
+             "Command: `python bench.py --rank-sweep`", "",
+             "| layer | candidates | sampled | rho(rank) | rho(pred us) | top-1 loss | top-2 loss | top-5 loss "
+             "| MOpt-1 us | MOpt-5 us | best sampled us (variant) |",
+             "|---|---|---|---|---|---|---|---|---|---|---|"]
+    for name, r in res.items():
+        b = r["best_sampled"]
+        lines.append(f"| {name} | {r['candidates']} | {r['sampled']} | {r['spearman_rank_vs_measured']:.2f} | "
+                     f"{r['spearman_pred_us_vs_measured']:.2f} | {100 * r['top1_loss']:.1f}% | "
+                     f"{100 * r['top2_loss']:.1f}% | {100 * r['top5_loss']:.1f}% | {r['mopt1_us']:.1f} | "
+                     f"{r['mopt5_us']:.1f} | {b['measured_us']:.1f} (v{b['variant']}, rank {b['model_rank']}) |")
+    return "\n".join(lines) + "\n"
+
+
 def cpu_baseline(c, budget_s=10.0):
     """The fp64 oracle on this host's cores over a bounded batch sample."""
     import numpy as np
@@ -339,6 +510,10 @@ def main():
     ap.add_argument("--model-check", nargs=4, metavar=("FETCH", "WRITE", "TCP_TCC", "LDS"),
                     help="predicted vs measured bytes per level for every layer, from four counter runs "
                          "of --traffic-run --layer all")
+    ap.add_argument("--rank-sweep", nargs="?", const=100, type=int, metavar="N",
+                    help="model validation: time the model's top 5 and a uniform sample of the other "
+                         "candidates (N plans per layer, default 100) of every layer; writes "
+                         "profiles/model_rank_sweep.{json,md}")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU (got --gpus {args.gpus}); "
@@ -349,7 +524,7 @@ def main():
     import torch
 
     from paper_2101_09808_amd import conv as B
-    from paper_2101_09808_amd.workloads import BY_NAME, CONFIGS
+    from paper_2101_09808_amd.workloads import BY_NAME, CONFIGS, make_inputs
 
     if args.traffic_parse:  # host-only: reads the counter files of two earlier runs
         traffic_parse(BY_NAME[args.layer], args.traffic_parse[0], args.traffic_parse[1], TRAFFIC_FILE)
@@ -363,6 +538,15 @@ def main():
     B.lib()  # fail loudly if the HIP library is missing
     if args.traffic_run:
         traffic_run(list(CONFIGS) if args.layer == "all" else [BY_NAME[args.layer]])
+        return
+    if args.rank_sweep:
+        res = rank_sweep(list(CONFIGS) if args.layer in ("all", HEADLINE) else [BY_NAME[args.layer]],
+                         n=args.rank_sweep)
+        res["_meta"] = {"kernel_sha": kernel_source_hash(), "command": "python bench.py --rank-sweep"}
+        json.dump(res, open(RANK_JSON, "w"), indent=1)
+        md = rank_report({k: v for k, v in res.items() if not k.startswith("_")})
+        open(RANK_MD, "w").write(md)
+        print(md, flush=True)
         return
     c = BY_NAME[args.layer]
 
@@ -411,19 +595,30 @@ def main():
         layers = {}
         for lc in CONFIGS:
             try:
-                lr = time_layer(lc, 50, 5)
+                lr = time_layer(lc, 50, 5, queued=True)
             except B.ConvError as e:
                 layers[lc.name] = {"error": str(e)}
                 continue
             lk = lr["mean_kernel_ms"] * 1e-3
             lpeak = PEAK["bf16_mfma_tflops"] if lc.dtype == "bf16" else PEAK["fp32_mfma_tflops"]
+            lplan = B.conv_fwd_plan(*lc.key(), dtype=B.CONV_DTYPE_BF16 if lc.dtype == "bf16" else B.CONV_DTYPE_F32)
             layers[lc.name] = {
-                "dtype": lc.dtype, "kernel_us": lk * 1e6, "gflops": flops(lc) / lk / 1e9,
+                "dtype": lc.dtype, "variant": lplan["variant"], "split_c": lplan["split_c"],
+                "kernel_us": lk * 1e6, "gflops": flops(lc) / lk / 1e9,
                 "pct_fp32_mfma_peak": 100 * flops(lc) / lk / 1e12 / PEAK["fp32_mfma_tflops"],
                 "pct_dtype_mfma_peak": 100 * flops(lc) / lk / 1e12 / lpeak,
                 "alg_hbm_gbs": alg_bytes(lc) / lk / 1e9,
                 "pct_hbm_peak": 100 * alg_bytes(lc) / lk / 1e9 / PEAK["hbm_gbs"],
             }
+            # Sec. 10 MOpt-5: the fastest of the model's top 5 plans, kept as
+            # the shape's plan by conv_fwd_tune, timed the same way
+            In_t, Ker_t = make_inputs(lc)
+            _, tplan, _ = B.conv_fwd_tune(In_t.cuda(), Ker_t.cuda(), top_n=5, reps=5)
+            del In_t, Ker_t
+            tk = time_layer(lc, 50, 5, queued=True)["mean_kernel_ms"] * 1e-3
+            layers[lc.name].update({"mopt5_variant": tplan["variant"], "mopt5_split_c": tplan["split_c"],
+                                    "mopt5_kernel_us": tk * 1e6, "mopt5_gflops": flops(lc) / tk / 1e9,
+                                    "mopt5_pct_hbm_peak": 100 * alg_bytes(lc) / tk / 1e9 / PEAK["hbm_gbs"]})
         out["per_layer"] = layers
     print(json.dumps(out), flush=True)
 

@@ -19,11 +19,11 @@
  * re-derived for the gfx950 memory hierarchy; see conv_fwd_plan.
  *
  * Ownership: every tensor pointer is DEVICE memory allocated and freed by
- * the caller.  The library keeps a host-side plan cache only; its one device
- * allocation is the temporary workspace of plans that split the channel
- * reduction (split_c > 1), taken from and returned to the device's default
- * memory pool in stream order within the call.  In, Ker and Out must not
- * overlap.
+ * the caller.  The library keeps a host-side plan cache only; its device
+ * allocations are the temporary workspace of plans that split the channel
+ * reduction (split_c > 1) and the scratch buffer of conv_fwd_tune, taken
+ * from and returned to the device's default memory pool in stream order
+ * within the call.  In, Ker and Out must not overlap.
  *
  * Asynchrony: the compute calls enqueue kernels on `stream` (a hipStream_t;
  * NULL = the default stream) and return without synchronising.  A return of
@@ -152,6 +152,35 @@ int conv_fwd_with_plan(int N, int C, int K, int H, int W, int R, int S,
  */
 int conv_fwd_candidates(int N, int C, int K, int H, int W, int R, int S, int dtype,
                         conv_plan_t* plans, int cap);
+
+/*
+ * Limited empirical tuning over the model's best plans (the MOpt-5 variant
+ * of Sec. 10: the model ranks the configurations, the top few are run and
+ * the fastest is kept, which sidesteps effects the model does not capture).
+ *
+ * Times the first `top_n` candidates of conv_fwd_candidates (best first)
+ * that run with these tensors' alignment: each gets one untimed launch and
+ * then `reps` launches on `stream`, each between its own two HIP events and
+ * after a read pass over a 512 MB scratch buffer, so that the caches hold
+ * none of In (as when each call of a network brings new data); the median
+ * launch time in microseconds goes to times_us[i] (times_us may be NULL;
+ * else room for top_n floats).  The scratch buffer is taken from and
+ * returned to the device's default memory pool in stream order.  The fastest plan is written to *plan_out and
+ * becomes the cached plan of this shape, dtype and tensor alignment: later
+ * conv_fwd / conv_fwd_bf16 / conv_fwd_plan calls for them return or run it.
+ *   dtype      : CONV_DTYPE_*; In and Ker as for conv_fwd or conv_fwd_bf16
+ *   Out        : overwritten with Eq. (1) (every candidate computes it)
+ *   top_n      : 1 .. CONV_TUNE_MAX;  reps : 1 .. 1000
+ * Unlike the other compute calls this one blocks until the stream has run
+ * the timed launches (it waits on the second event of each candidate).
+ * Returns the number of plans timed (>= 1), or a negative conv_status_t; on
+ * an error after the first launch Out may hold a partial result and the
+ * cache is unchanged.
+ */
+#define CONV_TUNE_MAX 64
+int conv_fwd_tune(int N, int C, int K, int H, int W, int R, int S, int dtype,
+                  const void* In, const void* Ker, float* Out, int top_n, int reps,
+                  void* stream, conv_plan_t* plan_out, float* times_us);
 
 /*
  * Host-only: the paper's single-level data-movement volume (Sec. 3.2) for a

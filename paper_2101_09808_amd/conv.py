@@ -76,6 +76,9 @@ def lib():
         L.conv_fwd_with_plan.restype = _i32
         L.conv_fwd_candidates.argtypes = shape7 + [_i32, ctypes.POINTER(ConvPlan), _i32]
         L.conv_fwd_candidates.restype = _i32
+        L.conv_fwd_tune.argtypes = shape7 + [_i32, _vp, _vp, _vp, _i32, _i32, _vp, ctypes.POINTER(ConvPlan),
+                                             ctypes.POINTER(ctypes.c_float)]
+        L.conv_fwd_tune.restype = _i32
         L.conv_model_volume.argtypes = [ctypes.POINTER(_i32), ctypes.POINTER(_i64),
                                         ctypes.POINTER(_i64), _i32, ctypes.POINTER(_dbl)]
         L.conv_model_volume.restype = _i32
@@ -163,6 +166,27 @@ def conv_fwd_with_plan(In, Ker, plan, out=None, stream=None):
     if st != CONV_OK:
         raise ConvError(st, "conv_fwd_with_plan")
     return out
+
+
+CONV_TUNE_MAX = 64
+
+
+def conv_fwd_tune(In, Ker, top_n=5, reps=3, out=None, stream=None):
+    """Time the model's `top_n` best plans on these tensors and keep the
+    fastest as the shape's cached plan (Sec. 10, MOpt-5).  In/Ker are fp32
+    or bf16.  Blocks until the timed launches have run.  Returns (out, the
+    chosen plan as a dict, mean launch time in us of each timed plan in the
+    model's order -- the first candidates that suit the tensors' alignment)."""
+    dtype = CONV_DTYPE_BF16 if In.dtype == torch.bfloat16 else CONV_DTYPE_F32
+    shape = _check_inputs(In, Ker, torch.bfloat16 if dtype == CONV_DTYPE_BF16 else torch.float32)
+    out = _out_for(In, shape, out)
+    plan = ConvPlan()
+    times = (ctypes.c_float * max(1, min(int(top_n), CONV_TUNE_MAX)))()
+    n = lib().conv_fwd_tune(*shape, dtype, In.data_ptr(), Ker.data_ptr(), out.data_ptr(), int(top_n),
+                            int(reps), _stream_ptr(stream), ctypes.byref(plan), times)
+    if n < 0:
+        raise ConvError(n, "conv_fwd_tune")
+    return out, plan.to_dict(), [float(times[i]) for i in range(n)]
 
 
 def conv_fwd_plan(N, C, K, H, W, R, S, dtype=CONV_DTYPE_F32):

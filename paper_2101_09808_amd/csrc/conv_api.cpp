@@ -179,6 +179,48 @@ int conv_fwd_candidates(int N, int C, int K, int H, int W, int R, int S, int dty
   return n > 0 ? n : CONV_ENOPLAN;
 }
 
+int conv_fwd_tune(int N, int C, int K, int H, int W, int R, int S, int dtype, const void* In,
+                  const void* Ker, float* Out, int top_n, int reps, void* stream,
+                  conv_plan_t* plan_out, float* times_us) {
+  int st = validate_shape(N, C, K, H, W, R, S);
+  if (st != CONV_OK) return st;
+  if (!In || !Ker || !Out || !plan_out) return CONV_ENULL;
+  if (dtype != CONV_DTYPE_F32 && dtype != CONV_DTYPE_BF16) return CONV_EINVAL;
+  if (top_n < 1 || top_n > CONV_TUNE_MAX || reps < 1 || reps > 1000) return CONV_EINVAL;
+  const Shape s{N, C, K, H, W, R, S};
+  const int align = alignment_of(In, Ker);
+  // the model's best plans (best first) that run with these tensors
+  std::vector<conv_plan_t> buf(4096);
+  const int n = enumerate_plans(s, dtype, buf.data(), (int)buf.size());
+  std::vector<Entry> cand;
+  for (int i = 0; i < n && i < (int)buf.size() && (int)cand.size() < top_n; ++i) {
+    Entry e;
+    e.plan = buf[i];
+    e.v = find_variant(buf[i].variant);
+    if (!e.v || !variant_fits(*e.v, dtype, align) || !resolve_geom(s, *e.v, e.plan, &e.g, nullptr)) continue;
+    cand.push_back(e);
+  }
+  if (cand.empty()) return CONV_ENOPLAN;
+  size_t best = 0;
+  float best_us = 0.f;
+  for (size_t i = 0; i < cand.size(); ++i) {
+    float us = 0.f;
+    st = time_launches(*cand[i].v, cand[i].g, In, Ker, Out, stream, reps, &us);
+    if (st != CONV_OK) return st;
+    if (times_us) times_us[i] = us;
+    if (i == 0 || us < best_us) {
+      best = i;
+      best_us = us;
+    }
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_cache[Key{N, C, K, H, W, R, S, dtype, align}] = cand[best];
+  }
+  *plan_out = cand[best].plan;
+  return (int)cand.size();
+}
+
 int conv_model_volume(const int perm[7], const int64_t N[7], const int64_t T[7], int out_factor,
                       double dv[3]) {
   if (!perm || !N || !T || !dv) return CONV_ENULL;

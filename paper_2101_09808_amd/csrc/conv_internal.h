@@ -73,6 +73,12 @@ bool resolve_geom(const Shape& s, const Variant& v, const conv_plan_t& plan, Geo
 
 // Launch the kernel of variant v (asynchronous).  Returns a conv_status_t.
 int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, float* Out, void* stream);
+// Median duration in microseconds of `reps` launches on `stream` after one
+// untimed launch, each between its own two HIP events and preceded by a pass
+// over a 512 MB stream-ordered scratch buffer (cold caches); waits for the
+// stream.
+int time_launches(const Variant& v, const Geom& g, const void* In, const void* Ker, float* Out,
+                  void* stream, int reps, float* us);
 
 // Selector entry points (host only, no HIP calls).
 int select_plan(const Shape& s, int dtype, conv_plan_t* out);

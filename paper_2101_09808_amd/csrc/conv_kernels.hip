@@ -28,6 +28,7 @@
 #include <mutex>
 #include <type_traits>
 #include <utility>
+#include <vector>
 
 #include "conv_internal.h"
 
@@ -1553,8 +1554,9 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
     lds_bytes = g.stage_elems;  // bytes
   else lds_bytes = 2 * (g.lds_in_elems + g.lds_ker_elems) * (int)sizeof(float);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int ker_elem = v.dtype == CONV_DTYPE_BF16 ? 2 : 4;
   if (v.family != FAMILY_BF16 && v.ker_vec > 1 &&
-      (reinterpret_cast<uintptr_t>(Ker) % (4 * v.ker_vec)) != 0)
+      (reinterpret_cast<uintptr_t>(Ker) % std::min(16, ker_elem * v.ker_vec)) != 0)
     return CONV_EINVAL;
   const void* fn = inst->f32 ? reinterpret_cast<const void*>(inst->f32)
                              : reinterpret_cast<const void*>(inst->bf16);
@@ -1598,6 +1600,68 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
                        static_cast<const unsigned short*>(Ker), Out, g);
   }
   return hipGetLastError() == hipSuccess ? CONV_OK : CONV_EHIP;
+}
+
+// Holds the stream for `ticks` of the 100 MHz wall clock (bounded wait), so
+// that the launches queued behind it start back to back.
+__global__ void delay_kernel(unsigned long long ticks) {
+  const unsigned long long t0 = wall_clock64();
+  while (wall_clock64() - t0 < ticks) __builtin_amdgcn_s_sleep(8);
+}
+
+// Reads n4 float4 of a scratch buffer (its contents are irrelevant), so that
+// whatever a timed launch reads afterwards comes from HBM, not from the L2 or
+// the last-level cache.  The store never happens in practice; it keeps the
+// loads.
+__global__ void evict_kernel(const v4f* __restrict__ buf, int64_t n4, float* __restrict__ sink) {
+  float acc = 0.f;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+    const v4f v = buf[i];
+    acc += v[0] + v[1] + v[2] + v[3];
+  }
+  if (acc == -12345.678f) sink[threadIdx.x] = acc;
+}
+
+constexpr size_t kEvictBytes = size_t(512) << 20;  // twice the last-level cache
+
+int time_launches(const Variant& v, const Geom& g, const void* In, const void* Ker, float* Out,
+                  void* stream, int reps, float* us) {
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  int rc = launch(v, g, In, Ker, Out, stream);  // untimed: first-launch set-up, caches
+  if (rc != CONV_OK) return rc;
+  // Each launch runs after a pass over a 512 MB scratch buffer (so In comes
+  // from HBM, as in a network where every call has new data) and between its
+  // own two events; all of it queued behind a delay of 300 us per launch, so
+  // host time between launches does not count.
+  void* scratch = nullptr;
+  if (hipMallocAsync(&scratch, kEvictBytes, st) != hipSuccess) return CONV_EHIP;
+  std::vector<hipEvent_t> ev(2 * (size_t)reps, nullptr);
+  for (auto& e : ev)
+    if (rc == CONV_OK && hipEventCreate(&e) != hipSuccess) rc = CONV_EHIP;
+  if (rc == CONV_OK) {
+    hipLaunchKernelGGL(delay_kernel, dim3(1), dim3(64), 0, st, (unsigned long long)(100ull * 300 * reps));
+    if (hipGetLastError() != hipSuccess) rc = CONV_EHIP;
+  }
+  for (int i = 0; rc == CONV_OK && i < reps; ++i) {
+    hipLaunchKernelGGL(evict_kernel, dim3(2048), dim3(256), 0, st, static_cast<const v4f*>(scratch),
+                       (int64_t)(kEvictBytes / sizeof(v4f)), static_cast<float*>(scratch));
+    if (hipGetLastError() != hipSuccess) rc = CONV_EHIP;
+    if (rc == CONV_OK && hipEventRecord(ev[2 * i], st) != hipSuccess) rc = CONV_EHIP;
+    if (rc == CONV_OK) rc = launch(v, g, In, Ker, Out, stream);
+    if (rc == CONV_OK && hipEventRecord(ev[2 * i + 1], st) != hipSuccess) rc = CONV_EHIP;
+  }
+  const bool freed = hipFreeAsync(scratch, st) == hipSuccess;
+  if (rc == CONV_OK && !freed) rc = CONV_EHIP;
+  if (rc == CONV_OK && hipEventSynchronize(ev[2 * reps - 1]) != hipSuccess) rc = CONV_EHIP;
+  std::vector<float> t(reps, 0.f);
+  for (int i = 0; rc == CONV_OK && i < reps; ++i)
+    if (hipEventElapsedTime(&t[i], ev[2 * i], ev[2 * i + 1]) != hipSuccess) rc = CONV_EHIP;
+  for (auto& e : ev)
+    if (e) hipEventDestroy(e);
+  if (rc != CONV_OK) return rc;
+  std::sort(t.begin(), t.end());
+  *us = t[reps / 2] * 1000.f;  // median
+  return CONV_OK;
 }
 
 }  // namespace convfwd

@@ -22,7 +22,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     fns = declared_functions()
     for name in ("conv_fwd", "conv_fwd_bf16", "conv_fwd_plan", "conv_fwd_strerror",
-                 "conv_fwd_with_plan", "conv_fwd_candidates", "conv_model_volume"):
+                 "conv_fwd_with_plan", "conv_fwd_candidates", "conv_model_volume", "conv_fwd_tune"):
         assert name in fns
 
 
@@ -85,6 +85,19 @@ def test_bad_plan_rejected_without_launch():
     p.variant = 999
     assert L.conv_fwd_with_plan(*VALID, fake, fake, fake, ctypes.byref(p), None) == B.CONV_EINVAL
     assert L.conv_fwd_plan(*VALID, 7, ctypes.byref(B.ConvPlan())) == B.CONV_EINVAL
+
+
+def test_tune_arguments_rejected_without_launch():
+    L = B.lib()
+    fake = ctypes.c_void_p(0x1000)
+    p = B.ConvPlan()
+    t = (ctypes.c_float * 8)()
+    assert L.conv_fwd_tune(*VALID, 0, fake, fake, None, 5, 3, None, ctypes.byref(p), t) == B.CONV_ENULL
+    assert L.conv_fwd_tune(*VALID, 0, fake, fake, fake, 5, 3, None, None, t) == B.CONV_ENULL
+    assert L.conv_fwd_tune(*VALID, 2, fake, fake, fake, 5, 3, None, ctypes.byref(p), t) == B.CONV_EINVAL
+    for top_n, reps in ((0, 3), (B.CONV_TUNE_MAX + 1, 3), (5, 0), (5, 1001)):
+        assert L.conv_fwd_tune(*VALID, 0, fake, fake, fake, top_n, reps, None, ctypes.byref(p), t) == B.CONV_EINVAL
+    assert L.conv_fwd_tune(0, *VALID[1:], 0, fake, fake, fake, 5, 3, None, ctypes.byref(p), t) == B.CONV_EINVAL
 
 
 def test_strerror():

@@ -378,3 +378,40 @@ def test_split_reduction_parity_and_determinism():
         assert torch.equal(a, b), "two runs differ"
         assert rel_err(host(a), ref) <= TOL["f32"]
         assert np.array_equal(host(gpu_conv(s, In_i, Ker_i, plan=p)).astype(np.float64), ref_i)
+
+
+PLAN_KEYS = ("variant", "tile_k", "tile_rows", "tile_cols", "tile_c", "wave_k", "wave_px", "waves_k",
+             "waves_px", "grid_order", "split_c")
+
+
+def _same_plan(a, b):
+    return all(a[k] == b[k] for k in PLAN_KEYS)
+
+
+TUNE_SHAPES = [
+    ConvShape("tune_f32_3x3", 2, 24, 40, 14, 16, 3, 3, "f32", 81),
+    ConvShape("tune_bf16_c32", 1, 32, 48, 18, 34, 3, 3, "bf16", 82),
+]
+
+
+@pytest.mark.parametrize("shape", TUNE_SHAPES, ids=lambda s: s.name)
+def test_tune_keeps_fastest_of_model_top_plans(shape):
+    """Empirical pick among the model's best plans (Sec. 10): Out is Eq. (1),
+    the plan kept is one of the first top_n candidates with the least time,
+    and later calls for the shape run it."""
+    In, Ker = make_inputs(shape)
+    ref = oconv.conv_fwd(host(In), host(Ker))
+    dt = B.CONV_DTYPE_BF16 if shape.dtype == "bf16" else B.CONV_DTYPE_F32
+    In_d, Ker_d = In.to(DEV), Ker.to(DEV)
+    say(f"[gpu] tune {shape.name}")
+    out, plan, times = B.conv_fwd_tune(In_d, Ker_d, top_n=4, reps=2)
+    torch.cuda.synchronize()
+    assert rel_err(host(out), ref) <= TOL[shape.dtype]
+    cands = B.conv_fwd_candidates(*shape.key(), dtype=dt)[:len(times)]
+    assert 1 <= len(times) <= 4 and all(t > 0 for t in times)
+    idx = [i for i, c in enumerate(cands) if _same_plan(c, plan)]
+    assert idx and times[idx[0]] == min(times)
+    assert _same_plan(B.conv_fwd_plan(*shape.key(), dtype=dt), plan)
+    again = (B.conv_fwd_bf16 if dt == B.CONV_DTYPE_BF16 else B.conv_fwd)(In_d, Ker_d)
+    torch.cuda.synchronize()
+    assert rel_err(host(again), ref) <= TOL[shape.dtype]

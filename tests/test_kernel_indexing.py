@@ -173,3 +173,24 @@ def test_split_plans_indexing():
     assert len(plans) >= 2
     for p in plans:
         _check_all(SPLIT_SHAPE, p)
+
+
+def test_tune_plans_indexing():
+    """The plans the tuning GPU test times: the first four candidates of
+    each of its shapes, every workgroup emulated."""
+    from tests.test_gpu_parity import TUNE_SHAPES
+    from tests.kernel_emulator import emulate_bf16
+    for shape in TUNE_SHAPES:
+        dt = B.CONV_DTYPE_BF16 if shape.dtype == "bf16" else B.CONV_DTYPE_F32
+        for p in B.conv_fwd_candidates(*shape.key(), dtype=dt)[:4]:
+            if dt == B.CONV_DTYPE_BF16:
+                In, Ker = make_inputs(shape)
+                In64 = In.float().numpy().astype(np.float64)
+                Ker64 = Ker.float().numpy().astype(np.float64)
+                ref = oconv.conv_fwd(In64.astype(np.float32), Ker64.astype(np.float32)).reshape(-1)
+                g = B.conv_fwd_geometry(*shape.key(), p)
+                out, written = emulate_bf16(g, In64.reshape(-1), Ker64.reshape(-1))
+                assert np.all(written == 1)
+                assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
+            else:
+                _check_all(shape, p)
