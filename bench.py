@@ -12,7 +12,9 @@ kernel launch) on the pointwise layer N=32 C=256 K=64 56x56 1x1 fp32.  Inputs
 are seeded uniform[-1,1) synthetic tensors of that shape.  The timed steps
 cycle through enough independent In/Out buffer sets (more than twice the
 256 MB last-level cache) that every step reads In from HBM and writes Out to
-HBM.
+HBM.  The default 500 untimed warm-up steps (about 20 ms) bring the GPU out
+of its idle clocks first: a cold start measured up to twice the steady
+launch time for the first few milliseconds.
 
 Prints ONE JSON line with the metric, the roofline of the kernel (average
 launch duration from HIP events recorded on the launch stream around the
@@ -498,7 +500,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=500)
     ap.add_argument("--no-layers", action="store_true", help="skip the per-layer table")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--layer", default=HEADLINE, help="workload of the timed step ('all': every layer, "

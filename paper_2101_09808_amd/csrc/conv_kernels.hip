@@ -290,6 +290,7 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) float lds_float;
 
 constexpr unsigned kOob = 0x80000000u;  // past every buffer's range (tensors < 2 GB)
+constexpr int kStoreNT = 2;  // cache-policy operand of buffer stores: the gfx950 `nt` (streaming) bit
 
 __device__ __forceinline__ v4i make_rsrc(const void* base, unsigned bytes) {
   const unsigned long long p = reinterpret_cast<unsigned long long>(base);
@@ -898,9 +899,9 @@ conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short*
       d4[i] = __builtin_amdgcn_raw_buffer_load_b32(rsrc, ok && x + 8 < W ? off + 16u : kOob, 0, 0);
     }
   };
-  auto lstore = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < NIT; ++i) {
+  auto lstore = [&](auto&& after_item) __attribute__((always_inline)) {
+    static_for<NIT>([&](auto ic_) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic_)::value;
       const int row = irow0 + RPT * i;
       if (row < IN_ROWS) {
         unsigned dw[5];
@@ -919,31 +920,37 @@ conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short*
         }
         if constexpr (SC > 2) dst[32 * CP / 4] = v4u{dw[1], dw[2], dw[3], dw[4]};  // copy 2: x + 2
       }
-    }
+      after_item(ic_);
+    });
   };
 
   gload(t_begin);
-  __builtin_amdgcn_sched_barrier(0);  // both sets of loads in flight before the Ker scatter waits
-  // Ker -> LDS [k][tap][octet of channels, swizzled][8]: element m of the
-  // natural order is (k, c, tap) = (m / (32 RS), (m / RS) % 32, m % RS).
+  __builtin_amdgcn_sched_barrier(0);  // both sets of loads in flight before the Ker staging waits
+  // Ker -> LDS [k][tap][octet of channels, swizzled][8], through the (still
+  // unused) In region: the natural order first, with 16-byte writes, then
+  // each thread gathers the eight channels of one (k, tap, octet) and writes
+  // them as one 16-byte chunk (scattering single elements straight from the
+  // loaded vectors hit the same banks from many lanes).
+  static_assert(64 * 32 * RS * 2 <= SC * 32 * CP * 2, "Ker staging fits the In region");
 #pragma unroll
-  for (int i = 0; i < NKV; ++i) {
-    const int v = tid + i * kThreads;
+  for (int i = 0; i < NKV; ++i) reinterpret_cast<v4u*>(lin)[tid + i * kThreads] = kv[i];
+  __syncthreads();
+  for (int it = tid; it < 64 * RS * 4; it += kThreads) {
+    const int o = it & 3, rest = it >> 2;
+    const int rs = rest % RS, kl = rest / RS;
+    const unsigned short* src = lin + (kl * 32 + 8 * o) * RS + rs;  // element (kl, 8o + e, rs) at e*RS
+    v8u16 val;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const int m = 8 * v + t;
-      const int kl = m / (32 * RS), rem = m - kl * (32 * RS);
-      const int c = rem / RS, rs = rem - c * RS;
-      const unsigned short val = (unsigned short)(kv[i][t / 2] >> (16 * (t & 1)));
-      *reinterpret_cast<unsigned short*>(lker + ((size_t)kl * KPITCH + rs) * 64 + chunk_swz(c >> 3, kl) * 16 +
-                                         (c & 7) * 2) = val;
-    }
+    for (int e = 0; e < 8; ++e) val[e] = src[e * RS];
+    *reinterpret_cast<v8u16*>(lker + ((size_t)kl * KPITCH + rs) * 64 + chunk_swz(o, kl) * 16) = val;
   }
 
   // Results of the previous part, stored while the current part computes.
   // Lane (j, gq) holds Out[k = 16*kb + j][pixels 4*gq .. 4*gq+3 of block bi].
   // Buffer stores with 32-bit offsets (Out < 2 GB); a masked lane's offset is
-  // past the buffer's range, where the store is dropped.
+  // past the buffer's range, where the store is dropped.  Out is never read
+  // back here, so the stores carry the non-temporal hint (measured 3% faster
+  // on the 226^2 layer).
   const __amdgpu_buffer_rsrc_t orsrc = __builtin_amdgcn_make_buffer_rsrc(
       Out, (short)0, (int)((unsigned)g.N * K * P * Q * 4u), 0x00020000);
   v4f pend[PB][4];
@@ -957,23 +964,33 @@ conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short*
     const unsigned off = (unsigned)(pbase + kb * 16 * P * Q + (b / CBR) * Q + 16 * (b % CBR)) * 4u;
     if (vec_out) {
       __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, pend[bi][kb]), orsrc,
-                                             ok && col < Q ? off : kOob, 0, 0);
+                                             ok && col < Q ? off : kOob, 0, kStoreNT);
     } else {
       // (the whole vector is reinterpreted: a bit cast of one element
       // lvalue of a vector compiles to element 0 for every v)
       const v4u pv = __builtin_bit_cast(v4u, pend[bi][kb]);
 #pragma unroll
       for (int v = 0; v < 4; ++v)
-        __builtin_amdgcn_raw_buffer_store_b32(pv[v], orsrc, ok && col + v < Q ? off + 4u * v : kOob, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b32(pv[v], orsrc, ok && col + v < Q ? off + 4u * v : kOob, 0, kStoreNT);
     }
   };
 
   // transposing-read source of this lane: channel 8*gq + 4h + s/4, pixels
   // 4*(s%4).. of the block (s = lane % 16)
   const int src_c = 8 * gq + j / 4, src_x = 4 * (j % 4);
+  // The last part's stores: the first NST_COPY during the LDS copy phase
+  // (one or two per item), the rest over the first part's taps; HBM then
+  // receives writes during the copies too.
+  constexpr int NST_COPY = NST / 2;
   for (int T = t_begin; T < t_end; ++T) {
     __syncthreads();  // every wave is done with the previous tile's copies (and the Ker writes)
-    lstore();
+    lstore([&](auto ic_) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic_)::value;
+      constexpr int s0 = i * NST_COPY / NIT, s1 = (i + 1) * NST_COPY / NIT;
+      static_for<s1 - s0>([&](auto si) __attribute__((always_inline)) {
+        store_pend(std::integral_constant<int, s0 + decltype(si)::value>{});
+      });
+    });
     __syncthreads();
     if (T + 1 < t_end) gload(T + 1);  // in flight during this tile's MFMAs
     int n, p0, q0;
@@ -1006,8 +1023,10 @@ conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short*
           for (int kb = 0; kb < 4; ++kb)
             acc[bi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(iop, kop[kb], acc[bi][kb], 0, 0, 0);
         }
-        // this tap's share of the previous part's stores
-        constexpr int s0 = rs * NST / RS, s1 = (rs + 1) * NST / RS;
+        // this tap's share of the previous part's stores (for the first
+        // part, those not issued during the copies)
+        constexpr int SB = decltype(part)::value == 0 ? NST_COPY : 0;
+        constexpr int s0 = SB + rs * (NST - SB) / RS, s1 = SB + (rs + 1) * (NST - SB) / RS;
         static_for<s1 - s0>([&](auto si) __attribute__((always_inline)) {
           store_pend(std::integral_constant<int, s0 + decltype(si)::value>{});
         });
@@ -1200,7 +1219,9 @@ conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ke
       __builtin_amdgcn_sched_barrier(0);
     });
 
-    // stores: 32 consecutive pixels (two rows of k) or 16 (four rows) per instruction
+    // stores: 32 consecutive pixels (two rows of k) or 16 (four rows) per
+    // instruction, with the non-temporal hint (Out is not read back here;
+    // measured about 3% faster on the 56x56 layer)
 #pragma unroll
     for (int b = 0; b < NB32; ++b) {
       const int px = px_begin + 32 * b + l32;
@@ -1212,7 +1233,7 @@ conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ke
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int k = k0 + 32 * kb + 8 * (v / 4) + 4 * h32 + v % 4;
-            if (k < K) ob[(size_t)k * HW] = acc32[b][kb][v];
+            if (k < K) __builtin_nontemporal_store(acc32[b][kb][v], &ob[(size_t)k * HW]);
           }
       }
     }
@@ -1226,7 +1247,7 @@ conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ke
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             const int k = k0 + 16 * kb + 4 * h16 + v;
-            if (k < K) ob[(size_t)k * HW] = acc16[kb][v];
+            if (k < K) __builtin_nontemporal_store(acc16[kb][v], &ob[(size_t)k * HW]);
           }
       }
     }
@@ -1339,7 +1360,7 @@ conv1x1_stream_loop_kernel(const float* __restrict__ In, const float* __restrict
         }
       }
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
+      for (int b = 0; b < NB; ++b) {  // non-temporal stores, as in the unrolled kernel
         const int px = px_begin + (blk0 + b) * 16 + j;
         if (px < px_end) {
           const int n = px / HW, hw = px - n * HW;
@@ -1349,7 +1370,7 @@ conv1x1_stream_loop_kernel(const float* __restrict__ In, const float* __restrict
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
               const int k = k0 + kb * 16 + 4 * gq + v;
-              if (k < K) ob[(size_t)k * HW] = acc[kb][b][v];
+              if (k < K) __builtin_nontemporal_store(acc[kb][b][v], &ob[(size_t)k * HW]);
             }
         }
       }
@@ -1657,7 +1678,7 @@ int time_launches(const Variant& v, const Geom& g, const void* In, const void* K
   for (int i = 0; rc == CONV_OK && i < reps; ++i)
     if (hipEventElapsedTime(&t[i], ev[2 * i], ev[2 * i + 1]) != hipSuccess) rc = CONV_EHIP;
   for (auto& e : ev)
-    if (e) hipEventDestroy(e);
+    if (e) (void)hipEventDestroy(e);
   if (rc != CONV_OK) return rc;
   std::sort(t.begin(), t.end());
   *us = t[reps / 2] * 1000.f;  // median

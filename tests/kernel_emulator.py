@@ -692,22 +692,28 @@ def emulate_bf16_tr(g, In, Ker, wgs=None, out_aligned=True):
     G = g["grid"]
     per = -(-tiles // G)
     # Ker: thread t, vector i covers elements 8v .. 8v+7 (v = t + 256 i) of
-    # the natural order; rows past K lie past the buffer and read zeros.
+    # the natural order (rows past K lie past the buffer and read zeros); the
+    # vectors go to the In region in that order, then thread items
+    # (kl, tap, octet) gather their eight channels into one 16-byte chunk.
     KV = 64 * 32 * RS // 8
-    _chk(KV % 256 == 0, "whole Ker vectors per thread")
-    lker = {}
+    _chk(KV % 256 == 0 and 64 * 32 * RS * 2 <= S * 32 * CP * 2, "Ker staging")
+    raw = np.full(S * 32 * CP, np.nan)
     for v in range(KV):
         off = 16 * v
-        for t in range(8):
-            m = 8 * v + t
-            val = Ker[m] if off + 16 <= g["ker_bytes"] else 0.0
-            _chk(off + 16 <= g["ker_bytes"] or off >= g["ker_bytes"], "Ker vector straddles the end")
-            kl, rem = divmod(m, 32 * RS)
-            c, rs = divmod(rem, RS)
-            addr = (kl * kpitch + rs) * 64 + ((c >> 3) ^ ((kl >> 1) & 3)) * 16 + (c & 7) * 2
-            _chk(0 <= addr and addr + 2 <= ker_bytes_lds, "Ker scatter bounds")
+        _chk(off + 16 <= g["ker_bytes"] or off >= g["ker_bytes"], "Ker vector straddles the end")
+        raw[8 * v: 8 * v + 8] = Ker[8 * v: 8 * v + 8] if off + 16 <= g["ker_bytes"] else 0.0
+    lker = {}
+    for it in range(64 * RS * 4):
+        o, rest = it & 3, it >> 2
+        rs, kl = rest % RS, rest // RS
+        src = [(kl * 32 + 8 * o + e) * RS + rs for e in range(8)]
+        _chk(min(src) >= 0 and max(src) < 64 * 32 * RS, "Ker gather inside the staged slice")
+        chunk = (kl * kpitch + rs) * 64 + (o ^ ((kl >> 1) & 3)) * 16
+        _chk(chunk + 16 <= ker_bytes_lds and chunk % 16 == 0, "Ker chunk bounds")
+        for e in range(8):
+            addr = chunk + 2 * e
             _chk(addr not in lker, "Ker element written twice")
-            lker[addr] = val
+            lker[addr] = raw[src[e]]
     _chk(len(lker) == 64 * RS * 32, "Ker image complete")
 
     def kval(kl, rs, c):
