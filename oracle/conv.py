@@ -43,6 +43,10 @@ def _load():
         lib.oracle_conv_fwd.restype = i32
         lib.oracle_conv_fwd_points.argtypes = [i32] * 7 + [fp, fp, lp, i64, dp]
         lib.oracle_conv_fwd_points.restype = i32
+        lib.oracle_conv_fwd_ex.argtypes = [i32] * 11 + [fp, fp, dp]
+        lib.oracle_conv_fwd_ex.restype = i32
+        lib.oracle_conv_fwd_ex_points.argtypes = [i32] * 11 + [fp, fp, lp, i64, dp]
+        lib.oracle_conv_fwd_ex_points.restype = i32
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = i32
         _lib = lib
@@ -92,3 +96,48 @@ def conv_fwd_points(In, Ker, flat_idx):
 
 def num_threads():
     return int(_load().oracle_num_threads())
+
+
+def ex_extents(H, W, R, S, stride, pad):
+    """Output extents P, Q of the strided, padded form (None if undefined)."""
+    sh, sw = stride
+    ph, pw = pad
+    if sh <= 0 or sw <= 0 or ph < 0 or pw < 0 or H + 2 * ph < R or W + 2 * pw < S:
+        return None
+    return (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
+
+
+def conv_fwd_ex(In, Ker, stride=(1, 1), pad=(0, 0)):
+    """Strided, zero-padded correlation (see ``conv_ref.c``), float64 [N,K,P,Q]."""
+    In, pin = _f32(In)
+    Ker, pker = _f32(Ker)
+    N, C, H, W = In.shape
+    K, C2, R, S = Ker.shape
+    if C2 != C:
+        raise ValueError("channel mismatch")
+    ext = ex_extents(H, W, R, S, stride, pad)
+    if ext is None:
+        raise ValueError("undefined strided shape")
+    out = np.empty((N, K) + ext, dtype=np.float64)
+    rc = _load().oracle_conv_fwd_ex(N, C, K, H, W, R, S, stride[0], stride[1], pad[0], pad[1], pin, pker,
+                                    out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    if rc != 0:
+        raise ValueError(f"oracle_conv_fwd_ex returned {rc}")
+    return out
+
+
+def conv_fwd_ex_points(In, Ker, flat_idx, stride=(1, 1), pad=(0, 0)):
+    """Selected outputs of the strided, padded form (flat [N,K,P,Q] indices)."""
+    In, pin = _f32(In)
+    Ker, pker = _f32(Ker)
+    N, C, H, W = In.shape
+    K, C2, R, S = Ker.shape
+    idx = np.ascontiguousarray(flat_idx, dtype=np.int64)
+    out = np.empty(idx.size, dtype=np.float64)
+    rc = _load().oracle_conv_fwd_ex_points(
+        N, C, K, H, W, R, S, stride[0], stride[1], pad[0], pad[1], pin, pker,
+        idx.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), idx.size,
+        out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    if rc != 0:
+        raise ValueError(f"oracle_conv_fwd_ex_points returned {rc}")
+    return out

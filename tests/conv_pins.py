@@ -122,3 +122,95 @@ def pin_integer(conv, seed=5):
 
 
 ALL_PINS = (pin_im2col, pin_torch, pin_ones, pin_delta, pin_shift, pin_integer)
+
+
+# ---------------------------------------------------------------------------
+# Pins of the strided, zero-padded form (row f2).  Each takes
+# ``conv_ex(In, Ker, stride, pad) -> float64 [N,K,P,Q]``.
+
+# (N, C, K, H, W, R, S, (sh, sw), (ph, pw)): stride 1-3, unequal strides and
+# pads, 1x1 and 7x7 taps, outputs down to 1x1.
+STRIDED_SHAPES = (
+    (2, 3, 4, 9, 7, 3, 3, (2, 2), (1, 1)),
+    (1, 2, 3, 8, 11, 3, 2, (2, 3), (1, 0)),
+    (2, 4, 3, 6, 6, 1, 1, (2, 2), (0, 0)),
+    (1, 3, 2, 11, 11, 7, 7, (2, 2), (3, 3)),
+    (1, 2, 2, 5, 4, 3, 3, (1, 1), (2, 1)),
+    (2, 1, 3, 4, 4, 4, 4, (3, 3), (0, 0)),
+    (1, 3, 2, 7, 9, 2, 3, (3, 2), (1, 2)),
+)
+
+
+def _ex_extents(H, W, R, S, st, pd):
+    return (H + 2 * pd[0] - R) // st[0] + 1, (W + 2 * pd[1] - S) // st[1] + 1
+
+
+def pin_ex_torch(conv_ex, seed=21):
+    """The strided, padded form equals torch's conv2d with stride and padding."""
+    rng = np.random.default_rng(seed)
+    for (N, C, K, H, W, R, S, st, pd) in STRIDED_SHAPES:
+        In, Ker = rand_inputs((N, C, K, H, W, R, S), rng)
+        ref = torch.nn.functional.conv2d(torch.from_numpy(In).double(), torch.from_numpy(Ker).double(),
+                                         stride=st, padding=pd).numpy()
+        _close(conv_ex(In, Ker, st, pd), ref)
+
+
+def pin_ex_reduces_to_eq1(conv_ex, seed=22):
+    """Stride 1 and no padding is Eq. (1) (the im2col reference)."""
+    rng = np.random.default_rng(seed)
+    for shape in TINY_SHAPES:
+        In, Ker = rand_inputs(shape, rng)
+        _close(conv_ex(In, Ker, (1, 1), (0, 0)), im2col_reference(In, Ker))
+
+
+def pin_ex_subsample_of_padded(conv_ex, seed=23):
+    """Closed form: the strided output is every sh-th row and sw-th column of
+    the stride-1 correlation of the explicitly zero-padded input."""
+    rng = np.random.default_rng(seed)
+    for (N, C, K, H, W, R, S, st, pd) in STRIDED_SHAPES:
+        In, Ker = rand_inputs((N, C, K, H, W, R, S), rng)
+        Xp = np.pad(In, ((0, 0), (0, 0), (pd[0], pd[0]), (pd[1], pd[1])))
+        full = im2col_reference(Xp, Ker)
+        P, Q = _ex_extents(H, W, R, S, st, pd)
+        _close(conv_ex(In, Ker, st, pd), full[:, :, ::st[0], ::st[1]][:, :, :P, :Q])
+
+
+def pin_ex_hand_example(conv_ex):
+    """The worked example in tests/golden/strided_hand_example.json."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "strided_hand_example.json")))
+    H, W = g["input_hw"]
+    R, S = g["kernel_rs"]
+    In = np.arange(1, H * W + 1, dtype=np.float32).reshape(1, 1, H, W)
+    Ker = np.ones((1, 1, R, S), np.float32)
+    out = conv_ex(In, Ker, tuple(g["stride"]), tuple(g["pad"]))
+    assert np.array_equal(out[0, 0], np.array(g["expected"], np.float64)), out
+
+
+def pin_ex_integer_brute_force(conv_ex, seed=24):
+    """Integer inputs: exact against a pure-Python brute force of the definition."""
+    rng = np.random.default_rng(seed)
+    for (N, C, K, H, W, R, S, st, pd) in STRIDED_SHAPES[:4]:
+        In = rng.integers(-3, 4, (N, C, H, W))
+        Ker = rng.integers(-3, 4, (K, C, R, S))
+        P, Q = _ex_extents(H, W, R, S, st, pd)
+        ref = np.zeros((N, K, P, Q), np.int64)
+        for n in range(N):
+            for k in range(K):
+                for h in range(P):
+                    for w in range(Q):
+                        acc = 0
+                        for c in range(C):
+                            for r in range(R):
+                                for s in range(S):
+                                    y, x = h * st[0] + r - pd[0], w * st[1] + s - pd[1]
+                                    if 0 <= y < H and 0 <= x < W:
+                                        acc += int(In[n, c, y, x]) * int(Ker[k, c, r, s])
+                        ref[n, k, h, w] = acc
+        out = conv_ex(In.astype(np.float32), Ker.astype(np.float32), st, pd)
+        assert np.array_equal(out, ref.astype(np.float64)), "integer brute force"
+
+
+STRIDED_PINS = (pin_ex_torch, pin_ex_reduces_to_eq1, pin_ex_subsample_of_padded, pin_ex_hand_example,
+                pin_ex_integer_brute_force)
