@@ -80,13 +80,23 @@ def time_layer(c, steps, warmup, queued=False):
     ips = [t.data_ptr() for t in ins]
     ops = [t.data_ptr() for t in outs]
 
+    strided = c.stride != 1 or c.pad != 0
+    L = B.lib()
+    dt = B.CONV_DTYPE_BF16 if bf16 else B.CONV_DTYPE_F32
+
     def fn(i):
-        st = B.conv_fwd_ptr(*c.key(), ips[i], kp, ops[i], sp, bf16)
+        if strided:
+            st = L.conv_fwd_ex(*c.key(), c.stride, c.stride, c.pad, c.pad, dt, ips[i], kp, ops[i], sp)
+        else:
+            st = B.conv_fwd_ptr(*c.key(), ips[i], kp, ops[i], sp, bf16)
         if st != B.CONV_OK:
             raise B.ConvError(st, "conv_fwd")
 
     fn(0)  # checked call through the tensor API first
-    (B.conv_fwd_bf16 if bf16 else B.conv_fwd)(ins[0], Ker, out=outs[0])
+    if strided:
+        B.conv_fwd_ex(ins[0], Ker, c.stride, c.pad, out=outs[0])
+    else:
+        (B.conv_fwd_bf16 if bf16 else B.conv_fwd)(ins[0], Ker, out=outs[0])
     for i in range(warmup):
         fn(i % nsets)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -526,7 +536,7 @@ def main():
     import torch
 
     from paper_2101_09808_amd import conv as B
-    from paper_2101_09808_amd.workloads import BY_NAME, CONFIGS, make_inputs
+    from paper_2101_09808_amd.workloads import BY_NAME, CONFIGS, STRIDED_CONFIGS, make_inputs
 
     if args.traffic_parse:  # host-only: reads the counter files of two earlier runs
         traffic_parse(BY_NAME[args.layer], args.traffic_parse[0], args.traffic_parse[1], TRAFFIC_FILE)
@@ -621,6 +631,20 @@ def main():
             layers[lc.name].update({"mopt5_variant": tplan["variant"], "mopt5_split_c": tplan["split_c"],
                                     "mopt5_kernel_us": tk * 1e6, "mopt5_gflops": flops(lc) / tk / 1e9,
                                     "mopt5_pct_hbm_peak": 100 * alg_bytes(lc) / tk / 1e9 / PEAK["hbm_gbs"]})
+        # strided, padded Table 1 layers (conv_fwd_ex: polyphase rewrite, then
+        # the selected stride-1 plan of the inner problem), timed the same way
+        for lc in STRIDED_CONFIGS:
+            lk = time_layer(lc, 50, 5, queued=True)["mean_kernel_ms"] * 1e-3
+            inner = B.conv_fwd_ex_inner_shape(*lc.key(), lc.stride, lc.pad)
+            lplan = B.conv_fwd_plan(*inner[:7])
+            layers[lc.name] = {
+                "dtype": lc.dtype, "stride": lc.stride, "pad": lc.pad, "inner_shape": list(inner[:7]),
+                "variant": lplan["variant"], "split_c": lplan["split_c"], "kernel_us": lk * 1e6,
+                "gflops": flops(lc) / lk / 1e9,
+                "pct_fp32_mfma_peak": 100 * flops(lc) / lk / 1e12 / PEAK["fp32_mfma_tflops"],
+                "alg_hbm_gbs": alg_bytes(lc) / lk / 1e9,
+                "pct_hbm_peak": 100 * alg_bytes(lc) / lk / 1e9 / PEAK["hbm_gbs"],
+            }
         out["per_layer"] = layers
     print(json.dumps(out), flush=True)
 

@@ -124,6 +124,41 @@ int conv_fwd_bf16(int N, int C, int K, int H, int W, int R, int S,
                   const uint16_t* In, const uint16_t* Ker, float* Out, void* stream);
 
 /*
+ * Strided, zero-padded forward convolution.  The paper presents Eq. (1)
+ * without stride and notes that the method carries over (Sec. 3.1,
+ * footnote 1); Table 1 includes stride-2 layers.  The operation:
+ *
+ *   Out[n][k][h][w] = sum_{c<C, r<R, s<S} X[n][c][h*sh + r - ph][w*sw + s - pw] * Ker[k][c][r][s]
+ *
+ * with X = In inside [0,H) x [0,W) and zero outside, for
+ * h < P = (H + 2 ph - R) / sh + 1 and w < Q = (W + 2 pw - S) / sw + 1.
+ *   stride_h, stride_w : 1 .. 64;  pad_h, pad_w : 0 .. 4096 (zeros each side)
+ *   dtype : CONV_DTYPE_*; In/Ker fp32 or bf16 bit patterns as for conv_fwd
+ *           and conv_fwd_bf16 (same layouts); Out [N][K][P][Q] fp32
+ * Stride 1 without padding is conv_fwd / conv_fwd_bf16.  Otherwise the call
+ * rewrites the problem as a stride-1 valid convolution (each input channel
+ * becomes min(sh,R) x min(sw,S) phase images; Ker gets ceil(R/sh) x
+ * ceil(S/sw) taps, zero where no original tap lands): two small kernels
+ * write the phase images (and, when strided, the rearranged Ker) into a
+ * stream-ordered workspace from the device's default pool, the selected
+ * stride-1 plan of the inner problem (see conv_fwd_ex_inner_shape) runs on
+ * it, and the workspace is returned in stream order.  Asynchronous like
+ * conv_fwd.  Returns a conv_status_t.
+ */
+int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S,
+                int stride_h, int stride_w, int pad_h, int pad_w, int dtype,
+                const void* In, const void* Ker, float* Out, void* stream);
+
+/*
+ * Host-only: the inner stride-1 problem conv_fwd_ex runs for these
+ * arguments, as inner[0..8] = N, C', K, H', W', R', S' (the shape to pass to
+ * conv_fwd_plan / conv_fwd_candidates) followed by the output extents P, Q.
+ * Returns a conv_status_t.
+ */
+int conv_fwd_ex_inner_shape(int N, int C, int K, int H, int W, int R, int S,
+                            int stride_h, int stride_w, int pad_h, int pad_w, int32_t inner[9]);
+
+/*
  * Host-only: the tile plan the selector picks for this shape and dtype
  * (CONV_DTYPE_*), with its modelled per-level bytes.  Cached per shape.
  * Makes no HIP call.  Returns a conv_status_t.

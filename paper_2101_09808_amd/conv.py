@@ -79,6 +79,10 @@ def lib():
         L.conv_fwd_tune.argtypes = shape7 + [_i32, _vp, _vp, _vp, _i32, _i32, _vp, ctypes.POINTER(ConvPlan),
                                              ctypes.POINTER(ctypes.c_float)]
         L.conv_fwd_tune.restype = _i32
+        L.conv_fwd_ex.argtypes = shape7 + [_i32] * 5 + [_vp, _vp, _vp, _vp]
+        L.conv_fwd_ex.restype = _i32
+        L.conv_fwd_ex_inner_shape.argtypes = shape7 + [_i32] * 4 + [ctypes.POINTER(_i32)]
+        L.conv_fwd_ex_inner_shape.restype = _i32
         L.conv_model_volume.argtypes = [ctypes.POINTER(_i32), ctypes.POINTER(_i64),
                                         ctypes.POINTER(_i64), _i32, ctypes.POINTER(_dbl)]
         L.conv_model_volume.restype = _i32
@@ -166,6 +170,41 @@ def conv_fwd_with_plan(In, Ker, plan, out=None, stream=None):
     if st != CONV_OK:
         raise ConvError(st, "conv_fwd_with_plan")
     return out
+
+
+def _pair(x):
+    return (int(x), int(x)) if isinstance(x, int) else (int(x[0]), int(x[1]))
+
+
+def conv_fwd_ex(In, Ker, stride=1, pad=0, out=None, stream=None):
+    """Strided, zero-padded convolution (fp32 or bf16 In/Ker, fp32 Out
+    [N,K,P,Q] with P = (H + 2 ph - R) // sh + 1, Q likewise)."""
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    bf16 = In.dtype == torch.bfloat16
+    N, C, K, H, W, R, S = _check_inputs(In, Ker, torch.bfloat16 if bf16 else torch.float32)
+    inner = conv_fwd_ex_inner_shape(N, C, K, H, W, R, S, (sh, sw), (ph, pw))
+    P, Q = inner[7], inner[8]
+    if out is None:
+        out = torch.empty((N, K, P, Q), dtype=torch.float32, device=In.device)
+    elif out.shape != (N, K, P, Q) or out.dtype != torch.float32 or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous float32 {(N, K, P, Q)} tensor")
+    st = lib().conv_fwd_ex(N, C, K, H, W, R, S, sh, sw, ph, pw, CONV_DTYPE_BF16 if bf16 else CONV_DTYPE_F32,
+                           In.data_ptr(), Ker.data_ptr(), out.data_ptr(), _stream_ptr(stream))
+    if st != CONV_OK:
+        raise ConvError(st, "conv_fwd_ex")
+    return out
+
+
+def conv_fwd_ex_inner_shape(N, C, K, H, W, R, S, stride=1, pad=0):
+    """The stride-1 problem conv_fwd_ex runs: (N, C', K, H', W', R', S', P, Q)."""
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    buf = (_i32 * 9)()
+    st = lib().conv_fwd_ex_inner_shape(N, C, K, H, W, R, S, sh, sw, ph, pw, buf)
+    if st != CONV_OK:
+        raise ConvError(st, "conv_fwd_ex_inner_shape")
+    return tuple(buf)
 
 
 CONV_TUNE_MAX = 64

@@ -1,6 +1,7 @@
 // C ABI of the convolution library: argument validation, the per-shape plan
 // cache and dispatch to the kernels.  The declarations and their contracts
 // are in include/conv_fwd.h.
+#include <algorithm>
 #include <cstdint>
 #include <cstring>
 #include <map>
@@ -128,6 +129,31 @@ int run_selected(const Shape& s, int dtype, const void* In, const void* Ker, flo
   return launch(*e.v, e.g, In, Ker, Out, stream);
 }
 
+// Inner stride-1 problem of a strided, padded convolution (polyphase rewrite).
+int phase_geom(int N, int C, int K, int H, int W, int R, int S, int sh, int sw, int ph, int pw,
+               PhaseGeom* p) {
+  if (N <= 0 || C <= 0 || K <= 0 || H <= 0 || W <= 0 || R <= 0 || S <= 0) return CONV_EINVAL;
+  if (sh < 1 || sw < 1 || ph < 0 || pw < 0 || sh > 64 || sw > 64 || ph > 4096 || pw > 4096) return CONV_EINVAL;
+  if (H + 2 * ph < R || W + 2 * pw < S) return CONV_EINVAL;
+  PhaseGeom q;
+  q.N = N; q.C = C; q.K = K; q.H = H; q.W = W; q.R = R; q.S = S;
+  q.sh = sh; q.sw = sw; q.ph = ph; q.pw = pw;
+  q.P = (H + 2 * ph - R) / sh + 1;
+  q.Q = (W + 2 * pw - S) / sw + 1;
+  q.na = std::min(sh, R);
+  q.nb = std::min(sw, S);
+  q.Rp = (R + sh - 1) / sh;
+  q.Sp = (S + sw - 1) / sw;
+  q.Hp = q.P + q.Rp - 1;
+  q.Wp = q.Q + q.Sp - 1;
+  if ((int64_t)C * q.na * q.nb > kMaxElems) return CONV_ERANGE;
+  const int st = validate_shape(N, C * q.na * q.nb, K, q.Hp, q.Wp, q.Rp, q.Sp);
+  if (st != CONV_OK) return st;
+  if ((int64_t)N * C * H * W > kMaxElems) return CONV_ERANGE;
+  *p = q;
+  return CONV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -146,6 +172,45 @@ int conv_fwd_bf16(int N, int C, int K, int H, int W, int R, int S, const uint16_
   if (st != CONV_OK) return st;
   if (!In || !Ker || !Out) return CONV_ENULL;
   return run_selected(Shape{N, C, K, H, W, R, S}, CONV_DTYPE_BF16, In, Ker, Out, stream);
+}
+
+int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w, int pad_h,
+                int pad_w, int dtype, const void* In, const void* Ker, float* Out, void* stream) {
+  PhaseGeom p;
+  int st = phase_geom(N, C, K, H, W, R, S, stride_h, stride_w, pad_h, pad_w, &p);
+  if (st != CONV_OK) return st;
+  if (!In || !Ker || !Out) return CONV_ENULL;
+  if (dtype != CONV_DTYPE_F32 && dtype != CONV_DTYPE_BF16) return CONV_EINVAL;
+  if (stride_h == 1 && stride_w == 1 && pad_h == 0 && pad_w == 0)
+    return run_selected(Shape{N, C, K, H, W, R, S}, dtype, In, Ker, static_cast<float*>(Out), stream);
+  // stream-ordered workspace: the phase images of In, then (strided only)
+  // the rearranged Ker; at stride 1 the padded In meets the original Ker
+  const size_t e = dtype == CONV_DTYPE_BF16 ? 2 : 4;
+  const int Cp = C * p.na * p.nb;
+  const size_t in_bytes = ((size_t)N * Cp * p.Hp * p.Wp * e + 255) / 256 * 256;
+  const bool ker_moves = stride_h > 1 || stride_w > 1;
+  const size_t ker_bytes = ker_moves ? (size_t)K * Cp * p.Rp * p.Sp * e : 0;
+  void* wsv = nullptr;
+  st = stream_alloc(in_bytes + ker_bytes, stream, &wsv);
+  if (st != CONV_OK) return st;
+  char* ws = static_cast<char*>(wsv);
+  void* Kp = ker_moves ? ws + in_bytes : nullptr;
+  st = launch_phase_split(p, dtype, In, Ker, ws, Kp, stream);
+  if (st == CONV_OK)
+    st = run_selected(Shape{N, Cp, K, p.Hp, p.Wp, p.Rp, p.Sp}, dtype, ws, ker_moves ? Kp : Ker, Out, stream);
+  const int freed = stream_free(ws, stream);
+  return st == CONV_OK ? freed : st;
+}
+
+int conv_fwd_ex_inner_shape(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w,
+                            int pad_h, int pad_w, int32_t inner[9]) {
+  if (!inner) return CONV_ENULL;
+  PhaseGeom p;
+  const int st = phase_geom(N, C, K, H, W, R, S, stride_h, stride_w, pad_h, pad_w, &p);
+  if (st != CONV_OK) return st;
+  const int32_t v[9] = {N, C * p.na * p.nb, K, p.Hp, p.Wp, p.Rp, p.Sp, p.P, p.Q};
+  for (int i = 0; i < 9; ++i) inner[i] = v[i];
+  return CONV_OK;
 }
 
 int conv_fwd_plan(int N, int C, int K, int H, int W, int R, int S, int dtype,

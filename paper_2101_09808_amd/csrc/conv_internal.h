@@ -1,6 +1,7 @@
 // Internal declarations shared by the selector, the dispatcher and the kernels.
 #pragma once
 
+#include <cstddef>
 #include <cstdint>
 
 #include "../../include/conv_fwd.h"
@@ -73,6 +74,25 @@ bool resolve_geom(const Shape& s, const Variant& v, const conv_plan_t& plan, Geo
 
 // Launch the kernel of variant v (asynchronous).  Returns a conv_status_t.
 int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, float* Out, void* stream);
+
+// Polyphase rewrite of a strided, padded convolution into a stride-1 valid
+// one (conv_fwd_ex): na x nb phases per input channel, inner extents
+// Hp x Wp and taps Rp x Sp.
+struct PhaseGeom {
+  int N, C, K, H, W, R, S;
+  int sh, sw, ph, pw;
+  int na, nb;  // phases along rows / columns: min(sh, R), min(sw, S)
+  int Hp, Wp;  // inner input extents: P + Rp - 1, Q + Sp - 1
+  int Rp, Sp;  // inner taps: ceil(R / sh), ceil(S / sw)
+  int P, Q;    // output extents
+};
+// Stream-ordered device memory from the default pool (hipMallocAsync /
+// hipFreeAsync on `stream`).
+int stream_alloc(size_t bytes, void* stream, void** out);
+int stream_free(void* p, void* stream);
+// Phase-split In into Inp and (Kp non-null) Ker into Kp, on `stream`.
+int launch_phase_split(const PhaseGeom& p, int dtype, const void* In, const void* Ker, void* Inp, void* Kp,
+                       void* stream);
 // Median duration in microseconds of `reps` launches on `stream` after one
 // untimed launch, each between its own two HIP events and preceded by a pass
 // over a 512 MB stream-ordered scratch buffer (cold caches); waits for the

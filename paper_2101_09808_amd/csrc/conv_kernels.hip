@@ -1415,6 +1415,56 @@ splitk_reduce_kernel(const float* __restrict__ W, float* __restrict__ Out, int64
   }
 }
 
+// ---------------------------------------------------------------------------
+// Strided, zero-padded convolution as a stride-1 valid one (polyphase or
+// space-to-depth rewrite).  With input row y = h*sh + r - ph, write the tap
+// r = sh*r' + a (a < sh): the row becomes sh*(h + r') + (a - ph), so phase
+// image a of the padded input, X_a[y'] = X[sh*y' + a - ph], is read at
+// h + r' -- a stride-1 correlation over r'.  Likewise for columns.  The
+// phases (a, b) become extra input channels, (c*na + a)*nb + b, with na =
+// min(sh, R) and nb = min(sw, S) (phases no tap reaches are left out), and
+// the kernel gets taps r' < ceil(R/sh), t' < ceil(S/sw), zero where
+// sh*r' + a >= R or sw*t' + b >= S.
+
+// Inp[n][(c*na + a)*nb + b][y][x] = In[n][c][y*sh + a - ph][x*sw + b - pw],
+// zero outside the input.  One element per thread, grid-stride.
+template <typename T>
+__global__ void __launch_bounds__(256)
+phase_split_kernel(const T* __restrict__ In, T* __restrict__ Inp, PhaseGeom p) {
+  const int Cp = p.C * p.na * p.nb;
+  const int64_t total = (int64_t)p.N * Cp * p.Hp * p.Wp;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    int64_t t = i;
+    const int x = (int)(t % p.Wp); t /= p.Wp;
+    const int y = (int)(t % p.Hp); t /= p.Hp;
+    const int cp = (int)(t % Cp);
+    const int n = (int)(t / Cp);
+    const int b = cp % p.nb, a = (cp / p.nb) % p.na, c = cp / (p.na * p.nb);
+    const int iy = y * p.sh + a - p.ph, ix = x * p.sw + b - p.pw;
+    Inp[i] = (iy >= 0 && iy < p.H && ix >= 0 && ix < p.W) ? In[(((int64_t)n * p.C + c) * p.H + iy) * p.W + ix]
+                                                          : T(0);
+  }
+}
+
+// Kp[k][(c*na + a)*nb + b][r'][t'] = Ker[k][c][r'*sh + a][t'*sw + b], zero
+// past the R x S taps.
+template <typename T>
+__global__ void __launch_bounds__(256)
+ker_phase_kernel(const T* __restrict__ Ker, T* __restrict__ Kp, PhaseGeom p) {
+  const int Cp = p.C * p.na * p.nb;
+  const int64_t total = (int64_t)p.K * Cp * p.Rp * p.Sp;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    int64_t t = i;
+    const int tt = (int)(t % p.Sp); t /= p.Sp;
+    const int rr = (int)(t % p.Rp); t /= p.Rp;
+    const int cp = (int)(t % Cp);
+    const int k = (int)(t / Cp);
+    const int b = cp % p.nb, a = (cp / p.nb) % p.na, c = cp / (p.na * p.nb);
+    const int r = rr * p.sh + a, s = tt * p.sw + b;
+    Kp[i] = (r < p.R && s < p.S) ? Ker[(((int64_t)k * p.C + c) * p.R + r) * p.S + s] : T(0);
+  }
+}
+
 #define F32_INST(ID, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV)                                  \
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STAGED, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV, 1, \
                    kThreads, 2},                                                             \
@@ -1518,6 +1568,9 @@ const Instance kInstances[] = {
     BF16_INST(203, 4, 2, 3, 3, 3),
     BF16_INST(204, 4, 4, 1, 1, 3),
     BF16_INST(205, 2, 2, 3, 3, 3),
+    // 2x2 and 4x4 taps: stride-2 3x3 and 7x7 layers after the polyphase rewrite
+    BF16_INST(206, 4, 4, 2, 2, 3),
+    BF16_INST(207, 4, 4, 4, 4, 3),
     // ---- register-staged, double buffered (any shape, any alignment)
     // 3x3 taps, Ker staged in float4
     F32_INST(1, 4, 4, 8, 3, 3, 8, 12, 4),
@@ -1562,6 +1615,37 @@ const Variant* variants(int* count) {
 const Variant* find_variant(int id) {
   const Instance* in = find_instance(id);
   return in ? &in->v : nullptr;
+}
+
+int stream_alloc(size_t bytes, void* stream, void** out) {
+  return hipMallocAsync(out, bytes, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? CONV_OK : CONV_EHIP;
+}
+
+int stream_free(void* p, void* stream) {
+  return hipFreeAsync(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? CONV_OK : CONV_EHIP;
+}
+
+int launch_phase_split(const PhaseGeom& p, int dtype, const void* In, const void* Ker, void* Inp, void* Kp,
+                       void* stream) {
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int64_t n_in = (int64_t)p.N * p.C * p.na * p.nb * p.Hp * p.Wp;
+  const int64_t n_ker = (int64_t)p.K * p.C * p.na * p.nb * p.Rp * p.Sp;
+  const int g_in = (int)std::min<int64_t>((n_in + 255) / 256, 8192);
+  const int g_ker = (int)std::min<int64_t>((n_ker + 255) / 256, 2048);
+  if (dtype == CONV_DTYPE_BF16) {
+    hipLaunchKernelGGL(phase_split_kernel<unsigned short>, dim3(g_in), dim3(256), 0, st,
+                       static_cast<const unsigned short*>(In), static_cast<unsigned short*>(Inp), p);
+    if (Kp)
+      hipLaunchKernelGGL(ker_phase_kernel<unsigned short>, dim3(g_ker), dim3(256), 0, st,
+                         static_cast<const unsigned short*>(Ker), static_cast<unsigned short*>(Kp), p);
+  } else {
+    hipLaunchKernelGGL(phase_split_kernel<float>, dim3(g_in), dim3(256), 0, st, static_cast<const float*>(In),
+                       static_cast<float*>(Inp), p);
+    if (Kp)
+      hipLaunchKernelGGL(ker_phase_kernel<float>, dim3(g_ker), dim3(256), 0, st, static_cast<const float*>(Ker),
+                         static_cast<float*>(Kp), p);
+  }
+  return hipGetLastError() == hipSuccess ? CONV_OK : CONV_EHIP;
 }
 
 int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, float* Out,

@@ -27,14 +27,16 @@ class ConvShape:
     S: int
     dtype: str = "f32"  # "f32", or "bf16" (bf16 In/Ker, fp32 accumulate and Out)
     seed: int = 0
+    stride: int = 1     # strided, zero-padded layers (conv_fwd_ex); square
+    pad: int = 0
 
     @property
     def P(self):
-        return self.H - self.R + 1
+        return (self.H + 2 * self.pad - self.R) // self.stride + 1
 
     @property
     def Q(self):
-        return self.W - self.S + 1
+        return (self.W + 2 * self.pad - self.S) // self.stride + 1
 
     def key(self):
         return (self.N, self.C, self.K, self.H, self.W, self.R, self.S)
@@ -51,7 +53,16 @@ CONFIGS = (
     ConvShape("conv3x3_bf16_n16_c32_k64_in226", 16, 32, 64, 226, 226, 3, 3, "bf16", 5000),
 )
 
-BY_NAME = {c.name: c for c in CONFIGS}
+# Strided, "same"-padded layers of Table 1 (ResNet-18 R1*, R4*, R5*) at batch
+# 32, for the strided path (conv_fwd_ex); not part of the five
+# configurations above.
+STRIDED_CONFIGS = (
+    ConvShape("conv7x7s2p3_n32_c3_k64_in224", 32, 3, 64, 224, 224, 7, 7, "f32", 6000, 2, 3),
+    ConvShape("conv3x3s2p1_n32_c64_k128_in56", 32, 64, 128, 56, 56, 3, 3, "f32", 7000, 2, 1),
+    ConvShape("conv1x1s2_n32_c64_k128_in56", 32, 64, 128, 56, 56, 1, 1, "f32", 8000, 2, 0),
+)
+
+BY_NAME = {c.name: c for c in CONFIGS + STRIDED_CONFIGS}
 
 
 def make_inputs(shape, seed=None, kind="uniform"):

@@ -810,3 +810,47 @@ def emulate_bf16_tr(g, In, Ker, wgs=None, out_aligned=True):
                                         out[dst] = vals[v]
                                         written[dst] += 1
     return out, written
+
+
+def emulate_phase_split(In, Ker, stride, pad):
+    """The two rewrite kernels of conv_fwd_ex, element by element (vectorised
+    over the flat output index exactly as the kernels decompose it).  In
+    [N,C,H,W], Ker [K,C,R,S] numpy arrays -> (Inp, Kp, (N, C', K, H', W', R',
+    S', P, Q)).  Every source index is bounds-checked."""
+    N, C, H, W = In.shape
+    K, _, R, S = Ker.shape
+    sh, sw = stride
+    ph, pw = pad
+    P, Q = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
+    na, nb = min(sh, R), min(sw, S)
+    Rp, Sp = -(-R // sh), -(-S // sw)
+    Hp, Wp = P + Rp - 1, Q + Sp - 1
+    Cp = C * na * nb
+    # phase_split_kernel
+    i = np.arange(N * Cp * Hp * Wp, dtype=np.int64)
+    t = i
+    x = t % Wp; t = t // Wp
+    y = t % Hp; t = t // Hp
+    cp = t % Cp
+    n = t // Cp
+    b, a, c = cp % nb, (cp // nb) % na, cp // (na * nb)
+    iy, ix = y * sh + a - ph, x * sw + b - pw
+    inside = (iy >= 0) & (iy < H) & (ix >= 0) & (ix < W)
+    src = ((n * C + c) * H + iy) * W + ix
+    _chk(np.all((src[inside] >= 0) & (src[inside] < In.size)), "phase split source inside In")
+    flat = In.reshape(-1)
+    Inp = np.where(inside, flat[np.where(inside, src, 0)], 0.0).reshape(N, Cp, Hp, Wp)
+    # ker_phase_kernel
+    i = np.arange(K * Cp * Rp * Sp, dtype=np.int64)
+    t = i
+    tt = t % Sp; t = t // Sp
+    rr = t % Rp; t = t // Rp
+    cp = t % Cp
+    k = t // Cp
+    b, a, c = cp % nb, (cp // nb) % na, cp // (na * nb)
+    r, s = rr * sh + a, tt * sw + b
+    inside = (r < R) & (s < S)
+    src = ((k * C + c) * R + r) * S + s
+    _chk(np.all((src[inside] >= 0) & (src[inside] < Ker.size)), "Ker rewrite source inside Ker")
+    Kp = np.where(inside, Ker.reshape(-1)[np.where(inside, src, 0)], 0.0).reshape(K, Cp, Rp, Sp)
+    return Inp, Kp, (N, Cp, K, Hp, Wp, Rp, Sp, P, Q)

@@ -22,7 +22,8 @@ def declared_functions():
 def test_header_declares_the_boundary():
     fns = declared_functions()
     for name in ("conv_fwd", "conv_fwd_bf16", "conv_fwd_plan", "conv_fwd_strerror",
-                 "conv_fwd_with_plan", "conv_fwd_candidates", "conv_model_volume", "conv_fwd_tune"):
+                 "conv_fwd_with_plan", "conv_fwd_candidates", "conv_model_volume", "conv_fwd_tune",
+                 "conv_fwd_ex", "conv_fwd_ex_inner_shape"):
         assert name in fns
 
 
@@ -98,6 +99,28 @@ def test_tune_arguments_rejected_without_launch():
     for top_n, reps in ((0, 3), (B.CONV_TUNE_MAX + 1, 3), (5, 0), (5, 1001)):
         assert L.conv_fwd_tune(*VALID, 0, fake, fake, fake, top_n, reps, None, ctypes.byref(p), t) == B.CONV_EINVAL
     assert L.conv_fwd_tune(0, *VALID[1:], 0, fake, fake, fake, 5, 3, None, ctypes.byref(p), t) == B.CONV_EINVAL
+
+
+@pytest.mark.parametrize("args,status", [
+    ((0, 1, 0, 0), B.CONV_EINVAL),    # stride 0
+    ((1, 1, -1, 0), B.CONV_EINVAL),   # negative pad
+    ((65, 1, 0, 0), B.CONV_EINVAL),   # stride above 64
+    ((2, 2, 0, 0), B.CONV_OK),
+])
+def test_ex_arguments(args, status):
+    L = B.lib()
+    inner = (ctypes.c_int32 * 9)()
+    assert L.conv_fwd_ex_inner_shape(*VALID, *args, inner) == status
+    if status == B.CONV_OK:
+        assert list(inner)[7:] == [(6 - 3) // 2 + 1] * 2
+    fake = ctypes.c_void_p(0x1000)
+    if status != B.CONV_OK:
+        assert L.conv_fwd_ex(*VALID, *args, 0, fake, fake, fake, None) == status
+    # kernel larger than the padded input; null pointers; bad dtype
+    assert L.conv_fwd_ex(1, 4, 8, 2, 6, 5, 3, 1, 1, 1, 0, 0, fake, fake, fake, None) == B.CONV_EINVAL
+    assert L.conv_fwd_ex(*VALID, 2, 2, 1, 1, 0, None, fake, fake, None) == B.CONV_ENULL
+    assert L.conv_fwd_ex(*VALID, 2, 2, 1, 1, 5, fake, fake, fake, None) == B.CONV_EINVAL
+    assert L.conv_fwd_ex_inner_shape(*VALID, 1, 1, 0, 0, None) == B.CONV_ENULL
 
 
 def test_strerror():

@@ -268,6 +268,9 @@ BF16_VARIANT_SHAPES = [
     ConvShape("bf16_c32_k64", 1, 32, 64, 58, 66, 3, 3, "bf16", 54),
     # Q % 4 != 0: 4-byte stores; K < 64
     ConvShape("bf16_c32_q42", 1, 32, 40, 10, 44, 3, 3, "bf16", 55),
+    # 2x2 and 4x4 taps (inner problems of stride-2 layers)
+    ConvShape("bf16_var2x2", 2, 40, 72, 11, 13, 2, 2, "bf16", 56),
+    ConvShape("bf16_var4x4", 1, 24, 40, 12, 14, 4, 4, "bf16", 57),
 ]
 # kernel families each shape is there for (others are covered by the shapes before)
 BF16_SHAPE_FAMILIES = {"bf16_c32_k64": {6}, "bf16_c32_q42": {6}}
@@ -415,3 +418,52 @@ def test_tune_keeps_fastest_of_model_top_plans(shape):
     again = (B.conv_fwd_bf16 if dt == B.CONV_DTYPE_BF16 else B.conv_fwd)(In_d, Ker_d)
     torch.cuda.synchronize()
     assert rel_err(host(again), ref) <= TOL[shape.dtype]
+
+
+# ---------------------------------------------------------------------------
+# Strided, zero-padded convolution (conv_fwd_ex)
+
+STRIDED_SHAPES = [
+    ConvShape("s2p1_3x3", 2, 3, 4, 9, 7, 3, 3, "f32", 91, 2, 1),
+    ConvShape("s2p1_3x3_c16", 2, 16, 32, 20, 20, 3, 3, "f32", 92, 2, 1),
+    ConvShape("s2_1x1", 2, 24, 40, 15, 17, 1, 1, "f32", 93, 2, 0),
+    ConvShape("s2p3_7x7_c3", 1, 3, 16, 30, 30, 7, 7, "f32", 94, 2, 3),
+    ConvShape("s1p1_3x3", 2, 8, 16, 12, 12, 3, 3, "f32", 95, 1, 1),
+    ConvShape("s3p2_5x5", 1, 6, 10, 17, 14, 5, 5, "f32", 96, 3, 2),
+    ConvShape("s2p1_3x3_bf16", 1, 16, 32, 22, 22, 3, 3, "bf16", 97, 2, 1),
+    ConvShape("s2p1_3x3_c32_bf16", 1, 32, 64, 34, 34, 3, 3, "bf16", 98, 2, 1),
+]
+
+
+@pytest.mark.parametrize("shape", STRIDED_SHAPES, ids=lambda s: s.name)
+def test_strided_padded_parity(shape):
+    In, Ker = make_inputs(shape)
+    ref = oconv.conv_fwd_ex(host(In), host(Ker), (shape.stride,) * 2, (shape.pad,) * 2)
+    say(f"[gpu] strided {shape.name} inner {B.conv_fwd_ex_inner_shape(*shape.key(), shape.stride, shape.pad)}")
+    out = B.conv_fwd_ex(In.to(DEV), Ker.to(DEV), shape.stride, shape.pad)
+    torch.cuda.synchronize()
+    assert out.shape == ref.shape
+    assert rel_err(host(out), ref) <= TOL[shape.dtype]
+
+
+def test_strided_asymmetric_stride_and_pad():
+    shape = ConvShape("s23p10", 1, 8, 12, 13, 10, 3, 2, "f32", 99)
+    In, Ker = make_inputs(shape)
+    ref = oconv.conv_fwd_ex(host(In), host(Ker), (2, 3), (1, 0))
+    out = B.conv_fwd_ex(In.to(DEV), Ker.to(DEV), (2, 3), (1, 0))
+    torch.cuda.synchronize()
+    assert rel_err(host(out), ref) <= TOL["f32"]
+
+
+@pytest.mark.parametrize("cfg", __import__("paper_2101_09808_amd.workloads", fromlist=["x"]).STRIDED_CONFIGS,
+                         ids=lambda c: c.name)
+def test_strided_full_config_sampled(cfg):
+    """Table 1 strided layers at batch 32: sampled outputs against the oracle."""
+    In, Ker = make_inputs(cfg)
+    say(f"[gpu] strided full {cfg.name}")
+    out = host(B.conv_fwd_ex(In.to(DEV), Ker.to(DEV), cfg.stride, cfg.pad))
+    rng = np.random.default_rng(cfg.seed)
+    idx = np.unique(np.concatenate([rng.integers(0, out.size, 3000), [0, out.size - 1]]))
+    ref = oconv.conv_fwd_ex_points(host(In), host(Ker), idx, (cfg.stride,) * 2, (cfg.pad,) * 2)
+    got = out.reshape(-1)[idx]
+    assert np.max(np.abs(got - ref)) <= TOL["f32"] * max(1.0, np.max(np.abs(ref)))

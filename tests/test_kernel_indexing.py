@@ -194,3 +194,44 @@ def test_tune_plans_indexing():
                 assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
             else:
                 _check_all(shape, p)
+
+
+
+def test_phase_split_rewrite_equals_strided_definition():
+    """conv_fwd_ex's rewrite (the two kernels' index maps, emulated) followed
+    by Eq. (1) equals the strided, padded oracle; the library reports the
+    same inner problem."""
+    from tests.kernel_emulator import emulate_phase_split
+    from tests.test_gpu_parity import STRIDED_SHAPES
+    for shape in STRIDED_SHAPES + [ConvShape("s23p10", 1, 8, 12, 13, 10, 3, 2, "f32", 99)]:
+        st = (shape.stride, shape.stride) if shape.name != "s23p10" else (2, 3)
+        pd = (shape.pad, shape.pad) if shape.name != "s23p10" else (1, 0)
+        In, Ker = make_inputs(shape)
+        In64, Ker64 = In.float().numpy().astype(np.float64), Ker.float().numpy().astype(np.float64)
+        Inp, Kp, inner = emulate_phase_split(In64, Ker64, st, pd)
+        assert tuple(B.conv_fwd_ex_inner_shape(*shape.key(), st, pd)) == inner
+        ref = oconv.conv_fwd_ex(In64.astype(np.float32), Ker64.astype(np.float32), st, pd)
+        got = oconv.conv_fwd(Inp.astype(np.float32), Kp.astype(np.float32))
+        assert got.shape == ref.shape
+        assert np.max(np.abs(got - ref)) <= 1e-12 * max(1.0, np.max(np.abs(ref)))
+
+
+def test_strided_inner_plans_indexing():
+    """The plans the strided GPU tests run on their inner stride-1 problems."""
+    from tests.kernel_emulator import emulate_bf16
+    from tests.test_gpu_parity import STRIDED_SHAPES
+    for shape in STRIDED_SHAPES:
+        inner = B.conv_fwd_ex_inner_shape(*shape.key(), shape.stride, shape.pad)
+        ish = ConvShape(shape.name + "_inner", *inner[:7], shape.dtype, shape.seed)
+        dt = B.CONV_DTYPE_BF16 if shape.dtype == "bf16" else B.CONV_DTYPE_F32
+        p = B.conv_fwd_plan(*ish.key(), dtype=dt)
+        if dt == B.CONV_DTYPE_BF16:
+            In, Ker = make_inputs(ish)
+            In64 = In.float().numpy().astype(np.float64)
+            Ker64 = Ker.float().numpy().astype(np.float64)
+            ref = oconv.conv_fwd(In64.astype(np.float32), Ker64.astype(np.float32)).reshape(-1)
+            out, written = emulate_bf16(B.conv_fwd_geometry(*ish.key(), p), In64.reshape(-1), Ker64.reshape(-1))
+            assert np.all(written == 1)
+            assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
+        else:
+            _check_all(ish, p)
