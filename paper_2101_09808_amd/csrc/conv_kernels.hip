@@ -1529,6 +1529,13 @@ const Instance kInstances[] = {
     F32_DMA(106, 1, 7, 8, 8, 3, 3, 3, 5, 1, 3, 4),
     F32_DMA(107, 1, 4, 8, 8, 3, 3, 3, 4, 1, 3, 4),
     F32_DMA(108, 2, 4, 8, 8, 3, 3, 3, 6, 1, 3, 4),
+    // 2x2 and 4x4 taps: stride-2 3x3 and 7x7 layers after the polyphase rewrite
+    F32_DMA(109, 4, 4, 4, 8, 2, 2, 3, 12, 1, 5, 4),
+    F32_DMA(110, 1, 7, 8, 8, 2, 2, 3, 5, 1, 2, 4),
+    F32_DMA(111, 2, 4, 8, 8, 2, 2, 3, 6, 1, 2, 4),
+    F32_DMA(112, 4, 4, 4, 8, 4, 4, 3, 14, 1, 8, 4),
+    F32_DMA(113, 1, 7, 8, 8, 4, 4, 3, 6, 1, 5, 4),
+    F32_DMA(114, 2, 4, 8, 8, 4, 4, 3, 7, 1, 5, 4),
     // squat wave tiles (4 k blocks x 4..8 pixel blocks), Ker rows loaded
     // element-wise so their LDS pitch can be conflict-free
     F32_DMA(141, 4, 4, 4, 8, 3, 3, 3, 7, 1, 19, 1),

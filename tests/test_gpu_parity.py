@@ -238,6 +238,9 @@ VARIANT_SHAPES = [
     ConvShape("var3x3", 3, 20, 72, 19, 23, 3, 3, "f32", 31),
     ConvShape("var1x1", 3, 40, 72, 13, 11, 1, 1, "f32", 32),
     ConvShape("var2x4", 2, 9, 40, 12, 13, 2, 4, "f32", 33),
+    # 2x2 and 4x4 taps: the inner problems of stride-2 layers
+    ConvShape("var2x2", 2, 40, 72, 11, 13, 2, 2, "f32", 38),
+    ConvShape("var4x4", 2, 24, 72, 12, 14, 4, 4, "f32", 39),
     # pointwise layers whose channel count has a fully unrolled streaming kernel
     ConvShape("var1x1_c64", 2, 64, 72, 13, 11, 1, 1, "f32", 34),
     ConvShape("var1x1_c128", 3, 128, 64, 7, 9, 1, 1, "f32", 35),
