@@ -6,6 +6,7 @@
     python bench.py --traffic-run --layer all  (under rocprofv3 --pmc, one counter per run)
     python bench.py --model-check FETCH_DIR WRITE_DIR TCP_TCC_DIR LDS_DIR
     python bench.py --rank-sweep [N]           (model rank vs measured time, every layer)
+    python bench.py --table1                   (Table 1 layers at batch 1, stride and same padding)
 
 A step is one conv_fwd call (tile selection is cached, so the step is the
 kernel launch) on the pointwise layer N=32 C=256 K=64 56x56 1x1 fp32.  Inputs
@@ -474,6 +475,57 @@ def rank_report(res):
     return "\n".join(lines) + "\n"
 
 
+TABLE1_JSON = os.path.join(ROOT, "profiles", "table1_sweep.json")
+TABLE1_MD = os.path.join(ROOT, "profiles", "table1_sweep.md")
+
+
+def table1_sweep():
+    """Every conv2d layer of Table 1 (Yolo-9000, ResNet-18) at batch 1 with
+    its stride and same padding: launch time (median of queued launches on
+    rotating buffers), achieved rates and the roofline bound of the layer."""
+    from paper_2101_09808_amd import conv as B
+    from paper_2101_09808_amd.workloads import TABLE1
+    rows = {}
+    for c in TABLE1:
+        lk = time_layer(c, 30, 5, queued=True)["mean_kernel_ms"] * 1e-3
+        inner = B.conv_fwd_ex_inner_shape(*c.key(), c.stride, c.pad)
+        plan = B.conv_fwd_plan(*inner[:7])
+        F, Bt = flops(c), alg_bytes(c)
+        t_mfma, t_hbm = F / (PEAK["fp32_mfma_tflops"] * 1e12), Bt / (PEAK["hbm_gbs"] * 1e9)
+        bound = "mfma" if t_mfma >= t_hbm else "hbm"
+        rows[c.name] = {
+            "K": c.K, "C": c.C, "HW": c.H, "RS": c.R, "stride": c.stride, "pad": c.pad,
+            "inner_shape": list(inner[:7]), "variant": plan["variant"], "split_c": plan["split_c"],
+            "pred_us": plan["pred_total_us"], "kernel_us": lk * 1e6, "gflops": F / lk / 1e9,
+            "pct_fp32_mfma_peak": 100 * F / lk / 1e12 / PEAK["fp32_mfma_tflops"],
+            "alg_hbm_gbs": Bt / lk / 1e9, "pct_hbm_peak": 100 * Bt / lk / 1e9 / PEAK["hbm_gbs"],
+            "bound": bound, "roofline_frac": max(t_mfma, t_hbm) / lk,
+        }
+        print(f"[table1] {c.name} {lk * 1e6:.1f} us", flush=True)
+    return rows
+
+
+def table1_report(rows):
+    lines = ["# Table 1 conv2d layers at batch 1 (Yolo-9000, ResNet-18), MI355X, fp32", "",
+             "Each layer with the table's stride and same padding (R // 2), through conv_fwd_ex: "
+             "strided or padded layers are rewritten as a stride-1 valid convolution (inner shape "
+             "C', H', R') and run with the selector's plan.  Time = mean of 30 launches queued behind a "
+             "spin kernel on rotating buffer sets, from HIP events.  Roofline fraction = time at the "
+             "layer's bound (fp32 MFMA 157.3 TFLOP/s or HBM 8 TB/s) over the measured time.  The "
+             "depth-wise MobileNet layers are not Eq. (1).", "",
+             "Command: `python bench.py --table1`", "",
+             "| layer | K | C | H=W | R=S | stride | inner (C', H', R') | plan | us | GFLOP/s | % fp32 peak "
+             "| GB/s | bound | roofline frac |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for name, r in rows.items():
+        ic = r["inner_shape"]
+        lines.append(f"| {name.split('_', 1)[1]} | {r['K']} | {r['C']} | {r['HW']} | {r['RS']} | {r['stride']} | "
+                     f"({ic[1]}, {ic[3]}, {ic[5]}) | v{r['variant']}/{r['split_c']} | {r['kernel_us']:.1f} | "
+                     f"{r['gflops']:.0f} | {r['pct_fp32_mfma_peak']:.1f} | {r['alg_hbm_gbs']:.0f} | {r['bound']} | "
+                     f"{r['roofline_frac']:.3f} |")
+    return "\n".join(lines) + "\n"
+
+
 def cpu_baseline(c, budget_s=10.0):
     """The fp64 oracle on this host's cores over a bounded batch sample."""
     import numpy as np
@@ -526,6 +578,9 @@ def main():
                     help="model validation: time the model's top 5 and a uniform sample of the other "
                          "candidates (N plans per layer, default 100) of every layer; writes "
                          "profiles/model_rank_sweep.{json,md}")
+    ap.add_argument("--table1", action="store_true",
+                    help="every conv2d layer of Table 1 at batch 1 (stride, same padding); writes "
+                         "profiles/table1_sweep.{json,md}")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU (got --gpus {args.gpus}); "
@@ -550,6 +605,15 @@ def main():
     B.lib()  # fail loudly if the HIP library is missing
     if args.traffic_run:
         traffic_run(list(CONFIGS) if args.layer == "all" else [BY_NAME[args.layer]])
+        return
+    if args.table1:
+        rows = table1_sweep()
+        json.dump({"layers": rows, "_meta": {"kernel_sha": kernel_source_hash(),
+                                             "command": "python bench.py --table1"}},
+                  open(TABLE1_JSON, "w"), indent=1)
+        md = table1_report(rows)
+        open(TABLE1_MD, "w").write(md)
+        print(md, flush=True)
         return
     if args.rank_sweep:
         res = rank_sweep(list(CONFIGS) if args.layer in ("all", HEADLINE) else [BY_NAME[args.layer]],

@@ -62,7 +62,24 @@ STRIDED_CONFIGS = (
     ConvShape("conv1x1s2_n32_c64_k128_in56", 32, 64, 128, 56, 56, 1, 1, "f32", 8000, 2, 0),
 )
 
-BY_NAME = {c.name: c for c in CONFIGS + STRIDED_CONFIGS}
+# Table 1's conv2d layers (Yolo-9000 and ResNet-18) at batch 1, fp32, with
+# the table's stride and "same" padding (R // 2 on each side), as the
+# networks use them.  MobileNet's depth-wise layers are not an instance of
+# Eq. (1) and are left out.  (K, C, H = W, R = S, stride) per layer.
+_TABLE1 = (
+    ("Y0", 32, 3, 544, 3, 1), ("Y2", 64, 32, 272, 3, 1), ("Y4", 128, 64, 136, 3, 1),
+    ("Y5", 64, 128, 136, 1, 1), ("Y8", 256, 128, 68, 3, 1), ("Y9", 128, 256, 68, 1, 1),
+    ("Y12", 512, 256, 34, 3, 1), ("Y13", 256, 512, 34, 1, 1), ("Y18", 1024, 512, 17, 3, 1),
+    ("Y19", 512, 1024, 17, 1, 1), ("Y23", 28269, 1024, 17, 1, 1),
+    ("R1", 64, 3, 224, 7, 2), ("R2", 64, 64, 56, 3, 1), ("R3", 64, 64, 56, 1, 1),
+    ("R4", 128, 64, 56, 3, 2), ("R5", 128, 64, 56, 1, 2), ("R6", 128, 128, 28, 3, 1),
+    ("R7", 256, 128, 28, 3, 2), ("R8", 256, 128, 28, 3, 1), ("R9", 256, 256, 14, 3, 1),
+    ("R10", 512, 256, 14, 3, 2), ("R11", 512, 256, 14, 1, 2), ("R12", 512, 512, 7, 3, 1),
+)
+TABLE1 = tuple(ConvShape(f"table1_{name}", 1, C, K, HW, HW, RS, RS, "f32", 9000 + i, st, RS // 2)
+               for i, (name, K, C, HW, RS, st) in enumerate(_TABLE1))
+
+BY_NAME = {c.name: c for c in CONFIGS + STRIDED_CONFIGS + TABLE1}
 
 
 def make_inputs(shape, seed=None, kind="uniform"):

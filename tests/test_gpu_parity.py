@@ -470,3 +470,18 @@ def test_strided_full_config_sampled(cfg):
     ref = oconv.conv_fwd_ex_points(host(In), host(Ker), idx, (cfg.stride,) * 2, (cfg.pad,) * 2)
     got = out.reshape(-1)[idx]
     assert np.max(np.abs(got - ref)) <= TOL["f32"] * max(1.0, np.max(np.abs(ref)))
+
+
+@pytest.mark.parametrize("cfg", __import__("paper_2101_09808_amd.workloads", fromlist=["x"]).TABLE1,
+                         ids=lambda c: c.name)
+def test_table1_layer_sampled(cfg):
+    """Table 1 layers at batch 1 with stride and same padding: sampled
+    outputs against the strided oracle."""
+    In, Ker = make_inputs(cfg)
+    say(f"[gpu] {cfg.name}")
+    out = host(B.conv_fwd_ex(In.to(DEV), Ker.to(DEV), cfg.stride, cfg.pad))
+    assert out.shape == (cfg.N, cfg.K, cfg.P, cfg.Q)
+    rng = np.random.default_rng(cfg.seed)
+    idx = np.unique(np.concatenate([rng.integers(0, out.size, 2000), [0, out.size - 1]]))
+    ref = oconv.conv_fwd_ex_points(host(In), host(Ker), idx, (cfg.stride,) * 2, (cfg.pad,) * 2)
+    assert np.max(np.abs(out.reshape(-1)[idx] - ref)) <= TOL["f32"] * max(1.0, np.max(np.abs(ref)))
