@@ -1427,22 +1427,24 @@ splitk_reduce_kernel(const float* __restrict__ W, float* __restrict__ Out, int64
 // sh*r' + a >= R or sw*t' + b >= S.
 
 // Inp[n][(c*na + a)*nb + b][y][x] = In[n][c][y*sh + a - ph][x*sw + b - pw],
-// zero outside the input.  One element per thread, grid-stride.
+// zero outside the input.  One element per thread, grid-stride; 32-bit
+// index arithmetic (both tensors hold fewer than 2^31 elements).
 template <typename T>
 __global__ void __launch_bounds__(256)
 phase_split_kernel(const T* __restrict__ In, T* __restrict__ Inp, PhaseGeom p) {
   const int Cp = p.C * p.na * p.nb;
-  const int64_t total = (int64_t)p.N * Cp * p.Hp * p.Wp;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
-    int64_t t = i;
-    const int x = (int)(t % p.Wp); t /= p.Wp;
-    const int y = (int)(t % p.Hp); t /= p.Hp;
-    const int cp = (int)(t % Cp);
-    const int n = (int)(t / Cp);
+  const int total = p.N * Cp * p.Hp * p.Wp;
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < total; i += gridDim.x * 256) {
+    int t = i;
+    const int x = t % p.Wp;
+    t /= p.Wp;
+    const int y = t % p.Hp;
+    t /= p.Hp;
+    const int cp = t % Cp;
+    const int n = t / Cp;
     const int b = cp % p.nb, a = (cp / p.nb) % p.na, c = cp / (p.na * p.nb);
     const int iy = y * p.sh + a - p.ph, ix = x * p.sw + b - p.pw;
-    Inp[i] = (iy >= 0 && iy < p.H && ix >= 0 && ix < p.W) ? In[(((int64_t)n * p.C + c) * p.H + iy) * p.W + ix]
-                                                          : T(0);
+    Inp[i] = (iy >= 0 && iy < p.H && ix >= 0 && ix < p.W) ? In[((n * p.C + c) * p.H + iy) * p.W + ix] : T(0);
   }
 }
 

@@ -579,6 +579,26 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
 }
 
 namespace {
+// Measured correction of the model per kernel family (the model does not
+// capture latency hiding or the inner loop's issue overhead): the unrolled
+// pointwise streaming kernel and the transposing bf16 kernel run about 20%
+// faster than the direct-to-LDS pipeline at equal predicted time, the looped
+// streaming kernel about 10% slower, and the register-staged kernel from
+// about as fast (tiny grids) to nearly three times slower (layer sweeps on
+// MI355X: the five configurations, the Table 1 layers at batch 1 and the
+// strided layers at batch 32; 2 keeps it for the small layers where it wins).
+// Plans are ranked by predicted time times this factor.
+double family_factor(int family) {
+  switch (family) {
+    case FAMILY_STREAM1X1:
+    case FAMILY_BF16_TR: return 0.8;
+    case FAMILY_DMA:
+    case FAMILY_BF16: return 1.0;
+    case FAMILY_STREAM1X1_LOOP: return 1.1;
+    default: return 2.0;
+  }
+}
+
 void fill_plan_fields(conv_plan_t* p, const Variant& v, int nwk, int nwp, int tr, int tw,
                       int order) {
   std::memset(p, 0, sizeof(*p));
@@ -599,23 +619,9 @@ void fill_plan_fields(conv_plan_t* p, const Variant& v, int nwk, int nwp, int tr
 // Deterministic preference among plans (tie-breaks: predicted time, total
 // predicted bytes, fewer workgroups, variant id, larger k tile, no split).
 bool better(const conv_plan_t& a, const conv_plan_t& b) {
-  // Family preference (measured, not modelled: the model does not capture
-  // latency hiding): the unrolled pointwise streaming kernel, then the
-  // direct-to-LDS pipeline (or the bf16 kernel), then the looped streaming
-  // kernel, then the register-staged fallback for shapes no other takes.
-  auto rank = [](int fam) {
-    switch (fam) {
-      case FAMILY_STREAM1X1:
-      case FAMILY_BF16_TR: return 0;
-      case FAMILY_DMA:
-      case FAMILY_BF16: return 1;
-      case FAMILY_STREAM1X1_LOOP: return 2;
-      default: return 3;
-    }
-  };
-  const int fa = rank(find_variant(a.variant)->family), fb = rank(find_variant(b.variant)->family);
-  if (fa != fb) return fa < fb;
-  if (a.pred_total_us != b.pred_total_us) return a.pred_total_us < b.pred_total_us;
+  const double ta = a.pred_total_us * family_factor(find_variant(a.variant)->family);
+  const double tb = b.pred_total_us * family_factor(find_variant(b.variant)->family);
+  if (ta != tb) return ta < tb;
   double ba = 0, bb = 0;
   for (int l = 0; l < CONV_NUM_LVLS; ++l) {
     ba += a.pred_bytes[l];

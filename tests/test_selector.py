@@ -91,20 +91,19 @@ def test_plan_invariants(shape):
     assert B.conv_fwd_plan(*dims, dtype=dtype) == plan
     cands = B.conv_fwd_candidates(*dims, dtype=dtype)
     assert cands[0] == plan
-    # families in the library's order of preference (unrolled pointwise
-    # streaming, then direct-to-LDS / bf16, then looped streaming, then
-    # register-staged), each by predicted time
-    rank = {4: 0, 6: 0, 2: 1, 3: 1, 5: 2, 1: 3}
+    # ranked by predicted time times the measured factor of the kernel
+    # family (unrolled streaming and transposing bf16 0.8, direct-to-LDS and
+    # bf16 1.0, looped streaming 1.1, register-staged 2.0)
+    factor = {4: 0.8, 6: 0.8, 2: 1.0, 3: 1.0, 5: 1.1, 1: 2.0}
     fam = [B.conv_fwd_geometry(*dims, c)["family"] for c in cands]
-    assert fam == sorted(fam, key=lambda f: rank[f])
-    for f in set(fam):
-        tot = [c["pred_total_us"] for c, ff in zip(cands, fam) if ff == f]
-        assert tot == sorted(tot)
+    eff = [c["pred_total_us"] * factor[f] for c, f in zip(cands, fam)]
+    assert all(x <= y * (1 + 1e-12) for x, y in zip(eff, eff[1:]))
 
 
 def test_selector_is_minimum_of_its_objective():
     """The chosen plan has the smallest predicted max-level time of all the
-    candidates of its kernel family (the min-max of Sec. 5)."""
+    candidates of its kernel family (the min-max of Sec. 5; across families
+    the measured family factor applies)."""
     for c in CONFIGS:
         if c.dtype != "f32":
             continue
