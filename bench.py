@@ -191,7 +191,16 @@ def calibrated(d, counter, unit_bytes, layers, launches):
     plain copies.  The first launch of each layer (which also faults in the
     buffers) is left out."""
     rows = counter_per_dispatch(d, counter)
-    conv = [v for n, v in rows if "convfwd::" in n]
+    # a split plan's launch is two dispatches: the main kernel, then the
+    # reduction of its channel ranges, counted together
+    conv = []
+    for n, v in rows:
+        if "convfwd::" not in n:
+            continue
+        if "splitk_reduce" in n and conv:
+            conv[-1] += v
+        else:
+            conv.append(v)
     # the calibration copies are the process's first copy kernels (later ones,
     # e.g. dtype conversions of the inputs, are not of known size)
     first_conv = next((i for i, (n, _) in enumerate(rows) if "convfwd::" in n), len(rows))

@@ -492,19 +492,33 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
       waves * steps * reads_per_step * 64 * ((plan->dtype == CONV_DTYPE_BF16) ? 16.0 : 4.0);
 
   // LDS: per workgroup, every channel brings its In halo rows and Ker rows.
-  double in_tiles = 0;  // sum over pixel tiles of the halo footprint (elements per channel)
+  // Memory moves whole 128-byte lines (Sec. 12 names spatial locality as the
+  // model's missing refinement): a contiguous run of L bytes at a random
+  // element alignment touches on average (L + 128 - e) / 128 lines, so each
+  // run is charged L + 128 - e bytes.  A tile's rows are runs of their own,
+  // unless the rows are so short that their lines overlap: a tile never
+  // touches more than the lines of the span from its first to its last
+  // element.  A Ker tile holding every channel is one run per k.
+  const double line = 128.0;
+  auto run_bytes = [&](double L) { return L > 0 ? L + line - e : 0.0; };
+  double in_tiles = 0;  // sum over pixel tiles of the halo footprint, bytes per channel, in lines
   for (int64_t rt = 0; rt < g.tiles_rows; ++rt) {
     const int64_t r0 = rt * g.tr, r1 = std::min<int64_t>(r0 + g.tr, NP) - 1;
     const int64_t nu0 = (r0 / g.P) * s.H + r0 % g.P, nu1 = (r1 / g.P) * s.H + r1 % g.P + s.R - 1;
+    const double rows = (double)(nu1 - nu0 + 1);
     for (int64_t ct = 0; ct < g.tiles_cols; ++ct) {
       const int64_t cols = std::min<int64_t>(g.tw, g.Q - ct * g.tw) + s.S - 1;
-      in_tiles += (double)(nu1 - nu0 + 1) * cols;
+      const double span = run_bytes(((rows - 1) * s.W + cols) * e);
+      in_tiles += std::min(span, rows * run_bytes((double)cols * e));
     }
   }
-  const double in_halo_bytes = in_tiles * s.C * e;     // one pass over all pixel tiles
-  const double ker_bytes = (double)s.K * s.C * RS * e;  // whole kernel tensor
+  const double in_halo_bytes = in_tiles * s.C;          // one pass over all pixel tiles
+  const double ker_bytes = (double)s.K * s.C * RS * e;  // whole kernel tensor (compulsory)
+  const double ker_line_bytes =                         // the same, fetched in tiles of lines
+      v->tc >= s.C ? (double)s.K * run_bytes((double)s.C * RS * e)
+                   : (double)s.K * g.nchunks * run_bytes((double)v->tc * RS * e);
   const double pix_tiles = (double)g.tiles_rows * g.tiles_cols;
-  plan->pred_bytes[CONV_LVL_LDS] = in_halo_bytes * g.tiles_k + ker_bytes * pix_tiles;
+  plan->pred_bytes[CONV_LVL_LDS] = in_halo_bytes * g.tiles_k + ker_line_bytes * pix_tiles;
 
   // L2: outer tile-loop order of the grid, per XCD.
   const double in_bytes = (double)s.N * s.C * s.H * s.W * e;
@@ -516,18 +530,18 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
     // in flight together on the XCD.
     double ker_l2;
     if (ker_bytes <= 0.5 * kHw.l2_bytes) {
-      ker_l2 = std::min<double>(kHw.xcds, pix_tiles) * ker_bytes;
+      ker_l2 = std::min<double>(kHw.xcds, pix_tiles) * ker_line_bytes;
     } else {
       const double occ = std::max(1, std::min(2, kHw.lds_bytes / std::max(1, lds)));
       const double resident = (double)kHw.cus / kHw.xcds * occ;
       const double inflight = std::max(1.0, resident / g.tiles_k);
-      ker_l2 = pix_tiles / inflight * ker_bytes;
+      ker_l2 = pix_tiles / inflight * ker_line_bytes;
     }
     plan->pred_bytes[CONV_LVL_L2] = in_halo_bytes + ker_l2;
     plan->class_lvl[CONV_LVL_L2] = 5;  // <{n,c,h,r,s}, w, k>: k innermost
   } else {
     // pixel tiles innermost: a k slice of Ker stays; In is re-read per k tile.
-    plan->pred_bytes[CONV_LVL_L2] = in_halo_bytes * g.tiles_k + ker_bytes;
+    plan->pred_bytes[CONV_LVL_L2] = in_halo_bytes * g.tiles_k + ker_line_bytes;
     plan->class_lvl[CONV_LVL_L2] = 1;  // <{k,c,r,s},{n,h},w>: pixels innermost
   }
   // split reduction: every range writes its partial Out to the workspace and
@@ -616,12 +630,15 @@ void fill_plan_fields(conv_plan_t* p, const Variant& v, int nwk, int nwp, int tr
   p->split_c = 1;
 }
 
-// Deterministic preference among plans (tie-breaks: predicted time, total
-// predicted bytes, fewer workgroups, variant id, larger k tile, no split).
+// Deterministic preference among plans (tie-breaks: predicted time times
+// the family factor, MFMA time, total predicted bytes, fewer workgroups,
+// variant id, larger k tile, no split).
 bool better(const conv_plan_t& a, const conv_plan_t& b) {
   const double ta = a.pred_total_us * family_factor(find_variant(a.variant)->family);
   const double tb = b.pred_total_us * family_factor(find_variant(b.variant)->family);
   if (ta != tb) return ta < tb;
+  // equal bound: less MFMA work (fewer padded pixels in partial tiles)
+  if (a.pred_mfma_us != b.pred_mfma_us) return a.pred_mfma_us < b.pred_mfma_us;
   double ba = 0, bb = 0;
   for (int l = 0; l < CONV_NUM_LVLS; ++l) {
     ba += a.pred_bytes[l];

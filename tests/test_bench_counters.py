@@ -51,3 +51,17 @@ def test_instruction_counters_are_not_scaled(tmp_path):
     _write(tmp_path / "c", rows, "SQ_INSTS_LDS")
     factor, _, per = bench.calibrated(str(tmp_path / "c"), "SQ_INSTS_LDS", 1.0, list(CONFIGS[:1]), 3)
     assert factor == 1.0 and per[CONFIGS[0].name]["per_dispatch"] == 7.0
+
+
+def test_split_plan_reduction_counts_with_its_launch(tmp_path):
+    """A split plan's second dispatch (the range reduction) is added to the
+    main kernel's counts for that launch."""
+    layers = list(CONFIGS[:1])
+    launches = 3
+    rows = [("__runtime_copyBuffer", [10.0])] * bench.COPY_REPS
+    for _ in range(launches):
+        rows.append(("void convfwd::conv_f32_dma_kernel<1>", [40.0]))
+        rows.append(("void convfwd::splitk_reduce_kernel<true>", [2.0]))
+    _write(tmp_path / "c", rows, "WRITE_SIZE")
+    _, _, per = bench.calibrated(str(tmp_path / "c"), "WRITE_SIZE", 1.0, layers, launches)
+    assert per[layers[0].name]["per_dispatch"] == pytest.approx(42.0)
