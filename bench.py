@@ -56,7 +56,7 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def time_layer(c, steps, warmup, queued=False):
+def time_layer(c, steps, warmup, queued=False, out_bf16=False):
     """Average launch duration from HIP events recorded on the launch stream
     around the `steps` back-to-back launches of the timed region (rotating
     buffer sets), and the host wall time of the same region.  queued: the
@@ -73,7 +73,8 @@ def time_layer(c, steps, warmup, queued=False):
     dev = torch.device("cuda:0")
     Ker = Ker0.to(dev)
     ins = [In0.to(dev) for _ in range(nsets)]
-    outs = [torch.empty(c.N, c.K, c.P, c.Q, device=dev) for _ in range(nsets)]
+    odt = torch.bfloat16 if out_bf16 else torch.float32
+    outs = [torch.empty(c.N, c.K, c.P, c.Q, device=dev, dtype=odt) for _ in range(nsets)]
     bf16 = c.dtype == "bf16"
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
@@ -86,7 +87,9 @@ def time_layer(c, steps, warmup, queued=False):
     dt = B.CONV_DTYPE_BF16 if bf16 else B.CONV_DTYPE_F32
 
     def fn(i):
-        if strided:
+        if out_bf16:
+            st = L.conv_fwd_bf16_out(*c.key(), ips[i], kp, ops[i], sp)
+        elif strided:
             st = L.conv_fwd_ex(*c.key(), c.stride, c.stride, c.pad, c.pad, dt, ips[i], kp, ops[i], sp)
         else:
             st = B.conv_fwd_ptr(*c.key(), ips[i], kp, ops[i], sp, bf16)
@@ -94,7 +97,9 @@ def time_layer(c, steps, warmup, queued=False):
             raise B.ConvError(st, "conv_fwd")
 
     fn(0)  # checked call through the tensor API first
-    if strided:
+    if out_bf16:
+        B.conv_fwd_bf16_out(ins[0], Ker, out=outs[0])
+    elif strided:
         B.conv_fwd_ex(ins[0], Ker, c.stride, c.pad, out=outs[0])
     else:
         (B.conv_fwd_bf16 if bf16 else B.conv_fwd)(ins[0], Ker, out=outs[0])
@@ -704,6 +709,17 @@ def main():
             layers[lc.name].update({"mopt5_variant": tplan["variant"], "mopt5_split_c": tplan["split_c"],
                                     "mopt5_kernel_us": tk * 1e6, "mopt5_gflops": flops(lc) / tk / 1e9,
                                     "mopt5_pct_hbm_peak": 100 * alg_bytes(lc) / tk / 1e9 / PEAK["hbm_gbs"]})
+        # the bf16 layer with bf16 Out (conv_fwd_bf16_out): half the write traffic
+        c5 = [lc for lc in CONFIGS if lc.dtype == "bf16"][0]
+        lk = time_layer(c5, 50, 5, queued=True, out_bf16=True)["mean_kernel_ms"] * 1e-3
+        ab = alg_bytes(c5) - c5.N * c5.K * c5.P * c5.Q * 2
+        layers[c5.name + "_bf16out"] = {
+            "dtype": "bf16", "out_dtype": "bf16", "variant": B.conv_fwd_plan(*c5.key(), dtype=B.CONV_DTYPE_BF16)["variant"],
+            "split_c": 1, "kernel_us": lk * 1e6, "gflops": flops(c5) / lk / 1e9,
+            "pct_fp32_mfma_peak": 100 * flops(c5) / lk / 1e12 / PEAK["fp32_mfma_tflops"],
+            "pct_dtype_mfma_peak": 100 * flops(c5) / lk / 1e12 / PEAK["bf16_mfma_tflops"],
+            "alg_hbm_gbs": ab / lk / 1e9, "pct_hbm_peak": 100 * ab / lk / 1e9 / PEAK["hbm_gbs"],
+        }
         # strided, padded Table 1 layers (conv_fwd_ex: polyphase rewrite, then
         # the selected stride-1 plan of the inner problem), timed the same way
         for lc in STRIDED_CONFIGS:

@@ -124,6 +124,21 @@ int conv_fwd_bf16(int N, int C, int K, int H, int W, int R, int S,
                   const uint16_t* In, const uint16_t* Ker, float* Out, void* stream);
 
 /*
+ * bf16-input forward convolution with bf16 output: as conv_fwd_bf16 (fp32
+ * products and sums), then each output rounded to the nearest bf16 (ties to
+ * even), halving the bytes written.  Out : [N][K][H-R+1][W-S+1] bf16 bit
+ * patterns, device.  The plan is the one conv_fwd_bf16 selects; the
+ * transposing-read bf16 kernel writes bf16 directly, any other kernel
+ * writes fp32 into a stream-ordered workspace (from the device's default
+ * pool, returned within the call) that a second kernel rounds into Out.
+ * The paper states single precision only; the other entry points write
+ * fp32 Out, and this one is the bf16-output refinement that makes bf16
+ * layers less write-bound.  Returns a conv_status_t.
+ */
+int conv_fwd_bf16_out(int N, int C, int K, int H, int W, int R, int S,
+                      const uint16_t* In, const uint16_t* Ker, uint16_t* Out, void* stream);
+
+/*
  * Strided, zero-padded forward convolution.  The paper presents Eq. (1)
  * without stride and notes that the method carries over (Sec. 3.1,
  * footnote 1); Table 1 includes stride-2 layers.  The operation:

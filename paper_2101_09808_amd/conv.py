@@ -79,6 +79,8 @@ def lib():
         L.conv_fwd_tune.argtypes = shape7 + [_i32, _vp, _vp, _vp, _i32, _i32, _vp, ctypes.POINTER(ConvPlan),
                                              ctypes.POINTER(ctypes.c_float)]
         L.conv_fwd_tune.restype = _i32
+        L.conv_fwd_bf16_out.argtypes = shape7 + [_vp, _vp, _vp, _vp]
+        L.conv_fwd_bf16_out.restype = _i32
         L.conv_fwd_ex.argtypes = shape7 + [_i32] * 5 + [_vp, _vp, _vp, _vp]
         L.conv_fwd_ex.restype = _i32
         L.conv_fwd_ex_inner_shape.argtypes = shape7 + [_i32] * 4 + [ctypes.POINTER(_i32)]
@@ -155,6 +157,22 @@ def conv_fwd_bf16(In, Ker, out=None, stream=None):
     st = lib().conv_fwd_bf16(*shape, In.data_ptr(), Ker.data_ptr(), out.data_ptr(), _stream_ptr(stream))
     if st != CONV_OK:
         raise ConvError(st, "conv_fwd_bf16")
+    return out
+
+
+def conv_fwd_bf16_out(In, Ker, out=None, stream=None):
+    """Eq. (1) for bf16 In and Ker with fp32 accumulation, Out rounded to
+    bf16 (nearest even); returns a bf16 [N,K,P,Q] tensor."""
+    shape = _check_inputs(In, Ker, torch.bfloat16)
+    N, C, K, H, W, R, S = shape
+    oshape = (N, K, H - R + 1, W - S + 1)
+    if out is None:
+        out = torch.empty(oshape, dtype=torch.bfloat16, device=In.device)
+    elif out.shape != oshape or out.dtype != torch.bfloat16 or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous bfloat16 {oshape} tensor")
+    st = lib().conv_fwd_bf16_out(*shape, In.data_ptr(), Ker.data_ptr(), out.data_ptr(), _stream_ptr(stream))
+    if st != CONV_OK:
+        raise ConvError(st, "conv_fwd_bf16_out")
     return out
 
 

@@ -174,6 +174,17 @@ int conv_fwd_bf16(int N, int C, int K, int H, int W, int R, int S, const uint16_
   return run_selected(Shape{N, C, K, H, W, R, S}, CONV_DTYPE_BF16, In, Ker, Out, stream);
 }
 
+int conv_fwd_bf16_out(int N, int C, int K, int H, int W, int R, int S, const uint16_t* In,
+                      const uint16_t* Ker, uint16_t* Out, void* stream) {
+  int st = validate_shape(N, C, K, H, W, R, S);
+  if (st != CONV_OK) return st;
+  if (!In || !Ker || !Out) return CONV_ENULL;
+  Entry e;
+  st = cached_entry(Shape{N, C, K, H, W, R, S}, CONV_DTYPE_BF16, alignment_of(In, Ker), &e);
+  if (st != CONV_OK) return st;
+  return launch_bf16_out(*e.v, e.g, In, Ker, Out, stream);
+}
+
 int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w, int pad_h,
                 int pad_w, int dtype, const void* In, const void* Ker, float* Out, void* stream) {
   PhaseGeom p;

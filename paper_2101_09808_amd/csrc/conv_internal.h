@@ -74,6 +74,10 @@ bool resolve_geom(const Shape& s, const Variant& v, const conv_plan_t& plan, Geo
 
 // Launch the kernel of variant v (asynchronous).  Returns a conv_status_t.
 int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, float* Out, void* stream);
+// Launch of a bf16-input plan writing bf16 Out (round to nearest even): the
+// transposing bf16 kernel writes it directly; other kernels write fp32 to a
+// stream-ordered workspace that a second kernel rounds into Out.
+int launch_bf16_out(const Variant& v, const Geom& g, const void* In, const void* Ker, void* Out, void* stream);
 
 // Polyphase rewrite of a strided, padded convolution into a stride-1 valid
 // one (conv_fwd_ex): na x nb phases per input channel, inner extents

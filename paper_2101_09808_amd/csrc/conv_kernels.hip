@@ -807,10 +807,11 @@ conv_bf16_kernel(const unsigned short* __restrict__ In, const unsigned short* __
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef short v8s __attribute__((ext_vector_type(8)));
 
-template <int TR, int TW, int RC, int SC>
+template <int TR, int TW, int RC, int SC, bool OUTB>
 __global__ void __launch_bounds__(kThreads)
 conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short* __restrict__ Ker,
                     float* __restrict__ Out, const Geom g) {
+  // OUTB: Out holds bf16 (the fp32 sums rounded to nearest even) instead of fp32
   static_assert(SC >= 1 && SC <= 3, "copies from two neighbouring dwords");
   static_assert(TW % 16 == 0 && (TR * (TW / 16)) % 4 == 0, "whole blocks of 16 for four waves");
   extern __shared__ __align__(16) unsigned char smem[];
@@ -845,8 +846,13 @@ conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short*
   const int per = (tiles + G - 1) / G;
   const int t_begin = L * per, t_end = min(tiles, t_begin + per);
   if (t_begin >= t_end) return;
-  // 16-byte output stores need Q % 4 == 0 and a 16-byte aligned Out
-  const bool vec_out = (Q & 3) == 0 && (reinterpret_cast<uintptr_t>(Out) & 15) == 0;
+  // vector output stores (4 pixels: 16 bytes, or 8 for bf16 Out) need
+  // Q % 4 == 0 and an Out aligned to that size
+  constexpr int OUT_E = OUTB ? 2 : 4;
+  const bool vec_out = (Q & 3) == 0 && (reinterpret_cast<uintptr_t>(Out) & (4 * OUT_E - 1)) == 0;
+  // bf16 Out in 16-byte pieces of two neighbouring blocks (see the stores)
+  constexpr bool PAIRED = OUTB && PB % 2 == 0 && CBR % 2 == 0;
+  const bool pair_out = PAIRED && (Q & 7) == 0 && (reinterpret_cast<uintptr_t>(Out) & 15) == 0;
 
   // Ker loads first (rows past K read zeros: past the buffer's range)
   const __amdgpu_buffer_rsrc_t krsrc =
@@ -952,7 +958,7 @@ conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short*
   // back here, so the stores carry the non-temporal hint (measured 3% faster
   // on the 226^2 layer).
   const __amdgpu_buffer_rsrc_t orsrc = __builtin_amdgcn_make_buffer_rsrc(
-      Out, (short)0, (int)((unsigned)g.N * K * P * Q * 4u), 0x00020000);
+      Out, (short)0, (int)((unsigned)g.N * K * P * Q * (unsigned)OUT_E), 0x00020000);
   v4f pend[PB][4];
   bool have_pend = false;
   int pbase = 0, pcol = 0, ppart = 0;  // element offset of (n, k = j, row p0, column q0 + 4 gq)
@@ -961,17 +967,56 @@ conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short*
     const int b = wave * WP + ppart * PB + bi;
     const int col = pcol + 16 * (b % CBR);
     const bool ok = have_pend && kb * 16 + j < K;
-    const unsigned off = (unsigned)(pbase + kb * 16 * P * Q + (b / CBR) * Q + 16 * (b % CBR)) * 4u;
-    if (vec_out) {
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, pend[bi][kb]), orsrc,
-                                             ok && col < Q ? off : kOob, 0, kStoreNT);
-    } else {
-      // (the whole vector is reinterpreted: a bit cast of one element
-      // lvalue of a vector compiles to element 0 for every v)
-      const v4u pv = __builtin_bit_cast(v4u, pend[bi][kb]);
+    const unsigned el = (unsigned)(pbase + kb * 16 * P * Q + (b / CBR) * Q + 16 * (b % CBR));
+    if constexpr (OUTB) {
+      // Round to bf16 (nearest even; the conversion instruction of gfx950).
+      // Four pixels of bf16 are only 8 bytes, and 32-byte pieces of a line
+      // write slowly; so two neighbouring blocks are stored together: lane
+      // pairs (gq, gq ^ 1) swap halves through ds_bpermute, and each lane
+      // stores 8 consecutive pixels (16 bytes): even gq those of block bi,
+      // odd gq those of block bi + 1, 64 bytes per k row.  Needs Q % 8 == 0
+      // and a 16-byte aligned Out; otherwise 2-byte stores per pixel.
+      auto cvt = [](const v4f& a, unsigned& lo, unsigned& hi) __attribute__((always_inline)) {
+        unsigned short h[4];
 #pragma unroll
-      for (int v = 0; v < 4; ++v)
-        __builtin_amdgcn_raw_buffer_store_b32(pv[v], orsrc, ok && col + v < Q ? off + 4u * v : kOob, 0, kStoreNT);
+        for (int v = 0; v < 4; ++v) h[v] = __builtin_bit_cast(unsigned short, (__bf16)a[v]);
+        lo = (unsigned)h[0] | ((unsigned)h[1] << 16);
+        hi = (unsigned)h[2] | ((unsigned)h[3] << 16);
+      };
+      if (pair_out) {
+        if constexpr (PAIRED && bi % 2 == 0) {
+          unsigned a0, a1, b0, b1;
+          cvt(pend[bi][kb], a0, a1);
+          cvt(pend[bi + 1][kb], b0, b1);
+          const bool even = (gq & 1) == 0;
+          const int partner = (lane ^ 16) * 4;
+          const unsigned r0 = (unsigned)__builtin_amdgcn_ds_bpermute(partner, (int)(even ? b0 : a0));
+          const unsigned r1 = (unsigned)__builtin_amdgcn_ds_bpermute(partner, (int)(even ? b1 : a1));
+          const v4u w = even ? v4u{a0, a1, r0, r1} : v4u{r0, r1, b0, b1};
+          const unsigned e8 = even ? el : el + 12u;  // odd: block bi + 1, pixels 4 (gq - 1) ..
+          const int c8 = even ? col : col + 12;
+          __builtin_amdgcn_raw_buffer_store_b128(w, orsrc, ok && c8 < Q ? e8 * 2u : kOob, 0, kStoreNT);
+        }
+      } else {
+        const v4f a = pend[bi][kb];
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (__bf16)a[v]), orsrc,
+                                                ok && col + v < Q ? (el + v) * 2u : kOob, 0, kStoreNT);
+      }
+    } else {
+      const unsigned off = el * 4u;
+      if (vec_out) {
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, pend[bi][kb]), orsrc,
+                                               ok && col < Q ? off : kOob, 0, kStoreNT);
+      } else {
+        // (the whole vector is reinterpreted: a bit cast of one element
+        // lvalue of a vector compiles to element 0 for every v)
+        const v4u pv = __builtin_bit_cast(v4u, pend[bi][kb]);
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          __builtin_amdgcn_raw_buffer_store_b32(pv[v], orsrc, ok && col + v < Q ? off + 4u * v : kOob, 0, kStoreNT);
+      }
     }
   };
 
@@ -1387,6 +1432,7 @@ struct Instance {
   Variant v;
   KernelF32 f32;
   KernelBF16 bf16;
+  KernelBF16 bf16_outb;  // the same kernel writing bf16 Out (transposing bf16 family only)
 };
 
 // ---------------------------------------------------------------------------
@@ -1467,6 +1513,14 @@ ker_phase_kernel(const T* __restrict__ Ker, T* __restrict__ Kp, PhaseGeom p) {
   }
 }
 
+// Out (bf16) = fp32 partial result rounded to nearest even, for the bf16
+// output of kernels that only write fp32.
+__global__ void __launch_bounds__(256)
+round_bf16_kernel(const float* __restrict__ src, unsigned short* __restrict__ dst, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    dst[i] = __builtin_bit_cast(unsigned short, (__bf16)src[i]);
+}
+
 #define F32_INST(ID, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV)                                  \
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STAGED, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV, 1, \
                    kThreads, 2},                                                             \
@@ -1496,7 +1550,8 @@ ker_phase_kernel(const T* __restrict__ Ker, T* __restrict__ Kp, PhaseGeom p) {
 #define BF16_TR_INST(ID, TR, TW, RC, SC)                                                       \
   Instance{Variant{ID, CONV_DTYPE_BF16, FAMILY_BF16_TR, 4, TR * TW / 64, 32, RC, SC, TR, TW, 8, 1, \
                    kThreads, 1},                                                                  \
-           nullptr, &conv_bf16_tr_kernel<TR, TW, RC, SC>}
+           nullptr, &conv_bf16_tr_kernel<TR, TW, RC, SC, false>,                                    \
+           &conv_bf16_tr_kernel<TR, TW, RC, SC, true>}
 
 #define BF16_INST(ID, WK, WP, RC, SC, MAXIT)                                                  \
   Instance{Variant{ID, CONV_DTYPE_BF16, FAMILY_BF16, WK, WP, 32, RC, SC, MAXIT, 0, 8, 8, kThreads, \
@@ -1655,6 +1710,46 @@ int launch_phase_split(const PhaseGeom& p, int dtype, const void* In, const void
                          static_cast<float*>(Kp), p);
   }
   return hipGetLastError() == hipSuccess ? CONV_OK : CONV_EHIP;
+}
+
+int launch_bf16_out(const Variant& v, const Geom& g, const void* In, const void* Ker, void* Out, void* stream) {
+  const Instance* inst = find_instance(v.id);
+  if (!inst) return CONV_EINVAL;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (inst->bf16_outb) {
+    // lds and alignment as for the fp32-Out launch of the same instance
+    static std::mutex mu;
+    static bool done[kNumInstances] = {};
+    const int idx = (int)(inst - kInstances);
+    {
+      std::lock_guard<std::mutex> lk(mu);
+      if (!done[idx]) {
+        if (hipFuncSetAttribute(reinterpret_cast<const void*>(inst->bf16_outb),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, 163840) != hipSuccess)
+          return CONV_EHIP;
+        done[idx] = true;
+      }
+    }
+    if ((reinterpret_cast<uintptr_t>(Ker) % 16) != 0) return CONV_EINVAL;
+    hipLaunchKernelGGL(inst->bf16_outb, dim3(g.grid), dim3(v.threads), g.stage_elems, st,
+                       static_cast<const unsigned short*>(In), static_cast<const unsigned short*>(Ker),
+                       static_cast<float*>(Out), g);
+    return hipGetLastError() == hipSuccess ? CONV_OK : CONV_EHIP;
+  }
+  // any other kernel: fp32 Out into a stream-ordered workspace, then rounded
+  const int64_t n = (int64_t)g.N * g.K * g.P * g.Q;
+  void* ws = nullptr;
+  int rc = stream_alloc((size_t)n * sizeof(float), stream, &ws);
+  if (rc != CONV_OK) return rc;
+  rc = launch(v, g, In, Ker, static_cast<float*>(ws), stream);
+  if (rc == CONV_OK) {
+    const int blocks = (int)std::min<int64_t>((n + 255) / 256, 8192);
+    hipLaunchKernelGGL(round_bf16_kernel, dim3(blocks), dim3(256), 0, st, static_cast<const float*>(ws),
+                       static_cast<unsigned short*>(Out), n);
+    if (hipGetLastError() != hipSuccess) rc = CONV_EHIP;
+  }
+  const int freed = stream_free(ws, stream);
+  return rc == CONV_OK ? freed : rc;
 }
 
 int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, float* Out,

@@ -317,11 +317,11 @@ def _swz(chunk, idx):
     return chunk ^ ((idx >> 1) & 3)
 
 
-def emulate_bf16(g, In, Ker, wgs=None, in_aligned=True, out_aligned=True):
+def emulate_bf16(g, In, Ker, wgs=None, in_aligned=True, out_aligned=True, out_bf16=False):
     """In, Ker: flat float64 arrays holding the bf16 values.  Emulates the
     workgroups ``wgs`` (default all) of the persistent grid."""
     if g["family"] == 6:
-        return emulate_bf16_tr(g, In, Ker, wgs, out_aligned)
+        return emulate_bf16_tr(g, In, Ker, wgs, out_aligned, out_bf16)
     N, C, K, H, W, R, S, P, Q = (g[x] for x in "N C K H W R S P Q".split())
     _chk(g["family"] == 3 and g["threads"] == 256, "bf16 family geometry")
     WK, WP, MAXIT = g["wk"], g["wp"], g["max_ni"]
@@ -649,7 +649,7 @@ def tr16_b64(M):
     return R
 
 
-def emulate_bf16_tr(g, In, Ker, wgs=None, out_aligned=True):
+def emulate_bf16_tr(g, In, Ker, wgs=None, out_aligned=True, out_bf16=False):
     """Transposing-read bf16 kernel (family 6): Ker read in 16-byte vectors of
     its natural order and scattered into the LDS image; per thread one In
     group (channel, 8 pixels) on every RPT-th tile row, shifted back at the
@@ -685,7 +685,8 @@ def emulate_bf16_tr(g, In, Ker, wgs=None, out_aligned=True):
          and g["ker_bytes"] == K * C * RS * 2, "sizes")
     _chk(out_size * 4 < 2 ** 31 and in_size * 2 < 2 ** 31, "32-bit buffer offsets")
     OOB = 0x80000000
-    vec_out = Q % 4 == 0 and out_aligned
+    vec_out = Q % 4 == 0 and out_aligned  # 16-byte (8-byte for bf16 Out) stores of 4 pixels
+    out_e = 2 if out_bf16 else 4
     out = np.full(out_size, np.nan)
     written = np.zeros(out_size, np.int64)
     tiles = g["tiles_rows"] * g["tiles_cols"]
@@ -762,6 +763,7 @@ def emulate_bf16_tr(g, In, Ker, wgs=None, out_aligned=True):
                         lin[sx * 32 * CP + dst: sx * 32 * CP + dst + 8] = px[sx:sx + 8]
             for wave in range(4):
                 for part in range(NPART):
+                    accs = []
                     for bi in range(PB):
                         bb = wave * WP + part * PB + bi
                         brow, bcol = bb // CBR, 16 * (bb % CBR)
@@ -786,21 +788,45 @@ def emulate_bf16_tr(g, In, Ker, wgs=None, out_aligned=True):
                                 for kb in range(4):
                                     Bm = np.array([[kval(kb * 16 + jj, rs, c) for jj in range(16)] for c in range(32)])
                                     acc[kb] += Am @ Bm
+                        accs.append((acc, brow, bcol))
+                    paired = out_bf16 and PB % 2 == 0 and CBR % 2 == 0 and Q % 8 == 0 and out_aligned
+                    for bi, (acc, brow, bcol) in enumerate(accs):
                         # stores: lane (j, gq) holds k = 16 kb + j, pixels 4 gq .. 4 gq + 3
+                        if paired and bi % 2 == 1:
+                            continue  # stored with block bi - 1
                         for jj in range(16):
                             for gq in range(4):
                                 pbase = ((n * K + jj) * P + p0) * Q + q0 + 4 * gq
                                 col = q0 + bcol + 4 * gq
                                 for kb in range(4):
                                     k = kb * 16 + jj
-                                    off = pbase + kb * 16 * P * Q + brow * Q + bcol
-                                    vals = acc[kb, 4 * gq: 4 * gq + 4, jj]
                                     if k >= K:
                                         continue
-                                    if vec_out:
+                                    off = pbase + kb * 16 * P * Q + brow * Q + bcol
+                                    if paired:
+                                        # 8 pixels per lane: even gq block bi, odd gq block bi + 1
+                                        acc1, brow1, bcol1 = accs[bi + 1]
+                                        _chk(brow1 == brow and bcol1 == bcol + 16, "paired blocks adjacent")
+                                        even = gq % 2 == 0
+                                        e8 = off if even else off + 12
+                                        c8 = col if even else col + 12
+                                        if c8 >= Q:
+                                            continue
+                                        _chk(e8 % 8 == 0 and c8 % 8 == 0 and c8 + 8 <= Q and (e8 + 8) <= out_size,
+                                             "16-byte bf16 store")
+                                        src_acc = acc if even else acc1
+                                        px0 = 4 * gq if even else 4 * (gq - 1)
+                                        for t in range(8):
+                                            dst = ((n * K + k) * P + p0 + brow) * Q + c8 + t
+                                            _chk(e8 + t == dst, "paired store offset")
+                                            out[dst] = src_acc[kb, px0 + t, jj]
+                                            written[dst] += 1
+                                        continue
+                                    vals = acc[kb, 4 * gq: 4 * gq + 4, jj]
+                                    if vec_out and not out_bf16:
                                         if col >= Q:
                                             continue
-                                        _chk(off % 4 == 0 and (off + 4) * 4 <= out_size * 4, "16-byte store")
+                                        _chk(off % 4 == 0 and (off + 4) * out_e <= out_size * out_e, "vector store")
                                         lanes = range(4)
                                     else:
                                         lanes = [v for v in range(4) if col + v < Q]

@@ -23,7 +23,7 @@ def test_header_declares_the_boundary():
     fns = declared_functions()
     for name in ("conv_fwd", "conv_fwd_bf16", "conv_fwd_plan", "conv_fwd_strerror",
                  "conv_fwd_with_plan", "conv_fwd_candidates", "conv_model_volume", "conv_fwd_tune",
-                 "conv_fwd_ex", "conv_fwd_ex_inner_shape"):
+                 "conv_fwd_ex", "conv_fwd_ex_inner_shape", "conv_fwd_bf16_out"):
         assert name in fns
 
 
@@ -72,6 +72,7 @@ def test_null_pointers_rejected(which):
     ptrs[which] = None
     assert L.conv_fwd(*VALID, *ptrs, None) == B.CONV_ENULL
     assert L.conv_fwd_bf16(*VALID, *ptrs, None) == B.CONV_ENULL
+    assert L.conv_fwd_bf16_out(*VALID, *ptrs, None) == B.CONV_ENULL
     assert L.conv_fwd_with_plan(*VALID, *ptrs, ctypes.byref(B.ConvPlan()), None) == B.CONV_ENULL
     assert L.conv_fwd_plan(*VALID, 0, None) == B.CONV_ENULL
 

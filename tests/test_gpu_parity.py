@@ -485,3 +485,83 @@ def test_table1_layer_sampled(cfg):
     idx = np.unique(np.concatenate([rng.integers(0, out.size, 2000), [0, out.size - 1]]))
     ref = oconv.conv_fwd_ex_points(host(In), host(Ker), idx, (cfg.stride,) * 2, (cfg.pad,) * 2)
     assert np.max(np.abs(out.reshape(-1)[idx] - ref)) <= TOL["f32"] * max(1.0, np.max(np.abs(ref)))
+
+
+
+# ---------------------------------------------------------------------------
+# bf16 output (conv_fwd_bf16_out)
+
+@pytest.mark.parametrize("shape_index", [0, 2], ids=["fallback_c40", "fallback_c32"])
+def test_bf16_out_parity_and_rounding(shape_index):
+    """bf16 Out through the fallback (fp32 workspace, then rounded): within
+    one bf16 rounding of the oracle, and bit-equal to the fp32-Out result of
+    the same plan rounded to nearest even by torch."""
+    shape = BF16_VARIANT_SHAPES[shape_index]
+    In, Ker = make_inputs(shape)
+    ref = oconv.conv_fwd(host(In), host(Ker))
+    In_d, Ker_d = In.to(DEV), Ker.to(DEV)
+    say(f"[gpu] bf16 out {shape.name}")
+    ob = B.conv_fwd_bf16_out(In_d, Ker_d)
+    of = B.conv_fwd_bf16(In_d, Ker_d)
+    torch.cuda.synchronize()
+    assert ob.dtype == torch.bfloat16 and ob.shape == of.shape
+    assert torch.equal(ob.view(torch.int16), of.to(torch.bfloat16).view(torch.int16))
+    got = host(ob.float())
+    scale = np.max(np.abs(ref))
+    assert np.all(np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + TOL["f32"] * scale)
+
+
+def test_bf16_out_transposing_kernel_full_layer():
+    """The 226x226 bf16 layer (transposing-read kernel, bf16 written by the
+    kernel itself): bit-equal to the fp32-Out result rounded by torch, and
+    sampled outputs within one bf16 rounding of the oracle."""
+    cfg = CONFIGS[4]
+    In, Ker = make_inputs(cfg)
+    In_d, Ker_d = In.to(DEV), Ker.to(DEV)
+    plan = B.conv_fwd_plan(*cfg.key(), dtype=B.CONV_DTYPE_BF16)
+    assert B.conv_fwd_geometry(*cfg.key(), plan)["family"] == 6
+    say(f"[gpu] bf16 out {cfg.name} v{plan['variant']}")
+    ob = B.conv_fwd_bf16_out(In_d, Ker_d)
+    of = B.conv_fwd_bf16(In_d, Ker_d)
+    torch.cuda.synchronize()
+    assert torch.equal(ob.view(torch.int16), of.to(torch.bfloat16).view(torch.int16))
+    got = host(ob.float()).reshape(-1)
+    rng = np.random.default_rng(cfg.seed)
+    idx = np.unique(np.concatenate([rng.integers(0, got.size, 3000), [0, got.size - 1]]))
+    ref = oconv.conv_fwd_points(host(In), host(Ker), idx)
+    assert np.all(np.abs(got[idx] - ref) <= 2.0 ** -8 * np.abs(ref) + TOL["f32"] * np.max(np.abs(ref)))
+
+
+def test_bf16_out_transposing_kernel_unaligned_out():
+    """The 226x226 layer's transposing kernel with Out 2 bytes past an 8-byte
+    boundary: 2-byte stores, bit-equal to the fp32 result rounded by torch,
+    nothing written outside Out."""
+    shape = CONFIGS[4]
+    In, Ker = make_inputs(shape)
+    In_d, Ker_d = In.to(DEV), Ker.to(DEV)
+    n = shape.N * shape.K * shape.P * shape.Q
+    buf = torch.zeros(n + 8, dtype=torch.bfloat16, device=DEV)
+    out = buf[1:1 + n].view(shape.N, shape.K, shape.P, shape.Q)
+    assert out.data_ptr() % 8 == 2
+    say(f"[gpu] bf16 out unaligned {shape.name}")
+    B.conv_fwd_bf16_out(In_d, Ker_d, out=out)
+    ref = B.conv_fwd_bf16(In_d, Ker_d).to(torch.bfloat16)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
+    assert buf[0].item() == 0 and (buf[1 + n:] == 0).all()
+
+
+def test_bf16_out_unaligned():
+    """bf16 Out 2 bytes past an 8-byte boundary: 2-byte stores."""
+    shape = BF16_VARIANT_SHAPES[2]
+    In, Ker = make_inputs(shape)
+    In_d, Ker_d = In.to(DEV), Ker.to(DEV)
+    n = shape.N * shape.K * shape.P * shape.Q
+    buf = torch.zeros(n + 8, dtype=torch.bfloat16, device=DEV)
+    out = buf[1:1 + n].view(shape.N, shape.K, shape.P, shape.Q)
+    assert out.data_ptr() % 8 == 2
+    B.conv_fwd_bf16_out(In_d, Ker_d, out=out)
+    ref = B.conv_fwd_bf16(In_d, Ker_d).to(torch.bfloat16)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
+    assert buf[0].item() == 0 and (buf[1 + n:] == 0).all()

@@ -235,3 +235,22 @@ def test_strided_inner_plans_indexing():
             assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
         else:
             _check_all(ish, p)
+
+
+
+@pytest.mark.parametrize("shape_index,aligned", [(2, True), (4, True), (2, False), (3, True)])
+def test_bf16_transposing_bf16_out_indexing(shape_index, aligned):
+    """Family 6 writing bf16 Out: 16-byte stores of eight pixels from lane
+    pairs of neighbouring blocks (2-byte stores when Q % 8 != 0, Out is not
+    16-byte aligned or the blocks do not pair), each output once."""
+    from tests.kernel_emulator import emulate_bf16
+    shape = BF16_VARIANT_SHAPES[shape_index]
+    In, Ker = make_inputs(shape)
+    In64 = In.float().numpy().astype(np.float64)
+    Ker64 = Ker.float().numpy().astype(np.float64)
+    ref = oconv.conv_fwd(In64.astype(np.float32), Ker64.astype(np.float32)).reshape(-1)
+    for p in [p for p in bf16_variant_plans(shape) if B.conv_fwd_geometry(*shape.key(), p)["family"] == 6]:
+        out, written = emulate_bf16(B.conv_fwd_geometry(*shape.key(), p), In64.reshape(-1), Ker64.reshape(-1),
+                                    out_aligned=aligned, out_bf16=True)
+        assert np.all(written == 1)
+        assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
