@@ -121,10 +121,37 @@ int run(const Shape& s, const void* In, const void* Ker, float* Out, const conv_
 }
 
 // Selected plan for a call: cached per shape and tensor alignment.
+// bf16 shapes that no bf16 kernel instance takes (other tap counts): the
+// inputs are widened exactly to fp32 in a stream-ordered workspace and the
+// fp32 plan runs -- the same products and fp32 sums.  out_bf16: Out is
+// bf16, written by rounding an fp32 result kept in the workspace.
+int run_bf16_widened(const Shape& s, const void* In, const void* Ker, void* Out, bool out_bf16, void* stream) {
+  const size_t n_in = (size_t)s.N * s.C * s.H * s.W, n_ker = (size_t)s.K * s.C * s.R * s.S;
+  const size_t n_out = out_bf16 ? (size_t)s.N * s.K * (s.H - s.R + 1) * (s.W - s.S + 1) : 0;
+  const size_t a_in = (n_in * 4 + 255) / 256 * 256, a_ker = (n_ker * 4 + 255) / 256 * 256;
+  void* ws = nullptr;
+  int st = stream_alloc(a_in + a_ker + n_out * 4, stream, &ws);
+  if (st != CONV_OK) return st;
+  float* in32 = static_cast<float*>(ws);
+  float* ker32 = reinterpret_cast<float*>(static_cast<char*>(ws) + a_in);
+  float* out32 = reinterpret_cast<float*>(static_cast<char*>(ws) + a_in + a_ker);
+  st = launch_widen_bf16(In, in32, (int64_t)n_in, stream);
+  if (st == CONV_OK) st = launch_widen_bf16(Ker, ker32, (int64_t)n_ker, stream);
+  if (st == CONV_OK) {
+    Entry e;
+    st = cached_entry(s, CONV_DTYPE_F32, alignment_of(in32, ker32), &e);
+    if (st == CONV_OK) st = launch(*e.v, e.g, in32, ker32, out_bf16 ? out32 : static_cast<float*>(Out), stream);
+  }
+  if (st == CONV_OK && out_bf16) st = launch_round_bf16(out32, Out, (int64_t)n_out, stream);
+  const int freed = stream_free(ws, stream);
+  return st == CONV_OK ? freed : st;
+}
+
 int run_selected(const Shape& s, int dtype, const void* In, const void* Ker, float* Out,
                  void* stream) {
   Entry e;
   const int st = cached_entry(s, dtype, alignment_of(In, Ker), &e);
+  if (st == CONV_ENOPLAN && dtype == CONV_DTYPE_BF16) return run_bf16_widened(s, In, Ker, Out, false, stream);
   if (st != CONV_OK) return st;
   return launch(*e.v, e.g, In, Ker, Out, stream);
 }
@@ -180,7 +207,9 @@ int conv_fwd_bf16_out(int N, int C, int K, int H, int W, int R, int S, const uin
   if (st != CONV_OK) return st;
   if (!In || !Ker || !Out) return CONV_ENULL;
   Entry e;
-  st = cached_entry(Shape{N, C, K, H, W, R, S}, CONV_DTYPE_BF16, alignment_of(In, Ker), &e);
+  const Shape sh{N, C, K, H, W, R, S};
+  st = cached_entry(sh, CONV_DTYPE_BF16, alignment_of(In, Ker), &e);
+  if (st == CONV_ENOPLAN) return run_bf16_widened(sh, In, Ker, Out, true, stream);
   if (st != CONV_OK) return st;
   return launch_bf16_out(*e.v, e.g, In, Ker, Out, stream);
 }

@@ -78,6 +78,10 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
 // transposing bf16 kernel writes it directly; other kernels write fp32 to a
 // stream-ordered workspace that a second kernel rounds into Out.
 int launch_bf16_out(const Variant& v, const Geom& g, const void* In, const void* Ker, void* Out, void* stream);
+// Exact bf16 -> fp32 widening, and fp32 -> bf16 rounding (nearest even), of
+// n elements on `stream`.
+int launch_widen_bf16(const void* src, float* dst, int64_t n, void* stream);
+int launch_round_bf16(const float* src, void* dst, int64_t n, void* stream);
 
 // Polyphase rewrite of a strided, padded convolution into a stride-1 valid
 // one (conv_fwd_ex): na x nb phases per input channel, inner extents

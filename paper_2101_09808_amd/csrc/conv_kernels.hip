@@ -1521,6 +1521,13 @@ round_bf16_kernel(const float* __restrict__ src, unsigned short* __restrict__ ds
     dst[i] = __builtin_bit_cast(unsigned short, (__bf16)src[i]);
 }
 
+// fp32 = the bf16 value (exact: the bf16 bits are the high half).
+__global__ void __launch_bounds__(256)
+widen_bf16_kernel(const unsigned short* __restrict__ src, float* __restrict__ dst, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    dst[i] = __builtin_bit_cast(float, (unsigned)src[i] << 16);
+}
+
 #define F32_INST(ID, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV)                                  \
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STAGED, WK, WP, TC, RC, SC, MAXNI, MAXNK, KV, 1, \
                    kThreads, 2},                                                             \
@@ -1709,6 +1716,20 @@ int launch_phase_split(const PhaseGeom& p, int dtype, const void* In, const void
       hipLaunchKernelGGL(ker_phase_kernel<float>, dim3(g_ker), dim3(256), 0, st, static_cast<const float*>(Ker),
                          static_cast<float*>(Kp), p);
   }
+  return hipGetLastError() == hipSuccess ? CONV_OK : CONV_EHIP;
+}
+
+int launch_widen_bf16(const void* src, float* dst, int64_t n, void* stream) {
+  const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, 8192));
+  hipLaunchKernelGGL(widen_bf16_kernel, dim3(blocks), dim3(256), 0, reinterpret_cast<hipStream_t>(stream),
+                     static_cast<const unsigned short*>(src), dst, n);
+  return hipGetLastError() == hipSuccess ? CONV_OK : CONV_EHIP;
+}
+
+int launch_round_bf16(const float* src, void* dst, int64_t n, void* stream) {
+  const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, 8192));
+  hipLaunchKernelGGL(round_bf16_kernel, dim3(blocks), dim3(256), 0, reinterpret_cast<hipStream_t>(stream), src,
+                     static_cast<unsigned short*>(dst), n);
   return hipGetLastError() == hipSuccess ? CONV_OK : CONV_EHIP;
 }
 

@@ -254,3 +254,35 @@ def test_bf16_transposing_bf16_out_indexing(shape_index, aligned):
                                     out_aligned=aligned, out_bf16=True)
         assert np.all(written == 1)
         assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
+
+
+
+def test_random_shapes_emulated():
+    """The plans the random-shape GPU test runs (the selected plan of each
+    layer, or of its inner stride-1 problem; bf16 layers without a bf16
+    kernel run the fp32 plan on widened inputs), every workgroup emulated."""
+    from tests.kernel_emulator import emulate_bf16, emulate_phase_split
+    from tests.test_gpu_parity import RANDOM_SHAPES
+    for shape in RANDOM_SHAPES:
+        In, Ker = make_inputs(shape)
+        In64, Ker64 = In.float().numpy().astype(np.float64), Ker.float().numpy().astype(np.float64)
+        st, pd = (shape.stride,) * 2, (shape.pad,) * 2
+        if shape.stride != 1 or shape.pad != 0:
+            In64, Ker64, inner = emulate_phase_split(In64, Ker64, st, pd)
+            key = inner[:7]
+        else:
+            key = shape.key()
+        ref = oconv.conv_fwd(In64.astype(np.float32), Ker64.astype(np.float32)).reshape(-1)
+        dt = B.CONV_DTYPE_BF16 if shape.dtype == "bf16" else B.CONV_DTYPE_F32
+        try:
+            p = B.conv_fwd_plan(*key, dtype=dt)
+        except B.ConvError as e:
+            assert dt == B.CONV_DTYPE_BF16 and e.status == B.CONV_ENOPLAN
+            dt, p = B.CONV_DTYPE_F32, B.conv_fwd_plan(*key)  # widened to fp32
+        g = B.conv_fwd_geometry(*key, p)
+        if g["family"] in (3, 6):
+            out, written = emulate_bf16(g, In64.reshape(-1), Ker64.reshape(-1))
+        else:
+            out, written = emulate(g, In64.reshape(-1), Ker64.reshape(-1))
+        assert np.all(written == 1), shape
+        assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref))), shape
