@@ -235,7 +235,7 @@ def _plans_per_variant(dims, dtype=B.CONV_DTYPE_F32, per_variant=3):
 
 
 VARIANT_SHAPES = [
-    ConvShape("var3x3", 3, 20, 72, 19, 23, 3, 3, "f32", 31),
+    ConvShape("var3x3", 2, 20, 72, 15, 19, 3, 3, "f32", 31),
     ConvShape("var1x1", 3, 40, 72, 13, 11, 1, 1, "f32", 32),
     ConvShape("var2x4", 2, 9, 40, 12, 13, 2, 4, "f32", 33),
     # 2x2 and 4x4 taps: the inner problems of stride-2 layers
@@ -264,7 +264,7 @@ def test_every_variant(shape):
 
 
 BF16_VARIANT_SHAPES = [
-    ConvShape("bf16_var3x3", 2, 40, 72, 11, 13, 3, 3, "bf16", 51),
+    ConvShape("bf16_var3x3", 1, 40, 72, 11, 13, 3, 3, "bf16", 51),
     ConvShape("bf16_var1x1", 2, 64, 80, 10, 12, 1, 1, "bf16", 52),
     # C = 32: the transposing-read kernel (tiles of 8 x 32, 4 x 64, 7 x 64)
     ConvShape("bf16_var_c32", 2, 32, 48, 18, 42, 3, 3, "bf16", 53),
@@ -276,7 +276,7 @@ BF16_VARIANT_SHAPES = [
     ConvShape("bf16_var4x4", 1, 24, 40, 12, 14, 4, 4, "bf16", 57),
 ]
 # kernel families each shape is there for (others are covered by the shapes before)
-BF16_SHAPE_FAMILIES = {"bf16_c32_k64": {6}, "bf16_c32_q42": {6}}
+BF16_SHAPE_FAMILIES = {"bf16_var_c32": {6}, "bf16_c32_k64": {6}, "bf16_c32_q42": {6}}
 
 
 def bf16_variant_plans(shape):
