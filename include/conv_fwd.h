@@ -19,11 +19,13 @@
  * re-derived for the gfx950 memory hierarchy; see conv_fwd_plan.
  *
  * Ownership: every tensor pointer is DEVICE memory allocated and freed by
- * the caller.  The library keeps a host-side plan cache only; its device
- * allocations are the temporary workspace of plans that split the channel
- * reduction (split_c > 1) and the scratch buffer of conv_fwd_tune, taken
- * from and returned to the device's default memory pool in stream order
- * within the call.  In, Ker and Out must not overlap.
+ * the caller.  The library keeps a host-side plan cache; its device
+ * allocations are temporary workspaces (split reductions, the strided
+ * rewrite, bf16 fallbacks, conv_fwd_tune's scratch), taken and returned in
+ * stream order within the call from a memory pool the library creates per
+ * device, which keeps up to 1 GB of freed blocks for reuse until the
+ * process ends.  The calling thread's current device must own the stream.
+ * In, Ker and Out must not overlap.
  *
  * Asynchrony: the compute calls enqueue kernels on `stream` (a hipStream_t;
  * NULL = the default stream) and return without synchronising.  A return of
@@ -92,9 +94,9 @@ typedef struct {
                          (0 or 1 = none).  Above 1 (direct-to-LDS plans only),
                          each range's partial Out goes to a stream-ordered
                          temporary workspace of split_c x |Out| floats
-                         (hipMallocAsync / hipFreeAsync on the call's
-                         stream) and a second kernel adds the ranges in
-                         fixed order, so results stay deterministic.       */
+                         (the library's pool, on the call's stream) and a
+                         second kernel adds the ranges in fixed order, so
+                         results stay deterministic.                       */
   int reserved;       /* 0                                                   */
   int lds_bytes;      /* dynamic LDS per workgroup                           */
   int64_t num_wg;     /* workgroups launched                                 */
@@ -129,7 +131,7 @@ int conv_fwd_bf16(int N, int C, int K, int H, int W, int R, int S,
  * even), halving the bytes written.  Out : [N][K][H-R+1][W-S+1] bf16 bit
  * patterns, device.  The plan is the one conv_fwd_bf16 selects; the
  * transposing-read bf16 kernel writes bf16 directly, any other kernel
- * writes fp32 into a stream-ordered workspace (from the device's default
+ * writes fp32 into a stream-ordered workspace (from the library's
  * pool, returned within the call) that a second kernel rounds into Out.
  * The paper states single precision only; the other entry points write
  * fp32 Out, and this one is the bf16-output refinement that makes bf16
@@ -155,7 +157,7 @@ int conv_fwd_bf16_out(int N, int C, int K, int H, int W, int R, int S,
  * becomes min(sh,R) x min(sw,S) phase images; Ker gets ceil(R/sh) x
  * ceil(S/sw) taps, zero where no original tap lands): two small kernels
  * write the phase images (and, when strided, the rearranged Ker) into a
- * stream-ordered workspace from the device's default pool, the selected
+ * stream-ordered workspace from the library's pool, the selected
  * stride-1 plan of the inner problem (see conv_fwd_ex_inner_shape) runs on
  * it, and the workspace is returned in stream order.  Asynchronous like
  * conv_fwd.  Returns a conv_status_t.
@@ -215,8 +217,9 @@ int conv_fwd_candidates(int N, int C, int K, int H, int W, int R, int S, int dty
  * none of In (as when each call of a network brings new data); the median
  * launch time in microseconds goes to times_us[i] (times_us may be NULL;
  * else room for top_n floats).  The scratch buffer is taken from and
- * returned to the device's default memory pool in stream order.  The fastest plan is written to *plan_out and
- * becomes the cached plan of this shape, dtype and tensor alignment: later
+ * returned to the library's memory pool in stream order.  The fastest plan
+ * is written to *plan_out and becomes the cached plan of this shape, dtype
+ * and tensor alignment: later
  * conv_fwd / conv_fwd_bf16 / conv_fwd_plan calls for them return or run it.
  *   dtype      : CONV_DTYPE_*; In and Ker as for conv_fwd or conv_fwd_bf16
  *   Out        : overwritten with Eq. (1) (every candidate computes it)

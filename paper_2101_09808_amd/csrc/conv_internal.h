@@ -94,8 +94,8 @@ struct PhaseGeom {
   int Rp, Sp;  // inner taps: ceil(R / sh), ceil(S / sw)
   int P, Q;    // output extents
 };
-// Stream-ordered device memory from the default pool (hipMallocAsync /
-// hipFreeAsync on `stream`).
+// Stream-ordered device memory from the library's per-device pool
+// (hipMallocFromPoolAsync / hipFreeAsync on `stream`).
 int stream_alloc(size_t bytes, void* stream, void** out);
 int stream_free(void* p, void* stream);
 // Phase-split In into Inp and (Kp non-null) Ker into Kp, on `stream`.

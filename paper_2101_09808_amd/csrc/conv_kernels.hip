@@ -1688,8 +1688,34 @@ const Variant* find_variant(int id) {
   return in ? &in->v : nullptr;
 }
 
+// Workspaces come from a memory pool the library owns, one per device,
+// which keeps up to 1 GB of freed blocks for reuse (the default pool hands
+// freed memory back at each synchronisation, so every call would map fresh
+// pages).  The calling thread's current device must own the stream.
 int stream_alloc(size_t bytes, void* stream, void** out) {
-  return hipMallocAsync(out, bytes, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? CONV_OK : CONV_EHIP;
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static hipMemPool_t pools[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return CONV_EHIP;
+  hipMemPool_t pool = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(mu);
+    if (!pools[dev]) {
+      hipMemPoolProps props = {};
+      props.allocType = hipMemAllocationTypePinned;
+      props.location.type = hipMemLocationTypeDevice;
+      props.location.id = dev;
+      hipMemPool_t p = nullptr;
+      if (hipMemPoolCreate(&p, &props) != hipSuccess) return CONV_EHIP;
+      uint64_t keep = uint64_t(1) << 30;
+      if (hipMemPoolSetAttribute(p, hipMemPoolAttrReleaseThreshold, &keep) != hipSuccess) return CONV_EHIP;
+      pools[dev] = p;
+    }
+    pool = pools[dev];
+  }
+  return hipMallocFromPoolAsync(out, bytes, pool, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? CONV_OK
+                                                                                                      : CONV_EHIP;
 }
 
 int stream_free(void* p, void* stream) {
@@ -1808,7 +1834,7 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
     // stream-ordered workspace, then the fixed-order sum into Out.
     const int64_t n = (int64_t)g.N * g.K * g.P * g.Q;
     float* ws = nullptr;
-    if (hipMallocAsync(reinterpret_cast<void**>(&ws), (size_t)g.split * n * sizeof(float), st) != hipSuccess)
+    if (stream_alloc((size_t)g.split * n * sizeof(float), stream, reinterpret_cast<void**>(&ws)) != CONV_OK)
       return CONV_EHIP;
     hipLaunchKernelGGL(inst->f32, dim3(g.grid), dim3(v.threads), lds_bytes, st,
                        static_cast<const float*>(In), static_cast<const float*>(Ker), ws, g);
@@ -1864,7 +1890,7 @@ int time_launches(const Variant& v, const Geom& g, const void* In, const void* K
   // own two events; all of it queued behind a delay of 300 us per launch, so
   // host time between launches does not count.
   void* scratch = nullptr;
-  if (hipMallocAsync(&scratch, kEvictBytes, st) != hipSuccess) return CONV_EHIP;
+  if (stream_alloc(kEvictBytes, stream, &scratch) != CONV_OK) return CONV_EHIP;
   std::vector<hipEvent_t> ev(2 * (size_t)reps, nullptr);
   for (auto& e : ev)
     if (rc == CONV_OK && hipEventCreate(&e) != hipSuccess) rc = CONV_EHIP;
