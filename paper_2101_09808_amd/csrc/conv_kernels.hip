@@ -1692,6 +1692,16 @@ const Variant* find_variant(int id) {
 // which keeps up to 1 GB of freed blocks for reuse (the default pool hands
 // freed memory back at each synchronisation, so every call would map fresh
 // pages).  The calling thread's current device must own the stream.
+// Raise a kernel's dynamic LDS limit to what the CU's 160 KB leave beside
+// its static LDS.
+int allow_dynamic_lds(const void* fn) {
+  hipFuncAttributes attr;
+  if (hipFuncGetAttributes(&attr, fn) != hipSuccess) return CONV_EHIP;
+  const int limit = 163840 - (int)attr.sharedSizeBytes;
+  return hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, limit) == hipSuccess ? CONV_OK
+                                                                                                  : CONV_EHIP;
+}
+
 int stream_alloc(size_t bytes, void* stream, void** out) {
   constexpr int kMaxDevices = 64;
   static std::mutex mu;
@@ -1771,9 +1781,7 @@ int launch_bf16_out(const Variant& v, const Geom& g, const void* In, const void*
     {
       std::lock_guard<std::mutex> lk(mu);
       if (!done[idx]) {
-        if (hipFuncSetAttribute(reinterpret_cast<const void*>(inst->bf16_outb),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, 163840) != hipSuccess)
-          return CONV_EHIP;
+        if (allow_dynamic_lds(reinterpret_cast<const void*>(inst->bf16_outb)) != CONV_OK) return CONV_EHIP;
         done[idx] = true;
       }
     }
@@ -1824,8 +1832,7 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
     const int idx = (int)(inst - kInstances);
     std::lock_guard<std::mutex> lk(mu);
     if (!done[idx]) {
-      if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, 163840) != hipSuccess)
-        return CONV_EHIP;
+      if (allow_dynamic_lds(fn) != CONV_OK) return CONV_EHIP;
       done[idx] = true;
     }
   }
