@@ -19,8 +19,8 @@ launch time for the first few milliseconds.
 
 Prints ONE JSON line with the metric, the roofline of the kernel (average
 launch duration from HIP events recorded on the launch stream around the
-timed region), the HBM traffic measured by the counter passes when they match
-the current kernel sources, the CPU oracle timed on this host (cpu_baseline),
+timed region), the HBM traffic measured by the counter passes when they were
+taken on the launched kernel's current source and plan, the CPU oracle timed on this host (cpu_baseline),
 and a per-layer table for the other layer configurations.
 """
 import argparse
@@ -53,6 +53,36 @@ def kernel_source_hash():
     for f in ("conv_kernels.hip", "select.cpp"):
         with open(os.path.join(ROOT, "paper_2101_09808_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+KERNEL_FUNCTIONS = {1: "conv_f32_kernel", 2: "conv_f32_dma_kernel", 3: "conv_bf16_kernel",
+                    4: "conv1x1_stream_kernel", 5: "conv1x1_stream_loop_kernel", 6: "conv_bf16_tr_kernel"}
+
+
+def plan_kernel_hash(c, plan):
+    """Hash of what one launch of `plan` runs: the source text of its kernel
+    template, the instance line that fixes the template arguments, the launch
+    geometry struct, and the plan's tile fields.  Counter figures taken for
+    the plan stay valid while this hash does."""
+    from paper_2101_09808_amd import conv as B
+
+    src = open(os.path.join(ROOT, "paper_2101_09808_amd", "csrc", "conv_kernels.hip")).read()
+    hdr = open(os.path.join(ROOT, "paper_2101_09808_amd", "csrc", "conv_internal.h")).read()
+    fam = B.conv_fwd_geometry(*c.key(), plan)["family"]
+    name = KERNEL_FUNCTIONS[fam]
+    at = src.index("\n" + name + "(")
+    begin = src.rindex("\ntemplate <", 0, at)
+    end = src.index("\n}\n", at) + 3
+    inst = [ln.strip() for ln in src.splitlines() if ln.strip().startswith(("F32_", "BF16_"))
+            and "(%d," % plan["variant"] in ln]
+    geom = hdr[hdr.index("struct Geom {"):]
+    geom = geom[:geom.index("};") + 2]
+    tiles = {k: plan[k] for k in ("variant", "tile_k", "tile_rows", "tile_cols", "tile_c", "waves_k",
+                                  "waves_px", "grid_order", "split_c")}
+    h = hashlib.sha256()
+    for part in (src[begin:end], "\n".join(inst), geom, json.dumps(tiles, sort_keys=True)):
+        h.update(part.encode())
     return h.hexdigest()[:16]
 
 
@@ -226,7 +256,7 @@ def calibrated(d, counter, unit_bytes, layers, launches):
 def traffic_parse(c, fetch_dir, write_dir, out_path, launches=6):
     """HBM bytes per launch of the timed layer from the FETCH_SIZE and
     WRITE_SIZE runs (KiB per dispatch, scaled by the plain copy), stored with
-    a hash of the kernel sources."""
+    the hash of the launched kernel's source and plan (plan_kernel_hash)."""
     from paper_2101_09808_amd import conv as B
 
     res = {}
@@ -236,7 +266,7 @@ def traffic_parse(c, fetch_dir, write_dir, out_path, launches=6):
                     "factor": factor, "bytes_per_launch": per_layer[c.name]["bytes_per_launch"]}
     dtype_code = B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32
     plan = B.conv_fwd_plan(*c.key(), dtype=dtype_code)
-    out = {"workload": c.name, "kernel_sha": kernel_source_hash(), "plan_variant": plan["variant"],
+    out = {"workload": c.name, "kernel_sha": plan_kernel_hash(c, plan), "plan_variant": plan["variant"],
            "copy_bytes": COPY_BYTES, "copy_reps": COPY_REPS,
            "fetch": res["fetch"], "write": res["write"],
            "hbm_bytes_per_launch": res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"],
@@ -658,7 +688,7 @@ def main():
     roof["traffic"] = None
     if c.name == HEADLINE and os.path.exists(TRAFFIC_FILE):
         t = json.load(open(TRAFFIC_FILE))
-        if t.get("kernel_sha") == kernel_source_hash() and t.get("plan_variant") == plan["variant"]:
+        if t.get("kernel_sha") == plan_kernel_hash(c, plan) and t.get("plan_variant") == plan["variant"]:
             roof["traffic"] = t["hbm_bytes_per_launch"]
     roof["kernel_ms"] = r["mean_kernel_ms"]
     roof["alg_bytes"] = Bt

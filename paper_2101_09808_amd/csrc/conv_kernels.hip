@@ -1688,10 +1688,6 @@ const Variant* find_variant(int id) {
   return in ? &in->v : nullptr;
 }
 
-// Workspaces come from a memory pool the library owns, one per device,
-// which keeps up to 1 GB of freed blocks for reuse (the default pool hands
-// freed memory back at each synchronisation, so every call would map fresh
-// pages).  The calling thread's current device must own the stream.
 // Raise a kernel's dynamic LDS limit to what the CU's 160 KB leave beside
 // its static LDS.
 int allow_dynamic_lds(const void* fn) {
@@ -1702,6 +1698,10 @@ int allow_dynamic_lds(const void* fn) {
                                                                                                   : CONV_EHIP;
 }
 
+// Workspaces come from a memory pool the library owns, one per device,
+// which keeps up to 1 GB of freed blocks for reuse (the default pool hands
+// freed memory back at each synchronisation, so every call would map fresh
+// pages).  The calling thread's current device must own the stream.
 int stream_alloc(size_t bytes, void* stream, void** out) {
   constexpr int kMaxDevices = 64;
   static std::mutex mu;
