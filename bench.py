@@ -181,6 +181,8 @@ def traffic_run(layers, launches=6):
     torch.cuda.synchronize()
     del src, dst
     for c in layers:
+        if c.stride != 1 or c.pad != 0:
+            raise ValueError(f"{c.name}: the traffic run launches stride-1 valid layers only")
         bf16 = c.dtype == "bf16"
         edt = torch.bfloat16 if bf16 else torch.float32
         set_bytes = c.N * c.C * c.H * c.W * (2 if bf16 else 4) + c.N * c.K * c.P * c.Q * 4
@@ -428,6 +430,12 @@ def time_plan(c, plan, ins, outs, Ker, reps=10):
     from paper_2101_09808_amd import conv as B
     L = B.lib()
     p = B.ConvPlan.from_dict(plan)
+    # the plan runs the stride-1 valid problem of c.key(): Out must hold it
+    N, C, K, H, W, R, S = c.key()
+    if any(t.numel() < N * K * (H - R + 1) * (W - S + 1) for t in outs):
+        raise ValueError("Out buffers smaller than the valid convolution's output")
+    if any(t.numel() < N * C * H * W for t in ins) or Ker.numel() < K * C * R * S:
+        raise ValueError("input buffers smaller than the shape")
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
     kp = Ker.data_ptr()

@@ -263,11 +263,13 @@ int conv_model_volume(const int perm[7], const int64_t N[7], const int64_t T[7],
  *   width, pipeline stages, LDS elements per stage (family 3: LDS bytes), In
  *   elements per stage (family 2), In and Ker bytes, workgroups launched;
  *   three reserved zeros; channel ranges of the reduction, pipeline steps
- *   per range; 1 if the inner loop is on 32x32x2 MFMAs (family 2).
+ *   per range; 1 if the inner loop is on 32x32x2 MFMAs (family 2); groups
+ *   of waves that split each pipeline step's channels inside the workgroup
+ *   (family 2; 1 otherwise).
  * Writes min(cap, CONV_GEOM_FIELDS) values and returns CONV_GEOM_FIELDS, or
  * a negative conv_status_t (CONV_EINVAL for a plan the kernels cannot run).
  */
-#define CONV_GEOM_FIELDS 51
+#define CONV_GEOM_FIELDS 52
 int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S,
                       const conv_plan_t* plan, int32_t* out, int cap);
 

@@ -286,7 +286,7 @@ GEOM_FIELDS = (
     "lds_in_elems", "lds_ker_elems", "ni_in", "ni_ker", "nchunks",
     "wk", "wp", "tc", "rc", "sc", "max_ni", "max_nk", "ker_vec", "threads", "lds_bytes",
     "family", "in_vec", "stages", "stage_elems", "in_region", "in_bytes", "ker_bytes", "grid",
-    "reserved0", "reserved1", "reserved2", "split", "cps", "mfma32",
+    "reserved0", "reserved1", "reserved2", "split", "cps", "mfma32", "nwc",
 )
 
 

@@ -358,7 +358,7 @@ int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S, const con
       g.lds_in_elems, g.lds_ker_elems, g.ni_in, g.ni_ker, g.nchunks,
       v->wk, v->wp, v->tc, v->rc, v->sc, v->max_ni, v->max_nk, v->ker_vec, v->threads, lds,
       v->family, v->in_vec, v->stages, g.stage_elems, g.in_region, (int32_t)g.in_bytes,
-      (int32_t)g.ker_bytes, g.grid, 0, 0, 0, g.split, g.cps, v->mfma32};
+      (int32_t)g.ker_bytes, g.grid, 0, 0, 0, g.split, g.cps, v->mfma32, v->groups()};
   for (int i = 0; i < cap && i < CONV_GEOM_FIELDS; ++i) out[i] = f[i];
   return CONV_GEOM_FIELDS;
 }

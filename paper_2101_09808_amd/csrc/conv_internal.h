@@ -44,6 +44,8 @@ struct Variant {
   int threads;    // threads per workgroup
   int stages;     // pipeline depth (LDS buffers)
   int mfma32;     // DMA: 1 = 32x32x2 inner loop (64-row k tile, 32-pixel blocks)
+  int nwc;        // DMA: groups of waves splitting each step's channels (0 = 1, no split)
+  int groups() const { return nwc > 1 ? nwc : 1; }
 };
 
 // Fully resolved launch geometry, passed by value to the kernels.

@@ -335,12 +335,21 @@ __device__ __forceinline__ void wait_vmcnt_opaque() {
 // (WK = 4) times WP/2 blocks of 32 pixels on v_mfma_f32_32x32x2f32 (two
 // channels per step), whose accumulators need no dependency padding and
 // which reads half the operand registers per flop.
+//
+// NWC > 1 splits the reduction inside the workgroup: NWC groups of
+// nwk x nwp waves share every staged chunk, group wc taking the channel
+// slice [wc * TC / NWC, (wc + 1) * TC / NWC) of each step, and the groups'
+// accumulators are summed through LDS at the end (in group order, so the
+// result is deterministic).  Small layers then keep every SIMD busy without
+// a second, reducing kernel.
 template <int WK, int WP, int NW, int TC, int RC, int SC, int NS, int NLI, int KVI, int NLK, int KVK,
-          bool MF32 = false>
+          bool MF32 = false, int NWC = 1>
 __global__ void __launch_bounds__(NW * 64)
 conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
                     float* __restrict__ Out, const Geom g) {
   static_assert(NS >= 2 && NS <= 4, "pipeline depth");
+  static_assert(NWC == 1 || (!MF32 && NW % NWC == 0 && TC % (4 * NWC) == 0),
+                "channel groups: 16x16x4 loop, whole waves and whole channel quads per group");
   extern __shared__ __align__(16) float lds[];
   constexpr int IN_REGION = NLI * NW * 64 * KVI;
   constexpr int KER_REGION = NLK * NW * 64 * KVK;
@@ -349,7 +358,9 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int j = lane & 15, gq = lane >> 4;
-  const int wk = wave % g.nwk, wp = wave / g.nwk;
+  constexpr int NWG = NW / NWC;  // waves per channel group
+  const int wg = wave % NWG, wc = wave / NWG;
+  const int wk = wg % g.nwk, wp = wg / g.nwk;
   const int BK = 16 * WK * g.nwk;
   const int R = RC ? RC : g.R, S = SC ? SC : g.S;
   const int RS = R * S;
@@ -459,11 +470,12 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
   // the matrix core instead of stalling it.
   static_assert(RC > 0 && SC > 0, "compile-time taps");
   constexpr int CG = MF32 ? 2 : 4;  // channels per step
-  constexpr int NSTEP = (TC / CG) * RC * SC;
+  constexpr int NSTEP = (TC / CG / NWC) * RC * SC;
   const int cl = MF32 ? h32 : gq;   // this lane's channel within a group
   auto compute = [&](int buf) {
-    const float* lin = lds + buf * STAGE;
-    const float* lk = lin + IN_REGION;
+    // this wave's channel slice of the chunk
+    const float* lin = lds + buf * STAGE + wc * (TC / NWC) * g.in_cstride;
+    const float* lk = lds + buf * STAGE + IN_REGION + wc * (TC / NWC) * RS;
     float a[2][NKB], b[2][NPB];
     auto fetch = [&](int st, int slot) {
       const int cs = st / (RC * SC), rs = st % (RC * SC);
@@ -514,6 +526,41 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
   // (32x32x2); a split plan writes range split_r's partial sums to slice
   // split_r of the workspace passed as Out.
   const size_t PQ = (size_t)g.P * g.Q;
+  if constexpr (NWC > 1) {
+    // Every wave parks its accumulators in LDS, register r of wave w at
+    // [(w * NREG + r) * 64 + lane]; then the wave of group wc sums registers
+    // [wc * NREG / NWC, (wc + 1) * NREG / NWC) over the groups in order and
+    // stores them.  The last step's loads have all landed (vmcnt 0 above),
+    // and the barrier keeps the pipeline's last reads before the writes.
+    constexpr int NREG = NKB * NPB * 4;
+    constexpr int RPW = NREG / NWC;
+    static_assert(NREG % NWC == 0, "registers per group");
+    static_assert(NW * NREG * 64 <= NS * STAGE, "reduction fits the pipeline's LDS");
+    __syncthreads();
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) lds[(wave * NREG + (kb * NPB + pb) * 4 + v) * 64 + lane] = acc[kb][pb][v];
+    __syncthreads();
+    for (int i = 0; i < RPW; ++i) {
+      const int r = wc * RPW + i;
+      const int kb = r / (NPB * 4), pb = (r / 4) % NPB, v = r % 4;
+      float sum = lds[(wg * NREG + r) * 64 + lane];
+#pragma unroll
+      for (int c = 1; c < NWC; ++c) sum += lds[((c * NWG + wg) * NREG + r) * 64 + lane];
+      const int px = wp * WP * 16 + pb * 16 + j;
+      const int row_i = px / g.tw, col = px - row_i * g.tw;
+      const int rho = t.rho0 + row_i;
+      const int k = t.k0 + (wk * WK + kb) * 16 + 4 * gq + v;
+      if (px < tpx && rho < t.rho_end && col < t.tw_eff && k < K) {
+        const int n = rho / g.P, p = rho - n * g.P;
+        Out[(size_t)split_r * g.N * K * PQ + (((size_t)n * K + k) * g.P + p) * g.Q + t.q0 + col] = sum;
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int pb = 0; pb < NPB; ++pb) {
     const int px = wp * WP * 16 + pb * BW + jl;
@@ -1538,6 +1585,12 @@ widen_bf16_kernel(const unsigned short* __restrict__ src, float* __restrict__ ds
                    NS, 0},                                                                       \
            &conv_f32_dma_kernel<WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK>, nullptr}
 
+// the same pipeline with NWC channel groups of waves (16x16x4 loop)
+#define F32_DMA_CG(ID, WK, WP, NW, NWC, TC, RC, SC, NS, NLI, KVI, NLK, KVK)                      \
+  Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_DMA, WK, WP, TC, RC, SC, NLI, NLK, KVK, KVI, NW * 64, \
+                   NS, 0, NWC},                                                                  \
+           &conv_f32_dma_kernel<WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK, false, NWC>, nullptr}
+
 // the same pipeline with the 32x32x2 inner loop (WK = 4, WP even)
 #define F32_DMA32(ID, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK)                                \
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_DMA, 4, WP, TC, RC, SC, NLI, NLK, KVK, KVI, NW * 64, \
@@ -1607,6 +1660,14 @@ const Instance kInstances[] = {
     F32_DMA(143, 2, 4, 8, 8, 3, 3, 3, 4, 1, 10, 1),
     F32_DMA(144, 4, 2, 4, 8, 3, 3, 3, 4, 1, 19, 1),
     F32_DMA(145, 2, 8, 8, 8, 3, 3, 3, 7, 1, 10, 1),
+    // channel groups of waves (WK, WP, waves, groups, channels per step, ...):
+    // small layers without a split reduction
+    F32_DMA_CG(161, 2, 2, 4, 4, 16, 3, 3, 3, 7, 1, 5, 4),
+    F32_DMA_CG(162, 2, 2, 8, 8, 32, 3, 3, 2, 7, 1, 5, 4),
+    F32_DMA_CG(163, 1, 4, 4, 4, 16, 3, 3, 3, 11, 1, 3, 4),
+    F32_DMA_CG(164, 2, 4, 8, 4, 16, 3, 3, 2, 8, 1, 5, 4),
+    F32_DMA_CG(165, 4, 4, 4, 4, 16, 3, 3, 3, 8, 1, 10, 4),
+    F32_DMA_CG(166, 2, 2, 8, 4, 16, 3, 3, 2, 6, 1, 5, 4),
     // 32x32x2 inner loop, 3x3 taps: (pixel units of 16 per wave, waves, ...)
     F32_DMA32(151, 4, 4, 8, 3, 3, 3, 12, 1, 10, 4),
     F32_DMA32(152, 4, 4, 8, 3, 3, 3, 7, 1, 19, 1),

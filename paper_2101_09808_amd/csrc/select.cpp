@@ -109,7 +109,8 @@ struct Hw {
       8.0e12,             // HBM
   };
   int mfma_f32_cycles = 32;  // 16x16x4 f32 per SIMD
-  double launch_us = 3.0;    // one more kernel launch in the stream (measured gap, order of)
+  double launch_us = 5.0;    // one more kernel launch in the stream: a split plan's reduce pass
+                             // measured 4-5 us over the same plan unsplit on small layers
 };
 const Hw kHw;
 
@@ -262,7 +263,7 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
   if (v.rc && (s.R != v.rc || s.S != v.sc)) return false;
   if (plan.tile_c != v.tc) return false;
   const int nwk = plan.waves_k, nwp = plan.waves_px;
-  if (nwk < 1 || nwp < 1 || nwk * nwp * 64 != v.threads) return false;
+  if (nwk < 1 || nwp < 1 || nwk * nwp * v.groups() * 64 != v.threads) return false;
   const int BK = 16 * v.wk * nwk, BP = 16 * v.wp * nwp;
   if (plan.tile_k != BK || plan.wave_k != 16 * v.wk || plan.wave_px != 16 * v.wp) return false;
   if (plan.grid_order != 0 && plan.grid_order != 1) return false;
@@ -483,6 +484,8 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
 
   // REG: per wave and per (4 channels, tap), WK + WP operand reads of 64
   // lanes; the 32x32x2 loop reads 2 + WP/2 operands per (2 channels, tap).
+  // (Channel groups of waves share each tile's steps: the count per tile is
+  // the same.)
   const double waves = (double)g.num_tiles * (g.nwk * g.nwp);
   const int kdepth = (plan->dtype == CONV_DTYPE_BF16) ? 32 : 4;  // reduction per MFMA
   const double steps = (double)g.nchunks * (v->tc / kdepth) * RS;
@@ -561,10 +564,11 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
   // ceil(workgroups / cus) workgroups whose waves share its SIMDs.
   const double mfma_per_step = (double)v->wk * v->wp;
   const double mfma_cycles = (plan->dtype == CONV_DTYPE_BF16) ? 16.0 : kHw.mfma_f32_cycles;
-  const double wave_cycles = steps * ((double)g.cps / g.nchunks) * mfma_per_step * mfma_cycles;
+  const int groups = v->groups();
+  const double wave_cycles = steps * ((double)g.cps / g.nchunks) * mfma_per_step * mfma_cycles / groups;
   // tile executions: grid = tiles x ranges, or fewer persistent workgroups
   const double per_cu = std::ceil((double)g.num_tiles * g.split / kHw.cus);
-  const double waves_per_simd = per_cu * (g.nwk * g.nwp) / kHw.simds_per_cu;
+  const double waves_per_simd = per_cu * (g.nwk * g.nwp * groups) / kHw.simds_per_cu;
   plan->pred_mfma_us = waves_per_simd * wave_cycles / kHw.clock_hz * 1e6;
   if (plan->dtype == CONV_DTYPE_F32) {
     // Issue efficiency of the fp32 inner loop.  Each step of a WK x WP wave
@@ -574,7 +578,7 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
     // one wave per SIMD; c = 0.70, cap 0.82 when two or more waves share a
     // SIMD and cover each other's operand waits.
     const double reads_per_mfma = (double)(v->wk + v->wp) / ((double)v->wk * v->wp);
-    const bool shared = (g.nwk * g.nwp) > kHw.simds_per_cu;
+    const bool shared = (g.nwk * g.nwp * groups) > kHw.simds_per_cu;
     double eff = std::min(shared ? 0.82 : 0.78, (shared ? 0.70 : 0.53) / reads_per_mfma);
     // 32x32x2 loop: full-rate MFMAs from 4 accumulators on and fewer operand
     // reads per flop, yet measured on the 3x3 layers the MFMA pipe is busy
@@ -687,7 +691,7 @@ int enumerate_plans(const Shape& s0, int dtype, conv_plan_t* plans, int cap) {
       }
       continue;
     }
-    const int nw = v.threads / 64;
+    const int nw = v.threads / 64 / v.groups();  // waves per channel group
     for (int nwk = 1; nwk <= nw; ++nwk) {
       if (nw % nwk) continue;
       const int nwp = nw / nwk;
@@ -720,12 +724,18 @@ int enumerate_plans(const Shape& s0, int dtype, conv_plan_t* plans, int cap) {
             conv_plan_t p;
             fill_plan_fields(&p, v, nwk, nwp, tr, tw, order);
             if (score_plan(s0, &p) != CONV_OK) continue;
+            // Channel groups of waves pay the pipeline's fill and the LDS
+            // reduction once per workgroup, with one workgroup per CU: they
+            // are for grids that fit the CUs in one round (measured on
+            // MI355X, they win there and lose up to 1.8x on larger grids).
+            const int max_wg = v.groups() > 1 ? kHw.cus : 2 * kHw.cus;
+            if (v.groups() > 1 && p.num_wg > max_wg) continue;
             all.push_back(p);
             // Too few workgroups to fill the CUs: also split the channel
             // reduction into ranges (direct-to-LDS kernel only).
             if (v.family == FAMILY_DMA && p.num_wg < kHw.cus) {
               for (int split : {2, 3, 4, 6, 8, 12, 16}) {
-                if (p.num_wg * split > 2 * kHw.cus) break;
+                if (p.num_wg * split > max_wg) break;
                 conv_plan_t q = p;
                 q.split_c = split;
                 if (score_plan(s0, &q) == CONV_OK) all.push_back(q);

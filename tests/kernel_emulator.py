@@ -63,7 +63,8 @@ def emulate(g, In, Ker, wgs=None):
     WK, WP, TC, KV, NT = g["wk"], g["wp"], g["tc"], g["ker_vec"], g["threads"]
     _chk(NT == 256 or (g["family"] == 2 and NT in (256, 512)), "threads per workgroup")
     nwk, nwp = g["nwk"], g["nwp"]
-    _chk(nwk * nwp * 64 == NT, "waves do not fill the workgroup")
+    NWC = g.get("nwc", 1)  # groups of waves splitting each step's channels
+    _chk(nwk * nwp * NWC * 64 == NT, "waves do not fill the workgroup")
     BK = 16 * WK * nwk
     RS = R * S
     if g["rc"]:
@@ -74,6 +75,7 @@ def emulate(g, In, Ker, wgs=None):
     MF32 = bool(g.get("mfma32", 0))
     _chk(not MF32 or (dma and WK == 4 and WP % 2 == 0), "32x32x2 loop: 64-row k tile, pairs of 16-pixel units")
     NPB, BW, NKB, CG = (WP // 2, 32, 2, 2) if MF32 else (WP, 16, WK, 4)
+    _chk(NWC == 1 or (dma and not MF32 and TC % (CG * NWC) == 0), "channel groups of waves")
     l32, h32 = np.arange(64) & 31, np.arange(64) >> 5
     jl = l32 if MF32 else (np.arange(64) & 15)
     chl = h32 if MF32 else (np.arange(64) >> 4)  # this lane's channel within a step's group
@@ -147,8 +149,9 @@ def emulate(g, In, Ker, wgs=None):
         # blocks and 32-row k blocks, lane (l32, h32))
         tpx = g["tr"] * g["tw"]
         waves = []
-        for wave in range(nwk * nwp):
-            wk, wp = wave % nwk, wave // nwk
+        for wave in range(nwk * nwp * NWC):
+            wg, wc = wave % (nwk * nwp), wave // (nwk * nwp)
+            wk, wp = wg % nwk, wg // nwk
             poff, pvalid, pinfo = [], [], []
             for pb in range(NPB):
                 px = wp * WP * 16 + pb * BW + jl
@@ -164,7 +167,7 @@ def emulate(g, In, Ker, wgs=None):
                 koff = [(wk * 64 + kb * 32 + l32) * g["ker_rstride"] for kb in range(NKB)]
             else:
                 koff = [((wk * WK + kb) * 16 + j) * g["ker_rstride"] for kb in range(NKB)]
-            waves.append(dict(wk=wk, wp=wp, poff=poff, pvalid=pvalid, pinfo=pinfo, koff=koff,
+            waves.append(dict(wk=wk, wp=wp, wg=wg, wc=wc, poff=poff, pvalid=pvalid, pinfo=pinfo, koff=koff,
                               acc=np.zeros((NKB, NPB, BW, BW))))
         lin = [np.full(lin_n, np.nan), np.full(lin_n, np.nan)]
         lker = [np.full(lker_n, np.nan), np.full(lker_n, np.nan)]
@@ -240,7 +243,8 @@ def emulate(g, In, Ker, wgs=None):
 
         def compute(buf):
             for wv in waves:
-                for cs in range(TC // CG):
+                per = TC // CG // NWC  # channel groups of this wave's slice
+                for cs in range(wv["wc"] * per, (wv["wc"] + 1) * per):
                     for r in range(R):
                         for s in range(S):
                             tap = r * g["in_wp"] + s
@@ -272,12 +276,29 @@ def emulate(g, In, Ker, wgs=None):
             compute(ch & 1)
             if ch + 1 < nch:
                 stage((ch0 + ch + 1) * TC, (ch + 1) & 1)
+        if NWC > 1:
+            # accumulators parked in LDS per wave and register, summed over
+            # the groups in order; wave (wg, wc) stores registers
+            # [wc * NREG / NWC, (wc + 1) * NREG / NWC)
+            NREG = NKB * NPB * 4
+            _chk(NREG % NWC == 0, "registers per group")
+            _chk(NT // 64 * NREG * 64 <= g["stages"] * g["stage_elems"], "reduction exceeds the LDS")
+            NG = nwk * nwp
+            for wg in range(NG):
+                tot = waves[wg]["acc"].copy()
+                for c in range(1, NWC):
+                    tot = tot + waves[c * NG + wg]["acc"]
+                for c in range(NWC):
+                    waves[c * NG + wg]["red"] = tot
+                    waves[c * NG + wg]["regs"] = set(range(c * NREG // NWC, (c + 1) * NREG // NWC))
         for wv in waves:
             for pb in range(NPB):
                 valid = wv["pvalid"][pb]
                 n, p, col = wv["pinfo"][pb]
                 for kb in range(NKB):
                     for v in range(16 if MF32 else 4):
+                        if NWC > 1 and (kb * NPB + pb) * 4 + v not in wv["regs"]:
+                            continue
                         if MF32:
                             i = 8 * (v // 4) + 4 * h32 + v % 4
                             k = t["k0"] + wv["wk"] * 64 + kb * 32 + i
@@ -287,7 +308,7 @@ def emulate(g, In, Ker, wgs=None):
                         st = valid & (k < K)
                         dst = ((n * K + k) * P + p) * Q + t["q0"] + col
                         _chk((dst[st] >= 0) & (dst[st] < out_size), "Out store out of bounds")
-                        vals = wv["acc"][kb, pb][i, jl]
+                        vals = (wv["red"] if NWC > 1 else wv["acc"])[kb, pb][i, jl]
                         if split > 1:
                             wdst = split_r * out_size + dst
                             ws[wdst[st]] = vals[st]
