@@ -1668,6 +1668,10 @@ const Instance kInstances[] = {
     F32_DMA_CG(164, 2, 4, 8, 4, 16, 3, 3, 2, 8, 1, 5, 4),
     F32_DMA_CG(165, 4, 4, 4, 4, 16, 3, 3, 3, 8, 1, 10, 4),
     F32_DMA_CG(166, 2, 2, 8, 4, 16, 3, 3, 2, 6, 1, 5, 4),
+    // 1x1 taps: deep channel ranges on few pixels
+    F32_DMA_CG(171, 2, 2, 4, 4, 64, 1, 1, 3, 9, 1, 3, 4),
+    F32_DMA_CG(172, 2, 2, 8, 8, 128, 1, 1, 2, 9, 1, 3, 4),
+    F32_DMA_CG(173, 4, 2, 4, 4, 64, 1, 1, 3, 9, 1, 5, 4),
     // 32x32x2 inner loop, 3x3 taps: (pixel units of 16 per wave, waves, ...)
     F32_DMA32(151, 4, 4, 8, 3, 3, 3, 12, 1, 10, 4),
     F32_DMA32(152, 4, 4, 8, 3, 3, 3, 7, 1, 19, 1),
@@ -1680,6 +1684,9 @@ const Instance kInstances[] = {
     F32_DMA(134, 4, 8, 4, 16, 1, 1, 3, 8, 4, 5, 1),
     F32_DMA(135, 4, 6, 4, 16, 1, 1, 3, 6, 4, 5, 1),
     F32_DMA(136, 4, 8, 8, 16, 1, 1, 3, 8, 4, 3, 1),
+    // scalar In loads: any row length (Q % 4 != 0)
+    F32_DMA(137, 4, 4, 4, 16, 1, 1, 3, 17, 1, 5, 4),
+    F32_DMA(138, 4, 4, 4, 8, 1, 1, 4, 9, 1, 3, 4),
     F32_DMA(121, 1, 25, 4, 16, 1, 1, 4, 7, 4, 2, 4),
     F32_DMA(126, 1, 13, 8, 16, 1, 1, 4, 4, 4, 1, 4),
     F32_DMA(127, 1, 7, 8, 16, 1, 1, 4, 2, 4, 1, 4),

@@ -727,15 +727,16 @@ int enumerate_plans(const Shape& s0, int dtype, conv_plan_t* plans, int cap) {
             // Channel groups of waves pay the pipeline's fill and the LDS
             // reduction once per workgroup, with one workgroup per CU: they
             // are for grids that fit the CUs in one round (measured on
-            // MI355X, they win there and lose up to 1.8x on larger grids).
-            const int max_wg = v.groups() > 1 ? kHw.cus : 2 * kHw.cus;
-            if (v.groups() > 1 && p.num_wg > max_wg) continue;
+            // MI355X, they win there and lose up to 1.8x on larger grids),
+            // and they replace the split reduction rather than add to it
+            // (each split measured slower than the same plan unsplit).
+            if (v.groups() > 1 && p.num_wg > kHw.cus) continue;
             all.push_back(p);
             // Too few workgroups to fill the CUs: also split the channel
             // reduction into ranges (direct-to-LDS kernel only).
-            if (v.family == FAMILY_DMA && p.num_wg < kHw.cus) {
+            if (v.family == FAMILY_DMA && v.groups() == 1 && p.num_wg < kHw.cus) {
               for (int split : {2, 3, 4, 6, 8, 12, 16}) {
-                if (p.num_wg * split > max_wg) break;
+                if (p.num_wg * split > 2 * kHw.cus) break;
                 conv_plan_t q = p;
                 q.split_c = split;
                 if (score_plan(s0, &q) == CONV_OK) all.push_back(q);
