@@ -1653,6 +1653,13 @@ const Instance kInstances[] = {
     F32_DMA(112, 4, 4, 4, 8, 4, 4, 3, 14, 1, 8, 4),
     F32_DMA(113, 1, 7, 8, 8, 4, 4, 3, 6, 1, 5, 4),
     F32_DMA(114, 2, 4, 8, 8, 4, 4, 3, 7, 1, 5, 4),
+    // 4x4 taps, four channels per step (the 7x7 stride-2 layer's 12 phase
+    // channels in three whole steps); 2x2 taps, sixteen per step (more
+    // MFMAs between barriers on deep channel ranges)
+    F32_DMA(115, 1, 7, 8, 4, 4, 4, 2, 3, 1, 3, 4),
+    F32_DMA(116, 2, 4, 8, 4, 4, 4, 2, 3, 1, 3, 4),
+    F32_DMA(117, 4, 4, 4, 16, 2, 2, 3, 6, 1, 5, 4),
+    F32_DMA(118, 2, 4, 8, 16, 2, 2, 3, 10, 1, 3, 4),
     // squat wave tiles (4 k blocks x 4..8 pixel blocks), Ker rows loaded
     // element-wise so their LDS pitch can be conflict-free
     F32_DMA(141, 4, 4, 4, 8, 3, 3, 3, 7, 1, 19, 1),
