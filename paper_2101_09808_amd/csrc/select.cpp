@@ -471,7 +471,12 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
     // SIMD; a second wave per SIMD (unrolled kernel with max_nk > 0) hides
     // the operand waits and measured 9% faster
     const bool two_waves = v->family == FAMILY_STREAM1X1 && v->max_nk > 0;
-    const double issue_eff = two_waves ? 0.96 : 0.88;
+    double issue_eff = two_waves ? 0.96 : 0.88;
+    // A pixel range that is not a whole number of 16-pixel blocks masks part
+    // of its last block and starts the next wave's range off a 64-byte
+    // boundary: measured 17-28% slower than whole blocks at the same MFMA
+    // count (60 plans of the 1x1 N=32 C=256 K=64 layer).
+    if (g.tw % 16) issue_eff *= 0.8;
     plan->pred_mfma_us = rounds * nb * 4 * nq * kHw.mfma_f32_cycles / kHw.clock_hz * 1e6 / issue_eff;
     plan->pred_total_us = std::max(tmax, plan->pred_mfma_us);
     return CONV_OK;
