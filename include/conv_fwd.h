@@ -265,13 +265,34 @@ int conv_model_volume(const int perm[7], const int64_t N[7], const int64_t T[7],
  *   three reserved zeros; channel ranges of the reduction, pipeline steps
  *   per range; 1 if the inner loop is on 32x32x2 MFMAs (family 2); groups
  *   of waves that split each pipeline step's channels inside the workgroup
- *   (family 2; 1 otherwise).
+ *   (family 2; 1 otherwise); then the direct phase addressing of
+ *   conv_fwd_ex_geometry (all zero here): phases per input channel
+ *   (0 = none), phases along rows and columns, stride (rows, columns),
+ *   padding (rows, columns), the caller's In channels, height and width,
+ *   and the inner row width of a 1x1 problem run as one row of pixels per
+ *   image (0 otherwise).
  * Writes min(cap, CONV_GEOM_FIELDS) values and returns CONV_GEOM_FIELDS, or
  * a negative conv_status_t (CONV_EINVAL for a plan the kernels cannot run).
  */
-#define CONV_GEOM_FIELDS 52
+#define CONV_GEOM_FIELDS 63
 int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S,
                       const conv_plan_t* plan, int32_t* out, int cap);
+
+/*
+ * Host only: the launch geometry conv_fwd_ex uses for `plan`, a plan of its
+ * inner stride-1 problem (conv_fwd_ex_inner_shape).  The layout is that of
+ * conv_fwd_geometry.  When the plan's kernel reads the caller's In directly
+ * through the phase mapping (fp32, the direct-to-LDS family with scalar In
+ * loads and whole channels per pipeline step, In below 2 GB), the last
+ * eleven fields describe that mapping: inner channel c' = (c * na + a) * nb + b at
+ * inner pixel (y', x') reads In[c][sh * y' + a - ph][sw * x' + b - pw], zero
+ * outside the image (Sec. 3 defines the loop nest; stride and padding are
+ * the rewrite of conv_fwd_ex).  Otherwise those fields are zero and
+ * conv_fwd_ex phase-splits In into a workspace first.  Returns
+ * CONV_GEOM_FIELDS or a negative conv_status_t.
+ */
+int conv_fwd_ex_geometry(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w,
+                         int pad_h, int pad_w, const conv_plan_t* plan, int32_t* out, int cap);
 
 /* Static string for a conv_status_t. */
 const char* conv_fwd_strerror(int status);

@@ -90,6 +90,9 @@ def lib():
         L.conv_model_volume.restype = _i32
         L.conv_fwd_geometry.argtypes = shape7 + [ctypes.POINTER(ConvPlan), ctypes.POINTER(_i32), _i32]
         L.conv_fwd_geometry.restype = _i32
+        L.conv_fwd_ex_geometry.argtypes = shape7 + [_i32] * 4 + [ctypes.POINTER(ConvPlan), ctypes.POINTER(_i32),
+                                                                 _i32]
+        L.conv_fwd_ex_geometry.restype = _i32
         L.conv_fwd_strerror.argtypes = [_i32]
         L.conv_fwd_strerror.restype = ctypes.c_char_p
         _lib = L
@@ -287,6 +290,7 @@ GEOM_FIELDS = (
     "wk", "wp", "tc", "rc", "sc", "max_ni", "max_nk", "ker_vec", "threads", "lds_bytes",
     "family", "in_vec", "stages", "stage_elems", "in_region", "in_bytes", "ker_bytes", "grid",
     "reserved0", "reserved1", "reserved2", "split", "cps", "mfma32", "nwc",
+    "nph", "na", "nb", "sh", "sw", "ph", "pw", "C0", "H0", "W0", "Wi",
 )
 
 
@@ -298,4 +302,19 @@ def conv_fwd_geometry(N, C, K, H, W, R, S, plan):
     st = lib().conv_fwd_geometry(N, C, K, H, W, R, S, ctypes.byref(plan), buf, len(GEOM_FIELDS))
     if st < 0:
         raise ConvError(st, "conv_fwd_geometry")
+    return dict(zip(GEOM_FIELDS, list(buf)[:len(GEOM_FIELDS)]))
+
+
+def conv_fwd_ex_geometry(N, C, K, H, W, R, S, stride, pad, plan):
+    """The launch geometry conv_fwd_ex uses for `plan` (a plan of its inner
+    stride-1 problem), with the direct phase-addressing fields (host only)."""
+    if isinstance(plan, dict):
+        plan = ConvPlan.from_dict(plan)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    buf = (_i32 * len(GEOM_FIELDS))()
+    st = lib().conv_fwd_ex_geometry(N, C, K, H, W, R, S, sh, sw, ph, pw, ctypes.byref(plan), buf,
+                                    len(GEOM_FIELDS))
+    if st < 0:
+        raise ConvError(st, "conv_fwd_ex_geometry")
     return dict(zip(GEOM_FIELDS, list(buf)[:len(GEOM_FIELDS)]))

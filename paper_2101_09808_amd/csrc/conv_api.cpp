@@ -181,6 +181,23 @@ int phase_geom(int N, int C, int K, int H, int W, int R, int S, int sh, int sw, 
   return CONV_OK;
 }
 
+// The fields of conv_fwd_geometry, in the header's order.
+int export_geometry(const Variant& vr, const Geom& g, int lds, int32_t* out, int cap) {
+  const Variant* v = &vr;
+  const int32_t f[CONV_GEOM_FIELDS] = {
+      g.N, g.C, g.K, g.H, g.W, g.R, g.S, g.P, g.Q,
+      g.tr, g.tw, g.tiles_rows, g.tiles_cols, g.tiles_k,
+      g.in_rows, g.in_wp, g.in_cstride, g.ker_rstride,
+      g.nwk, g.nwp, g.order, g.num_tiles,
+      g.lds_in_elems, g.lds_ker_elems, g.ni_in, g.ni_ker, g.nchunks,
+      v->wk, v->wp, v->tc, v->rc, v->sc, v->max_ni, v->max_nk, v->ker_vec, v->threads, lds,
+      v->family, v->in_vec, v->stages, g.stage_elems, g.in_region, (int32_t)g.in_bytes,
+      (int32_t)g.ker_bytes, g.grid, 0, 0, 0, g.split, g.cps, v->mfma32, v->groups(),
+      g.nph, g.na, g.nb, g.sh, g.sw, g.ph, g.pw, g.C0, g.H0, g.W0, g.Wi};
+  for (int i = 0; i < cap && i < CONV_GEOM_FIELDS; ++i) out[i] = f[i];
+  return CONV_GEOM_FIELDS;
+}
+
 }  // namespace
 
 extern "C" {
@@ -223,12 +240,33 @@ int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S, int stride_h, i
   if (dtype != CONV_DTYPE_F32 && dtype != CONV_DTYPE_BF16) return CONV_EINVAL;
   if (stride_h == 1 && stride_w == 1 && pad_h == 0 && pad_w == 0)
     return run_selected(Shape{N, C, K, H, W, R, S}, dtype, In, Ker, static_cast<float*>(Out), stream);
-  // stream-ordered workspace: the phase images of In, then (strided only)
-  // the rearranged Ker; at stride 1 the padded In meets the original Ker
   const size_t e = dtype == CONV_DTYPE_BF16 ? 2 : 4;
   const int Cp = C * p.na * p.nb;
-  const size_t in_bytes = ((size_t)N * Cp * p.Hp * p.Wp * e + 255) / 256 * 256;
   const bool ker_moves = stride_h > 1 || stride_w > 1;
+  const Shape inner{N, Cp, K, p.Hp, p.Wp, p.Rp, p.Sp};
+  {
+    // Direct path: the inner plan's direct-to-LDS kernel reads the caller's
+    // In through the phase mapping (no pass over In); only a strided Ker is
+    // rearranged first, into a workspace (256-byte aligned).
+    Entry d;
+    const int align = alignment_of(In, Ker) | (ker_moves ? ALIGN_KER : 0);
+    if (cached_entry(inner, dtype, align, &d) == CONV_OK) {
+      Geom g = d.g;
+      if (phase_direct(*d.v, p, dtype, &g)) {
+        if (!ker_moves) return launch(*d.v, g, In, Ker, Out, stream);
+        void* kp = nullptr;
+        st = stream_alloc((size_t)K * Cp * p.Rp * p.Sp * e, stream, &kp);
+        if (st != CONV_OK) return st;
+        st = launch_phase_split(p, dtype, In, Ker, nullptr, kp, stream);
+        if (st == CONV_OK) st = launch(*d.v, g, In, kp, Out, stream);
+        const int freed = stream_free(kp, stream);
+        return st == CONV_OK ? freed : st;
+      }
+    }
+  }
+  // stream-ordered workspace: the phase images of In, then (strided only)
+  // the rearranged Ker; at stride 1 the padded In meets the original Ker
+  const size_t in_bytes = ((size_t)N * Cp * p.Hp * p.Wp * e + 255) / 256 * 256;
   const size_t ker_bytes = ker_moves ? (size_t)K * Cp * p.Rp * p.Sp * e : 0;
   void* wsv = nullptr;
   st = stream_alloc(in_bytes + ker_bytes, stream, &wsv);
@@ -237,7 +275,7 @@ int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S, int stride_h, i
   void* Kp = ker_moves ? ws + in_bytes : nullptr;
   st = launch_phase_split(p, dtype, In, Ker, ws, Kp, stream);
   if (st == CONV_OK)
-    st = run_selected(Shape{N, Cp, K, p.Hp, p.Wp, p.Rp, p.Sp}, dtype, ws, ker_moves ? Kp : Ker, Out, stream);
+    st = run_selected(inner, dtype, ws, ker_moves ? Kp : Ker, Out, stream);
   const int freed = stream_free(ws, stream);
   return st == CONV_OK ? freed : st;
 }
@@ -350,17 +388,24 @@ int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S, const con
   Geom g;
   int lds = 0;
   if (!resolve_geom(Shape{N, C, K, H, W, R, S}, *v, *plan, &g, &lds)) return CONV_EINVAL;
-  const int32_t f[CONV_GEOM_FIELDS] = {
-      g.N, g.C, g.K, g.H, g.W, g.R, g.S, g.P, g.Q,
-      g.tr, g.tw, g.tiles_rows, g.tiles_cols, g.tiles_k,
-      g.in_rows, g.in_wp, g.in_cstride, g.ker_rstride,
-      g.nwk, g.nwp, g.order, g.num_tiles,
-      g.lds_in_elems, g.lds_ker_elems, g.ni_in, g.ni_ker, g.nchunks,
-      v->wk, v->wp, v->tc, v->rc, v->sc, v->max_ni, v->max_nk, v->ker_vec, v->threads, lds,
-      v->family, v->in_vec, v->stages, g.stage_elems, g.in_region, (int32_t)g.in_bytes,
-      (int32_t)g.ker_bytes, g.grid, 0, 0, 0, g.split, g.cps, v->mfma32, v->groups()};
-  for (int i = 0; i < cap && i < CONV_GEOM_FIELDS; ++i) out[i] = f[i];
-  return CONV_GEOM_FIELDS;
+  return export_geometry(*v, g, lds, out, cap);
+}
+
+int conv_fwd_ex_geometry(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w, int pad_h,
+                         int pad_w, const conv_plan_t* plan, int32_t* out, int cap) {
+  PhaseGeom p;
+  int st = phase_geom(N, C, K, H, W, R, S, stride_h, stride_w, pad_h, pad_w, &p);
+  if (st != CONV_OK) return st;
+  if (!plan || (cap > 0 && !out)) return CONV_ENULL;
+  const Variant* v = find_variant(plan->variant);
+  if (!v) return CONV_EINVAL;
+  Geom g;
+  int lds = 0;
+  const Shape inner{N, C * p.na * p.nb, K, p.Hp, p.Wp, p.Rp, p.Sp};
+  if (!resolve_geom(inner, *v, *plan, &g, &lds)) return CONV_EINVAL;
+  const bool rewrite = stride_h > 1 || stride_w > 1 || pad_h > 0 || pad_w > 0;
+  if (rewrite) phase_direct(*v, p, plan->dtype, &g);  // leaves nph = 0 where it does not apply
+  return export_geometry(*v, g, lds, out, cap);
 }
 
 const char* conv_fwd_strerror(int status) {

@@ -66,6 +66,14 @@ struct Geom {
                                          // (bf16 family: stage_elems = LDS bytes)
   int grid;                              // workgroups launched
   int split, cps;                        // channel ranges of the reduction; pipeline steps per range
+  // Direct polyphase addressing (direct-to-LDS kernel, strided or padded
+  // layers): In is the caller's tensor of C0 x H0 x W0 per image; inner
+  // channel c' = (c * na + a) * nb + b at inner pixel (y', x') reads
+  // In[c][sh * y' + a - ph][sw * x' + b - pw], zero outside the image.
+  // nph = na * nb, or 0 when In is the inner tensor itself.  Wi: inner row
+  // width when a 1x1 problem runs in its kernel view (one row of H' x W'
+  // pixels per image), else 0.
+  int nph, na, nb, sh, sw, ph, pw, C0, H0, W0, Wi;
 };
 
 const Variant* variants(int* count);
@@ -96,11 +104,17 @@ struct PhaseGeom {
   int Rp, Sp;  // inner taps: ceil(R / sh), ceil(S / sw)
   int P, Q;    // output extents
 };
+// Geometry g of an inner plan (variant v) rewritten to read the caller's In
+// of the strided, padded problem p through the phase mapping; false when the
+// kernel cannot (not the direct-to-LDS family, vector In loads, a pipeline
+// step that splits a channel's phases, or In of 2 GB or more).
+bool phase_direct(const Variant& v, const PhaseGeom& p, int dtype, Geom* g);
 // Stream-ordered device memory from the library's per-device pool
 // (hipMallocFromPoolAsync / hipFreeAsync on `stream`).
 int stream_alloc(size_t bytes, void* stream, void** out);
 int stream_free(void* p, void* stream);
-// Phase-split In into Inp and (Kp non-null) Ker into Kp, on `stream`.
+// Phase-split In into Inp (Inp non-null) and Ker into Kp (Kp non-null), on
+// `stream`.
 int launch_phase_split(const PhaseGeom& p, int dtype, const void* In, const void* Ker, void* Inp, void* Kp,
                        void* stream);
 // Median duration in microseconds of `reps` launches on `stream` after one

@@ -388,7 +388,19 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
         if (row < t.nrows && x < ncols) {
           const int nu = t.nu0 + row;
           const int n = nu / H, y = nu - n * H;
-          in_goff[i] = ((n * C + cl) * H + y) * W + t.q0 + x;
+          if (g.nph == 0) {
+            in_goff[i] = ((n * C + cl) * H + y) * W + t.q0 + x;
+          } else {
+            // phase (a, b) of input channel c: a chunk holds whole channels
+            const int c = cl / g.nph, f = cl - c * g.nph, a = f / g.nb, b = f - a * g.nb;
+            int yi = y, xi = t.q0 + x;
+            if (g.Wi) {  // 1x1 kernel view: one row of H' x W' pixels
+              yi = xi / g.Wi;
+              xi -= yi * g.Wi;
+            }
+            const int iy = yi * g.sh + a - g.ph, ix = xi * g.sw + b - g.pw;
+            if (iy >= 0 && iy < g.H0 && ix >= 0 && ix < g.W0) in_goff[i] = ((n * g.C0 + c) * g.H0 + iy) * g.W0 + ix;
+          }
           in_cl[i] = cl;
         }
       }
@@ -438,7 +450,7 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
   auto issue = [&](int ch, int slot) {  // pipeline step ch into stage buffer slot % NS
     const int c0 = ch * TC;
     const unsigned stage = lds_base + (unsigned)((slot % NS) * STAGE) * 4u;
-    const int coff = c0 * H * W;
+    const int coff = g.nph ? (c0 / g.nph) * g.H0 * g.W0 : c0 * H * W;
 #pragma unroll
     for (int i = 0; i < NLI; ++i) {
       const unsigned voff =
@@ -1815,14 +1827,16 @@ int launch_phase_split(const PhaseGeom& p, int dtype, const void* In, const void
   const int g_in = (int)std::min<int64_t>((n_in + 255) / 256, 8192);
   const int g_ker = (int)std::min<int64_t>((n_ker + 255) / 256, 2048);
   if (dtype == CONV_DTYPE_BF16) {
-    hipLaunchKernelGGL(phase_split_kernel<unsigned short>, dim3(g_in), dim3(256), 0, st,
-                       static_cast<const unsigned short*>(In), static_cast<unsigned short*>(Inp), p);
+    if (Inp)
+      hipLaunchKernelGGL(phase_split_kernel<unsigned short>, dim3(g_in), dim3(256), 0, st,
+                         static_cast<const unsigned short*>(In), static_cast<unsigned short*>(Inp), p);
     if (Kp)
       hipLaunchKernelGGL(ker_phase_kernel<unsigned short>, dim3(g_ker), dim3(256), 0, st,
                          static_cast<const unsigned short*>(Ker), static_cast<unsigned short*>(Kp), p);
   } else {
-    hipLaunchKernelGGL(phase_split_kernel<float>, dim3(g_in), dim3(256), 0, st, static_cast<const float*>(In),
-                       static_cast<float*>(Inp), p);
+    if (Inp)
+      hipLaunchKernelGGL(phase_split_kernel<float>, dim3(g_in), dim3(256), 0, st, static_cast<const float*>(In),
+                         static_cast<float*>(Inp), p);
     if (Kp)
       hipLaunchKernelGGL(ker_phase_kernel<float>, dim3(g_ker), dim3(256), 0, st, static_cast<const float*>(Ker),
                          static_cast<float*>(Kp), p);

@@ -427,6 +427,21 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
   return true;
 }
 
+bool phase_direct(const Variant& v, const PhaseGeom& p, int dtype, Geom* g) {
+  const int nph = p.na * p.nb;
+  if (dtype != CONV_DTYPE_F32 || v.family != FAMILY_DMA || v.in_vec != 1 || v.tc % nph) return false;
+  const int64_t in_bytes = (int64_t)p.N * p.C * p.H * p.W * 4;
+  if (in_bytes >= (int64_t(1) << 31)) return false;  // 32-bit byte offsets below the out-of-range marker
+  g->nph = nph;
+  g->na = p.na; g->nb = p.nb;
+  g->sh = p.sh; g->sw = p.sw;
+  g->ph = p.ph; g->pw = p.pw;
+  g->C0 = p.C; g->H0 = p.H; g->W0 = p.W;
+  g->Wi = (p.Rp == 1 && p.Sp == 1) ? p.Wp : 0;  // kernel_view flattens 1x1 problems
+  g->in_bytes = (unsigned)in_bytes;
+  return true;
+}
+
 // Fill the model fields of a plan whose tile fields are set.  0 or an error.
 int score_plan(const Shape& s0, conv_plan_t* plan) {
   const Variant* v = find_variant(plan->variant);

@@ -70,6 +70,12 @@ def emulate(g, In, Ker, wgs=None):
     if g["rc"]:
         _chk(g["rc"] == R and g["sc"] == S, "compile-time taps differ from the shape")
     in_size, ker_size, out_size = N * C * H * W, K * C * R * S, N * K * P * Q
+    # direct phase addressing (conv_fwd_ex): In is the caller's outer tensor
+    nph = g.get("nph", 0)
+    if nph:
+        _chk(g["family"] == 2 and g["in_vec"] == 1 and g["tc"] % nph == 0, "direct phase addressing")
+        _chk(nph == g["na"] * g["nb"] and C == g["C0"] * nph, "phase counts")
+        in_size = N * g["C0"] * g["H0"] * g["W0"]
     _chk(In.size == in_size and Ker.size == ker_size, "input sizes")
     dma = g["family"] == 2
     MF32 = bool(g.get("mfma32", 0))
@@ -183,9 +189,23 @@ def emulate(g, In, Ker, wgs=None):
                 valid = (e < TC * g["in_cstride"]) & (row < t["nrows"]) & (x < ncols) & (c0 + cl < C)
                 nu = t["nu0"] + row
                 n, y = nu // H, nu % H
-                goff = ((n * C + cl) * H + y) * W + t["q0"] + x
+                if nph:
+                    # chunk-local input channel and phase, as the kernel splits them
+                    _chk(c0 % nph == 0, "a pipeline step splits a channel's phases")
+                    cr, f = cl // nph, cl % nph
+                    a, b = f // g["nb"], f % g["nb"]
+                    yi, xi = y, t["q0"] + x
+                    if g["Wi"]:  # 1x1 kernel view: one row of H' x W' pixels per image
+                        yi, xi = xi // g["Wi"], xi % g["Wi"]
+                    iy, ix = yi * g["sh"] + a - g["ph"], xi * g["sw"] + b - g["pw"]
+                    valid = valid & (iy >= 0) & (iy < g["H0"]) & (ix >= 0) & (ix < g["W0"])
+                    goff = ((n * g["C0"] + cr) * g["H0"] + iy) * g["W0"] + ix
+                    coff = (c0 // nph) * g["H0"] * g["W0"]
+                else:
+                    goff = ((n * C + cl) * H + y) * W + t["q0"] + x
+                    coff = c0 * H * W
                 for q in range(KVI):
-                    src = c0 * H * W + goff + q
+                    src = coff + goff + q
                     _chk((src[valid] >= 0) & (src[valid] < in_size), "In read out of bounds")
                     _chk(~valid | (src * 4 < 2 ** 31), "In byte offset overflows")
                     vals = np.where(valid, In[np.clip(src, 0, in_size - 1)], 0.0)

@@ -246,6 +246,48 @@ def test_strided_inner_plans_indexing():
 
 
 
+def _direct_cases():
+    from tests.test_gpu_parity import STRIDED_SHAPES
+    cases = [s for s in STRIDED_SHAPES if s.dtype == "f32"]
+    # stride 1 with same padding, and a 1x1 stride-2 layer on a channel-group kernel
+    cases += [ConvShape("pad1_3x3", 2, 24, 40, 13, 11, 3, 3, "f32", 71, 1, 1),
+              ConvShape("s2_1x1_c64", 1, 64, 72, 14, 12, 1, 1, "f32", 72, 2, 0)]
+    return cases
+
+
+@pytest.mark.parametrize("shape", _direct_cases(), ids=lambda s: s.name)
+def test_direct_phase_addressing_indexing(shape):
+    """conv_fwd_ex's direct path: the inner plan's direct-to-LDS kernel reads
+    the caller's In through the phase mapping (zero outside the image) and the
+    rearranged Ker; every inner plan of that family which takes the mapping,
+    one per variant, against the strided, padded oracle."""
+    from tests.kernel_emulator import emulate_phase_split
+    In, Ker = make_inputs(shape)
+    In64, Ker64 = In.float().numpy().astype(np.float64), Ker.float().numpy().astype(np.float64)
+    st, pd = (shape.stride, shape.stride), (shape.pad, shape.pad)
+    _, Kp, inner = emulate_phase_split(In64, Ker64, st, pd)
+    ref = oconv.conv_fwd_ex(In64.astype(np.float32), Ker64.astype(np.float32), st, pd).reshape(-1)
+    plans, seen = [], set()
+    for p in B.conv_fwd_candidates(*inner[:7]):
+        g = B.conv_fwd_ex_geometry(*shape.key(), st, pd, p)
+        if g["nph"] and p["variant"] not in seen:
+            seen.add(p["variant"])
+            plans.append((p, g))
+    if shape.name == "s3p2_5x5":
+        # nine phases per channel: no pipeline step holds whole channels, so
+        # conv_fwd_ex phase-splits In first
+        assert not plans and B.conv_fwd_ex_geometry(*shape.key(), st, pd, B.conv_fwd_plan(*inner[:7]))["nph"] == 0
+        return
+    assert plans
+    for p, g in plans:
+        out, written = emulate(g, In64.reshape(-1), Kp.reshape(-1))
+        assert np.all(written == 1), p
+        assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref))), p
+    sel = B.conv_fwd_plan(*inner[:7])
+    if B.conv_fwd_geometry(*inner[:7], sel)["family"] == 2:
+        assert B.conv_fwd_ex_geometry(*shape.key(), st, pd, sel)["nph"] in (0, inner[1] // shape.C)
+
+
 @pytest.mark.parametrize("shape_index,aligned", [(2, True), (4, True), (2, False)])
 def test_bf16_transposing_bf16_out_indexing(shape_index, aligned):
     """Family 6 writing bf16 Out: 16-byte stores of eight pixels from lane
