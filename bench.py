@@ -541,14 +541,14 @@ def table1_sweep():
     for c in TABLE1:
         lk = time_layer(c, 30, 5, queued=True)["mean_kernel_ms"] * 1e-3
         inner = B.conv_fwd_ex_inner_shape(*c.key(), c.stride, c.pad)
-        plan = B.conv_fwd_plan(*inner[:7])
+        plan, direct = B.conv_fwd_ex_plan(*c.key(), c.stride, c.pad)
         F, Bt = flops(c), alg_bytes(c)
         t_mfma, t_hbm = F / (PEAK["fp32_mfma_tflops"] * 1e12), Bt / (PEAK["hbm_gbs"] * 1e9)
         bound = "mfma" if t_mfma >= t_hbm else "hbm"
         rows[c.name] = {
             "K": c.K, "C": c.C, "HW": c.H, "RS": c.R, "stride": c.stride, "pad": c.pad,
             "inner_shape": list(inner[:7]), "variant": plan["variant"], "split_c": plan["split_c"],
-            "pred_us": plan["pred_total_us"], "kernel_us": lk * 1e6, "gflops": F / lk / 1e9,
+            "direct": direct, "pred_us": plan["pred_total_us"], "kernel_us": lk * 1e6, "gflops": F / lk / 1e9,
             "pct_fp32_mfma_peak": 100 * F / lk / 1e12 / PEAK["fp32_mfma_tflops"],
             "alg_hbm_gbs": Bt / lk / 1e9, "pct_hbm_peak": 100 * Bt / lk / 1e9 / PEAK["hbm_gbs"],
             "bound": bound, "roofline_frac": max(t_mfma, t_hbm) / lk,
@@ -561,7 +561,9 @@ def table1_report(rows):
     lines = ["# Table 1 conv2d layers at batch 1 (Yolo-9000, ResNet-18), MI355X, fp32", "",
              "Each layer with the table's stride and same padding (R // 2), through conv_fwd_ex: "
              "strided or padded layers are rewritten as a stride-1 valid convolution (inner shape "
-             "C', H', R') and run with the selector's plan.  Time = mean of 30 launches queued behind a "
+             "C', H', R') and run with the selector's plan, which reads the caller's In through the phase "
+             "mapping where its kernel can (plan marked d) and otherwise runs on a phase-split or padded "
+             "copy of In.  Time = mean of 30 launches queued behind a "
              "spin kernel on rotating buffer sets, from HIP events.  Roofline fraction = time at the "
              "layer's bound (fp32 MFMA 157.3 TFLOP/s or HBM 8 TB/s) over the measured time.  The "
              "depth-wise MobileNet layers are not Eq. (1).", "",
@@ -572,7 +574,8 @@ def table1_report(rows):
     for name, r in rows.items():
         ic = r["inner_shape"]
         lines.append(f"| {name.split('_', 1)[1]} | {r['K']} | {r['C']} | {r['HW']} | {r['RS']} | {r['stride']} | "
-                     f"({ic[1]}, {ic[3]}, {ic[5]}) | v{r['variant']}/{r['split_c']} | {r['kernel_us']:.1f} | "
+                     f"({ic[1]}, {ic[3]}, {ic[5]}) | v{r['variant']}/{r['split_c']}{' d' if r.get('direct') else ''} | "
+                     f"{r['kernel_us']:.1f} | "
                      f"{r['gflops']:.0f} | {r['pct_fp32_mfma_peak']:.1f} | {r['alg_hbm_gbs']:.0f} | {r['bound']} | "
                      f"{r['roofline_frac']:.3f} |")
     return "\n".join(lines) + "\n"
@@ -760,15 +763,17 @@ def main():
                                     "mopt5_kernel_us": tk * 1e6, "mopt5_gflops": flops(lc) / tk / 1e9,
                                     "mopt5_pct_hbm_peak": 100 * alg_bytes(lc) / tk / 1e9 / PEAK["hbm_gbs"]})
         layers[c5.name + "_bf16out"] = bf16out_row
-        # strided, padded Table 1 layers (conv_fwd_ex: polyphase rewrite, then
-        # the selected stride-1 plan of the inner problem), timed the same way
+        # strided, padded Table 1 layers (conv_fwd_ex: the selected stride-1
+        # plan of the polyphase inner problem, reading In through the phase
+        # mapping where its kernel can), timed the same way
         for lc in STRIDED_CONFIGS:
             lk = time_layer(lc, 50, 5, queued=True)["mean_kernel_ms"] * 1e-3
             inner = B.conv_fwd_ex_inner_shape(*lc.key(), lc.stride, lc.pad)
-            lplan = B.conv_fwd_plan(*inner[:7])
+            lplan, ldirect = B.conv_fwd_ex_plan(*lc.key(), lc.stride, lc.pad)
             layers[lc.name] = {
                 "dtype": lc.dtype, "stride": lc.stride, "pad": lc.pad, "inner_shape": list(inner[:7]),
-                "variant": lplan["variant"], "split_c": lplan["split_c"], "kernel_us": lk * 1e6,
+                "variant": lplan["variant"], "split_c": lplan["split_c"], "direct": ldirect,
+                "kernel_us": lk * 1e6,
                 "gflops": flops(lc) / lk / 1e9,
                 "pct_fp32_mfma_peak": 100 * flops(lc) / lk / 1e12 / PEAK["fp32_mfma_tflops"],
                 "alg_hbm_gbs": alg_bytes(lc) / lk / 1e9,

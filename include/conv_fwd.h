@@ -294,6 +294,18 @@ int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S,
 int conv_fwd_ex_geometry(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w,
                          int pad_h, int pad_w, const conv_plan_t* plan, int32_t* out, int cap);
 
+/*
+ * Host only: the plan conv_fwd_ex runs for this layer with 16-byte aligned
+ * tensors -- the selector's plan of its inner stride-1 problem.  *direct (if
+ * non-null) is set to 1 when that plan's kernel reads the caller's In
+ * through the phase mapping (fp32 layers with stride or padding, see
+ * conv_fwd_ex_geometry), else 0 (In is phase-split into a workspace first,
+ * or the layer needs no rewrite).  Returns CONV_OK or a negative
+ * conv_status_t.
+ */
+int conv_fwd_ex_plan(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w, int pad_h,
+                     int pad_w, int dtype, conv_plan_t* plan_out, int32_t* direct);
+
 /* Static string for a conv_status_t. */
 const char* conv_fwd_strerror(int status);
 

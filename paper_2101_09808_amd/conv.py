@@ -93,6 +93,8 @@ def lib():
         L.conv_fwd_ex_geometry.argtypes = shape7 + [_i32] * 4 + [ctypes.POINTER(ConvPlan), ctypes.POINTER(_i32),
                                                                  _i32]
         L.conv_fwd_ex_geometry.restype = _i32
+        L.conv_fwd_ex_plan.argtypes = shape7 + [_i32] * 5 + [ctypes.POINTER(ConvPlan), ctypes.POINTER(_i32)]
+        L.conv_fwd_ex_plan.restype = _i32
         L.conv_fwd_strerror.argtypes = [_i32]
         L.conv_fwd_strerror.restype = ctypes.c_char_p
         _lib = L
@@ -303,6 +305,20 @@ def conv_fwd_geometry(N, C, K, H, W, R, S, plan):
     if st < 0:
         raise ConvError(st, "conv_fwd_geometry")
     return dict(zip(GEOM_FIELDS, list(buf)[:len(GEOM_FIELDS)]))
+
+
+def conv_fwd_ex_plan(N, C, K, H, W, R, S, stride=1, pad=0, dtype=CONV_DTYPE_F32):
+    """(plan, direct): the plan conv_fwd_ex runs for this layer (a plan of its
+    inner stride-1 problem, host only), and whether its kernel reads In
+    through the phase mapping instead of a phase-split copy."""
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    p = ConvPlan()
+    d = _i32(0)
+    st = lib().conv_fwd_ex_plan(N, C, K, H, W, R, S, sh, sw, ph, pw, dtype, ctypes.byref(p), ctypes.byref(d))
+    if st != CONV_OK:
+        raise ConvError(st, "conv_fwd_ex_plan")
+    return p.to_dict(), bool(d.value)
 
 
 def conv_fwd_ex_geometry(N, C, K, H, W, R, S, stride, pad, plan):

@@ -156,6 +156,59 @@ int run_selected(const Shape& s, int dtype, const void* In, const void* Ker, flo
   return launch(*e.v, e.g, In, Ker, Out, stream);
 }
 
+// conv_fwd_ex's plan for an fp32 strided or padded layer: the selector's
+// plan of the inner problem (the best one whose loads suit the tensors as
+// the kernel will see them), run reading In through the phase mapping when
+// its kernel can.  Cached per layer, stride, padding and alignment.
+struct ExEntry {
+  Entry e;
+  bool direct;  // e.g carries the phase mapping
+};
+typedef std::tuple<int, int, int, int, int, int, int, int, int, int, int, int> ExKey;
+std::map<ExKey, ExEntry> g_ex_cache;
+
+int select_ex_entry(const PhaseGeom& p, int align_direct, int align_split, ExEntry* out) {
+  const Shape inner{p.N, p.C * p.na * p.nb, p.K, p.Hp, p.Wp, p.Rp, p.Sp};
+  // (Ranking the candidates with the phase-split pass charged to plans that
+  // cannot read In directly picked worse plans on the small layers, whose
+  // predicted times are least reliable: Table 1's R1 28 -> 54 us.)
+  std::vector<conv_plan_t> buf(4096);
+  const int n = std::min<int>(enumerate_plans(inner, CONV_DTYPE_F32, buf.data(), (int)buf.size()), (int)buf.size());
+  for (int i = 0; i < n; ++i) {
+    const Variant* v = find_variant(buf[i].variant);
+    Geom g;
+    if (!v || !resolve_geom(inner, *v, buf[i], &g, nullptr)) continue;
+    Geom gd = g;
+    const bool direct = variant_fits(*v, CONV_DTYPE_F32, align_direct) && phase_direct(*v, p, CONV_DTYPE_F32, &gd);
+    if (!direct && !variant_fits(*v, CONV_DTYPE_F32, align_split)) continue;
+    out->e.plan = buf[i];
+    out->e.v = v;
+    out->e.g = direct ? gd : g;
+    out->direct = direct;
+    return CONV_OK;
+  }
+  return CONV_ENOPLAN;
+}
+
+int cached_ex_entry(const PhaseGeom& p, int align_direct, int align_split, ExEntry* out) {
+  const ExKey key{p.N, p.C, p.K, p.H, p.W, p.R, p.S, p.sh, p.sw, p.ph, p.pw, align_direct * 8 + align_split};
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_ex_cache.find(key);
+    if (it != g_ex_cache.end()) {
+      *out = it->second;
+      return CONV_OK;
+    }
+  }
+  ExEntry e;
+  const int st = select_ex_entry(p, align_direct, align_split, &e);
+  if (st != CONV_OK) return st;
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_ex_cache[key] = e;
+  *out = e;
+  return CONV_OK;
+}
+
 // Inner stride-1 problem of a strided, padded convolution (polyphase rewrite).
 int phase_geom(int N, int C, int K, int H, int W, int R, int S, int sh, int sw, int ph, int pw,
                PhaseGeom* p) {
@@ -244,28 +297,34 @@ int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S, int stride_h, i
   const int Cp = C * p.na * p.nb;
   const bool ker_moves = stride_h > 1 || stride_w > 1;
   const Shape inner{N, Cp, K, p.Hp, p.Wp, p.Rp, p.Sp};
-  {
-    // Direct path: the inner plan's direct-to-LDS kernel reads the caller's
-    // In through the phase mapping (no pass over In); only a strided Ker is
-    // rearranged first, into a workspace (256-byte aligned).
-    Entry d;
-    const int align = alignment_of(In, Ker) | (ker_moves ? ALIGN_KER : 0);
-    if (cached_entry(inner, dtype, align, &d) == CONV_OK) {
-      Geom g = d.g;
-      if (phase_direct(*d.v, p, dtype, &g)) {
-        if (!ker_moves) return launch(*d.v, g, In, Ker, Out, stream);
-        void* kp = nullptr;
-        st = stream_alloc((size_t)K * Cp * p.Rp * p.Sp * e, stream, &kp);
-        if (st != CONV_OK) return st;
-        st = launch_phase_split(p, dtype, In, Ker, nullptr, kp, stream);
-        if (st == CONV_OK) st = launch(*d.v, g, In, kp, Out, stream);
-        const int freed = stream_free(kp, stream);
-        return st == CONV_OK ? freed : st;
-      }
-    }
+  if (dtype == CONV_DTYPE_F32) {
+    // The plan either reads the caller's In through the phase mapping
+    // (direct-to-LDS kernel: no pass over In) or runs on phase-split copies
+    // in a workspace; a strided Ker is rearranged first either way.  The
+    // workspaces are 256-byte aligned.
+    const int ker_al = ker_moves ? ALIGN_KER : (alignment_of(In, Ker) & ALIGN_KER);
+    const int al_direct = (alignment_of(In, Ker) & (ALIGN_IN | ALIGN_IN4)) | ker_al;
+    const int al_split = ALIGN_IN | ALIGN_IN4 | ker_al;
+    ExEntry x;
+    st = cached_ex_entry(p, al_direct, al_split, &x);
+    if (st != CONV_OK) return st;
+    const size_t in_ws = x.direct ? 0 : ((size_t)N * Cp * p.Hp * p.Wp * e + 255) / 256 * 256;
+    const size_t ker_ws = ker_moves ? (size_t)K * Cp * p.Rp * p.Sp * e : 0;
+    if (in_ws + ker_ws == 0) return launch(*x.e.v, x.e.g, In, Ker, Out, stream);
+    void* wsv = nullptr;
+    st = stream_alloc(in_ws + ker_ws, stream, &wsv);
+    if (st != CONV_OK) return st;
+    char* ws = static_cast<char*>(wsv);
+    void* Kp = ker_moves ? ws + in_ws : nullptr;
+    st = launch_phase_split(p, dtype, In, Ker, x.direct ? nullptr : ws, Kp, stream);
+    if (st == CONV_OK)
+      st = launch(*x.e.v, x.e.g, x.direct ? In : ws, ker_moves ? Kp : Ker, Out, stream);
+    const int freed = stream_free(ws, stream);
+    return st == CONV_OK ? freed : st;
   }
-  // stream-ordered workspace: the phase images of In, then (strided only)
-  // the rearranged Ker; at stride 1 the padded In meets the original Ker
+  // bf16: stream-ordered workspace with the phase images of In, then
+  // (strided only) the rearranged Ker; at stride 1 the padded In meets the
+  // original Ker
   const size_t in_bytes = ((size_t)N * Cp * p.Hp * p.Wp * e + 255) / 256 * 256;
   const size_t ker_bytes = ker_moves ? (size_t)K * Cp * p.Rp * p.Sp * e : 0;
   void* wsv = nullptr;
@@ -278,6 +337,26 @@ int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S, int stride_h, i
     st = run_selected(inner, dtype, ws, ker_moves ? Kp : Ker, Out, stream);
   const int freed = stream_free(ws, stream);
   return st == CONV_OK ? freed : st;
+}
+
+int conv_fwd_ex_plan(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w, int pad_h,
+                     int pad_w, int dtype, conv_plan_t* plan_out, int32_t* direct) {
+  PhaseGeom p;
+  int st = phase_geom(N, C, K, H, W, R, S, stride_h, stride_w, pad_h, pad_w, &p);
+  if (st != CONV_OK) return st;
+  if (!plan_out) return CONV_ENULL;
+  if (dtype != CONV_DTYPE_F32 && dtype != CONV_DTYPE_BF16) return CONV_EINVAL;
+  const bool rewrite = stride_h > 1 || stride_w > 1 || pad_h > 0 || pad_w > 0;
+  if (dtype == CONV_DTYPE_F32 && rewrite) {
+    ExEntry x;
+    st = cached_ex_entry(p, ALIGN_ALL, ALIGN_ALL, &x);
+    if (st != CONV_OK) return st;
+    *plan_out = x.e.plan;
+    if (direct) *direct = x.direct ? 1 : 0;
+    return CONV_OK;
+  }
+  if (direct) *direct = 0;
+  return cached_plan(Shape{N, C * p.na * p.nb, K, p.Hp, p.Wp, p.Rp, p.Sp}, dtype, plan_out);
 }
 
 int conv_fwd_ex_inner_shape(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w,

@@ -427,6 +427,15 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
   return true;
 }
 
+namespace {
+double family_factor(int family);
+// Ranking time of a scored plan: predicted time times the kernel family's
+// measured factor.
+double rank_time(const conv_plan_t& p) {
+  return p.pred_total_us * family_factor(find_variant(p.variant)->family);
+}
+}  // namespace
+
 bool phase_direct(const Variant& v, const PhaseGeom& p, int dtype, Geom* g) {
   const int nph = p.na * p.nb;
   if (dtype != CONV_DTYPE_F32 || v.family != FAMILY_DMA || v.in_vec != 1 || v.tc % nph) return false;
@@ -658,8 +667,7 @@ void fill_plan_fields(conv_plan_t* p, const Variant& v, int nwk, int nwp, int tr
 // the family factor, MFMA time, total predicted bytes, fewer workgroups,
 // variant id, larger k tile, no split).
 bool better(const conv_plan_t& a, const conv_plan_t& b) {
-  const double ta = a.pred_total_us * family_factor(find_variant(a.variant)->family);
-  const double tb = b.pred_total_us * family_factor(find_variant(b.variant)->family);
+  const double ta = rank_time(a), tb = rank_time(b);
   if (ta != tb) return ta < tb;
   // equal bound: less MFMA work (fewer padded pixels in partial tiles)
   if (a.pred_mfma_us != b.pred_mfma_us) return a.pred_mfma_us < b.pred_mfma_us;

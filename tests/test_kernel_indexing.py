@@ -225,15 +225,27 @@ def test_phase_split_rewrite_equals_strided_definition():
 
 
 def test_strided_inner_plans_indexing():
-    """The plans the strided GPU tests run on their inner stride-1 problems."""
-    from tests.kernel_emulator import emulate_bf16
+    """The plans the strided GPU tests run (conv_fwd_ex_plan): on the inner
+    stride-1 problem, or reading In through the phase mapping."""
+    from tests.kernel_emulator import emulate_bf16, emulate_phase_split
     from tests.test_gpu_parity import STRIDED_SHAPES
     for shape in STRIDED_SHAPES:
         inner = B.conv_fwd_ex_inner_shape(*shape.key(), shape.stride, shape.pad)
         ish = ConvShape(shape.name + "_inner", *inner[:7], shape.dtype, shape.seed)
         dt = B.CONV_DTYPE_BF16 if shape.dtype == "bf16" else B.CONV_DTYPE_F32
-        p = B.conv_fwd_plan(*ish.key(), dtype=dt)
-        if dt == B.CONV_DTYPE_BF16:
+        p, direct = B.conv_fwd_ex_plan(*shape.key(), shape.stride, shape.pad, dtype=dt)
+        g = B.conv_fwd_ex_geometry(*shape.key(), shape.stride, shape.pad, p)
+        assert bool(g["nph"]) == direct
+        if direct:
+            In, Ker = make_inputs(shape)
+            In64, Ker64 = In.float().numpy().astype(np.float64), Ker.float().numpy().astype(np.float64)
+            st, pd = (shape.stride, shape.stride), (shape.pad, shape.pad)
+            _, Kp, _ = emulate_phase_split(In64, Ker64, st, pd)
+            ref = oconv.conv_fwd_ex(In64.astype(np.float32), Ker64.astype(np.float32), st, pd).reshape(-1)
+            out, written = emulate(g, In64.reshape(-1), Kp.reshape(-1))
+            assert np.all(written == 1)
+            assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
+        elif dt == B.CONV_DTYPE_BF16:
             In, Ker = make_inputs(ish)
             In64 = In.float().numpy().astype(np.float64)
             Ker64 = Ker.float().numpy().astype(np.float64)
