@@ -1706,6 +1706,8 @@ const Instance kInstances[] = {
     // scalar In loads: any row length (Q % 4 != 0)
     F32_DMA(137, 4, 4, 4, 16, 1, 1, 3, 17, 1, 5, 4),
     F32_DMA(138, 4, 4, 4, 8, 1, 1, 4, 9, 1, 3, 4),
+    F32_DMA(139, 4, 5, 4, 32, 1, 1, 3, 21, 1, 5, 4),
+    F32_DMA(140, 4, 4, 4, 32, 1, 1, 3, 17, 1, 5, 4),
     F32_DMA(121, 1, 25, 4, 16, 1, 1, 4, 7, 4, 2, 4),
     F32_DMA(126, 1, 13, 8, 16, 1, 1, 4, 4, 4, 1, 4),
     F32_DMA(127, 1, 7, 8, 16, 1, 1, 4, 2, 4, 1, 4),
