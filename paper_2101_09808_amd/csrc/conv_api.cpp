@@ -295,7 +295,9 @@ int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S, int stride_h, i
     return run_selected(Shape{N, C, K, H, W, R, S}, dtype, In, Ker, static_cast<float*>(Out), stream);
   const size_t e = dtype == CONV_DTYPE_BF16 ? 2 : 4;
   const int Cp = C * p.na * p.nb;
-  const bool ker_moves = stride_h > 1 || stride_w > 1;
+  // The rearranged Ker differs from Ker only with more than one phase (one
+  // phase per axis means stride 1 or a single tap along it).
+  const bool ker_moves = p.na * p.nb > 1;
   const Shape inner{N, Cp, K, p.Hp, p.Wp, p.Rp, p.Sp};
   if (dtype == CONV_DTYPE_F32) {
     // The plan either reads the caller's In through the phase mapping
