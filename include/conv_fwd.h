@@ -20,11 +20,15 @@
  *
  * Ownership: every tensor pointer is DEVICE memory allocated and freed by
  * the caller.  The library keeps a host-side plan cache; its device
- * allocations are temporary workspaces (split reductions, the strided
- * rewrite, bf16 fallbacks, conv_fwd_tune's scratch), taken and returned in
- * stream order within the call from a memory pool the library creates per
- * device, which keeps up to 1 GB of freed blocks for reuse until the
- * process ends.  The calling thread's current device must own the stream.
+ * allocations are workspaces (split reductions, the strided rewrite, bf16
+ * fallbacks, conv_fwd_tune's scratch) from a memory pool the library
+ * creates per device, which keeps up to 1 GB of freed blocks for reuse.
+ * The workspaces of the compute calls are kept per device, stream and
+ * nesting level and reused by the next call on that stream (stream order
+ * makes that safe); each grows to the largest size a call on that stream
+ * needed and is held until the process ends.  A call that finds its buffer
+ * held by another host thread takes and returns a fresh one in stream order.
+ * The calling thread's current device must own the stream.
  * In, Ker and Out must not overlap.
  *
  * Asynchrony: the compute calls enqueue kernels on `stream` (a hipStream_t;

@@ -129,9 +129,10 @@ int run_bf16_widened(const Shape& s, const void* In, const void* Ker, void* Out,
   const size_t n_in = (size_t)s.N * s.C * s.H * s.W, n_ker = (size_t)s.K * s.C * s.R * s.S;
   const size_t n_out = out_bf16 ? (size_t)s.N * s.K * (s.H - s.R + 1) * (s.W - s.S + 1) : 0;
   const size_t a_in = (n_in * 4 + 255) / 256 * 256, a_ker = (n_ker * 4 + 255) / 256 * 256;
-  void* ws = nullptr;
-  int st = stream_alloc(a_in + a_ker + n_out * 4, stream, &ws);
+  Workspace w;
+  int st = workspace_acquire(0, a_in + a_ker + n_out * 4, stream, &w);
   if (st != CONV_OK) return st;
+  void* ws = w.ptr;
   float* in32 = static_cast<float*>(ws);
   float* ker32 = reinterpret_cast<float*>(static_cast<char*>(ws) + a_in);
   float* out32 = reinterpret_cast<float*>(static_cast<char*>(ws) + a_in + a_ker);
@@ -143,7 +144,7 @@ int run_bf16_widened(const Shape& s, const void* In, const void* Ker, void* Out,
     if (st == CONV_OK) st = launch(*e.v, e.g, in32, ker32, out_bf16 ? out32 : static_cast<float*>(Out), stream);
   }
   if (st == CONV_OK && out_bf16) st = launch_round_bf16(out32, Out, (int64_t)n_out, stream);
-  const int freed = stream_free(ws, stream);
+  const int freed = workspace_release(w, stream);
   return st == CONV_OK ? freed : st;
 }
 
@@ -313,15 +314,15 @@ int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S, int stride_h, i
     const size_t in_ws = x.direct ? 0 : ((size_t)N * Cp * p.Hp * p.Wp * e + 255) / 256 * 256;
     const size_t ker_ws = ker_moves ? (size_t)K * Cp * p.Rp * p.Sp * e : 0;
     if (in_ws + ker_ws == 0) return launch(*x.e.v, x.e.g, In, Ker, Out, stream);
-    void* wsv = nullptr;
-    st = stream_alloc(in_ws + ker_ws, stream, &wsv);
+    Workspace w;
+    st = workspace_acquire(0, in_ws + ker_ws, stream, &w);
     if (st != CONV_OK) return st;
-    char* ws = static_cast<char*>(wsv);
+    char* ws = static_cast<char*>(w.ptr);
     void* Kp = ker_moves ? ws + in_ws : nullptr;
     st = launch_phase_split(p, dtype, In, Ker, x.direct ? nullptr : ws, Kp, stream);
     if (st == CONV_OK)
       st = launch(*x.e.v, x.e.g, x.direct ? In : ws, ker_moves ? Kp : Ker, Out, stream);
-    const int freed = stream_free(ws, stream);
+    const int freed = workspace_release(w, stream);
     return st == CONV_OK ? freed : st;
   }
   // bf16: stream-ordered workspace with the phase images of In, then
@@ -329,15 +330,15 @@ int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S, int stride_h, i
   // original Ker
   const size_t in_bytes = ((size_t)N * Cp * p.Hp * p.Wp * e + 255) / 256 * 256;
   const size_t ker_bytes = ker_moves ? (size_t)K * Cp * p.Rp * p.Sp * e : 0;
-  void* wsv = nullptr;
-  st = stream_alloc(in_bytes + ker_bytes, stream, &wsv);
+  Workspace w;
+  st = workspace_acquire(0, in_bytes + ker_bytes, stream, &w);
   if (st != CONV_OK) return st;
-  char* ws = static_cast<char*>(wsv);
+  char* ws = static_cast<char*>(w.ptr);
   void* Kp = ker_moves ? ws + in_bytes : nullptr;
   st = launch_phase_split(p, dtype, In, Ker, ws, Kp, stream);
   if (st == CONV_OK)
     st = run_selected(inner, dtype, ws, ker_moves ? Kp : Ker, Out, stream);
-  const int freed = stream_free(ws, stream);
+  const int freed = workspace_release(w, stream);
   return st == CONV_OK ? freed : st;
 }
 

@@ -113,6 +113,19 @@ bool phase_direct(const Variant& v, const PhaseGeom& p, int dtype, Geom* g);
 // (hipMallocFromPoolAsync / hipFreeAsync on `stream`).
 int stream_alloc(size_t bytes, void* stream, void** out);
 int stream_free(void* p, void* stream);
+// A call's workspace: the buffer the library keeps for (current device,
+// stream, nesting level) -- levels 0 (conv_fwd_ex, bf16 widening), 1 (bf16
+// Out staging), 2 (split partial sums) let nested steps of one call hold
+// theirs together -- or, while another host thread holds that buffer, a
+// fresh stream-ordered allocation.  Release enqueues nothing for a kept
+// buffer: the next call on the stream reuses it in stream order.
+struct Workspace {
+  void* ptr = nullptr;
+  bool cached = false;
+  int level = 0;
+};
+int workspace_acquire(int level, size_t bytes, void* stream, Workspace* w);
+int workspace_release(const Workspace& w, void* stream);
 // Phase-split In into Inp (Inp non-null) and Ker into Kp (Kp non-null), on
 // `stream`.
 int launch_phase_split(const PhaseGeom& p, int dtype, const void* In, const void* Ker, void* Inp, void* Kp,

@@ -25,7 +25,9 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <map>
 #include <mutex>
+#include <tuple>
 #include <type_traits>
 #include <utility>
 #include <vector>
@@ -1824,6 +1826,56 @@ int stream_free(void* p, void* stream) {
   return hipFreeAsync(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? CONV_OK : CONV_EHIP;
 }
 
+namespace {
+// Workspaces kept per (device, stream, nesting level): the kernels of the
+// calls on one stream run in stream order, so a call can reuse the buffer
+// the previous call on that stream used.  A buffer grows by a stream-ordered
+// free and a new allocation; while another host thread holds it, a call
+// takes a fresh stream-ordered allocation instead.
+struct CachedWorkspace {
+  void* ptr = nullptr;
+  size_t size = 0;
+  bool busy = false;
+};
+std::mutex g_ws_mu;
+std::map<std::tuple<int, void*, int>, CachedWorkspace> g_ws;
+}  // namespace
+
+int workspace_acquire(int level, size_t bytes, void* stream, Workspace* w) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return CONV_EHIP;
+  w->cached = false;
+  w->level = level;
+  {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    CachedWorkspace& c = g_ws[std::make_tuple(dev, stream, level)];
+    if (!c.busy) {
+      if (c.size < bytes) {
+        if (c.ptr && stream_free(c.ptr, stream) != CONV_OK) return CONV_EHIP;
+        c.ptr = nullptr;
+        c.size = 0;
+        const size_t sz = (bytes + (size_t(1) << 20) - 1) >> 20 << 20;  // whole MiB
+        if (stream_alloc(sz, stream, &c.ptr) != CONV_OK) return CONV_EHIP;
+        c.size = sz;
+      }
+      c.busy = true;
+      w->ptr = c.ptr;
+      w->cached = true;
+      return CONV_OK;
+    }
+  }
+  return stream_alloc(bytes, stream, &w->ptr);
+}
+
+int workspace_release(const Workspace& w, void* stream) {
+  if (!w.cached) return stream_free(w.ptr, stream);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return CONV_EHIP;
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  g_ws[std::make_tuple(dev, stream, w.level)].busy = false;
+  return CONV_OK;
+}
+
 int launch_phase_split(const PhaseGeom& p, int dtype, const void* In, const void* Ker, void* Inp, void* Kp,
                        void* stream) {
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
@@ -1887,9 +1939,10 @@ int launch_bf16_out(const Variant& v, const Geom& g, const void* In, const void*
   }
   // any other kernel: fp32 Out into a stream-ordered workspace, then rounded
   const int64_t n = (int64_t)g.N * g.K * g.P * g.Q;
-  void* ws = nullptr;
-  int rc = stream_alloc((size_t)n * sizeof(float), stream, &ws);
+  Workspace w;
+  int rc = workspace_acquire(1, (size_t)n * sizeof(float), stream, &w);
   if (rc != CONV_OK) return rc;
+  void* ws = w.ptr;
   rc = launch(v, g, In, Ker, static_cast<float*>(ws), stream);
   if (rc == CONV_OK) {
     const int blocks = (int)std::min<int64_t>((n + 255) / 256, 8192);
@@ -1897,7 +1950,7 @@ int launch_bf16_out(const Variant& v, const Geom& g, const void* In, const void*
                        static_cast<unsigned short*>(Out), n);
     if (hipGetLastError() != hipSuccess) rc = CONV_EHIP;
   }
-  const int freed = stream_free(ws, stream);
+  const int freed = workspace_release(w, stream);
   return rc == CONV_OK ? freed : rc;
 }
 
@@ -1934,9 +1987,9 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
     // Split reduction: partial outputs of the channel ranges into a
     // stream-ordered workspace, then the fixed-order sum into Out.
     const int64_t n = (int64_t)g.N * g.K * g.P * g.Q;
-    float* ws = nullptr;
-    if (stream_alloc((size_t)g.split * n * sizeof(float), stream, reinterpret_cast<void**>(&ws)) != CONV_OK)
-      return CONV_EHIP;
+    Workspace w;
+    if (workspace_acquire(2, (size_t)g.split * n * sizeof(float), stream, &w) != CONV_OK) return CONV_EHIP;
+    float* ws = static_cast<float*>(w.ptr);
     hipLaunchKernelGGL(inst->f32, dim3(g.grid), dim3(v.threads), lds_bytes, st,
                        static_cast<const float*>(In), static_cast<const float*>(Ker), ws, g);
     const bool vec4 = (n % 4 == 0) && (reinterpret_cast<uintptr_t>(Out) % 16 == 0);
@@ -1945,8 +1998,8 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
     if (vec4) hipLaunchKernelGGL(splitk_reduce_kernel<true>, dim3(blocks), dim3(256), 0, st, ws, Out, n, g.split);
     else hipLaunchKernelGGL(splitk_reduce_kernel<false>, dim3(blocks), dim3(256), 0, st, ws, Out, n, g.split);
     const hipError_t launched = hipGetLastError();
-    const hipError_t freed = hipFreeAsync(ws, st);
-    return (launched == hipSuccess && freed == hipSuccess) ? CONV_OK : CONV_EHIP;
+    const int freed = workspace_release(w, stream);
+    return (launched == hipSuccess && freed == CONV_OK) ? CONV_OK : CONV_EHIP;
   }
   if (inst->f32) {
     hipLaunchKernelGGL(inst->f32, dim3(g.grid), dim3(v.threads), lds_bytes, st,
