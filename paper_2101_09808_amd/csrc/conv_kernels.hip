@@ -1681,6 +1681,10 @@ const Instance kInstances[] = {
     F32_DMA(143, 2, 4, 8, 8, 3, 3, 3, 4, 1, 10, 1),
     F32_DMA(144, 4, 2, 4, 8, 3, 3, 3, 4, 1, 19, 1),
     F32_DMA(145, 2, 8, 8, 8, 3, 3, 3, 7, 1, 10, 1),
+    // few input channels (the first layer of a network): four per step,
+    // 32-row k tiles
+    F32_DMA(146, 2, 4, 8, 4, 3, 3, 3, 7, 1, 3, 1),
+    F32_DMA(147, 2, 2, 4, 4, 3, 3, 3, 7, 1, 5, 1),
     // channel groups of waves (WK, WP, waves, groups, channels per step, ...):
     // small layers without a split reduction
     F32_DMA_CG(161, 2, 2, 4, 4, 16, 3, 3, 3, 7, 1, 5, 4),
