@@ -612,3 +612,38 @@ def test_random_shape_parity(shape):
         ob = B.conv_fwd_bf16_out(In_d, Ker_d)
         torch.cuda.synchronize()
         assert torch.equal(ob.view(torch.int16), out.to(torch.bfloat16).view(torch.int16))
+
+
+@pytest.mark.gpu
+def test_workspaces_reused_across_calls_and_streams():
+    """The per-stream workspaces: a strided layer (rearranged Ker), then a
+    split plan (partial sums), each on two streams in turn, a larger call
+    growing the buffer and a smaller one reusing it; every result against
+    the oracle."""
+    big = ConvShape("ws_s2p1_big", 2, 16, 32, 30, 30, 3, 3, "f32", 81, 2, 1)
+    small = ConvShape("ws_s2p1_small", 1, 8, 16, 12, 12, 3, 3, "f32", 82, 2, 1)
+    split_shape = ConvShape("ws_split", 2, 40, 72, 11, 13, 3, 3, "f32", 83)
+    split_plan = next(p for p in B.conv_fwd_candidates(*split_shape.key()) if p["split_c"] > 1
+                      and B.conv_fwd_geometry(*split_shape.key(), p)["family"] == 2)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    runs = []
+    for rep in range(2):
+        for si, st in enumerate(streams):
+            for shape in (big, small):
+                In, Ker = make_inputs(shape, seed=shape.seed + 10 * rep + si)
+                In_d, Ker_d = In.to(DEV), Ker.to(DEV)
+                torch.cuda.synchronize()
+                with torch.cuda.stream(st):
+                    out = B.conv_fwd_ex(In_d, Ker_d, shape.stride, shape.pad, stream=st)
+                runs.append((shape, In, Ker, out, (shape.stride, shape.stride), (shape.pad, shape.pad), In_d, Ker_d))
+            In, Ker = make_inputs(split_shape, seed=split_shape.seed + 10 * rep + si)
+            In_d, Ker_d = In.to(DEV), Ker.to(DEV)
+            torch.cuda.synchronize()
+            with torch.cuda.stream(st):
+                out = B.conv_fwd_with_plan(In_d, Ker_d, split_plan, stream=st)
+            runs.append((split_shape, In, Ker, out, (1, 1), (0, 0), In_d, Ker_d))
+    torch.cuda.synchronize()
+    for shape, In, Ker, out, st, pd, _, _ in runs:  # (device inputs kept alive until here)
+        say(f"[gpu] workspace reuse {shape.name} stride={st} pad={pd}")
+        ref = oconv.conv_fwd_ex(host(In), host(Ker), st, pd)
+        assert rel_err(host(out), ref) <= TOL["f32"], shape.name
