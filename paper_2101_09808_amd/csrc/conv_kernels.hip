@@ -1700,6 +1700,7 @@ const Instance kInstances[] = {
     F32_DMA_CG(171, 2, 2, 4, 4, 64, 1, 1, 3, 9, 1, 3, 4),
     F32_DMA_CG(172, 2, 2, 8, 8, 128, 1, 1, 2, 9, 1, 3, 4),
     F32_DMA_CG(173, 4, 2, 4, 4, 64, 1, 1, 3, 9, 1, 5, 4),
+    F32_DMA_CG(174, 4, 4, 4, 4, 64, 1, 1, 3, 17, 1, 5, 4),
     // 32x32x2 inner loop, 3x3 taps: (pixel units of 16 per wave, waves, ...)
     F32_DMA32(151, 4, 4, 8, 3, 3, 3, 12, 1, 10, 4),
     F32_DMA32(152, 4, 4, 8, 3, 3, 3, 7, 1, 19, 1),
