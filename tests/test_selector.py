@@ -111,3 +111,25 @@ def test_selector_is_minimum_of_its_objective():
         fam0 = B.conv_fwd_geometry(*c.key(), cands[0])["family"]
         same = [x for x in cands if B.conv_fwd_geometry(*c.key(), x)["family"] == fam0]
         assert cands[0]["pred_total_us"] == min(x["pred_total_us"] for x in same)
+
+
+def test_enumeration_rules_for_channel_groups_and_narrow_steps():
+    """Candidate-set rules of the enumerator: channel-group plans (groups of
+    waves splitting each step's channels) only on grids of at most 256
+    workgroups and never with a split reduction; pipeline steps of four
+    channels only for layers with fewer than 16 channels."""
+    from paper_2101_09808_amd.workloads import TABLE1
+    shapes = [c.key() for c in CONFIGS if c.dtype == "f32"]
+    shapes += [tuple(B.conv_fwd_ex_inner_shape(*c.key(), c.stride, c.pad))[:7] for c in TABLE1]
+    seen_groups = seen_narrow = False
+    for key in shapes:
+        for p in B.conv_fwd_candidates(*key):
+            g = B.conv_fwd_geometry(*key, p)
+            if g["nwc"] > 1:
+                seen_groups = True
+                assert g["family"] == 2 and p["split_c"] == 1 and p["num_wg"] <= 256, (key, p)
+                assert g["nwk"] * g["nwp"] * g["nwc"] * 64 == g["threads"]
+            if g["family"] == 2 and g["tc"] < 8:
+                seen_narrow = True
+                assert key[1] < 16, (key, p)
+    assert seen_groups and seen_narrow
