@@ -65,3 +65,20 @@ def test_split_plan_reduction_counts_with_its_launch(tmp_path):
     _write(tmp_path / "c", rows, "WRITE_SIZE")
     _, _, per = bench.calibrated(str(tmp_path / "c"), "WRITE_SIZE", 1.0, layers, launches)
     assert per[layers[0].name]["per_dispatch"] == pytest.approx(42.0)
+
+
+def test_plan_kernel_hash_follows_the_launched_kernel_and_plan():
+    """The traffic figures are keyed to the launched kernel's source, its
+    instance line, the geometry struct and the plan: the same plan hashes
+    the same, another tile of the same variant or another variant does not."""
+    from paper_2101_09808_amd import conv as B
+    from paper_2101_09808_amd.workloads import BY_NAME
+    c = BY_NAME[bench.HEADLINE]
+    cands = B.conv_fwd_candidates(*c.key())
+    p0 = cands[0]
+    h0 = bench.plan_kernel_hash(c, p0)
+    assert len(h0) == 16 and h0 == bench.plan_kernel_hash(c, dict(p0))
+    other_tile = next(p for p in cands if p["variant"] == p0["variant"] and p["tile_cols"] != p0["tile_cols"])
+    other_variant = next(p for p in cands if p["variant"] != p0["variant"])
+    assert bench.plan_kernel_hash(c, other_tile) != h0
+    assert bench.plan_kernel_hash(c, other_variant) != h0
