@@ -1696,6 +1696,7 @@ const Instance kInstances[] = {
     F32_DMA_CG(164, 2, 4, 8, 4, 16, 3, 3, 2, 8, 1, 5, 4),
     F32_DMA_CG(165, 4, 4, 4, 4, 16, 3, 3, 3, 8, 1, 10, 4),
     F32_DMA_CG(166, 2, 2, 8, 4, 16, 3, 3, 2, 6, 1, 5, 4),
+    F32_DMA_CG(167, 4, 2, 8, 4, 16, 3, 3, 2, 8, 1, 5, 4),
     // 2x2 taps (inner problems of stride-2 3x3 layers): deep channel ranges
     F32_DMA_CG(168, 2, 2, 8, 8, 64, 2, 2, 2, 6, 1, 5, 4),
     F32_DMA_CG(169, 2, 2, 4, 4, 32, 2, 2, 3, 6, 1, 5, 4),
