@@ -1700,6 +1700,7 @@ const Instance kInstances[] = {
     // 2x2 taps (inner problems of stride-2 3x3 layers): deep channel ranges
     F32_DMA_CG(168, 2, 2, 8, 8, 64, 2, 2, 2, 6, 1, 5, 4),
     F32_DMA_CG(169, 2, 2, 4, 4, 32, 2, 2, 3, 6, 1, 5, 4),
+    F32_DMA_CG(178, 1, 2, 8, 8, 64, 2, 2, 2, 6, 1, 3, 4),
     // 1x1 taps: deep channel ranges on few pixels
     F32_DMA_CG(171, 2, 2, 4, 4, 64, 1, 1, 3, 9, 1, 3, 4),
     F32_DMA_CG(172, 2, 2, 8, 8, 128, 1, 1, 2, 9, 1, 3, 4),
