@@ -159,12 +159,14 @@ int conv_fwd_bf16_out(int N, int C, int K, int H, int W, int R, int S,
  * Stride 1 without padding is conv_fwd / conv_fwd_bf16.  Otherwise the call
  * rewrites the problem as a stride-1 valid convolution (each input channel
  * becomes min(sh,R) x min(sw,S) phase images; Ker gets ceil(R/sh) x
- * ceil(S/sw) taps, zero where no original tap lands): two small kernels
- * write the phase images (and, when strided, the rearranged Ker) into a
- * stream-ordered workspace from the library's pool, the selected
- * stride-1 plan of the inner problem (see conv_fwd_ex_inner_shape) runs on
- * it, and the workspace is returned in stream order.  Asynchronous like
- * conv_fwd.  Returns a conv_status_t.
+ * ceil(S/sw) taps, zero where no original tap lands) and runs the selected
+ * stride-1 plan of the inner problem (see conv_fwd_ex_inner_shape and
+ * conv_fwd_ex_plan).  For fp32 plans on the direct-to-LDS kernel the kernel
+ * reads In through the phase mapping (see conv_fwd_ex_geometry); otherwise a
+ * small kernel writes the phase images into a workspace first.  With more
+ * than one phase per channel, another small kernel writes the rearranged
+ * Ker into a workspace.  Workspaces are the per-stream ones described under
+ * Ownership.  Asynchronous like conv_fwd.  Returns a conv_status_t.
  */
 int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S,
                 int stride_h, int stride_w, int pad_h, int pad_w, int dtype,
