@@ -253,9 +253,64 @@ def test_multilevel_counts_outer_tiles():
         assert dv[0] == 2 * cm.data_volume(p0, T1, T0)
 
 
-def test_minmax_objective():
-    N = dict(n=4, k=8, c=8, r=3, s=3, h=6, w=6)
-    T0 = dict(n=1, k=4, c=2, r=3, s=3, h=3, w=6)
+def test_minmax_objective_hand_computed():
+    """Sec. 5 objective on a two-level example worked by hand, with the
+    dominant level switching with the bandwidths.
+
+    N = (n1 k2 c2 r1 s1 h1 w4); level-0 tile T0 = (n1 k1 c1 r1 s1 h1 w4) in
+    the order n,k,h,w,c,r,s; level 1 is the whole problem.
+    Level 0 (Sec. 3.2 rule, positions counted from the innermost s = 1):
+      In  -- innermost present iterator s (sliding case, N_s - T_s = 0):
+             (N/T over n,k,h,w,c,r = 1*2*1*1*2*1 = 4) x footprint 1*1*1*4 = 16
+      Ker -- innermost present s: ratio over all seven = 4, footprint 1 -> 4
+      Out -- innermost present w (position 4): ratio over n,k,h,w = 2,
+             footprint 4 -> 8, read and written -> 16
+      DV^0 = 36.
+    Level 1 (T = N): compulsory In 8 + Ker 4 + 2 * Out 8 = 28.
+    """
+    N = dict(n=1, k=2, c=2, r=1, s=1, h=1, w=4)
+    T0 = dict(n=1, k=1, c=1, r=1, s=1, h=1, w=4)
     perms = [cm.REPRESENTATIVES[2], cm.REPRESENTATIVES[0]]
-    dv = cm.level_volumes(perms, [T0, dict(N)], N)
-    assert cm.minmax_cost(perms, [T0, dict(N)], N, [2, 1]) == max(Fraction(dv[0], 2), dv[1])
+    assert cm.level_volumes(perms, [T0, dict(N)], N) == [36, 28]
+    # DV^0 / 4 = 9 < DV^1 / 1 = 28: level 1 bounds
+    assert cm.minmax_cost(perms, [T0, dict(N)], N, [4, 1]) == 28
+    # DV^0 / 1 = 36 > DV^1 / 4 = 7: level 0 bounds
+    assert cm.minmax_cost(perms, [T0, dict(N)], N, [1, 4]) == 36
+    # equal bandwidths of 3: max(12, 28/3) = 12
+    assert cm.minmax_cost(perms, [T0, dict(N)], N, [3, 3]) == 12
+
+
+def test_capacity_eq4_hand_computed():
+    """Eq. (4) on a tile worked by hand: T = (n1 k4 c2 r3 s3 h3 w6) touches
+    In 1*2*(3+3-1)*(6+3-1) = 80, Ker 4*2*3*3 = 72 and Out 1*4*3*6 = 72
+    elements, 224 in all."""
+    T = dict(n=1, k=4, c=2, r=3, s=3, h=3, w=6)
+    assert [cm.footprint(a, T) for a in cm.ARRAYS] == [80, 72, 72]
+    assert cm.capacity_ok(T, 224)
+    assert not cm.capacity_ok(T, 223)
+
+
+def test_footprints_count_distinct_elements_brute_force():
+    """Each footprint of Sec. 3.1 equals the number of distinct elements one
+    tile touches, enumerated index by index from Eq. (1)'s subscripts."""
+    rng = random.Random(29)
+    for _ in range(40):
+        T = {j: rng.randint(1, 4) for j in cm.ITERS}
+        o = {j: rng.randint(0, 5) for j in cm.ITERS}  # tile origin
+        rng_ = {j: range(o[j], o[j] + T[j]) for j in cm.ITERS}
+        ins, kers, outs = set(), set(), set()
+        for n in rng_["n"]:
+            for k in rng_["k"]:
+                for c in rng_["c"]:
+                    for r in rng_["r"]:
+                        for s_ in rng_["s"]:
+                            for h in rng_["h"]:
+                                for w in rng_["w"]:
+                                    ins.add((n, c, h + r, w + s_))
+                                    kers.add((k, c, r, s_))
+                                    outs.add((n, k, h, w))
+        assert cm.footprint("In", T) == len(ins)
+        assert cm.footprint("Ker", T) == len(kers)
+        assert cm.footprint("Out", T) == len(outs)
+        total = len(ins) + len(kers) + len(outs)
+        assert cm.capacity_ok(T, total) and not cm.capacity_ok(T, total - 1)

@@ -17,6 +17,11 @@ MUTATIONS = {
     "ker_missing_c": ('return T["k"] * T["c"] * T["r"] * T["s"]', 'return T["k"] * T["r"] * T["s"]'),
     "k_present_in_in": ('"In": frozenset("nchrws")', '"In": frozenset("nchrwsk")'),
     "r_not_sliding": ('SLIDING = frozenset("whsr")', 'SLIDING = frozenset("whs")'),
+    "capacity_strict": ("for a in ARRAYS) <= capacity", "for a in ARRAYS) < capacity"),
+    "capacity_drops_out": ("sum(footprint(a, T) for a in ARRAYS)", "sum(footprint(a, T) for a in ARRAYS[:2])"),
+    "minmax_takes_min": ("return max(Fraction(d) / Fraction(bw)", "return min(Fraction(d) / Fraction(bw)"),
+    "minmax_multiplies_bw": ("Fraction(d) / Fraction(bw) for d, bw", "Fraction(d) * Fraction(bw) for d, bw"),
+    "multilevel_no_outer_reps": ("out.append(reps * data_volume(", "out.append(data_volume("),
 }
 
 PIN_FUNCS = (
@@ -25,6 +30,9 @@ PIN_FUNCS = (
     lambda: pins.test_full_tiles_give_compulsory_volume(),
     lambda: pins.test_rule_matches_previous_tile_cache_simulation(),
     lambda: pins.test_r_a_worked_example(),
+    lambda: pins.test_capacity_eq4_hand_computed(),
+    lambda: pins.test_minmax_objective_hand_computed(),
+    lambda: pins.test_multilevel_counts_outer_tiles(),
 )
 
 
