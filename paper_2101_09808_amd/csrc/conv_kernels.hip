@@ -1776,15 +1776,20 @@ const Instance* find_instance(int id) {
 
 }  // namespace
 
-const Variant* variants(int* count) {
-  static Variant table[kNumInstances];
-  static bool init = false;
-  if (!init) {
-    for (int i = 0; i < kNumInstances; ++i) table[i] = kInstances[i].v;
-    init = true;
+namespace {
+struct VariantTable {
+  Variant v[kNumInstances];
+  VariantTable() {
+    for (int i = 0; i < kNumInstances; ++i) v[i] = kInstances[i].v;
   }
+};
+}  // namespace
+
+const Variant* variants(int* count) {
+  // A function-local static: initialised once, thread-safe (C++11).
+  static const VariantTable table;
   *count = kNumInstances;
-  return table;
+  return table.v;
 }
 
 const Variant* find_variant(int id) {
