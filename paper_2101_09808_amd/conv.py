@@ -237,7 +237,7 @@ def conv_fwd_tune(In, Ker, top_n=5, reps=3, out=None, stream=None):
     """Time the model's `top_n` best plans on these tensors and keep the
     fastest as the shape's cached plan (Sec. 10, MOpt-5).  In/Ker are fp32
     or bf16.  Blocks until the timed launches have run.  Returns (out, the
-    chosen plan as a dict, mean launch time in us of each timed plan in the
+    chosen plan as a dict, median launch time in us of each timed plan in the
     model's order -- the first candidates that suit the tensors' alignment)."""
     dtype = CONV_DTYPE_BF16 if In.dtype == torch.bfloat16 else CONV_DTYPE_F32
     shape = _check_inputs(In, Ker, torch.bfloat16 if dtype == CONV_DTYPE_BF16 else torch.float32)
