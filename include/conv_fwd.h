@@ -54,7 +54,9 @@ typedef enum {
   CONV_ENULL = -2,   /* a null tensor or output-struct pointer */
   CONV_ERANGE = -3,  /* a tensor of 2^31 elements or more */
   CONV_ENOPLAN = -4, /* no kernel configuration fits the shape */
-  CONV_EHIP = -5     /* the HIP runtime reported an error at launch */
+  CONV_EHIP = -5,    /* the HIP runtime reported an error at launch */
+  CONV_ESCRATCH = -6 /* conv_fwd_ex_noalloc: the call needs more scratch than
+                        CONV_NOALLOC_SCRATCH_BYTES */
 } conv_status_t;
 
 /* Element types of In and Ker (Out and accumulation are always fp32). */
@@ -171,6 +173,27 @@ int conv_fwd_bf16_out(int N, int C, int K, int H, int W, int R, int S,
 int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S,
                 int stride_h, int stride_w, int pad_h, int pad_w, int dtype,
                 const void* In, const void* Ker, float* Out, void* stream);
+
+/*
+ * Allocation-free variant of conv_fwd_ex, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, layouts, operation and
+ * results as conv_fwd_ex (the same plans and kernels run), but every
+ * workspace the call needs (phase images of In, the rearranged Ker, split
+ * partial sums, bf16 widening) is carved from one static device array of
+ * CONV_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends; the call makes no hipMalloc, hipFree or other
+ * allocating call.  A call that would need more scratch returns
+ * CONV_ESCRATCH before launching anything.  Every call on one GPU shares
+ * that GPU's array (which keeps the previous call's contents, and nothing
+ * in it is assumed zero): calls that overlap on one GPU -- on different
+ * streams, or from different host threads -- race and must be serialised
+ * by the caller.  Returns a conv_status_t.
+ */
+#define CONV_NOALLOC_SCRATCH_BYTES (64 * 1024 * 1024)
+int conv_fwd_ex_noalloc(int N, int C, int K, int H, int W, int R, int S,
+                        int stride_h, int stride_w, int pad_h, int pad_w, int dtype,
+                        const void* In, const void* Ker, float* Out, void* stream);
 
 /*
  * Host-only: the inner stride-1 problem conv_fwd_ex runs for these

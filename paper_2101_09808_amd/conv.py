@@ -13,7 +13,8 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libconvfwd.so")
 
-CONV_OK, CONV_EINVAL, CONV_ENULL, CONV_ERANGE, CONV_ENOPLAN, CONV_EHIP = 0, -1, -2, -3, -4, -5
+CONV_OK, CONV_EINVAL, CONV_ENULL, CONV_ERANGE, CONV_ENOPLAN, CONV_EHIP, CONV_ESCRATCH = 0, -1, -2, -3, -4, -5, -6
+CONV_NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
 CONV_DTYPE_F32, CONV_DTYPE_BF16 = 0, 1
 LEVELS = ("reg", "lds", "l2", "hbm")
 ITER_CODE = {"n": 0, "k": 1, "c": 2, "r": 3, "s": 4, "h": 5, "w": 6}
@@ -83,6 +84,8 @@ def lib():
         L.conv_fwd_bf16_out.restype = _i32
         L.conv_fwd_ex.argtypes = shape7 + [_i32] * 5 + [_vp, _vp, _vp, _vp]
         L.conv_fwd_ex.restype = _i32
+        L.conv_fwd_ex_noalloc.argtypes = shape7 + [_i32] * 5 + [_vp, _vp, _vp, _vp]
+        L.conv_fwd_ex_noalloc.restype = _i32
         L.conv_fwd_ex_inner_shape.argtypes = shape7 + [_i32] * 4 + [ctypes.POINTER(_i32)]
         L.conv_fwd_ex_inner_shape.restype = _i32
         L.conv_model_volume.argtypes = [ctypes.POINTER(_i32), ctypes.POINTER(_i64),
@@ -202,6 +205,17 @@ def _pair(x):
 def conv_fwd_ex(In, Ker, stride=1, pad=0, out=None, stream=None):
     """Strided, zero-padded convolution (fp32 or bf16 In/Ker, fp32 Out
     [N,K,P,Q] with P = (H + 2 ph - R) // sh + 1, Q likewise)."""
+    return _conv_fwd_ex("conv_fwd_ex", In, Ker, stride, pad, out, stream)
+
+
+def conv_fwd_ex_noalloc(In, Ker, stride=1, pad=0, out=None, stream=None):
+    """conv_fwd_ex through the allocation-free entry point: the library's
+    workspaces come from its static per-GPU scratch array (out=None still
+    lets torch allocate Out; pass `out` to allocate nothing)."""
+    return _conv_fwd_ex("conv_fwd_ex_noalloc", In, Ker, stride, pad, out, stream)
+
+
+def _conv_fwd_ex(fn, In, Ker, stride, pad, out, stream):
     sh, sw = _pair(stride)
     ph, pw = _pair(pad)
     bf16 = In.dtype == torch.bfloat16
@@ -212,10 +226,10 @@ def conv_fwd_ex(In, Ker, stride=1, pad=0, out=None, stream=None):
         out = torch.empty((N, K, P, Q), dtype=torch.float32, device=In.device)
     elif out.shape != (N, K, P, Q) or out.dtype != torch.float32 or not out.is_contiguous():
         raise ValueError(f"out must be a contiguous float32 {(N, K, P, Q)} tensor")
-    st = lib().conv_fwd_ex(N, C, K, H, W, R, S, sh, sw, ph, pw, CONV_DTYPE_BF16 if bf16 else CONV_DTYPE_F32,
-                           In.data_ptr(), Ker.data_ptr(), out.data_ptr(), _stream_ptr(stream))
+    st = getattr(lib(), fn)(N, C, K, H, W, R, S, sh, sw, ph, pw, CONV_DTYPE_BF16 if bf16 else CONV_DTYPE_F32,
+                            In.data_ptr(), Ker.data_ptr(), out.data_ptr(), _stream_ptr(stream))
     if st != CONV_OK:
-        raise ConvError(st, "conv_fwd_ex")
+        raise ConvError(st, fn)
     return out
 
 

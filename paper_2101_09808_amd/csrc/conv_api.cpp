@@ -285,14 +285,15 @@ int conv_fwd_bf16_out(int N, int C, int K, int H, int W, int R, int S, const uin
   return launch_bf16_out(*e.v, e.g, In, Ker, Out, stream);
 }
 
-int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w, int pad_h,
-                int pad_w, int dtype, const void* In, const void* Ker, float* Out, void* stream) {
-  PhaseGeom p;
-  int st = phase_geom(N, C, K, H, W, R, S, stride_h, stride_w, pad_h, pad_w, &p);
-  if (st != CONV_OK) return st;
-  if (!In || !Ker || !Out) return CONV_ENULL;
-  if (dtype != CONV_DTYPE_F32 && dtype != CONV_DTYPE_BF16) return CONV_EINVAL;
-  if (stride_h == 1 && stride_w == 1 && pad_h == 0 && pad_w == 0)
+}  // extern "C"
+
+namespace {
+
+// The body of conv_fwd_ex (arguments already validated).
+int run_ex(const PhaseGeom& p, int dtype, const void* In, const void* Ker, float* Out, void* stream) {
+  const int N = p.N, C = p.C, K = p.K, H = p.H, W = p.W, R = p.R, S = p.S;
+  int st = CONV_OK;
+  if (p.sh == 1 && p.sw == 1 && p.ph == 0 && p.pw == 0)
     return run_selected(Shape{N, C, K, H, W, R, S}, dtype, In, Ker, static_cast<float*>(Out), stream);
   const size_t e = dtype == CONV_DTYPE_BF16 ? 2 : 4;
   const int Cp = C * p.na * p.nb;
@@ -340,6 +341,107 @@ int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S, int stride_h, i
     st = run_selected(inner, dtype, ws, ker_moves ? Kp : Ker, Out, stream);
   const int freed = workspace_release(w, stream);
   return st == CONV_OK ? freed : st;
+}
+
+// Scratch bytes run_ex needs for these arguments, summed over the
+// workspaces it takes in order, each rounded up to the 256-byte alignment
+// of the arena's bump allocation.  Mirrors the dispatch of run_ex,
+// run_selected, run_bf16_widened and launch (split partial sums); any
+// workspace the library carves is 256-byte aligned, which is what the
+// alignment of the plans that run on workspaces is computed with.
+size_t up256(size_t b) { return (b + 255) / 256 * 256; }
+
+size_t split_need(const Geom& g) {
+  return g.split > 1 ? up256((size_t)g.split * g.N * g.K * g.P * g.Q * sizeof(float)) : 0;
+}
+
+int selected_need(const Shape& s, int dtype, int align, size_t* need) {
+  Entry e;
+  int st = cached_entry(s, dtype, align, &e);
+  if (st == CONV_ENOPLAN && dtype == CONV_DTYPE_BF16) {
+    // run_bf16_widened: exact fp32 copies of In and Ker, then the fp32 plan
+    const size_t n_in = (size_t)s.N * s.C * s.H * s.W, n_ker = (size_t)s.K * s.C * s.R * s.S;
+    const size_t wide = up256(up256(n_in * 4) + up256(n_ker * 4));
+    st = cached_entry(s, CONV_DTYPE_F32, ALIGN_ALL, &e);
+    if (st != CONV_OK) return st;
+    *need = wide + split_need(e.g);
+    return CONV_OK;
+  }
+  if (st != CONV_OK) return st;
+  *need = split_need(e.g);
+  return CONV_OK;
+}
+
+int ex_need(const PhaseGeom& p, int dtype, const void* In, const void* Ker, size_t* need) {
+  const Shape s{p.N, p.C, p.K, p.H, p.W, p.R, p.S};
+  if (p.sh == 1 && p.sw == 1 && p.ph == 0 && p.pw == 0) return selected_need(s, dtype, alignment_of(In, Ker), need);
+  const size_t e = dtype == CONV_DTYPE_BF16 ? 2 : 4;
+  const int Cp = p.C * p.na * p.nb;
+  const bool ker_moves = p.na * p.nb > 1;
+  const Shape inner{p.N, Cp, p.K, p.Hp, p.Wp, p.Rp, p.Sp};
+  if (dtype == CONV_DTYPE_F32) {
+    const int ker_al = ker_moves ? ALIGN_KER : (alignment_of(In, Ker) & ALIGN_KER);
+    const int al_direct = (alignment_of(In, Ker) & (ALIGN_IN | ALIGN_IN4)) | ker_al;
+    const int al_split = ALIGN_IN | ALIGN_IN4 | ker_al;
+    ExEntry x;
+    const int st = cached_ex_entry(p, al_direct, al_split, &x);
+    if (st != CONV_OK) return st;
+    const size_t in_ws = x.direct ? 0 : up256((size_t)p.N * Cp * p.Hp * p.Wp * e);
+    const size_t ker_ws = ker_moves ? (size_t)p.K * Cp * p.Rp * p.Sp * e : 0;
+    *need = (in_ws + ker_ws ? up256(in_ws + ker_ws) : 0) + split_need(x.e.g);
+    return CONV_OK;
+  }
+  const size_t in_bytes = up256((size_t)p.N * Cp * p.Hp * p.Wp * e);
+  const size_t ker_bytes = ker_moves ? (size_t)p.K * Cp * p.Rp * p.Sp * e : 0;
+  // the inner plan runs on the (aligned) phase images and the rearranged or
+  // the caller's Ker
+  const int align = ALIGN_IN | ALIGN_IN4 | (ker_moves ? ALIGN_KER : (alignment_of(In, Ker) & ALIGN_KER));
+  size_t inner_need = 0;
+  const int st = selected_need(inner, dtype, align, &inner_need);
+  if (st != CONV_OK) return st;
+  *need = up256(in_bytes + ker_bytes) + inner_need;
+  return CONV_OK;
+}
+
+// Installs an arena on the calling thread for the lifetime of the guard.
+struct ArenaGuard {
+  explicit ArenaGuard(ScratchArena* a) { set_thread_arena(a); }
+  ~ArenaGuard() { set_thread_arena(nullptr); }
+};
+
+}  // namespace
+
+extern "C" {
+
+int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w, int pad_h,
+                int pad_w, int dtype, const void* In, const void* Ker, float* Out, void* stream) {
+  PhaseGeom p;
+  const int st = phase_geom(N, C, K, H, W, R, S, stride_h, stride_w, pad_h, pad_w, &p);
+  if (st != CONV_OK) return st;
+  if (!In || !Ker || !Out) return CONV_ENULL;
+  if (dtype != CONV_DTYPE_F32 && dtype != CONV_DTYPE_BF16) return CONV_EINVAL;
+  return run_ex(p, dtype, In, Ker, Out, stream);
+}
+
+int conv_fwd_ex_noalloc(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w, int pad_h,
+                        int pad_w, int dtype, const void* In, const void* Ker, float* Out, void* stream) {
+  PhaseGeom p;
+  int st = phase_geom(N, C, K, H, W, R, S, stride_h, stride_w, pad_h, pad_w, &p);
+  if (st != CONV_OK) return st;
+  if (!In || !Ker || !Out) return CONV_ENULL;
+  if (dtype != CONV_DTYPE_F32 && dtype != CONV_DTYPE_BF16) return CONV_EINVAL;
+  size_t need = 0;
+  st = ex_need(p, dtype, In, Ker, &need);
+  if (st != CONV_OK) return st;
+  if (need > (size_t)CONV_NOALLOC_SCRATCH_BYTES) return CONV_ESCRATCH;
+  void* base = nullptr;
+  if (need > 0) {
+    st = noalloc_scratch(&base);
+    if (st != CONV_OK) return st;
+  }
+  ScratchArena arena{static_cast<char*>(base), need > 0 ? (size_t)CONV_NOALLOC_SCRATCH_BYTES : 0, 0};
+  ArenaGuard guard(&arena);
+  return run_ex(p, dtype, In, Ker, Out, stream);
 }
 
 int conv_fwd_ex_plan(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w, int pad_h,
@@ -498,6 +600,7 @@ const char* conv_fwd_strerror(int status) {
     case CONV_ERANGE: return "tensor too large (2^31 elements or more)";
     case CONV_ENOPLAN: return "no kernel configuration fits this shape";
     case CONV_EHIP: return "HIP runtime error at launch";
+    case CONV_ESCRATCH: return "the call needs more scratch than the allocation-free entry point holds";
     default: return "unknown status";
   }
 }

@@ -122,10 +122,23 @@ int stream_free(void* p, void* stream);
 struct Workspace {
   void* ptr = nullptr;
   bool cached = false;
+  bool arena = false;  // carved from the calling thread's ScratchArena
   int level = 0;
 };
 int workspace_acquire(int level, size_t bytes, void* stream, Workspace* w);
 int workspace_release(const Workspace& w, void* stream);
+// Allocation-free calls: while an arena is installed on the calling thread,
+// workspace_acquire carves every workspace from it (bump allocation,
+// 256-byte aligned; CONV_ESCRATCH when it is full) and release is a no-op.
+struct ScratchArena {
+  char* base;
+  size_t cap;
+  size_t used;
+};
+void set_thread_arena(ScratchArena* a);
+// Device address of the current device's copy of the library's static
+// scratch array (CONV_NOALLOC_SCRATCH_BYTES), looked up once per device.
+int noalloc_scratch(void** base);
 // Phase-split In into Inp (Inp non-null) and Ker into Kp (Kp non-null), on
 // `stream`.
 int launch_phase_split(const PhaseGeom& p, int dtype, const void* In, const void* Ker, void* Inp, void* Kp,

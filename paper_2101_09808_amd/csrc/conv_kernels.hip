@@ -1811,8 +1811,9 @@ int allow_dynamic_lds(const void* fn) {
 // which keeps up to 1 GB of freed blocks for reuse (the default pool hands
 // freed memory back at each synchronisation, so every call would map fresh
 // pages).  The calling thread's current device must own the stream.
+constexpr int kMaxDevices = 64;
+
 int stream_alloc(size_t bytes, void* stream, void** out) {
-  constexpr int kMaxDevices = 64;
   static std::mutex mu;
   static hipMemPool_t pools[kMaxDevices] = {};
   int dev = 0;
@@ -1841,6 +1842,30 @@ int stream_free(void* p, void* stream) {
   return hipFreeAsync(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? CONV_OK : CONV_EHIP;
 }
 
+// ---------------------------------------------------------------------------
+// Scratch of the allocation-free entry point: a static device array.  Every
+// GPU that loads the library's code object holds its own copy (at its own
+// address) until the process ends.  Host code must not use the array's name
+// as a device address (on the host it names a host-side stand-in); it uses
+// the per-device address that hipGetSymbolAddress reports, taken once per
+// device with that device current.
+static __device__ __align__(256) char scratch[CONV_NOALLOC_SCRATCH_BYTES];
+
+int noalloc_scratch(void** base) {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return CONV_EHIP;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return CONV_EHIP;
+    addr[dev] = p;
+  }
+  *base = addr[dev];
+  return CONV_OK;
+}
+
 namespace {
 // Workspaces kept per (device, stream, nesting level): the kernels of the
 // calls on one stream run in stream order, so a call can reuse the buffer
@@ -1854,13 +1879,28 @@ struct CachedWorkspace {
 };
 std::mutex g_ws_mu;
 std::map<std::tuple<int, void*, int>, CachedWorkspace> g_ws;
+
+// The arena of the calling thread's allocation-free call, if one is running.
+thread_local ScratchArena* t_arena = nullptr;
 }  // namespace
 
+void set_thread_arena(ScratchArena* a) { t_arena = a; }
+
 int workspace_acquire(int level, size_t bytes, void* stream, Workspace* w) {
+  w->cached = false;
+  w->arena = false;
+  w->level = level;
+  if (t_arena) {
+    // bump allocation from the caller's scratch, 256-byte aligned
+    const size_t off = (t_arena->used + 255) / 256 * 256;
+    if (off > t_arena->cap || bytes > t_arena->cap - off) return CONV_ESCRATCH;
+    w->ptr = t_arena->base + off;
+    w->arena = true;
+    t_arena->used = off + bytes;
+    return CONV_OK;
+  }
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return CONV_EHIP;
-  w->cached = false;
-  w->level = level;
   {
     std::lock_guard<std::mutex> lk(g_ws_mu);
     CachedWorkspace& c = g_ws[std::make_tuple(dev, stream, level)];
@@ -1883,6 +1923,7 @@ int workspace_acquire(int level, size_t bytes, void* stream, Workspace* w) {
 }
 
 int workspace_release(const Workspace& w, void* stream) {
+  if (w.arena) return CONV_OK;
   if (!w.cached) return stream_free(w.ptr, stream);
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return CONV_EHIP;
@@ -2003,7 +2044,8 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
     // stream-ordered workspace, then the fixed-order sum into Out.
     const int64_t n = (int64_t)g.N * g.K * g.P * g.Q;
     Workspace w;
-    if (workspace_acquire(2, (size_t)g.split * n * sizeof(float), stream, &w) != CONV_OK) return CONV_EHIP;
+    const int got = workspace_acquire(2, (size_t)g.split * n * sizeof(float), stream, &w);
+    if (got != CONV_OK) return got;
     float* ws = static_cast<float*>(w.ptr);
     hipLaunchKernelGGL(inst->f32, dim3(g.grid), dim3(v.threads), lds_bytes, st,
                        static_cast<const float*>(In), static_cast<const float*>(Ker), ws, g);
@@ -2058,8 +2100,8 @@ int time_launches(const Variant& v, const Geom& g, const void* In, const void* K
   // from HBM, as in a network where every call has new data) and between its
   // own two events; all of it queued behind a delay of 300 us per launch, so
   // host time between launches does not count.
-  void* scratch = nullptr;
-  if (stream_alloc(kEvictBytes, stream, &scratch) != CONV_OK) return CONV_EHIP;
+  void* evict_buf = nullptr;
+  if (stream_alloc(kEvictBytes, stream, &evict_buf) != CONV_OK) return CONV_EHIP;
   std::vector<hipEvent_t> ev(2 * (size_t)reps, nullptr);
   for (auto& e : ev)
     if (rc == CONV_OK && hipEventCreate(&e) != hipSuccess) rc = CONV_EHIP;
@@ -2068,14 +2110,14 @@ int time_launches(const Variant& v, const Geom& g, const void* In, const void* K
     if (hipGetLastError() != hipSuccess) rc = CONV_EHIP;
   }
   for (int i = 0; rc == CONV_OK && i < reps; ++i) {
-    hipLaunchKernelGGL(evict_kernel, dim3(2048), dim3(256), 0, st, static_cast<const v4f*>(scratch),
-                       (int64_t)(kEvictBytes / sizeof(v4f)), static_cast<float*>(scratch));
+    hipLaunchKernelGGL(evict_kernel, dim3(2048), dim3(256), 0, st, static_cast<const v4f*>(evict_buf),
+                       (int64_t)(kEvictBytes / sizeof(v4f)), static_cast<float*>(evict_buf));
     if (hipGetLastError() != hipSuccess) rc = CONV_EHIP;
     if (rc == CONV_OK && hipEventRecord(ev[2 * i], st) != hipSuccess) rc = CONV_EHIP;
     if (rc == CONV_OK) rc = launch(v, g, In, Ker, Out, stream);
     if (rc == CONV_OK && hipEventRecord(ev[2 * i + 1], st) != hipSuccess) rc = CONV_EHIP;
   }
-  const bool freed = hipFreeAsync(scratch, st) == hipSuccess;
+  const bool freed = hipFreeAsync(evict_buf, st) == hipSuccess;
   if (rc == CONV_OK && !freed) rc = CONV_EHIP;
   if (rc == CONV_OK && hipEventSynchronize(ev[2 * reps - 1]) != hipSuccess) rc = CONV_EHIP;
   std::vector<float> t(reps, 0.f);
