@@ -36,6 +36,9 @@ sys.path.insert(0, ROOT)
 PEAK = {"fp32_mfma_tflops": 157.3, "bf16_mfma_tflops": 2516.6, "hbm_gbs": 8000.0}
 HEADLINE = "conv1x1_n32_c256_k64_in56"
 MALL_BYTES = 256 * 2 ** 20
+FLUSH_BYTES = 512 * 2 ** 20  # read between timed runs: twice the last-level cache
+PROTOCOL_RUNS = 50           # timed runs per layer (Sec. 10: 50 runs, the first excluded)
+RAMP_S = 0.1                 # back-to-back launches before any timing, independent of --warmup
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_conv1x1_n32_c256_k64_in56.json")
 
 
@@ -86,68 +89,219 @@ def plan_kernel_hash(c, plan):
     return h.hexdigest()[:16]
 
 
-def time_layer(c, steps, warmup, queued=False, out_bf16=False):
-    """Average launch duration from HIP events recorded on the launch stream
-    around the `steps` back-to-back launches of the timed region (rotating
-    buffer sets), and the host wall time of the same region.  queued: the
-    launches first queue up behind a bounded spin kernel, so that for layers
-    shorter than the host's per-call time the events still see back-to-back
-    kernels (the wall time then includes the spin)."""
-    import torch
-    from paper_2101_09808_amd import conv as B
-    from paper_2101_09808_amd.workloads import make_inputs
+class LayerRunner:
+    """Device buffers and a raw-pointer launcher for one layer: In/Out buffer
+    sets rotate (more than twice the 256 MB last-level cache in all) so that
+    back-to-back launches read In from HBM and write Out to HBM."""
 
-    In0, Ker0 = make_inputs(c)
-    set_bytes = In0.numel() * In0.element_size() + c.N * c.K * c.P * c.Q * 4
-    nsets = max(2, -(-2 * MALL_BYTES // set_bytes) + 1)
-    dev = torch.device("cuda:0")
-    Ker = Ker0.to(dev)
-    ins = [In0.to(dev) for _ in range(nsets)]
-    odt = torch.bfloat16 if out_bf16 else torch.float32
-    outs = [torch.empty(c.N, c.K, c.P, c.Q, device=dev, dtype=odt) for _ in range(nsets)]
-    bf16 = c.dtype == "bf16"
-    stream = torch.cuda.current_stream()
-    sp = stream.cuda_stream
-    kp = Ker.data_ptr()
-    ips = [t.data_ptr() for t in ins]
-    ops = [t.data_ptr() for t in outs]
+    def __init__(self, c, out_bf16=False):
+        import torch
+        from paper_2101_09808_amd import conv as B
+        from paper_2101_09808_amd.workloads import make_inputs
 
-    strided = c.stride != 1 or c.pad != 0
-    L = B.lib()
-    dt = B.CONV_DTYPE_BF16 if bf16 else B.CONV_DTYPE_F32
+        self.c = c
+        In0, Ker0 = make_inputs(c)
+        set_bytes = In0.numel() * In0.element_size() + c.N * c.K * c.P * c.Q * 4
+        self.nsets = max(2, -(-2 * MALL_BYTES // set_bytes) + 1)
+        dev = torch.device("cuda:0")
+        self.Ker = Ker0.to(dev)
+        self.ins = [In0.to(dev) for _ in range(self.nsets)]
+        odt = torch.bfloat16 if out_bf16 else torch.float32
+        self.outs = [torch.empty(c.N, c.K, c.P, c.Q, device=dev, dtype=odt) for _ in range(self.nsets)]
+        bf16 = c.dtype == "bf16"
+        self.stream = torch.cuda.current_stream()
+        sp = self.stream.cuda_stream
+        kp = self.Ker.data_ptr()
+        ips = [t.data_ptr() for t in self.ins]
+        ops = [t.data_ptr() for t in self.outs]
+        strided = c.stride != 1 or c.pad != 0
+        L = B.lib()
+        dt = B.CONV_DTYPE_BF16 if bf16 else B.CONV_DTYPE_F32
 
-    def fn(i):
+        def fn(i):
+            if out_bf16:
+                st = L.conv_fwd_bf16_out(*c.key(), ips[i], kp, ops[i], sp)
+            elif strided:
+                st = L.conv_fwd_ex(*c.key(), c.stride, c.stride, c.pad, c.pad, dt, ips[i], kp, ops[i], sp)
+            else:
+                st = B.conv_fwd_ptr(*c.key(), ips[i], kp, ops[i], sp, bf16)
+            if st != B.CONV_OK:
+                raise B.ConvError(st, "conv_fwd")
+
+        self.fn = fn
+        # checked call through the tensor API first
         if out_bf16:
-            st = L.conv_fwd_bf16_out(*c.key(), ips[i], kp, ops[i], sp)
+            B.conv_fwd_bf16_out(self.ins[0], self.Ker, out=self.outs[0])
         elif strided:
-            st = L.conv_fwd_ex(*c.key(), c.stride, c.stride, c.pad, c.pad, dt, ips[i], kp, ops[i], sp)
+            B.conv_fwd_ex(self.ins[0], self.Ker, c.stride, c.pad, out=self.outs[0])
         else:
-            st = B.conv_fwd_ptr(*c.key(), ips[i], kp, ops[i], sp, bf16)
-        if st != B.CONV_OK:
-            raise B.ConvError(st, "conv_fwd")
+            (B.conv_fwd_bf16 if bf16 else B.conv_fwd)(self.ins[0], self.Ker, out=self.outs[0])
+        torch.cuda.synchronize()
 
-    fn(0)  # checked call through the tensor API first
-    if out_bf16:
-        B.conv_fwd_bf16_out(ins[0], Ker, out=outs[0])
-    elif strided:
-        B.conv_fwd_ex(ins[0], Ker, c.stride, c.pad, out=outs[0])
-    else:
-        (B.conv_fwd_bf16 if bf16 else B.conv_fwd)(ins[0], Ker, out=outs[0])
-    for i in range(warmup):
-        fn(i % nsets)
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    def ramp(self, seconds=RAMP_S):
+        """Launch back to back for a fixed wall time, whatever --warmup says,
+        so that the clocks have left their idle state before timing."""
+        import torch
+        t0 = time.perf_counter()
+        i = 0
+        while time.perf_counter() - t0 < seconds:
+            for _ in range(16):
+                self.fn(i % self.nsets)
+                i += 1
+            torch.cuda.synchronize()
+        return i
+
+    def back_to_back(self, steps, warmup, queued=False):
+        """Average launch duration from HIP events recorded on the launch
+        stream around `steps` back-to-back launches (rotating buffer sets),
+        and the host wall time of the same region.  queued: the launches first
+        queue up behind a bounded spin kernel, so that for layers shorter than
+        the host's per-call time the events still see back-to-back kernels
+        (the wall time then includes the spin)."""
+        import torch
+        for i in range(warmup):
+            self.fn(i % self.nsets)
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        if queued:
+            torch.cuda._sleep(int(sleep_cycles_per_us() * 60 * steps))
+        start.record(self.stream)
+        for i in range(steps):
+            self.fn(i % self.nsets)
+        end.record(self.stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ev_ms = start.elapsed_time(end)
+        return dict(mean_kernel_ms=ev_ms / steps, wall_ms_per_step=wall * 1e3 / steps, buffer_sets=self.nsets)
+
+    def cold_runs(self, flush, runs=PROTOCOL_RUNS):
+        """The paper's protocol (Sec. 10): one untimed run, then `runs` runs,
+        each after a read pass over a 512 MB buffer (twice the last-level
+        cache: In, Ker and Out start in HBM) and between its own two HIP
+        events on the launch stream.  Returns the per-run times in us."""
+        import torch
+        self.fn(0)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(runs)]
+        sink = torch.empty((), device=flush.device)
+        for i, (a, b) in enumerate(evs):
+            torch.sum(flush, 0, out=sink)
+            a.record(self.stream)
+            self.fn(i % self.nsets)
+            b.record(self.stream)
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) * 1e3 for a, b in evs]
+
+
+def summary(ts):
+    """Mean, median, standard deviation and 95% confidence half-width of the
+    mean (Student t) of per-run times in us."""
+    import statistics
+
+    from scipy import stats
+
+    n = len(ts)
+    mean = statistics.fmean(ts)
+    sd = statistics.stdev(ts) if n > 1 else 0.0
+    half = float(stats.t.ppf(0.975, n - 1)) * sd / n ** 0.5 if n > 1 else 0.0
+    return {"runs": n, "mean_us": mean, "median_us": statistics.median(ts), "min_us": min(ts), "max_us": max(ts),
+            "std_us": sd, "ci95_us": [mean - half, mean + half]}
+
+
+def flush_buffer():
+    import torch
+    return torch.ones(FLUSH_BYTES // 4, device="cuda:0")
+
+
+def empty_kernel_floor(flush, runs=PROTOCOL_RUNS):
+    """Event-timed duration of a kernel that does nothing (torch's bounded
+    spin kernel asked to spin for 0 cycles), measured exactly as cold_runs
+    times a layer: the fixed cost any single launch pays between its events."""
+    import torch
+    stream = torch.cuda.current_stream()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(runs)]
+    sink = torch.empty((), device="cuda:0")
+    torch.cuda._sleep(0)
+    for a, b in evs:
+        torch.sum(flush, 0, out=sink)
+        a.record(stream)
+        torch.cuda._sleep(0)
+        b.record(stream)
     torch.cuda.synchronize()
+    cold = summary([a.elapsed_time(b) * 1e3 for a, b in evs])
+    # back to back, amortised (100 launches queued behind a spin)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(int(sleep_cycles_per_us() * 2000))
+    a.record(stream)
+    for _ in range(100):
+        torch.cuda._sleep(0)
+    b.record(stream)
+    torch.cuda.synchronize()
+    return {"cold": cold, "back_to_back_us": a.elapsed_time(b) * 1e3 / 100}
+
+
+def observed_sclk(runner, seconds=2.0):
+    """Shader clock observed while the layer runs back to back: amd-smi (or
+    rocm-smi) sampled from a helper thread during `seconds` of launches.
+    Returns the samples in MHz and the tool used, or the reason none was read."""
+    import re
+    import shutil
+    import subprocess
+    import threading
+
+    import torch
+
+    cmds = []
+    if shutil.which("amd-smi"):
+        cmds.append(["amd-smi", "metric", "-g", "0", "-c"])
+    if shutil.which("rocm-smi"):
+        cmds.append(["rocm-smi", "-d", "0", "--showclocks"])
+    if not cmds:
+        return {"mhz": None, "tool": None, "note": "no amd-smi or rocm-smi on this host"}
+    samples, used, errors = [], [], []
+    stop = threading.Event()
+
+    def sample():
+        while not stop.is_set():
+            for cmd in cmds:
+                try:
+                    r = subprocess.run(cmd, capture_output=True, text=True, timeout=10)
+                except (OSError, subprocess.SubprocessError) as e:
+                    errors.append(f"{cmd[0]}: {e}")
+                    continue
+                txt = r.stdout
+                if cmd[0] == "amd-smi":  # one GFX_i clock per XCD: their mean
+                    v = [float(x) for x in re.findall(r"GFX_\d+:\s*CLK:\s*([0-9.]+)\s*MHz", txt)]
+                else:
+                    v = [float(x) for x in re.findall(r"sclk clock level:.*?\(([0-9.]+)\s*Mhz\)", txt, flags=re.I)]
+                if v:
+                    samples.append(sum(v) / len(v))
+                    used.append(cmd[0])
+                    break
+                errors.append(f"{cmd[0]}: no clock in output ({txt[:80]!r})")
+
+    th = threading.Thread(target=sample, daemon=True)
+    th.start()
     t0 = time.perf_counter()
-    if queued:
-        torch.cuda._sleep(int(sleep_cycles_per_us() * 60 * steps))
-    start.record(stream)
-    for i in range(steps):
-        fn(i % nsets)
-    end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ev_ms = start.elapsed_time(end)
-    return dict(mean_kernel_ms=ev_ms / steps, wall_ms_per_step=wall * 1e3 / steps, buffer_sets=nsets)
+    i = 0
+    while time.perf_counter() - t0 < seconds or (not samples and time.perf_counter() - t0 < 3 * seconds):
+        for _ in range(32):
+            runner.fn(i % runner.nsets)
+            i += 1
+        torch.cuda.synchronize()
+    stop.set()
+    th.join(timeout=15)
+    if not samples:
+        return {"mhz": None, "tool": None, "note": "; ".join(errors[:2]) or "no sample"}
+    return {"mhz": samples, "tool": used[0], "note": "sampled while the layer ran back to back"}
+
+
+def time_layer(c, steps, warmup, queued=False, out_bf16=False):
+    """Back-to-back timing of one layer (LayerRunner.back_to_back) after the
+    fixed clock ramp."""
+    r = LayerRunner(c, out_bf16=out_bf16)
+    r.ramp()
+    return r.back_to_back(steps, warmup, queued)
 
 
 COPY_BYTES = 256 * 2 ** 20  # plain device-to-device copy used to scale the HBM byte counters
@@ -321,6 +475,7 @@ def model_check_parse(layers, dirs, launches=6):
         hbm = m["FETCH_SIZE"]["bytes_per_launch"] + m["WRITE_SIZE"]["bytes_per_launch"]
         l2cu = m["TCP_TCC_READ_REQ_sum"]["bytes_per_launch"]
         rows.append({"workload": c.name, "plan_variant": plan["variant"], "family": fam,
+                     "plan_kernel_sha": plan_kernel_hash(c, plan),
                      "hbm_pred": pb["hbm"], "hbm_meas": hbm, "hbm_ratio": hbm / pb["hbm"],
                      "l2_pred": pb["l2"] + out_bytes, "l2_ratio": hbm / (pb["l2"] + out_bytes),
                      "l2cu_pred": pred_l2cu, "l2cu_meas": l2cu, "l2cu_ratio": l2cu / pred_l2cu,
@@ -613,6 +768,43 @@ def cpu_baseline(c, budget_s=10.0):
                       f"{dt:.2f} s"}
 
 
+def cpu_baseline_one_thread(c):
+    """The oracle on one host thread over the whole layer."""
+    from oracle import conv as oconv
+    from paper_2101_09808_amd.workloads import make_inputs
+
+    In, Ker = make_inputs(c)
+    In, Ker = In.float().numpy(), Ker.float().numpy()
+    prev = oconv.set_num_threads(1)
+    try:
+        t0 = time.perf_counter()
+        oconv.conv_fwd(In, Ker)
+        dt = time.perf_counter() - t0
+        cores = oconv.num_threads()
+    finally:
+        oconv.set_num_threads(prev)
+    return {"value": flops(c) / dt / 1e9, "unit": "GFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"all of {c.name}, one pass (fp64 plain loops), {dt:.2f} s"}
+
+
+def layer_counters():
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated) of each
+    layer from the last counter passes, keyed by (layer, plan_kernel_hash):
+    a figure is reported only for the plan and kernel source it was taken on."""
+    path = MODEL_CHECK_FILE + ".json"
+    if not os.path.exists(path):
+        return {}
+    d = json.load(open(path))
+    out = {}
+    for row in d.get("layers", []):
+        h = row.get("plan_kernel_sha")
+        if h and "fetch_bytes" in row:
+            out[(row["workload"], h)] = {"fetch_bytes": row["fetch_bytes"], "write_bytes": row["write_bytes"],
+                                        "hbm_bytes": row["fetch_bytes"] + row["write_bytes"],
+                                        "ratio_to_alg": row.get("hbm_ratio")}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -683,7 +875,13 @@ def main():
 
     dtype_code = B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32
     plan = B.conv_fwd_plan(*c.key(), dtype=dtype_code)
-    r = time_layer(c, args.steps, args.warmup)
+    runner = LayerRunner(c)
+    ramp_launches = runner.ramp()
+    r = runner.back_to_back(args.steps, args.warmup)
+    flush = flush_buffer()
+    cold = summary(runner.cold_runs(flush))
+    sclk = observed_sclk(runner)
+    del runner
     F, Bt = flops(c), alg_bytes(c)
     ms = r["wall_ms_per_step"]
     value = F / (ms * 1e-3) / 1e9
@@ -719,15 +917,27 @@ def main():
                                                  "grid_order", "num_wg")}},
         "pct_fp32_mfma_peak": 100.0 * F / kern_s / 1e12 / PEAK["fp32_mfma_tflops"],
         "roofline": roof,
+        "ramp": {"seconds": RAMP_S, "launches": ramp_launches},
+        "protocol": {"cold": cold, "gflops_at_mean": F / (cold["mean_us"] * 1e-6) / 1e9,
+                     "pct_fp32_mfma_peak_at_mean": 100 * F / (cold["mean_us"] * 1e-6) / 1e12 / PEAK["fp32_mfma_tflops"],
+                     "note": f"1 untimed + {PROTOCOL_RUNS} runs, each after a read pass over "
+                             f"{FLUSH_BYTES >> 20} MB and between its own HIP events"},
+        "sclk": sclk,
     }
+    out["empty_kernel_floor"] = empty_kernel_floor(flush)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(c)
+        out["cpu_baseline_1thread"] = cpu_baseline_one_thread(CONFIGS[0])
     if not args.no_layers:
         layers = {}
         # the bf16 layer with bf16 Out (conv_fwd_bf16_out): half the write
         # traffic; timed before the tuning below replaces any cached plan
         c5 = [lc for lc in CONFIGS if lc.dtype == "bf16"][0]
-        lk = time_layer(c5, 50, 5, queued=True, out_bf16=True)["mean_kernel_ms"] * 1e-3
+        lr5 = LayerRunner(c5, out_bf16=True)
+        lr5.ramp()
+        lk = lr5.back_to_back(50, 5, queued=True)["mean_kernel_ms"] * 1e-3
+        cold5 = summary(lr5.cold_runs(flush))
+        del lr5
         ab = alg_bytes(c5) - c5.N * c5.K * c5.P * c5.Q * 2
         bf16out_row = {
             "dtype": "bf16", "out_dtype": "bf16", "variant": B.conv_fwd_plan(*c5.key(), dtype=B.CONV_DTYPE_BF16)["variant"],
@@ -735,24 +945,37 @@ def main():
             "pct_fp32_mfma_peak": 100 * flops(c5) / lk / 1e12 / PEAK["fp32_mfma_tflops"],
             "pct_dtype_mfma_peak": 100 * flops(c5) / lk / 1e12 / PEAK["bf16_mfma_tflops"],
             "alg_hbm_gbs": ab / lk / 1e9, "pct_hbm_peak": 100 * ab / lk / 1e9 / PEAK["hbm_gbs"],
+            "cold": cold5,
         }
+        counters = layer_counters()
         for lc in CONFIGS:
             try:
-                lr = time_layer(lc, 50, 5, queued=True)
+                lrun = LayerRunner(lc)
             except B.ConvError as e:
                 layers[lc.name] = {"error": str(e)}
                 continue
+            lrun.ramp()
+            lr = lrun.back_to_back(50, 5, queued=True)
+            lcold = summary(lrun.cold_runs(flush))
+            del lrun
             lk = lr["mean_kernel_ms"] * 1e-3
             lpeak = PEAK["bf16_mfma_tflops"] if lc.dtype == "bf16" else PEAK["fp32_mfma_tflops"]
             lplan = B.conv_fwd_plan(*lc.key(), dtype=B.CONV_DTYPE_BF16 if lc.dtype == "bf16" else B.CONV_DTYPE_F32)
             layers[lc.name] = {
                 "dtype": lc.dtype, "variant": lplan["variant"], "split_c": lplan["split_c"],
+                "num_wg": lplan["num_wg"],
                 "kernel_us": lk * 1e6, "gflops": flops(lc) / lk / 1e9,
                 "pct_fp32_mfma_peak": 100 * flops(lc) / lk / 1e12 / PEAK["fp32_mfma_tflops"],
                 "pct_dtype_mfma_peak": 100 * flops(lc) / lk / 1e12 / lpeak,
                 "alg_hbm_gbs": alg_bytes(lc) / lk / 1e9,
                 "pct_hbm_peak": 100 * alg_bytes(lc) / lk / 1e9 / PEAK["hbm_gbs"],
+                "cold": lcold,
+                "cold_pct_fp32_mfma_peak_at_mean": 100 * flops(lc) / (lcold["mean_us"] * 1e-6) / 1e12
+                / PEAK["fp32_mfma_tflops"],
+                "traffic": counters.get((lc.name, plan_kernel_hash(lc, lplan))),
             }
+            if not args.no_cpu:
+                layers[lc.name]["cpu_oracle"] = cpu_baseline(lc, budget_s=3.0)
             # Sec. 10 MOpt-5: the fastest of the model's top 5 plans, kept as
             # the shape's plan by conv_fwd_tune, timed the same way
             In_t, Ker_t = make_inputs(lc)
@@ -762,12 +985,17 @@ def main():
             layers[lc.name].update({"mopt5_variant": tplan["variant"], "mopt5_split_c": tplan["split_c"],
                                     "mopt5_kernel_us": tk * 1e6, "mopt5_gflops": flops(lc) / tk / 1e9,
                                     "mopt5_pct_hbm_peak": 100 * alg_bytes(lc) / tk / 1e9 / PEAK["hbm_gbs"]})
+            torch.cuda.empty_cache()
         layers[c5.name + "_bf16out"] = bf16out_row
         # strided, padded Table 1 layers (conv_fwd_ex: the selected stride-1
         # plan of the polyphase inner problem, reading In through the phase
         # mapping where its kernel can), timed the same way
         for lc in STRIDED_CONFIGS:
-            lk = time_layer(lc, 50, 5, queued=True)["mean_kernel_ms"] * 1e-3
+            lrun = LayerRunner(lc)
+            lrun.ramp()
+            lk = lrun.back_to_back(50, 5, queued=True)["mean_kernel_ms"] * 1e-3
+            lcold = summary(lrun.cold_runs(flush))
+            del lrun
             inner = B.conv_fwd_ex_inner_shape(*lc.key(), lc.stride, lc.pad)
             lplan, ldirect = B.conv_fwd_ex_plan(*lc.key(), lc.stride, lc.pad)
             layers[lc.name] = {
@@ -778,7 +1006,9 @@ def main():
                 "pct_fp32_mfma_peak": 100 * flops(lc) / lk / 1e12 / PEAK["fp32_mfma_tflops"],
                 "alg_hbm_gbs": alg_bytes(lc) / lk / 1e9,
                 "pct_hbm_peak": 100 * alg_bytes(lc) / lk / 1e9 / PEAK["hbm_gbs"],
+                "cold": lcold,
             }
+            torch.cuda.empty_cache()
         out["per_layer"] = layers
     print(json.dumps(out), flush=True)
 

@@ -26,8 +26,13 @@
  * The workspaces of the compute calls are kept per device, stream and
  * nesting level and reused by the next call on that stream (stream order
  * makes that safe); each grows to the largest size a call on that stream
- * needed and is held until the process ends.  A call that finds its buffer
- * held by another host thread takes and returns a fresh one in stream order.
+ * needed and is held until conv_fwd_release_workspaces(stream) frees it or
+ * the process ends.  Call conv_fwd_release_workspaces before destroying a
+ * stream: a buffer kept for a destroyed stream stays held, and a new stream
+ * that gets the same handle value would reuse it in its own stream order,
+ * which is safe only once the old stream's work has finished.  A call that
+ * finds its buffer held by another host thread takes and returns a fresh one
+ * in stream order.  conv_fwd_ex_noalloc allocates nothing (see there).
  * The calling thread's current device must own the stream.
  * In, Ker and Out must not overlap.
  *
@@ -36,7 +41,12 @@
  * CONV_OK means the launch was enqueued; faults inside the kernel surface at
  * the caller's next synchronisation.
  *
- * Errors: on any error the call launches nothing and leaves Out untouched.
+ * Errors: argument and plan validation errors (CONV_EINVAL, CONV_ENULL,
+ * CONV_ERANGE, CONV_ENOPLAN, CONV_ESCRATCH) are reported before anything is
+ * launched, and Out is untouched.  A call that runs several kernels (the
+ * strided rewrite, bf16 widening or bf16 Out staging, split reductions) can
+ * return CONV_EHIP after an earlier kernel of the call was enqueued; Out is
+ * then unspecified.
  * Thread safety: all entry points are reentrant.
  */
 #ifndef CONV_FWD_H
@@ -215,8 +225,10 @@ int conv_fwd_plan(int N, int C, int K, int H, int W, int R, int S, int dtype,
 /*
  * Forward convolution with an explicit plan (as returned by conv_fwd_plan,
  * possibly with other tile fields, e.g. for model-validation sweeps).  The
- * plan is re-validated: only its dtype, variant, tile_* , wave_*, waves_* and
- * grid_order fields are read; the rest is recomputed.  `In`/`Ker` are fp32
+ * plan is re-validated: only its dtype, variant, tile_* , wave_*, waves_*,
+ * grid_order and split_c fields are read; the rest is recomputed.  A split_c
+ * above 1 runs the split reduction with its workspace of split_c x |Out|
+ * floats.  `In`/`Ker` are fp32
  * or bf16 per plan->dtype.  Returns CONV_EINVAL for a plan the kernels cannot
  * run -- including a plan whose vector loads need 16-byte aligned In or Ker
  * when the tensors passed are not -- else as conv_fwd.
@@ -334,6 +346,14 @@ int conv_fwd_ex_geometry(int N, int C, int K, int H, int W, int R, int S, int st
  */
 int conv_fwd_ex_plan(int N, int C, int K, int H, int W, int R, int S, int stride_h, int stride_w, int pad_h,
                      int pad_w, int dtype, conv_plan_t* plan_out, int32_t* direct);
+
+/*
+ * Frees, in the order of `stream` (hipFreeAsync), the workspaces the compute
+ * calls keep for that stream on the calling thread's current device (see
+ * Ownership).  Call it before destroying a stream the library has used; a
+ * later call on the stream takes a new workspace.  Returns a conv_status_t.
+ */
+int conv_fwd_release_workspaces(void* stream);
 
 /* Static string for a conv_status_t. */
 const char* conv_fwd_strerror(int status);

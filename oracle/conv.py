@@ -47,6 +47,8 @@ def _load():
         lib.oracle_conv_fwd_ex.restype = i32
         lib.oracle_conv_fwd_ex_points.argtypes = [i32] * 11 + [fp, fp, lp, i64, dp]
         lib.oracle_conv_fwd_ex_points.restype = i32
+        lib.oracle_set_num_threads.argtypes = [i32]
+        lib.oracle_set_num_threads.restype = i32
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = i32
         _lib = lib
@@ -96,6 +98,11 @@ def conv_fwd_points(In, Ker, flat_idx):
 
 def num_threads():
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n):
+    """Threads of the oracle's later OpenMP regions; returns the previous count."""
+    return int(_load().oracle_set_num_threads(int(n)))
 
 
 def ex_extents(H, W, R, S, stride, pad):

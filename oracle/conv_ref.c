@@ -175,6 +175,19 @@ int oracle_conv_fwd_ex_points(int N, int C, int K, int H, int W, int R, int S, i
   return 0;
 }
 
+/* Sets the number of host threads later OpenMP regions of this library use
+   (n >= 1); returns the previous number. */
+int oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  const int prev = omp_get_max_threads();
+  if (n >= 1) omp_set_num_threads(n);
+  return prev;
+#else
+  (void)n;
+  return 1;
+#endif
+}
+
 /* Number of host threads an OpenMP region of this library would use. */
 int oracle_num_threads(void) {
 #ifdef _OPENMP

@@ -98,10 +98,20 @@ def lib():
         L.conv_fwd_ex_geometry.restype = _i32
         L.conv_fwd_ex_plan.argtypes = shape7 + [_i32] * 5 + [ctypes.POINTER(ConvPlan), ctypes.POINTER(_i32)]
         L.conv_fwd_ex_plan.restype = _i32
+        L.conv_fwd_release_workspaces.argtypes = [_vp]
+        L.conv_fwd_release_workspaces.restype = _i32
         L.conv_fwd_strerror.argtypes = [_i32]
         L.conv_fwd_strerror.restype = ctypes.c_char_p
         _lib = L
     return _lib
+
+
+def release_workspaces(stream=None):
+    """Free the workspaces the library keeps for `stream` (default: the
+    current stream) on the current device, in stream order."""
+    st = lib().conv_fwd_release_workspaces(_stream_ptr(stream))
+    if st != CONV_OK:
+        raise ConvError(st, "conv_fwd_release_workspaces")
 
 
 def strerror(status):

@@ -592,6 +592,8 @@ int conv_fwd_ex_geometry(int N, int C, int K, int H, int W, int R, int S, int st
   return export_geometry(*v, g, lds, out, cap);
 }
 
+int conv_fwd_release_workspaces(void* stream) { return workspace_release_stream(stream); }
+
 const char* conv_fwd_strerror(int status) {
   switch (status) {
     case CONV_OK: return "ok";

@@ -127,6 +127,8 @@ struct Workspace {
 };
 int workspace_acquire(int level, size_t bytes, void* stream, Workspace* w);
 int workspace_release(const Workspace& w, void* stream);
+// Frees (stream-ordered) the buffers kept for `stream` on the current device.
+int workspace_release_stream(void* stream);
 // Allocation-free calls: while an arena is installed on the calling thread,
 // workspace_acquire carves every workspace from it (bump allocation,
 // 256-byte aligned; CONV_ESCRATCH when it is full) and release is a no-op.

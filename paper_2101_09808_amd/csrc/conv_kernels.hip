@@ -1932,6 +1932,22 @@ int workspace_release(const Workspace& w, void* stream) {
   return CONV_OK;
 }
 
+int workspace_release_stream(void* stream) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return CONV_EHIP;
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  int rc = CONV_OK;
+  for (auto it = g_ws.begin(); it != g_ws.end();) {
+    if (std::get<0>(it->first) == dev && std::get<1>(it->first) == stream && !it->second.busy) {
+      if (it->second.ptr && stream_free(it->second.ptr, stream) != CONV_OK) rc = CONV_EHIP;
+      it = g_ws.erase(it);
+    } else {
+      ++it;
+    }
+  }
+  return rc;
+}
+
 int launch_phase_split(const PhaseGeom& p, int dtype, const void* In, const void* Ker, void* Inp, void* Kp,
                        void* stream) {
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);

@@ -652,3 +652,23 @@ def test_workspaces_reused_across_calls_and_streams():
         say(f"[gpu] workspace reuse {shape.name} stride={st} pad={pd}")
         ref = oconv.conv_fwd_ex(host(In), host(Ker), st, pd)
         assert rel_err(host(out), ref) <= TOL["f32"], shape.name
+
+
+def test_release_workspaces_then_reuse():
+    """conv_fwd_release_workspaces frees the buffers kept for a stream; the
+    next call on that stream takes a new one and gives the same result."""
+    shape = ConvShape("rel_s2p1", 2, 16, 32, 30, 30, 3, 3, "f32", 85, 2, 1)
+    In, Ker = make_inputs(shape)
+    In_d, Ker_d = In.to(DEV), Ker.to(DEV)
+    st = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    say("[gpu] release workspaces")
+    with torch.cuda.stream(st):
+        a = B.conv_fwd_ex(In_d, Ker_d, shape.stride, shape.pad, stream=st)
+        B.release_workspaces(st)
+        b = B.conv_fwd_ex(In_d, Ker_d, shape.stride, shape.pad, stream=st)
+        B.release_workspaces(st)
+    st.synchronize()
+    assert torch.equal(a, b)
+    ref = oconv.conv_fwd_ex(host(In), host(Ker), (2, 2), (1, 1))
+    assert rel_err(host(a), ref) <= TOL["f32"]
