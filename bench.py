@@ -60,7 +60,8 @@ def kernel_source_hash():
 
 
 KERNEL_FUNCTIONS = {1: "conv_f32_kernel", 2: "conv_f32_dma_kernel", 3: "conv_bf16_kernel",
-                    4: "conv1x1_stream_kernel", 5: "conv1x1_stream_loop_kernel", 6: "conv_bf16_tr_kernel"}
+                    4: "conv1x1_stream_kernel", 5: "conv1x1_stream_loop_kernel", 6: "conv_bf16_tr_kernel",
+                    7: "conv1x1_bal_kernel"}
 
 
 def plan_kernel_hash(c, plan):

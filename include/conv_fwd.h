@@ -311,11 +311,16 @@ int conv_model_volume(const int perm[7], const int64_t N[7], const int64_t T[7],
  *   (0 = none), phases along rows and columns, stride (rows, columns),
  *   padding (rows, columns), the caller's In channels, height and width,
  *   and the inner row width of a 1x1 problem run as one row of pixels per
- *   image (0 otherwise).
+ *   image (0 otherwise); then, for the divisors the kernels' index maps use
+ *   (In channel stride, In row pitch, H, Ker row pitch, tile columns, P,
+ *   phases per channel, phases along columns, the 1x1 inner row width, k
+ *   tiles, column tiles, row tiles), the pair (m as a uint32 bit pattern, s)
+ *   with which the kernels compute n / d as (n * m) >> (31 + s) for
+ *   0 <= n < 2^31 (m = 0: not divided by).
  * Writes min(cap, CONV_GEOM_FIELDS) values and returns CONV_GEOM_FIELDS, or
  * a negative conv_status_t (CONV_EINVAL for a plan the kernels cannot run).
  */
-#define CONV_GEOM_FIELDS 63
+#define CONV_GEOM_FIELDS 87
 int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S,
                       const conv_plan_t* plan, int32_t* out, int cap);
 

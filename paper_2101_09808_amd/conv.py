@@ -317,7 +317,8 @@ GEOM_FIELDS = (
     "family", "in_vec", "stages", "stage_elems", "in_region", "in_bytes", "ker_bytes", "grid",
     "reserved0", "reserved1", "reserved2", "split", "cps", "mfma32", "nwc",
     "nph", "na", "nb", "sh", "sw", "ph", "pw", "C0", "H0", "W0", "Wi",
-)
+) + tuple(f"dv_{d}_{x}" for d in ("in_cstride", "in_wp", "H", "ker_rstride", "tw", "P", "nph", "nb", "Wi",
+                                  "tiles_k", "tiles_cols", "tiles_rows") for x in ("m", "s"))
 
 
 def conv_fwd_geometry(N, C, K, H, W, R, S, plan):
@@ -328,7 +329,15 @@ def conv_fwd_geometry(N, C, K, H, W, R, S, plan):
     st = lib().conv_fwd_geometry(N, C, K, H, W, R, S, ctypes.byref(plan), buf, len(GEOM_FIELDS))
     if st < 0:
         raise ConvError(st, "conv_fwd_geometry")
-    return dict(zip(GEOM_FIELDS, list(buf)[:len(GEOM_FIELDS)]))
+    return _geom_dict(buf)
+
+
+def _geom_dict(buf):
+    d = dict(zip(GEOM_FIELDS, list(buf)[:len(GEOM_FIELDS)]))
+    for k in d:
+        if k.startswith("dv_") and k.endswith("_m"):
+            d[k] &= 0xFFFFFFFF  # multipliers are uint32 bit patterns
+    return d
 
 
 def conv_fwd_ex_plan(N, C, K, H, W, R, S, stride=1, pad=0, dtype=CONV_DTYPE_F32):
@@ -357,4 +366,4 @@ def conv_fwd_ex_geometry(N, C, K, H, W, R, S, stride, pad, plan):
                                     len(GEOM_FIELDS))
     if st < 0:
         raise ConvError(st, "conv_fwd_ex_geometry")
-    return dict(zip(GEOM_FIELDS, list(buf)[:len(GEOM_FIELDS)]))
+    return _geom_dict(buf)

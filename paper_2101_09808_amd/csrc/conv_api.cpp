@@ -247,7 +247,12 @@ int export_geometry(const Variant& vr, const Geom& g, int lds, int32_t* out, int
       v->wk, v->wp, v->tc, v->rc, v->sc, v->max_ni, v->max_nk, v->ker_vec, v->threads, lds,
       v->family, v->in_vec, v->stages, g.stage_elems, g.in_region, (int32_t)g.in_bytes,
       (int32_t)g.ker_bytes, g.grid, 0, 0, 0, g.split, g.cps, v->mfma32, v->groups(),
-      g.nph, g.na, g.nb, g.sh, g.sw, g.ph, g.pw, g.C0, g.H0, g.W0, g.Wi};
+      g.nph, g.na, g.nb, g.sh, g.sw, g.ph, g.pw, g.C0, g.H0, g.W0, g.Wi,
+      (int32_t)g.dv_in_cstride.m, g.dv_in_cstride.s, (int32_t)g.dv_in_wp.m, g.dv_in_wp.s,
+      (int32_t)g.dv_H.m, g.dv_H.s, (int32_t)g.dv_ker_rstride.m, g.dv_ker_rstride.s,
+      (int32_t)g.dv_tw.m, g.dv_tw.s, (int32_t)g.dv_P.m, g.dv_P.s, (int32_t)g.dv_nph.m, g.dv_nph.s,
+      (int32_t)g.dv_nb.m, g.dv_nb.s, (int32_t)g.dv_Wi.m, g.dv_Wi.s, (int32_t)g.dv_tiles_k.m, g.dv_tiles_k.s,
+      (int32_t)g.dv_tiles_cols.m, g.dv_tiles_cols.s, (int32_t)g.dv_tiles_rows.m, g.dv_tiles_rows.s};
   for (int i = 0; i < cap && i < CONV_GEOM_FIELDS; ++i) out[i] = f[i];
   return CONV_GEOM_FIELDS;
 }

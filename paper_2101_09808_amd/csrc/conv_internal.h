@@ -23,6 +23,7 @@ enum {
   FAMILY_STREAM1X1 = 4,  // pointwise: Ker resident in LDS, In streamed to registers (unrolled C)
   FAMILY_STREAM1X1_LOOP = 5,  // the same for any C % 4 == 0, looped over channel quads
   FAMILY_BF16_TR = 6,  // bf16 inputs, C = 32: shifted pixel-fastest LDS copies, transposing reads
+  FAMILY_STREAM1X1_BAL = 7,  // pointwise, equal pixel share per workgroup: 32-pixel blocks in turn + k-split tail
 };
 
 // One compiled kernel instance (template parameters of the kernel family).
@@ -46,6 +47,17 @@ struct Variant {
   int mfma32;     // DMA: 1 = 32x32x2 inner loop (64-row k tile, 32-pixel blocks)
   int nwc;        // DMA: groups of waves splitting each step's channels (0 = 1, no split)
   int groups() const { return nwc > 1 ? nwc : 1; }
+};
+
+// Division by a divisor d >= 1 fixed for a launch, for numerators
+// 0 <= n < 2^31: with s = ceil(log2 d) and m = ceil(2^(31+s) / d) (below
+// 2^32), n / d = (n * m) >> (31 + s) exactly (the rounding error of m adds
+// less than 1/d to n/d).  A 64-bit multiply and a shift in place of a
+// 32-bit division (about 35 instructions per lane).  m = 0 marks a divisor
+// the launch never divides by.
+struct FastDiv {
+  unsigned m;
+  int s;
 };
 
 // Fully resolved launch geometry, passed by value to the kernels.
@@ -74,7 +86,13 @@ struct Geom {
   // width when a 1x1 problem runs in its kernel view (one row of H' x W'
   // pixels per image), else 0.
   int nph, na, nb, sh, sw, ph, pw, C0, H0, W0, Wi;
+  // The kernels' per-lane index maps divide by these (set_fast_divisors).
+  FastDiv dv_in_cstride, dv_in_wp, dv_H, dv_ker_rstride, dv_tw, dv_P, dv_nph, dv_nb, dv_Wi, dv_tiles_k,
+      dv_tiles_cols, dv_tiles_rows;
 };
+
+// Fills the FastDiv fields of g from its extents (after every other field).
+void set_fast_divisors(Geom* g);
 
 const Variant* variants(int* count);
 const Variant* find_variant(int id);

@@ -58,6 +58,11 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
   return (b < G8) ? (b & 7) * (G8 >> 3) + (b >> 3) : b;
 }
 
+// n / d for 0 <= n < 2^31 with the launch's precomputed multiplier (FastDiv).
+__device__ __forceinline__ int fdiv(int n, FastDiv f) {
+  return (int)(((unsigned long long)(unsigned)n * f.m) >> (31 + f.s));
+}
+
 struct TileCoord {
   int rho0, rho_end;  // output rows [rho0, rho_end) of the flattened n*P+h index
   int q0, tw_eff;     // output columns [q0, q0 + tw_eff)
@@ -70,15 +75,15 @@ __device__ __forceinline__ TileCoord tile_coord(const Geom& g, int BK, int b) {
   const int L = xcd_remap(b, g.num_tiles);
   int kt, ct, rt;
   if (g.order == 0) {
-    kt = L % g.tiles_k;
-    const int rest = L / g.tiles_k;
-    ct = rest % g.tiles_cols;
-    rt = rest / g.tiles_cols;
+    const int rest = fdiv(L, g.dv_tiles_k);
+    kt = L - rest * g.tiles_k;
+    rt = fdiv(rest, g.dv_tiles_cols);
+    ct = rest - rt * g.tiles_cols;
   } else {
-    ct = L % g.tiles_cols;
-    const int rest = L / g.tiles_cols;
-    rt = rest % g.tiles_rows;
-    kt = rest / g.tiles_rows;
+    const int rest = fdiv(L, g.dv_tiles_cols);
+    ct = L - rest * g.tiles_cols;
+    kt = fdiv(rest, g.dv_tiles_rows);
+    rt = rest - kt * g.tiles_rows;
   }
   TileCoord t;
   const int NP = g.N * g.P;
@@ -87,9 +92,9 @@ __device__ __forceinline__ TileCoord tile_coord(const Geom& g, int BK, int b) {
   t.q0 = ct * g.tw;
   t.tw_eff = min(g.tw, g.Q - t.q0);
   t.k0 = kt * BK;
-  const int nf = t.rho0 / g.P, pf = t.rho0 - nf * g.P;
+  const int nf = fdiv(t.rho0, g.dv_P), pf = t.rho0 - nf * g.P;
   t.nu0 = nf * g.H + pf;
-  const int nl = (t.rho_end - 1) / g.P, pl = (t.rho_end - 1) - nl * g.P;
+  const int nl = fdiv(t.rho_end - 1, g.dv_P), pl = (t.rho_end - 1) - nl * g.P;
   t.nrows = nl * g.H + pl + g.R - t.nu0;
   return t;
 }
@@ -385,19 +390,19 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
       in_goff[i] = -1;
       in_cl[i] = 0;
       if (e < TC * g.in_cstride) {
-        const int cl = e / g.in_cstride, pos = e - cl * g.in_cstride;
-        const int row = pos / g.in_wp, x = pos - row * g.in_wp;
+        const int cl = fdiv(e, g.dv_in_cstride), pos = e - cl * g.in_cstride;
+        const int row = fdiv(pos, g.dv_in_wp), x = pos - row * g.in_wp;
         if (row < t.nrows && x < ncols) {
           const int nu = t.nu0 + row;
-          const int n = nu / H, y = nu - n * H;
+          const int n = fdiv(nu, g.dv_H), y = nu - n * H;
           if (g.nph == 0) {
             in_goff[i] = ((n * C + cl) * H + y) * W + t.q0 + x;
           } else {
             // phase (a, b) of input channel c: a chunk holds whole channels
-            const int c = cl / g.nph, f = cl - c * g.nph, a = f / g.nb, b = f - a * g.nb;
+            const int c = fdiv(cl, g.dv_nph), f = cl - c * g.nph, a = fdiv(f, g.dv_nb), b = f - a * g.nb;
             int yi = y, xi = t.q0 + x;
             if (g.Wi) {  // 1x1 kernel view: one row of H' x W' pixels
-              yi = xi / g.Wi;
+              yi = fdiv(xi, g.dv_Wi);
               xi -= yi * g.Wi;
             }
             const int iy = yi * g.sh + a - g.ph, ix = xi * g.sw + b - g.pw;
@@ -415,7 +420,7 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
 #pragma unroll
   for (int i = 0; i < NLK; ++i) {
     const int e = ((i * NW + wave) * 64 + lane) * KVK;
-    const int kl = e / g.ker_rstride, m = e - kl * g.ker_rstride;
+    const int kl = fdiv(e, g.dv_ker_rstride), m = e - kl * g.ker_rstride;
     ker_goff[i] = -1;
     ker_m[i] = 0;
     if (kl < BK && m < TCRS && t.k0 + kl < K) {
@@ -434,11 +439,11 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
 #pragma unroll
   for (int pb = 0; pb < NPB; ++pb) {
     const int px = wp * WP * 16 + pb * BW + jl;
-    const int row_i = px / g.tw, col = px - row_i * g.tw;
+    const int row_i = fdiv(px, g.dv_tw), col = px - row_i * g.tw;
     const int rho = t.rho0 + row_i;
     int off = 0;
     if (px < tpx && rho < t.rho_end && col < t.tw_eff) {
-      const int n = rho / g.P, p = rho - n * g.P;
+      const int n = fdiv(rho, g.dv_P), p = rho - n * g.P;
       off = (n * H + p - t.nu0) * g.in_wp + col;
     }
     poff[pb] = off;
@@ -452,7 +457,7 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
   auto issue = [&](int ch, int slot) {  // pipeline step ch into stage buffer slot % NS
     const int c0 = ch * TC;
     const unsigned stage = lds_base + (unsigned)((slot % NS) * STAGE) * 4u;
-    const int coff = g.nph ? (c0 / g.nph) * g.H0 * g.W0 : c0 * H * W;
+    const int coff = g.nph ? fdiv(c0, g.dv_nph) * g.H0 * g.W0 : c0 * H * W;
 #pragma unroll
     for (int i = 0; i < NLI; ++i) {
       const unsigned voff =
@@ -518,20 +523,26 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
     }
   };
 
-  // This workgroup's channel range: pipeline steps [ch0, ch0 + nch).
+  // This workgroup's channel range: pipeline steps [ch0, ch0 + nch).  All
+  // NS stage buffers are filled up front (a short reduction is then one
+  // round trip to memory, not one per step); from the second step on, each
+  // iteration refills the buffer the previous one computed, which the
+  // barrier has freed, so NS - 1 steps stay in flight behind the current one.
   const int ch0 = split_r * g.cps;
   const int nch = min(g.cps, g.nchunks - ch0);
 #pragma unroll
-  for (int s = 0; s < NS - 1; ++s)
+  for (int s = 0; s < NS; ++s)
     if (s < nch) issue(ch0 + s, s);
   for (int ch = 0; ch < nch; ++ch) {
-    // wait for this step's loads: the later steps already issued may stay in flight
-    const int ahead = min(NS - 2, nch - 1 - ch);
-    if (NS >= 4 && ahead >= 2) wait_vmcnt<(NS >= 4 ? 2 * L : 0)>();
-    else if (NS >= 3 && ahead >= 1) wait_vmcnt<(NS >= 3 ? L : 0)>();
+    // wait for this step's loads: the later steps already issued may stay in
+    // flight (loads retire in order)
+    const int ahead = min(ch == 0 ? NS - 1 : NS - 2, nch - 1 - ch);
+    if (ahead >= 3) wait_vmcnt<(3 * L < 64 ? 3 * L : 63)>();
+    else if (ahead == 2) wait_vmcnt<(2 * L < 64 ? 2 * L : 63)>();
+    else if (ahead == 1) wait_vmcnt<(L < 64 ? L : 63)>();
     else wait_vmcnt<0>();
     __syncthreads();
-    if (ch + NS - 1 < nch) issue(ch0 + ch + NS - 1, ch + NS - 1);
+    if (ch >= 1 && ch + NS - 1 < nch) issue(ch0 + ch + NS - 1, ch + NS - 1);
     compute(ch % NS);
   }
 
@@ -565,11 +576,11 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
 #pragma unroll
       for (int c = 1; c < NWC; ++c) sum += lds[((c * NWG + wg) * NREG + r) * 64 + lane];
       const int px = wp * WP * 16 + pb * 16 + j;
-      const int row_i = px / g.tw, col = px - row_i * g.tw;
+      const int row_i = fdiv(px, g.dv_tw), col = px - row_i * g.tw;
       const int rho = t.rho0 + row_i;
       const int k = t.k0 + (wk * WK + kb) * 16 + 4 * gq + v;
       if (px < tpx && rho < t.rho_end && col < t.tw_eff && k < K) {
-        const int n = rho / g.P, p = rho - n * g.P;
+        const int n = fdiv(rho, g.dv_P), p = rho - n * g.P;
         Out[(size_t)split_r * g.N * K * PQ + (((size_t)n * K + k) * g.P + p) * g.Q + t.q0 + col] = sum;
       }
     }
@@ -578,10 +589,10 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
 #pragma unroll
   for (int pb = 0; pb < NPB; ++pb) {
     const int px = wp * WP * 16 + pb * BW + jl;
-    const int row_i = px / g.tw, col = px - row_i * g.tw;
+    const int row_i = fdiv(px, g.dv_tw), col = px - row_i * g.tw;
     const int rho = t.rho0 + row_i;
     if (px < tpx && rho < t.rho_end && col < t.tw_eff) {
-      const int n = rho / g.P, p = rho - n * g.P;
+      const int n = fdiv(rho, g.dv_P), p = rho - n * g.P;
       float* ob = Out + (size_t)split_r * g.N * K * PQ + ((size_t)n * K * g.P + p) * g.Q + t.q0 + col;
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb) {
@@ -1367,6 +1378,190 @@ conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ke
   body(std::integral_constant<int, UA>{}, simd_begin, min(simd_begin + 16 * UA, simd_end));
 }
 
+// Balanced pointwise kernel for a compile-time channel count C = 4 * NQ.
+//
+// The unrolled kernel above gives each SIMD a whole number of 16-pixel
+// units, so a pixel count that is not a multiple of 16 x 4 x 256 leaves CUs
+// idle or SIMDs uneven (the 1x1 N=32 C=256 56x56 layer: 7 units on each of
+// 896 SIMDs, 32 CUs idle).  Here every workgroup (four waves, one per SIMD)
+// takes the same share of PW = tile_cols consecutive pixels (the last one
+// fewer), PW = 128 * NB + T with 0 < T <= 16:
+//   * wave s computes the NB 32-pixel blocks at P0 + 32 * (4 j + s),
+//     j = 0 .. NB-1, one after another (so the four waves read adjacent
+//     128-byte pieces of each channel row).  Each block accumulates over all
+//     C channels, the even and odd channel pairs of each quad in separate
+//     accumulators (four independent 32x32x2 chains keep the MFMA pipe full
+//     with one wave per SIMD); the two are added and the block is stored
+//     while the next block computes, which spreads the Out writes over the
+//     whole kernel instead of one burst at the end;
+//   * the last T pixels form one 16-pixel block (masked past PW) whose 64
+//     rows of k are split among the four waves, 16 rows each on one 16x16x4
+//     accumulator, computed alongside each wave's last block.
+// In streams from HBM into a ring of registers D steps ahead (branch-free
+// raw buffer loads, masked lanes read zeros past the buffer's range).  Ker
+// (64 rows of this k tile, all C channels) is staged through registers into
+// LDS in chunks of 64 channels during the first block, each chunk requested
+// a whole chunk ahead; every load is visible to the compiler, so its waits
+// are exact.  Requires C % 64 == 0 and In below 1 GB (32-bit offsets).
+template <int NB, int D, int NQ>
+__global__ void __launch_bounds__(256)
+conv1x1_bal_kernel(const float* __restrict__ In, const float* __restrict__ Ker, float* __restrict__ Out,
+                   const Geom g) {
+  static_assert(NQ % 16 == 0, "Ker arrives in chunks of 16 channel quads");
+  static_assert(NB >= 1 && D >= 2 && 3 * D <= 60, "ring loads in flight stay within vmcnt");
+  constexpr int PITCH = 4 * NQ + 1;  // LDS Ker row pitch, floats
+  constexpr int NCH = NQ / 16;       // Ker chunks of 64 channels
+  constexpr int NSTEP = NB * NQ;     // one step = one channel quad of one block
+  extern __shared__ __align__(16) float lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, h32 = lane >> 5;  // 32x32x2 lane coordinates
+  const int l16 = lane & 15, h16 = lane >> 4;  // 16x16x4 lane coordinates
+  const int C = g.C, K = g.K;
+  const int HW = g.W;  // kernel view: one row of H*W pixels per image
+  const int total_px = g.N * HW;
+  const int kt = blockIdx.x % g.tiles_k;
+  const int pg = blockIdx.x / g.tiles_k;
+  const int k0 = kt * 64;
+  const int P0 = pg * g.tw;
+  const int Pend = min(P0 + g.tw, total_px);
+  const int ptail = P0 + 128 * NB;
+
+  __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(In), (short)0, (int)g.in_bytes, 0x00020000);
+  __amdgpu_buffer_rsrc_t krsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(Ker), (short)0, (int)g.ker_bytes, 0x00020000);
+  const unsigned cstride = 4u * (unsigned)HW;  // bytes between channels
+  auto in_off = [&](int px, int c) __attribute__((always_inline)) {
+    const int n = px / HW, hw = px - n * HW;
+    return (px < Pend) ? (unsigned)((n * C + c) * HW + hw) * 4u : kOob;
+  };
+  unsigned off32[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) off32[j] = in_off(P0 + 32 * (4 * j + wave) + l32, h32);
+  const unsigned off16 = in_off(ptail + l16, h16);
+
+  // Ker chunk ch: 64 rows x 64 channels; lane (wave, i, lane) holds row
+  // 16 * wave + 4 * i + lane / 16, channels 4 * (lane % 16) .. + 3.
+  v4f kst[4];
+  auto ker_load = [&](int ch) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int k = k0 + 16 * wave + 4 * i + (lane >> 4);
+      const unsigned voff = k < K ? (unsigned)(k * C + ch * 64 + 4 * (lane & 15)) * 4u : kOob;
+      kst[i] = __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(krsrc, voff, 0, 0));
+    }
+  };
+  auto ker_store = [&](int ch) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float* row = lds + (16 * wave + 4 * i + (lane >> 4)) * PITCH + ch * 64 + 4 * (lane & 15);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) row[e] = kst[i][e];
+    }
+  };
+
+  // ring slot of step t: two 32x32x2 B operands (channel pairs e = 0, 1 of
+  // the quad) and, in the last block, the tail block's 16x16x4 B operand
+  float ring32[D][2], ring16[D];
+  auto load = [&](auto t_c) __attribute__((always_inline)) {
+    constexpr int t = decltype(t_c)::value;
+    constexpr int j = t / NQ, q = t % NQ;
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+      ring32[t % D][e] = __builtin_bit_cast(
+          float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, off32[j] + (unsigned)(4 * q + 2 * e) * cstride, 0, 0));
+    if constexpr (j == NB - 1)
+      ring16[t % D] = __builtin_bit_cast(
+          float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, off16 + (unsigned)(4 * q) * cstride, 0, 0));
+  };
+  // A operands of quad q, read one step ahead: a32[e][kb] = Ker[k0 + 32 kb + l32][4q + 2e + h32],
+  // a16 = Ker[k0 + 16 wave + l16][4q + h16]
+  const float* arow32 = lds + l32 * PITCH + h32;
+  const float* arow16 = lds + (16 * wave + l16) * PITCH + h16;
+  float a32[2][2][2], a16[2];
+  auto read_a = [&](int q, int buf, bool tail) __attribute__((always_inline)) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) a32[buf][e][kb] = arow32[kb * 32 * PITCH + 4 * q + 2 * e];
+    if (tail) a16[buf] = arow16[4 * q];
+  };
+  v16f acc[2][2];  // [kb][e]
+  v4f acc16 = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int e = 0; e < 2; ++e) acc[kb][e] = v16f{};
+
+  // prologue: Ker chunk 0, the ring, then chunk 0 into LDS
+  ker_load(0);
+  static_for<D>([&](auto t_c) __attribute__((always_inline)) { load(t_c); });
+  ker_store(0);
+  if constexpr (NCH > 1) ker_load(1);
+  __syncthreads();
+  read_a(0, 0, NB == 1);
+
+  static_for<NSTEP>([&](auto t_c) __attribute__((always_inline)) {
+    constexpr int t = decltype(t_c)::value;
+    constexpr int j = t / NQ, q = t % NQ;
+    constexpr int buf = t & 1;
+    constexpr bool tail = j == NB - 1;
+    // end of a Ker chunk during the first block: the next chunk (requested
+    // a chunk ago) goes to LDS before its first A read
+    constexpr bool chunk_end = j == 0 && q % 16 == 15 && q / 16 + 1 < NCH;
+    constexpr int tn = t + 1;
+    if constexpr (tn < NSTEP && !chunk_end) read_a(tn % NQ, buf ^ 1, tn / NQ == NB - 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        acc[kb][e] = __builtin_amdgcn_mfma_f32_32x32x2f32(a32[buf][e][kb], ring32[t % D][e], acc[kb][e], 0, 0, 0);
+    if constexpr (tail) acc16 = __builtin_amdgcn_mfma_f32_16x16x4f32(a16[buf], ring16[t % D], acc16, 0, 0, 0);
+    if constexpr (t + D < NSTEP) load(std::integral_constant<int, t + D>{});
+    if constexpr (chunk_end) {
+      ker_store(q / 16 + 1);
+      if constexpr (q / 16 + 2 < NCH) ker_load(q / 16 + 2);
+      __syncthreads();
+      read_a(tn % NQ, buf ^ 1, tn / NQ == NB - 1);
+    }
+    if constexpr (q == NQ - 1) {
+      // block j done: add the two channel-pair halves and store 32 pixels
+      // (two rows of k per instruction, streaming hint), then restart
+      const int px = P0 + 32 * (4 * j + wave) + l32;
+      if (px < Pend) {
+        const int n = px / HW, hw = px - n * HW;
+        float* ob = Out + (size_t)n * K * HW + hw;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int k = k0 + 32 * kb + 8 * (v / 4) + 4 * h32 + v % 4;
+            if (k < K) __builtin_nontemporal_store(acc[kb][0][v] + acc[kb][1][v], &ob[(size_t)k * HW]);
+          }
+      }
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 2; ++e) acc[kb][e] = v16f{};
+    }
+    // keep each refill right behind the MFMAs that free its slot
+    __builtin_amdgcn_sched_barrier(0);
+  });
+  // the tail block's 16 rows of k owned by this wave
+  const int px = ptail + l16;
+  if (px < Pend) {
+    const int n = px / HW, hw = px - n * HW;
+    float* ob = Out + (size_t)n * K * HW + hw;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int k = k0 + 16 * wave + 4 * h16 + v;
+      if (k < K) __builtin_nontemporal_store(acc16[v], &ob[(size_t)k * HW]);
+    }
+  }
+}
+
 // Looped kernel for any channel count (C % 4 == 0): D quads per loop trip,
 // the Ker slice zero-padded to whole trips and copied to LDS up front; two
 // phases of NB1 and NB2 pixel blocks.
@@ -1619,6 +1814,11 @@ widen_bf16_kernel(const unsigned short* __restrict__ src, float* __restrict__ ds
                    (UB > 0 ? 512 : 256), D},                                                 \
            &conv1x1_stream_kernel<UA, UB, D, NQ>, nullptr}
 
+#define F32_STREAM1X1_BAL(ID, NB, D, NQ)                                                     \
+  Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STREAM1X1_BAL, 4, 2 * NB + 1, 4 * NQ, 1, 1, NB, 1, 4, 1, \
+                   kThreads, D},                                                                 \
+           &conv1x1_bal_kernel<NB, D, NQ>, nullptr}
+
 #define F32_STREAM1X1_LOOP(ID, NB1, NB2, D)                                                  \
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_STREAM1X1_LOOP, 4, NB1 + NB2, 0, 1, 1, NB1, NB2, \
                    1, 1, kThreads, D},                                                       \
@@ -1649,6 +1849,17 @@ const Instance kInstances[] = {
     F32_STREAM1X1(308, 4, 3, 6, 32),
     F32_STREAM1X1(309, 4, 3, 6, 128),
     // any C % 4 == 0: (phase-1 blocks, phase-2 blocks, quads per trip)
+    // balanced pointwise kernel: NB 32-pixel blocks per wave plus a k-split tail
+    F32_STREAM1X1_BAL(321, 3, 16, 64),
+    F32_STREAM1X1_BAL(322, 3, 12, 64),
+    F32_STREAM1X1_BAL(323, 2, 16, 64),
+    F32_STREAM1X1_BAL(324, 1, 16, 64),
+    F32_STREAM1X1_BAL(325, 3, 16, 32),
+    F32_STREAM1X1_BAL(326, 2, 16, 32),
+    F32_STREAM1X1_BAL(327, 3, 16, 16),
+    F32_STREAM1X1_BAL(328, 2, 16, 16),
+    F32_STREAM1X1_BAL(329, 2, 16, 128),
+    F32_STREAM1X1_BAL(330, 1, 16, 128),
     F32_STREAM1X1_LOOP(311, 4, 3, 8),
     F32_STREAM1X1_LOOP(312, 4, 0, 8),
     F32_STREAM1X1_LOOP(313, 2, 2, 8),
@@ -2033,7 +2244,7 @@ int launch(const Variant& v, const Geom& g, const void* In, const void* Ker, flo
   int lds_bytes;
   if (v.family == FAMILY_DMA) lds_bytes = v.stages * g.stage_elems * (int)sizeof(float);
   else if (v.family == FAMILY_BF16 || v.family == FAMILY_BF16_TR || v.family == FAMILY_STREAM1X1 ||
-           v.family == FAMILY_STREAM1X1_LOOP)
+           v.family == FAMILY_STREAM1X1_LOOP || v.family == FAMILY_STREAM1X1_BAL)
     lds_bytes = g.stage_elems;  // bytes
   else lds_bytes = 2 * (g.lds_in_elems + g.lds_ker_elems) * (int)sizeof(float);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);

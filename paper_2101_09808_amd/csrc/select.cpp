@@ -215,6 +215,34 @@ Shape kernel_view(const Shape& s) {
 }
 }  // namespace
 
+namespace {
+FastDiv make_fastdiv(int d) {
+  FastDiv f{0u, 0};
+  if (d <= 0) return f;
+  int s = 0;
+  while ((int64_t(1) << s) < d) ++s;
+  const uint64_t num = uint64_t(1) << (31 + s);
+  f.m = (unsigned)((num + (uint64_t)d - 1) / (uint64_t)d);
+  f.s = s;
+  return f;
+}
+}  // namespace
+
+void set_fast_divisors(Geom* g) {
+  g->dv_in_cstride = make_fastdiv(g->in_cstride);
+  g->dv_in_wp = make_fastdiv(g->in_wp);
+  g->dv_H = make_fastdiv(g->H);
+  g->dv_ker_rstride = make_fastdiv(g->ker_rstride);
+  g->dv_tw = make_fastdiv(g->tw);
+  g->dv_P = make_fastdiv(g->P);
+  g->dv_nph = make_fastdiv(g->nph);
+  g->dv_nb = make_fastdiv(g->nb);
+  g->dv_Wi = make_fastdiv(g->Wi);
+  g->dv_tiles_k = make_fastdiv(g->tiles_k);
+  g->dv_tiles_cols = make_fastdiv(g->tiles_cols);
+  g->dv_tiles_rows = make_fastdiv(g->tiles_rows);
+}
+
 bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Geom* g,
                   int* lds_bytes) {
   const Shape s = kernel_view(s0);
@@ -256,7 +284,51 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
     q.stage_elems = (int)bytes;
     q.in_bytes = (unsigned)std::min<int64_t>((int64_t)s.N * s.C * s.H * s.W * 4, 0xffffffffLL);
     q.ker_bytes = (unsigned)std::min<int64_t>((int64_t)s.K * s.C * 4, 0xffffffffLL);
-    if (g) *g = q;
+    if (g) {
+      set_fast_divisors(&q);
+      *g = q;
+    }
+    if (lds_bytes) *lds_bytes = (int)bytes;
+    return true;
+  }
+  if (v.family == FAMILY_STREAM1X1_BAL) {
+    // Balanced pointwise: tile_cols = pixels per workgroup PW, with
+    // 128 NB < PW <= 128 NB + 16 (NB 32-pixel blocks per wave, the rest one
+    // 16-pixel block split by k, which counts as one more 16-pixel unit of
+    // each wave: wave_px = 32 NB + 16); 64 output channels per workgroup, the
+    // whole channel range resident.
+    if (s0.R != 1 || s0.S != 1) return false;
+    if (plan.tile_k != 64 || plan.waves_k != 1 || plan.waves_px != 4 || plan.tile_rows != 1) return false;
+    if (plan.wave_k != 64 || plan.wave_px != 16 * v.wp || plan.tile_c != v.tc || v.tc != s.C) return false;
+    if (s.C % 64) return false;
+    const int pw = plan.tile_cols, nb = v.max_ni;
+    if (pw <= 128 * nb || pw > 128 * nb + 16) return false;
+    const int64_t total_px = (int64_t)s.N * s.W;
+    const int64_t groups = cdiv(total_px, pw);
+    const int64_t tiles_k = cdiv(s.K, 64);
+    const int64_t bytes = (int64_t)(s.C + 1) * 64 * 4;  // Ker rows [k][c] + 1 pad
+    if (bytes > kHw.lds_bytes || groups * tiles_k >= (int64_t(1) << 31)) return false;
+    if ((int64_t)s.N * s.C * s.W * 4 >= (int64_t(1) << 30)) return false;  // 32-bit byte offsets
+    if ((int64_t)s.K * s.C * 4 >= (int64_t(1) << 31)) return false;        // below the Ker sentinel
+    Geom q;
+    std::memset(&q, 0, sizeof(q));
+    q.N = s.N; q.C = s.C; q.K = s.K; q.H = s.H; q.W = s.W; q.R = 1; q.S = 1;
+    q.P = s.P(); q.Q = s.Q();
+    q.tr = 1; q.tw = pw;
+    q.tiles_rows = (int)groups; q.tiles_cols = 1; q.tiles_k = (int)tiles_k;
+    q.nwk = 1; q.nwp = 4;
+    q.num_tiles = (int)(groups * tiles_k);
+    q.grid = q.num_tiles;
+    q.nchunks = (int)cdiv(s.C, 4);
+    q.split = 1;
+    q.cps = q.nchunks;
+    q.stage_elems = (int)bytes;
+    q.in_bytes = (unsigned)std::min<int64_t>((int64_t)s.N * s.C * s.H * s.W * 4, 0xffffffffLL);
+    q.ker_bytes = (unsigned)std::min<int64_t>((int64_t)s.K * s.C * 4, 0xffffffffLL);
+    if (g) {
+      set_fast_divisors(&q);
+      *g = q;
+    }
     if (lds_bytes) *lds_bytes = (int)bytes;
     return true;
   }
@@ -319,7 +391,10 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
     q.grid = (int)std::min<int64_t>(num_tiles, (int64_t)kHw.cus);
     q.in_bytes = (unsigned)((int64_t)s.N * s.C * s.H * s.W * 2);
     q.ker_bytes = (unsigned)std::min<int64_t>((int64_t)s.K * s.C * RS * 2, 0xffffffffLL);
-    if (g) *g = q;
+    if (g) {
+      set_fast_divisors(&q);
+      *g = q;
+    }
     if (lds_bytes) *lds_bytes = (int)bytes_t;
     return true;
   }
@@ -349,7 +424,10 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
     q.grid = (int)std::min<int64_t>(num_tiles, (int64_t)kHw.cus * occ);
     q.in_bytes = (unsigned)std::min<int64_t>((int64_t)s.N * s.C * s.H * s.W * 2, 0xffffffffLL);
     q.ker_bytes = (unsigned)std::min<int64_t>((int64_t)s.K * s.C * RS * 2, 0xffffffffLL);
-    if (g) *g = q;
+    if (g) {
+      set_fast_divisors(&q);
+      *g = q;
+    }
     if (lds_bytes) *lds_bytes = (int)bytes_b;
     return true;
   }
@@ -422,7 +500,10 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
   q.stage_elems = (int)stage;
   q.in_region = (int)in_region;
   q.grid = (int)(num_tiles * split);
-  if (g) *g = q;
+  if (g) {
+    set_fast_divisors(&q);
+    *g = q;
+  }
   if (lds_bytes) *lds_bytes = (int)bytes;
   return true;
 }
@@ -448,6 +529,7 @@ bool phase_direct(const Variant& v, const PhaseGeom& p, int dtype, Geom* g) {
   g->C0 = p.C; g->H0 = p.H; g->W0 = p.W;
   g->Wi = (p.Rp == 1 && p.Sp == 1) ? p.Wp : 0;  // kernel_view flattens 1x1 problems
   g->in_bytes = (unsigned)in_bytes;
+  set_fast_divisors(g);
   return true;
 }
 
@@ -502,6 +584,37 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
     // count (60 plans of the 1x1 N=32 C=256 K=64 layer).
     if (g.tw % 16) issue_eff *= 0.8;
     plan->pred_mfma_us = rounds * nb * 4 * nq * kHw.mfma_f32_cycles / kHw.clock_hz * 1e6 / issue_eff;
+    plan->pred_total_us = std::max(tmax, plan->pred_mfma_us);
+    return CONV_OK;
+  }
+  if (v->family == FAMILY_STREAM1X1_BAL) {
+    // In moves HBM -> VGPR once; the Ker slice is staged into LDS once per
+    // workgroup; per channel quad each wave reads 16 B of A operands per
+    // lane for its 32-pixel block and 4 B for its quarter of the tail block.
+    plan->lds_bytes = lds;
+    plan->num_wg = g.grid;
+    const double in_b = (double)s.N * s.C * s.W * 4.0, ker_b = (double)s.K * s.C * 4.0;
+    const double out_b = (double)s.N * s.K * s.W * 4.0;
+    const double waves = (double)g.grid * 4;
+    const double nq = s.C / 4.0, nb = v->max_ni;
+    plan->pred_bytes[CONV_LVL_REG] = waves * nq * 64 * (16.0 * nb + 4.0);
+    plan->pred_bytes[CONV_LVL_LDS] = (double)g.grid * s.C * 64 * 4.0;
+    plan->pred_bytes[CONV_LVL_L2] = in_b * g.tiles_k + ker_b * std::min<double>(g.tiles_rows, kHw.xcds);
+    plan->pred_bytes[CONV_LVL_HBM] = in_b + ker_b + out_b;
+    plan->class_lvl[CONV_LVL_REG] = 3;
+    plan->class_lvl[CONV_LVL_LDS] = 3;
+    plan->class_lvl[CONV_LVL_L2] = 1;
+    plan->class_lvl[CONV_LVL_HBM] = 0;
+    double tmax = 0;
+    for (int l = 0; l < CONV_NUM_LVLS; ++l) {
+      plan->pred_us[l] = plan->pred_bytes[l] / kHw.bw[l] * 1e6;
+      tmax = std::max(tmax, plan->pred_us[l]);
+    }
+    // per wave and channel quad: 4 32x32x2 MFMAs (twice the 16x16x4 time)
+    // per block and one 16x16x4 for the tail; one wave per SIMD
+    const double rounds = std::ceil((double)g.grid / kHw.cus);
+    const double cycles = nq * (nb * 4 * 2 * kHw.mfma_f32_cycles + kHw.mfma_f32_cycles);
+    plan->pred_mfma_us = rounds * cycles / kHw.clock_hz * 1e6 / 0.92;
     plan->pred_total_us = std::max(tmax, plan->pred_mfma_us);
     return CONV_OK;
   }
@@ -638,6 +751,7 @@ namespace {
 double family_factor(int family) {
   switch (family) {
     case FAMILY_STREAM1X1:
+    case FAMILY_STREAM1X1_BAL:
     case FAMILY_BF16_TR: return 0.8;
     case FAMILY_DMA:
     case FAMILY_BF16: return 1.0;
@@ -713,6 +827,27 @@ int enumerate_plans(const Shape& s0, int dtype, conv_plan_t* plans, int cap) {
       for (int wpx : wpxs) {
         conv_plan_t p;
         fill_plan_fields(&p, v, 1, 4, 1, wpx, 0);
+        p.tile_k = 64;
+        p.wave_k = 64;
+        if (score_plan(s0, &p) == CONV_OK) all.push_back(p);
+      }
+      continue;
+    }
+    if (v.family == FAMILY_STREAM1X1_BAL) {
+      // pixels per workgroup: every share that leaves NB whole blocks per
+      // wave and at most 16 pixels for the k-split tail block
+      const int nb = v.max_ni;
+      const int64_t total_px = (int64_t)s.N * s.W;
+      std::vector<int> pws;
+      for (int64_t G = cdiv(total_px, 128 * nb + 16); G <= 65536; ++G) {
+        const int64_t pw = cdiv(total_px, G);
+        if (pw <= 128 * nb) break;
+        if (pw <= 128 * nb + 16 && std::find(pws.begin(), pws.end(), (int)pw) == pws.end())
+          pws.push_back((int)pw);
+      }
+      for (int pw : pws) {
+        conv_plan_t p;
+        fill_plan_fields(&p, v, 1, 4, 1, pw, 0);
         p.tile_k = 64;
         p.wave_k = 64;
         if (score_plan(s0, &p) == CONV_OK) all.push_back(p);

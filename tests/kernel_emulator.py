@@ -24,29 +24,49 @@ def _chk(cond, msg):
         raise EmulationError(msg)
 
 
+DIVISORS = {"in_cstride": "in_cstride", "in_wp": "in_wp", "H": "H", "ker_rstride": "ker_rstride", "tw": "tw",
+            "P": "P", "nph": "nph", "nb": "nb", "Wi": "Wi", "tiles_k": "tiles_k", "tiles_cols": "tiles_cols",
+            "tiles_rows": "tiles_rows"}
+
+
+def fdiv(n, g, name):
+    """n // g[name] as the kernels compute it, (n * m) >> (31 + s) with the
+    launch's exported multiplier; checked against floor division."""
+    m, s = g[f"dv_{name}_m"], g[f"dv_{name}_s"]
+    d = g[DIVISORS[name]]
+    nn = np.asarray(n, dtype=np.int64)
+    _chk((nn >= 0).all() and (nn < 2 ** 31).all(), f"numerator of /{name} outside [0, 2^31)")
+    _chk(m > 0 and d > 0, f"launch divides by {name} without a multiplier")
+    q = ((nn.astype(np.uint64) * np.uint64(m)) >> np.uint64(31 + s)).astype(np.int64)
+    _chk((q == nn // d).all(), f"fast division by {name} = {d} is not exact")
+    return q if np.ndim(n) else int(q)
+
+
 def tile_coord(g, b, BK):
     G = g["num_tiles"]
     G8 = G & ~7
     L = (b & 7) * (G8 >> 3) + (b >> 3) if b < G8 else b
     if g["order"] == 0:
-        kt = L % g["tiles_k"]
-        rest = L // g["tiles_k"]
-        ct = rest % g["tiles_cols"]
-        rt = rest // g["tiles_cols"]
+        rest = fdiv(L, g, "tiles_k")
+        kt = L - rest * g["tiles_k"]
+        rt = fdiv(rest, g, "tiles_cols")
+        ct = rest - rt * g["tiles_cols"]
     else:
-        ct = L % g["tiles_cols"]
-        rest = L // g["tiles_cols"]
-        rt = rest % g["tiles_rows"]
-        kt = rest // g["tiles_rows"]
+        rest = fdiv(L, g, "tiles_cols")
+        ct = L - rest * g["tiles_cols"]
+        kt = fdiv(rest, g, "tiles_rows")
+        rt = rest - kt * g["tiles_rows"]
     NP = g["N"] * g["P"]
     rho0 = rt * g["tr"]
     rho_end = min(rho0 + g["tr"], NP)
     q0 = ct * g["tw"]
     tw_eff = min(g["tw"], g["Q"] - q0)
     k0 = kt * BK
-    nf, pf = divmod(rho0, g["P"])
+    nf = fdiv(rho0, g, "P")
+    pf = rho0 - nf * g["P"]
     nu0 = nf * g["H"] + pf
-    nl, pl = divmod(rho_end - 1, g["P"])
+    nl = fdiv(rho_end - 1, g, "P")
+    pl = rho_end - 1 - nl * g["P"]
     nrows = nl * g["H"] + pl + g["R"] - nu0
     return L, dict(rho0=rho0, rho_end=rho_end, q0=q0, tw_eff=tw_eff, k0=k0, nu0=nu0, nrows=nrows)
 
@@ -59,6 +79,8 @@ def emulate(g, In, Ker, wgs=None):
     output element (NaN outputs where nothing was stored)."""
     if g["family"] in (4, 5):
         return emulate_stream1x1(g, In, Ker, wgs)
+    if g["family"] == 7:
+        return emulate_stream1x1_bal(g, In, Ker, wgs)
     N, C, K, H, W, R, S, P, Q = (g[x] for x in "N C K H W R S P Q".split())
     WK, WP, TC, KV, NT = g["wk"], g["wp"], g["tc"], g["ker_vec"], g["threads"]
     _chk(NT == 256 or (g["family"] == 2 and NT in (256, 512)), "threads per workgroup")
@@ -161,10 +183,18 @@ def emulate(g, In, Ker, wgs=None):
             poff, pvalid, pinfo = [], [], []
             for pb in range(NPB):
                 px = wp * WP * 16 + pb * BW + jl
-                row_i, col = px // g["tw"], px % g["tw"]
+                if dma:
+                    row_i = fdiv(px, g, "tw")
+                    col = px - row_i * g["tw"]
+                else:
+                    row_i, col = px // g["tw"], px % g["tw"]
                 rho = t["rho0"] + row_i
                 valid = (px < tpx) & (rho < t["rho_end"]) & (col < t["tw_eff"])
-                n, p = rho // P, rho % P
+                if dma:
+                    n = fdiv(rho, g, "P")
+                    p = rho - n * P
+                else:
+                    n, p = rho // P, rho % P
                 off = np.where(valid, (n * H + p - t["nu0"]) * g["in_wp"] + col, 0)
                 poff.append(off)
                 pvalid.append(valid)
@@ -184,23 +214,29 @@ def emulate(g, In, Ker, wgs=None):
             fresh_in = np.full(lin_n, np.nan)
             for i in range(NLI):
                 e = ((i * NW + wave) * 64 + lane_t) * KVI
-                cl, pos = e // g["in_cstride"], e % g["in_cstride"]
-                row, x = pos // g["in_wp"], pos % g["in_wp"]
+                cl = fdiv(e, g, "in_cstride")
+                pos = e - cl * g["in_cstride"]
+                row = fdiv(pos, g, "in_wp")
+                x = pos - row * g["in_wp"]
                 valid = (e < TC * g["in_cstride"]) & (row < t["nrows"]) & (x < ncols) & (c0 + cl < C)
                 nu = t["nu0"] + row
-                n, y = nu // H, nu % H
+                n = fdiv(nu, g, "H")
+                y = nu - n * H
                 if nph:
                     # chunk-local input channel and phase, as the kernel splits them
                     _chk(c0 % nph == 0, "a pipeline step splits a channel's phases")
-                    cr, f = cl // nph, cl % nph
-                    a, b = f // g["nb"], f % g["nb"]
+                    cr = fdiv(cl, g, "nph")
+                    f = cl - cr * nph
+                    a = fdiv(f, g, "nb")
+                    b = f - a * g["nb"]
                     yi, xi = y, t["q0"] + x
                     if g["Wi"]:  # 1x1 kernel view: one row of H' x W' pixels per image
-                        yi, xi = xi // g["Wi"], xi % g["Wi"]
+                        yi = fdiv(xi, g, "Wi")
+                        xi = xi - yi * g["Wi"]
                     iy, ix = yi * g["sh"] + a - g["ph"], xi * g["sw"] + b - g["pw"]
                     valid = valid & (iy >= 0) & (iy < g["H0"]) & (ix >= 0) & (ix < g["W0"])
                     goff = ((n * g["C0"] + cr) * g["H0"] + iy) * g["W0"] + ix
-                    coff = (c0 // nph) * g["H0"] * g["W0"]
+                    coff = fdiv(c0, g, "nph") * g["H0"] * g["W0"]
                 else:
                     goff = ((n * C + cl) * H + y) * W + t["q0"] + x
                     coff = c0 * H * W
@@ -218,7 +254,8 @@ def emulate(g, In, Ker, wgs=None):
             mlim = (C - c0) * RS
             for i in range(NLK):
                 e = ((i * NW + wave) * 64 + lane_t) * KV
-                kl, m = e // g["ker_rstride"], e % g["ker_rstride"]
+                kl = fdiv(e, g, "ker_rstride")
+                m = e - kl * g["ker_rstride"]
                 valid = (kl < BK) & (m < TCRS) & (t["k0"] + kl < K) & (m < mlim)
                 if KV > 1:
                     _chk(~valid | (m + KV <= mlim), "Ker vector straddles the channel range")
@@ -672,6 +709,123 @@ def emulate_stream1x1(g, In, Ker, wgs=None):
             else:
                 for bb in range(NB):
                     block16(lds, k0, px_begin, px_end, px_begin + 16 * bb, nq_run)
+    return out, written
+
+
+def emulate_stream1x1_bal(g, In, Ker, wgs=None):
+    """The balanced pointwise kernel (family 7, conv1x1_bal_kernel).
+
+    Per workgroup PW = tw consecutive pixels from P0 = group * PW, with
+    128 NB < PW <= 128 NB + 16 (NB = max_ni).  Ker rows [k][c] go to LDS
+    (pitch C + 1) from 16-byte loads: lane (wave, i, lane) row
+    16 wave + 4 i + lane // 16, channels 64 ch + 4 (lane % 16) .. + 3.
+    Wave s computes the 32-pixel blocks at P0 + 32 (4 j + s), j < NB, on
+    32x32x2 MFMAs, even and odd channel pairs in separate accumulators added
+    at the store, and k rows 16 s .. 16 s + 15 of the 16-pixel tail block at
+    P0 + 128 NB on 16x16x4 MFMAs.  In offsets are 32-bit byte offsets from
+    raw buffer loads (offsets at or past the buffer size read 0)."""
+    N, C, K, H, W = (g[x] for x in "N C K H W".split())
+    _chk(g["family"] == 7 and g["R"] == 1 and g["S"] == 1 and H == 1, "balanced pointwise geometry")
+    _chk(g["threads"] == 256 and g["nwp"] == 4 and g["nwk"] == 1, "four waves per workgroup")
+    NB = g["max_ni"]
+    _chk(g["tc"] == C and C % 64 == 0 and g["wp"] == 2 * NB + 1, "instance for this channel count")
+    HW = W
+    nq = C // 4
+    pitch = C + 1
+    pw = g["tw"]
+    _chk(128 * NB < pw <= 128 * NB + 16, "pixels per workgroup")
+    _chk(g["stage_elems"] == 64 * pitch * 4 == g["lds_bytes"] and g["lds_bytes"] <= 160 * 1024, "LDS bytes")
+    total_px = N * HW
+    _chk(g["tiles_rows"] == -(-total_px // pw) and g["grid"] == g["tiles_rows"] * g["tiles_k"], "grid")
+    in_size, ker_size, out_size = N * C * HW, K * C, N * K * HW
+    _chk(In.size == in_size and Ker.size == ker_size, "input sizes")
+    _chk(g["in_bytes"] == in_size * 4 and in_size * 4 < 2 ** 30, "In byte range below 1 GB")
+    _chk(g["ker_bytes"] == ker_size * 4 and ker_size * 4 < 2 ** 31, "Ker byte range below the sentinel")
+    out = np.full(out_size, np.nan)
+    written = np.zeros(out_size, np.int64)
+    lane = np.arange(64)
+    KOOB, M32 = 0x80000000, 0xFFFFFFFF
+    cstride = 4 * HW
+
+    def in_load(voff, byte_add, expect):
+        off = (voff + byte_add) & M32
+        hit = off < g["in_bytes"]
+        _chk((off[hit] % 4 == 0).all(), "misaligned In offset")
+        _chk((hit == expect).all(), "range check does not match the mask")
+        return np.where(hit, In[np.where(hit, off // 4, 0)], 0.0)
+
+    def lds_read(lds, idx):
+        _chk((idx >= 0).all() and (idx < lds.size).all(), "LDS Ker read out of range")
+        v = lds[idx]
+        _chk(not np.isnan(v).any(), "LDS Ker read of an unwritten element")
+        return v
+
+    def store(vals, k, px, valid):
+        n, hw = px // HW, px % HW
+        st = valid & (k < K)
+        dst = (n * K + k) * HW + hw
+        _chk((dst[st] >= 0).all() and (dst[st] < out_size).all(), "Out store range")
+        out[dst[st]] = vals[st]
+        np.add.at(written, dst[st], 1)
+
+    def in_off(px, c, pend):
+        n, hw = px // HW, px % HW
+        return np.where(px < pend, ((n * C + c) * HW + hw) * 4, KOOB), px < pend
+
+    for b in (range(g["grid"]) if wgs is None else wgs):
+        kt, pg = b % g["tiles_k"], b // g["tiles_k"]
+        k0 = kt * 64
+        P0 = pg * pw
+        pend = min(P0 + pw, total_px)
+        lds = np.full(64 * pitch, np.nan)  # the pad column is never read
+        for wave in range(4):
+            for ch in range(C // 64):
+                for i in range(4):
+                    row = 16 * wave + 4 * i + (lane >> 4)
+                    k = k0 + row
+                    off = np.where(k < K, (k * C + ch * 64 + 4 * (lane & 15)) * 4, KOOB)
+                    hit = off < g["ker_bytes"]
+                    _chk((hit == (k < K)).all(), "Ker range check does not match the row mask")
+                    _chk((off[hit] % 16 == 0).all(), "Ker 16-byte load misaligned")
+                    for e in range(4):
+                        dst = row * pitch + ch * 64 + 4 * (lane & 15) + e
+                        _chk(dst.max() < lds.size, "LDS Ker write out of range")
+                        lds[dst] = np.where(hit, Ker[np.where(hit, off // 4 + e, 0)], 0.0)
+        l32, h32 = lane & 31, lane >> 5
+        l16, h16 = lane & 15, lane >> 4
+        for wave in range(4):
+            for j in range(NB):
+                px = P0 + 32 * (4 * j + wave) + l32
+                voff, valid = in_off(px, h32, pend)
+                acc = np.zeros((2, 2, 32, 32))  # [kb][e]
+                for q in range(nq):
+                    for e in range(2):
+                        bv = in_load(voff, (4 * q + 2 * e) * cstride, valid)
+                        for kb in range(2):
+                            av = lds_read(lds, (kb * 32 + l32) * pitch + 4 * q + 2 * e + h32)
+                            Am = np.zeros((32, 2))
+                            Am[l32, h32] = av
+                            Bm = np.zeros((2, 32))
+                            Bm[h32, l32] = bv
+                            acc[kb, e] += Am @ Bm
+                for kb in range(2):
+                    for v in range(16):
+                        i = 8 * (v // 4) + 4 * h32 + v % 4
+                        store(acc[kb, 0][i, l32] + acc[kb, 1][i, l32], k0 + 32 * kb + i, px, valid)
+            # tail: 16 pixels at P0 + 128 NB, rows 16 wave .. 16 wave + 15
+            px = P0 + 128 * NB + l16
+            voff, valid = in_off(px, h16, pend)
+            acc16 = np.zeros((16, 16))
+            for q in range(nq):
+                bv = in_load(voff, 4 * q * cstride, valid)
+                av = lds_read(lds, (16 * wave + l16) * pitch + 4 * q + h16)
+                Am = np.zeros((16, 4))
+                Am[l16, h16] = av
+                Bm = np.zeros((4, 16))
+                Bm[h16, l16] = bv
+                acc16 += Am @ Bm
+            for v in range(4):
+                store(acc16[4 * h16 + v, l16], k0 + 16 * wave + 4 * h16 + v, px, valid)
     return out, written
 
 

@@ -236,7 +236,8 @@ def test_error_leaves_output_untouched():
 # ----------------------------------------------------------------- every kernel variant
 
 def _plans_per_variant(dims, dtype=B.CONV_DTYPE_F32, per_variant=3):
-    cands = B.conv_fwd_candidates(*dims, dtype=dtype)
+    n = B.lib().conv_fwd_candidates(*dims, dtype, None, 0)
+    cands = B.conv_fwd_candidates(*dims, dtype=dtype, cap=max(n, 1))
     chosen = {}
     for p in cands:
         key = (p["variant"], p["waves_k"], p["grid_order"], p.get("split_c", 1) > 1)
@@ -261,6 +262,13 @@ VARIANT_SHAPES = [
     ConvShape("var1x1_c128", 3, 128, 64, 7, 9, 1, 1, "f32", 35),
     ConvShape("var1x1_c256", 2, 256, 80, 8, 10, 1, 1, "f32", 36),
     ConvShape("var1x1_c512", 1, 512, 64, 7, 7, 1, 1, "f32", 37),
+    # 792 pixels: shares of 396, 264 and 132 pixels per workgroup, i.e. 3, 2
+    # and 1 blocks of 32 per wave plus a tail, for the balanced pointwise
+    # kernel (K = 80: a second, partial k tile)
+    ConvShape("var1x1_bal_c64", 2, 64, 80, 18, 22, 1, 1, "f32", 40),
+    ConvShape("var1x1_bal_c128", 2, 128, 64, 18, 22, 1, 1, "f32", 41),
+    ConvShape("var1x1_bal_c256", 2, 256, 80, 18, 22, 1, 1, "f32", 42),
+    ConvShape("var1x1_bal_c512", 2, 512, 64, 18, 22, 1, 1, "f32", 43),
 ]
 
 

@@ -38,7 +38,12 @@ def test_selected_plan_indexing(shape):
 def _variant_cases():
     cases = []
     for shape in VARIANT_SHAPES:
-        for v in sorted({p["variant"] for p in _plans_per_variant(shape.key())}):
+        plans = _plans_per_variant(shape.key())
+        if shape.name.startswith("var1x1_bal"):
+            # these shapes are there for the balanced pointwise family; the
+            # others are emulated on the shapes before
+            plans = [p for p in plans if B.conv_fwd_geometry(*shape.key(), p)["family"] == 7]
+        for v in sorted({p["variant"] for p in plans}):
             cases.append(pytest.param(shape, v, id=f"{shape.name}-v{v}"))
     return cases
 
