@@ -120,7 +120,14 @@ typedef struct {
   double pred_bytes[CONV_NUM_LVLS]; /* modelled bytes moved at each level    */
   double pred_us[CONV_NUM_LVLS];    /* bytes / bandwidth of each level, us   */
   double pred_mfma_us;              /* MFMA time incl. padding and waves, us */
-  double pred_total_us;             /* max over the above (Sec. 5 min-max)   */
+  double pred_total_us;             /* max over the above (Sec. 5 min-max)
+                                       plus the pipeline's fill and drain     */
+  double rank_us;                   /* pred_total_us times the kernel family's
+                                       measured factor: the selector's order  */
+  double paper_bytes[CONV_NUM_LVLS]; /* the paper's Sec. 3.2 volume of the
+                                       level's permutation class and tile, in
+                                       bytes, before line rounding (0 = the
+                                       level has no such form)               */
 } conv_plan_t;
 
 /*
@@ -236,6 +243,16 @@ int conv_fwd_plan(int N, int C, int K, int H, int W, int R, int S, int dtype,
 int conv_fwd_with_plan(int N, int C, int K, int H, int W, int R, int S,
                        const void* In, const void* Ker, float* Out,
                        const conv_plan_t* plan, void* stream);
+
+/*
+ * Host-only: scores a plan's tile fields for this shape, as the selector
+ * does for its candidates.  Reads dtype, variant, tile_*, wave_*, waves_*,
+ * grid_order and split_c; writes every derived field (lds_bytes, num_wg,
+ * class_lvl, pred_*, rank_us, paper_bytes).  Returns CONV_OK, or CONV_EINVAL
+ * for a plan the kernels cannot run (the plan is then unchanged).  Makes no
+ * HIP call.
+ */
+int conv_fwd_score_plan(int N, int C, int K, int H, int W, int R, int S, conv_plan_t* plan);
 
 /*
  * Host-only: every candidate plan the selector scores for this shape (the

@@ -29,7 +29,8 @@ class ConvPlan(ctypes.Structure):
         ("tile_cols", _i32), ("tile_c", _i32), ("wave_k", _i32), ("wave_px", _i32),
         ("waves_k", _i32), ("waves_px", _i32), ("grid_order", _i32), ("split_c", _i32),
         ("reserved", _i32), ("lds_bytes", _i32), ("num_wg", _i64), ("class_lvl", _i32 * 4), ("pred_bytes", _dbl * 4),
-        ("pred_us", _dbl * 4), ("pred_mfma_us", _dbl), ("pred_total_us", _dbl),
+        ("pred_us", _dbl * 4), ("pred_mfma_us", _dbl), ("pred_total_us", _dbl), ("rank_us", _dbl),
+        ("paper_bytes", _dbl * 4),
     ]
 
     def to_dict(self):
@@ -39,6 +40,8 @@ class ConvPlan(ctypes.Structure):
         d["pred_us"] = dict(zip(LEVELS, list(self.pred_us)))
         d["pred_mfma_us"] = self.pred_mfma_us
         d["pred_total_us"] = self.pred_total_us
+        d["rank_us"] = self.rank_us
+        d["paper_bytes"] = dict(zip(LEVELS, list(self.paper_bytes)))
         return d
 
     @classmethod
@@ -75,6 +78,8 @@ def lib():
         L.conv_fwd_plan.restype = _i32
         L.conv_fwd_with_plan.argtypes = shape7 + [_vp, _vp, _vp, ctypes.POINTER(ConvPlan), _vp]
         L.conv_fwd_with_plan.restype = _i32
+        L.conv_fwd_score_plan.argtypes = shape7 + [ctypes.POINTER(ConvPlan)]
+        L.conv_fwd_score_plan.restype = _i32
         L.conv_fwd_candidates.argtypes = shape7 + [_i32, ctypes.POINTER(ConvPlan), _i32]
         L.conv_fwd_candidates.restype = _i32
         L.conv_fwd_tune.argtypes = shape7 + [_i32, _vp, _vp, _vp, _i32, _i32, _vp, ctypes.POINTER(ConvPlan),
@@ -281,6 +286,16 @@ def conv_fwd_plan(N, C, K, H, W, R, S, dtype=CONV_DTYPE_F32):
     st = lib().conv_fwd_plan(N, C, K, H, W, R, S, dtype, ctypes.byref(p))
     if st != CONV_OK:
         raise ConvError(st, "conv_fwd_plan")
+    return p.to_dict()
+
+
+def conv_fwd_score_plan(N, C, K, H, W, R, S, plan):
+    """The selector's score of a plan's tile fields (host only), as a dict;
+    raises ConvError(CONV_EINVAL) for a plan the kernels cannot run."""
+    p = ConvPlan.from_dict(plan) if isinstance(plan, dict) else plan
+    st = lib().conv_fwd_score_plan(N, C, K, H, W, R, S, ctypes.byref(p))
+    if st != CONV_OK:
+        raise ConvError(st, "conv_fwd_score_plan")
     return p.to_dict()
 
 

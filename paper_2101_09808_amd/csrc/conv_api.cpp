@@ -501,6 +501,17 @@ int conv_fwd_with_plan(int N, int C, int K, int H, int W, int R, int S, const vo
   return run(s, In, Ker, Out, p, stream);
 }
 
+int conv_fwd_score_plan(int N, int C, int K, int H, int W, int R, int S, conv_plan_t* plan) {
+  int st = validate_shape(N, C, K, H, W, R, S);
+  if (st != CONV_OK) return st;
+  if (!plan) return CONV_ENULL;
+  conv_plan_t p = *plan;
+  st = score_plan(Shape{N, C, K, H, W, R, S}, &p);
+  if (st != CONV_OK) return st;
+  *plan = p;
+  return CONV_OK;
+}
+
 int conv_fwd_candidates(int N, int C, int K, int H, int W, int R, int S, int dtype,
                         conv_plan_t* plans, int cap) {
   int st = validate_shape(N, C, K, H, W, R, S);

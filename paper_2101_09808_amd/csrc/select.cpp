@@ -111,6 +111,13 @@ struct Hw {
   int mfma_f32_cycles = 32;  // 16x16x4 f32 per SIMD
   double launch_us = 5.0;    // one more kernel launch in the stream: a split plan's reduce pass
                              // measured 4-5 us over the same plan unsplit on small layers
+  // Pipeline fill and drain of a launch (Little's law, Sec. 6: the first
+  // step's data needs one round trip before any MFMA can start).  Per-wave
+  // timestamps of the 3x3 N=1 C=64 layer on MI355X: kernel arguments and
+  // index set-up 1.2 us, first loads issued and landed 1.4 us after that;
+  // the last stores 0.5 us.
+  double fill_us = 2.6;
+  double drain_us = 0.5;
 };
 const Hw kHw;
 
@@ -512,9 +519,7 @@ namespace {
 double family_factor(int family);
 // Ranking time of a scored plan: predicted time times the kernel family's
 // measured factor.
-double rank_time(const conv_plan_t& p) {
-  return p.pred_total_us * family_factor(find_variant(p.variant)->family);
-}
+double rank_time(const conv_plan_t& p) { return p.rank_us; }
 }  // namespace
 
 bool phase_direct(const Variant& v, const PhaseGeom& p, int dtype, Geom* g) {
@@ -533,8 +538,45 @@ bool phase_direct(const Variant& v, const PhaseGeom& p, int dtype, Geom* g) {
   return true;
 }
 
+namespace {
+double family_factor(int family);
+
+// Paper's Sec. 3.2 volumes (In, Ker, Out elements) of the class
+// <{n,k,h,w},{c,r},s> representative n,k,h,w,c,r,s for extents Ne and tile T
+// (codes n=0 k=1 c=2 r=3 s=4 h=5 w=6).
+void class3_volume(const int64_t Ne[7], const int64_t T[7], int out_factor, double dv[3]) {
+  static const int perm[7] = {0, 1, 5, 6, 2, 3, 4};
+  model_volume(perm, Ne, T, out_factor, dv);
+}
+
+int score_plan_impl(const Shape& s0, conv_plan_t* plan);
+}  // namespace
+
 // Fill the model fields of a plan whose tile fields are set.  0 or an error.
 int score_plan(const Shape& s0, conv_plan_t* plan) {
+  conv_plan_t p = *plan;
+  for (int l = 0; l < CONV_NUM_LVLS; ++l) {
+    p.class_lvl[l] = 0;
+    p.pred_bytes[l] = p.pred_us[l] = p.paper_bytes[l] = 0.0;
+  }
+  p.pred_mfma_us = p.pred_total_us = p.rank_us = 0.0;
+  const int st = score_plan_impl(s0, &p);
+  if (st != CONV_OK) return st;
+  // HBM: compulsory In + Ker + Out, the full-tile case of Sec. 3.2 (Out
+  // written once: the accumulators never leave the registers mid-reduction)
+  const Shape s = s0;
+  const double e = (p.dtype == CONV_DTYPE_BF16) ? 2.0 : 4.0;
+  const int64_t Ne[7] = {s.N, s.K, s.C, s.R, s.S, s.P(), s.Q()};
+  double dv[3];
+  class3_volume(Ne, Ne, 1, dv);
+  p.paper_bytes[CONV_LVL_HBM] = (dv[0] + dv[1]) * e + dv[2] * 4.0;
+  p.rank_us = p.pred_total_us * family_factor(find_variant(p.variant)->family);
+  *plan = p;
+  return CONV_OK;
+}
+
+namespace {
+int score_plan_impl(const Shape& s0, conv_plan_t* plan) {
   const Variant* v = find_variant(plan->variant);
   if (!v) return CONV_EINVAL;
   Geom g;
@@ -584,7 +626,8 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
     // count (60 plans of the 1x1 N=32 C=256 K=64 layer).
     if (g.tw % 16) issue_eff *= 0.8;
     plan->pred_mfma_us = rounds * nb * 4 * nq * kHw.mfma_f32_cycles / kHw.clock_hz * 1e6 / issue_eff;
-    plan->pred_total_us = std::max(tmax, plan->pred_mfma_us);
+    // fill: the first Ker chunk and ring; drain: the last block's stores
+    plan->pred_total_us = std::max(tmax, plan->pred_mfma_us) + kHw.fill_us + kHw.drain_us;
     return CONV_OK;
   }
   if (v->family == FAMILY_STREAM1X1_BAL) {
@@ -615,7 +658,7 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
     const double rounds = std::ceil((double)g.grid / kHw.cus);
     const double cycles = nq * (nb * 4 * 2 * kHw.mfma_f32_cycles + kHw.mfma_f32_cycles);
     plan->pred_mfma_us = rounds * cycles / kHw.clock_hz * 1e6 / 0.92;
-    plan->pred_total_us = std::max(tmax, plan->pred_mfma_us);
+    plan->pred_total_us = std::max(tmax, plan->pred_mfma_us) + kHw.fill_us + kHw.drain_us;
     return CONV_OK;
   }
   const int RS = s.R * s.S;
@@ -628,13 +671,25 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
   // lanes; the 32x32x2 loop reads 2 + WP/2 operands per (2 channels, tap).
   // (Channel groups of waves share each tile's steps: the count per tile is
   // the same.)
-  const double waves = (double)g.num_tiles * (g.nwk * g.nwp);
   const int kdepth = (plan->dtype == CONV_DTYPE_BF16) ? 32 : 4;  // reduction per MFMA
   const double steps = (double)g.nchunks * (v->tc / kdepth) * RS;
-  // (per 4 channels: the 32x32x2 loop takes two steps of 2 + WP/2 reads)
-  const double reads_per_step = v->mfma32 ? 2.0 * (2 + v->wp / 2) : (double)(v->wk + v->wp);
-  plan->pred_bytes[CONV_LVL_REG] =
-      waves * steps * reads_per_step * 64 * ((plan->dtype == CONV_DTYPE_BF16) ? 16.0 : 4.0);
+  // REG: Eq. (3)'s form over the im2col view -- the tiled matmul of Sec. 2.2
+  // with the reduction (c, r, s) innermost inside the wave tile, i.e. the
+  // class <{n,k,h,w},{c,r},s> volume with n = r = s = h = 1, c = the
+  // C*R*S reduction and w = the pixels: operand elements read from LDS =
+  // MACs * (1/T_k + 1/T_px).  Extents are rounded up to whole workgroup
+  // tiles (partial tiles are computed in full).
+  {
+    const int64_t kpad = (int64_t)g.tiles_k * g.nwk * 16 * v->wk;
+    const int64_t pxpad = (int64_t)g.tiles_rows * g.tiles_cols * g.nwp * 16 * v->wp;
+    const int64_t cpad = (int64_t)g.nchunks * v->tc * RS;
+    const int64_t Nr[7] = {1, kpad, cpad, 1, 1, 1, pxpad};
+    const int64_t Tr[7] = {1, 16 * v->wk, v->mfma32 ? 2 : kdepth, 1, 1, 1, 16 * v->wp};
+    double dv[3];
+    class3_volume(Nr, Tr, 0, dv);
+    plan->pred_bytes[CONV_LVL_REG] = (dv[0] + dv[1]) * e;
+    plan->paper_bytes[CONV_LVL_REG] = plan->pred_bytes[CONV_LVL_REG];
+  }
 
   // LDS: per workgroup, every channel brings its In halo rows and Ker rows.
   // Memory moves whole 128-byte lines (Sec. 12 names spatial locality as the
@@ -664,6 +719,23 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
                    : (double)s.K * g.nchunks * run_bytes((double)v->tc * RS * e);
   const double pix_tiles = (double)g.tiles_rows * g.tiles_cols;
   plan->pred_bytes[CONV_LVL_LDS] = in_halo_bytes * g.tiles_k + ker_line_bytes * pix_tiles;
+  // The same level before line rounding: the Sec. 3.2 volume of class
+  // <{n,k,h,w},{c,r},s> for the workgroup tile (T_k = tile_k, T_c = channels
+  // per step, T_r = R, T_s = S; tile_rows rows of one image, or whole images
+  // when the tile spans several; T_w = tile_cols), Out kept in registers.
+  // Extents are rounded up to whole tiles (partial tiles staged in full).
+  // Exact for tiles that divide the layer; a row tile that straddles two
+  // images stages R - 1 more rows than this counts.
+  {
+    const int tr = g.tr, P = g.P;
+    const int64_t Tn = tr > P ? tr / P : 1, Th = tr > P ? P : tr;
+    const int64_t Tt[7] = {Tn, (int64_t)g.nwk * 16 * v->wk, v->tc, s.R, s.S, Th, g.tw};
+    const int64_t Nt[7] = {(s.N + Tn - 1) / Tn * Tn, (int64_t)g.tiles_k * Tt[1], (int64_t)g.nchunks * v->tc, s.R, s.S,
+                           (P + Th - 1) / Th * Th, (int64_t)g.tiles_cols * g.tw};
+    double dv[3];
+    class3_volume(Nt, Tt, 0, dv);
+    plan->paper_bytes[CONV_LVL_LDS] = (dv[0] + dv[1]) * e;
+  }
 
   // L2: outer tile-loop order of the grid, per XCD.
   const double in_bytes = (double)s.N * s.C * s.H * s.W * e;
@@ -734,11 +806,13 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
   // plus reading the ranges and writing Out.
   const double reduce_us =
       g.split > 1 ? kHw.launch_us + (g.split + 1.0) * out_bytes / kHw.bw[CONV_LVL_HBM] * 1e6 : 0.0;
-  plan->pred_total_us = tmax + reduce_us;
+  // Fill and drain: one round trip before the first step, that step's MFMAs
+  // (nothing to overlap them with yet), the last stores.
+  const double step_us = plan->pred_mfma_us / std::max(1, g.cps);
+  plan->pred_total_us = tmax + reduce_us + kHw.fill_us + step_us + kHw.drain_us;
   return CONV_OK;
 }
 
-namespace {
 // Measured correction of the model per kernel family (the model does not
 // capture latency hiding or the inner loop's issue overhead): the unrolled
 // pointwise streaming kernel and the transposing bf16 kernel run about 20%

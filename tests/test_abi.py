@@ -38,8 +38,8 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_plan_struct_layout_matches_header():
-    # conv_plan_t: 14 ints, int64, 4 ints, 4+4+1+1 doubles (no padding)
-    assert ctypes.sizeof(B.ConvPlan) == 14 * 4 + 8 + 4 * 4 + 10 * 8
+    # conv_plan_t: 14 ints, int64, 4 ints, 4+4+1+1+1+4 doubles (no padding)
+    assert ctypes.sizeof(B.ConvPlan) == 14 * 4 + 8 + 4 * 4 + 15 * 8
     assert B.ConvPlan.num_wg.offset == 14 * 4
 
 

@@ -82,11 +82,10 @@ def test_plan_invariants(shape):
     assert plan["pred_bytes"]["hbm"] >= compulsory * (1 - 1e-12)
     # each level moves at least the bytes it must deliver once
     assert plan["pred_bytes"]["lds"] >= (N * C * H * W + K * C * R * S) * e * (1 - 1e-12) or R * S == 1
+    # the slowest level (Sec. 5 min-max) plus the pipeline's fill and drain
+    # (and a split plan's second pass)
     slowest = max(list(plan["pred_us"].values()) + [plan["pred_mfma_us"]])
-    if plan["split_c"] > 1:  # plus the second pass that adds the channel ranges
-        assert plan["pred_total_us"] > slowest
-    else:
-        assert plan["pred_total_us"] == slowest
+    assert plan["pred_total_us"] > slowest
     # deterministic and cached
     assert B.conv_fwd_plan(*dims, dtype=dtype) == plan
     cands = B.conv_fwd_candidates(*dims, dtype=dtype)
@@ -97,20 +96,8 @@ def test_plan_invariants(shape):
     factor = {4: 0.8, 6: 0.8, 7: 0.8, 2: 1.0, 3: 1.0, 5: 1.1, 1: 2.0}
     fam = [B.conv_fwd_geometry(*dims, c)["family"] for c in cands]
     eff = [c["pred_total_us"] * factor[f] for c, f in zip(cands, fam)]
+    assert all(c["rank_us"] == pytest.approx(x, rel=1e-12) for c, x in zip(cands, eff))
     assert all(x <= y * (1 + 1e-12) for x, y in zip(eff, eff[1:]))
-
-
-def test_selector_is_minimum_of_its_objective():
-    """The chosen plan has the smallest predicted max-level time of all the
-    candidates of its kernel family (the min-max of Sec. 5; across families
-    the measured family factor applies)."""
-    for c in CONFIGS:
-        if c.dtype != "f32":
-            continue
-        cands = B.conv_fwd_candidates(*c.key())
-        fam0 = B.conv_fwd_geometry(*c.key(), cands[0])["family"]
-        same = [x for x in cands if B.conv_fwd_geometry(*c.key(), x)["family"] == fam0]
-        assert cands[0]["pred_total_us"] == min(x["pred_total_us"] for x in same)
 
 
 def test_enumeration_rules_for_channel_groups_and_narrow_steps():
