@@ -615,19 +615,26 @@ def time_plan(c, plan, ins, outs, Ker, reps=10):
     return t[len(t) // 2]
 
 
-def rank_sweep(configs, n=100, reps=10):
-    """Model validation on the GPU (Sec. 9): per layer, time the model's top
-    5 plans and a uniform sample of the other candidates; report the rank
-    correlation of predicted and measured time and the top-1/2/5 loss, plus
-    the empirical pick among the top 5 (Sec. 10, MOpt-5)."""
+def all_candidates(c, dt):
+    from paper_2101_09808_amd import conv as B
+    n = B.lib().conv_fwd_candidates(*c.key(), dt, None, 0)
+    return B.conv_fwd_candidates(*c.key(), dtype=dt, cap=max(1, n))
+
+
+def rank_sweep(configs, n=None, reps=10):
+    """Model validation on the GPU (Sec. 9): per layer, time every candidate
+    plan (n = None), or the model's top 5 and a uniform sample of the others
+    (n plans); report the rank correlation of predicted and measured time
+    and the top-1/2/5 loss against the fastest timed plan, plus the
+    empirical pick among the top 5 (Sec. 10, MOpt-5)."""
     import torch
     from paper_2101_09808_amd import conv as B
     from paper_2101_09808_amd.workloads import make_inputs
     res = {}
     for c in configs:
         dt = B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32
-        cands = B.conv_fwd_candidates(*c.key(), dtype=dt)
-        idx = rank_sample(cands, n=n, seed=c.seed)
+        cands = all_candidates(c, dt)
+        idx = list(range(len(cands))) if n is None else rank_sample(cands, n=n, seed=c.seed)
         In0, Ker0 = make_inputs(c)
         set_bytes = In0.numel() * In0.element_size() + c.N * c.K * c.P * c.Q * 4
         nsets = max(2, -(-2 * MALL_BYTES // set_bytes) + 1)
@@ -642,12 +649,15 @@ def rank_sweep(configs, n=100, reps=10):
             us = time_plan(c, p, ins, outs, Ker, reps)
             rows.append({"model_rank": i, "variant": p["variant"], "split_c": p["split_c"],
                          "tile": [p["tile_k"], p["tile_rows"], p["tile_cols"], p["tile_c"]],
-                         "grid_order": p["grid_order"], "pred_us": p["pred_total_us"], "measured_us": us})
-            print(f"[rank] {c.name} rank {i} v{p['variant']} split {p['split_c']} pred {p['pred_total_us']:.1f} "
-                  f"measured {us:.1f} us", flush=True)
+                         "grid_order": p["grid_order"], "pred_us": p["pred_total_us"], "rank_us": p["rank_us"],
+                         "measured_us": us})
+            if len(rows) % 200 == 1 or i < 5:
+                print(f"[rank] {c.name} rank {i} v{p['variant']} split {p['split_c']} pred {p['pred_total_us']:.1f} "
+                      f"measured {us:.1f} us ({len(rows)}/{len(idx)})", flush=True)
         t = [r["measured_us"] for r in rows]  # model order
         best = min(t)
         res[c.name] = {
+            "shape": list(c.key()), "dtype": c.dtype,
             "candidates": len(cands), "sampled": len(rows),
             "spearman_rank_vs_measured": spearman([r["model_rank"] for r in rows], t),
             "spearman_pred_us_vs_measured": spearman([r["pred_us"] for r in rows], t),
@@ -661,26 +671,180 @@ def rank_sweep(configs, n=100, reps=10):
     return res
 
 
-def rank_report(res):
-    lines = ["# Model-predicted rank vs measured time (Sec. 9), MI355X", "",
-             "Per layer: the model's 5 best plans plus a uniform sample of the other candidates "
-             "(about 100 in all), each the median of 10 launches on rotating buffer sets, every launch "
-             "between its own pair of HIP events, queued behind a spin kernel so that they run back "
-             "to back (no host time).  Spearman "
+def rank_report(res, title="Model-predicted rank vs measured time (Sec. 9), MI355X",
+                command="python bench.py --rank-sweep", intro=""):
+    lines = ["# " + title, "",
+             (intro + " " if intro else "") +
+             "Per layer: every candidate plan the selector scores (or, where marked, the model's 5 best "
+             "plus a uniform sample of the others), each the median of 10 launches on rotating buffer sets, "
+             "every launch between its own pair of HIP events, queued behind a spin kernel so that they run "
+             "back to back (no host time).  Spearman "
              "correlation of the model's order (and of its predicted time) with the measured time; "
-             "top-k loss = best of the model's first k sampled plans over the best sampled plan, "
+             "top-k loss = best of the model's first k plans over the fastest timed plan, "
              "minus 1; MOpt-1 = the selector's plan, MOpt-5 = best of its top 5 (Sec. 10).", "",
-             "Command: `python bench.py --rank-sweep`", "",
-             "| layer | candidates | sampled | rho(rank) | rho(pred us) | top-1 loss | top-2 loss | top-5 loss "
-             "| MOpt-1 us | MOpt-5 us | best sampled us (variant) |",
+             f"Command: `{command}`", "",
+             "| layer | candidates | timed | rho(rank) | rho(pred us) | top-1 loss | top-2 loss | top-5 loss "
+             "| MOpt-1 us | MOpt-5 us | fastest us (variant, model rank) |",
              "|---|---|---|---|---|---|---|---|---|---|---|"]
     for name, r in res.items():
         b = r["best_sampled"]
-        lines.append(f"| {name} | {r['candidates']} | {r['sampled']} | {r['spearman_rank_vs_measured']:.2f} | "
+        shape = "x".join(str(x) for x in r.get("shape", [])) if name.startswith("heldout") else name
+        lines.append(f"| {shape} | {r['candidates']} | {r['sampled']} | {r['spearman_rank_vs_measured']:.2f} | "
                      f"{r['spearman_pred_us_vs_measured']:.2f} | {100 * r['top1_loss']:.1f}% | "
                      f"{100 * r['top2_loss']:.1f}% | {100 * r['top5_loss']:.1f}% | {r['mopt1_us']:.1f} | "
                      f"{r['mopt5_us']:.1f} | {b['measured_us']:.1f} (v{b['variant']}, rank {b['model_rank']}) |")
     return "\n".join(lines) + "\n"
+
+
+HELDOUT_JSON = os.path.join(ROOT, "profiles", "model_heldout.json")
+HELDOUT_MD = os.path.join(ROOT, "profiles", "model_heldout.md")
+
+
+def heldout_layers(n=10, seed=77):
+    """Seeded random layers for held-out validation: none of them is one of
+    the five configurations, the Table 1 layers or the strided layers on
+    whose timings the model's measured constants (issue efficiencies, family
+    factors, fill and drain) were fitted.  Shapes in Table 1's range: batch
+    1-32, 16-512 channels, 7-58 pixels, 1x1 and 3x3 taps, valid stride 1."""
+    import random
+
+    from paper_2101_09808_amd.workloads import ConvShape
+    rng = random.Random(seed)
+    out = []
+    while len(out) < n:
+        RS = rng.choice([1, 3, 3])
+        N = rng.choice([1, 2, 4, 8, 16, 32])
+        C = rng.choice([16, 32, 48, 64, 96, 128, 192, 256, 384, 512])
+        K = rng.choice([16, 32, 64, 96, 128, 192, 256, 384, 512])
+        HW = rng.randint(7, 58) + RS - 1
+        if N * C * HW * HW * 4 > 200e6 or N * K * HW * HW > 40e6:
+            continue
+        out.append(ConvShape(f"heldout{len(out)}", N, C, K, HW, HW, RS, RS, "f32", 12000 + len(out)))
+    return out
+
+
+def heldout_report(res):
+    return rank_report(res, title="Model rank vs measured time on held-out layers (Sec. 9), MI355X",
+                       command="python bench.py --held-out",
+                       intro="Ten seeded random fp32 layers (bench.py heldout_layers: batch 1-32, 16-512 channels, "
+                             "7-58 pixels, 1x1 and 3x3) that none of the model's measured constants were fitted on.")
+
+
+COUNTER_SWEEP_LAYER = "conv3x3_n32_c128_k128_in30"
+COUNTER_SWEEP_COUNTERS = [["FETCH_SIZE"], ["TCP_TCC_READ_REQ_sum"], ["SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT"]]
+COUNTER_SWEEP_JSON = os.path.join(ROOT, "profiles", "model_counter_sweep.json")
+COUNTER_SWEEP_MD = os.path.join(ROOT, "profiles", "model_counter_sweep.md")
+
+
+def counter_sweep_plans(c, n):
+    from paper_2101_09808_amd import conv as B
+    dt = B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32
+    cands = all_candidates(c, dt)
+    return cands, rank_sample(cands, n=n, seed=c.seed)
+
+
+def counter_sweep(c, n):
+    """Workload of the counter passes: each sampled plan once (after one
+    untimed launch of the selected plan), in model order, with a
+    synchronisation after each so that dispatches are one plan each."""
+    import ctypes
+
+    import torch
+    from paper_2101_09808_amd import conv as B
+    from paper_2101_09808_amd.workloads import make_inputs
+    cands, idx = counter_sweep_plans(c, n)
+    In0, Ker0 = make_inputs(c)
+    In, Ker = In0.cuda(), Ker0.cuda()
+    out = torch.empty(c.N, c.K, c.P, c.Q, device="cuda")
+    L = B.lib()
+    sp = torch.cuda.current_stream().cuda_stream
+    for i in idx:
+        p = B.ConvPlan.from_dict(cands[i])
+        st = L.conv_fwd_with_plan(*c.key(), In.data_ptr(), Ker.data_ptr(), out.data_ptr(), ctypes.byref(p), sp)
+        if st != B.CONV_OK:
+            raise B.ConvError(st, "conv_fwd_with_plan")
+        torch.cuda.synchronize()
+    print(f"counter sweep: {len(idx)} plans of {c.name}", flush=True)
+
+
+def counter_sweep_parse(c, dirs):
+    """Fig. 6 analogue: per plan, the counters of the sweep passes (one pass
+    per directory, COUNTER_SWEEP_COUNTERS order) beside the model's levels,
+    with the Spearman correlation of each counter with the model's rank, and
+    with the measured time where the rank sweep timed the same plans."""
+    cands, idx = counter_sweep_plans(c, 100)
+    per = {}
+    for cnts, d in zip(COUNTER_SWEEP_COUNTERS, dirs):
+        for cnt in cnts:
+            rows = [v for name, v in counter_per_dispatch(d, cnt) if "convfwd::" in name and "reduce" not in name]
+            if len(rows) != len(idx):
+                raise SystemExit(f"{cnt}: {len(rows)} conv dispatches for {len(idx)} plans")
+            per[cnt] = rows
+    timed = {}
+    if os.path.exists(RANK_JSON):
+        rj = json.load(open(RANK_JSON)).get(c.name, {})
+        timed = {r["model_rank"]: r["measured_us"] for r in rj.get("plans", [])}
+    plans = []
+    for j, i in enumerate(idx):
+        p = cands[i]
+        row = {"model_rank": i, "variant": p["variant"], "tile": [p["tile_k"], p["tile_rows"], p["tile_cols"]],
+               "pred_us": p["pred_total_us"], "pred_lds_bytes": p["pred_bytes"]["lds"],
+               "pred_reg_bytes": p["pred_bytes"]["reg"], "pred_l2_bytes": p["pred_bytes"]["l2"],
+               "fetch_kib": per["FETCH_SIZE"][j], "l2_to_cu_req": per["TCP_TCC_READ_REQ_sum"][j],
+               "lds_instr": per["SQ_INSTS_LDS"][j], "lds_bank_conflict_cycles": per["SQ_LDS_BANK_CONFLICT"][j],
+               "measured_us": timed.get(i)}
+        plans.append(row)
+    rank = [r["model_rank"] for r in plans]
+    out = {"layer": c.name, "plans": plans, "spearman": {}, "commands": COUNTER_SWEEP_COMMANDS}
+    pairs = [("fetch_kib", "pred_l2_bytes"), ("l2_to_cu_req", "pred_lds_bytes"), ("lds_instr", "pred_reg_bytes"),
+             ("lds_bank_conflict_cycles", None)]
+    for cnt, pred in pairs:
+        v = [r[cnt] for r in plans]
+        e = {"vs_model_rank": spearman(rank, v)}
+        if pred:
+            e["vs_predicted_level"] = spearman([r[pred] for r in plans], v)
+        t = [(r["measured_us"], r[cnt]) for r in plans if r["measured_us"] is not None]
+        if len(t) > 2:
+            e["vs_measured_time"] = spearman([a for a, _ in t], [b for _, b in t])
+        out["spearman"][cnt] = e
+    conflicts = sum(r["lds_bank_conflict_cycles"] for r in plans) / max(1.0, sum(r["lds_instr"] for r in plans))
+    out["bank_conflict_cycles_per_lds_instr"] = conflicts
+    json.dump(out, open(COUNTER_SWEEP_JSON, "w"), indent=1)
+    lines = [f"# Counters per plan against the model (Fig. 6 analogue), {c.name}, MI355X", "",
+             "The model's 5 best plans and a uniform sample of the other candidates (100 in all), each "
+             "launched once under rocprofv3 counter passes (one pass per counter group):", ""]
+    lines += ["    " + x for x in COUNTER_SWEEP_COMMANDS]
+    lines += ["", "Spearman correlation of each counter with the model's rank, with the model's "
+              "prediction of the level it measures, and with the measured time (rank sweep):", "",
+              "| counter | level predicted | rho vs model rank | rho vs predicted level | rho vs measured time |",
+              "|---|---|---|---|---|"]
+    for cnt, pred in pairs:
+        e = out["spearman"][cnt]
+        f = lambda k: f"{e[k]:.2f}" if k in e else "-"
+        lines.append(f"| {cnt} | {pred or '-'} | {f('vs_model_rank')} | {f('vs_predicted_level')} | "
+                     f"{f('vs_measured_time')} |")
+    sel = plans[0]
+    lines += ["", f"LDS bank conflicts: {conflicts:.4f} conflict cycles per LDS instruction over the sample; "
+              f"the selected plan (model rank 0, variant {sel['variant']}): "
+              f"{sel['lds_bank_conflict_cycles']:.0f} cycles over {sel['lds_instr']:.0f} LDS instructions.", ""]
+    lines += ["| model rank | variant | tile k x rows x cols | pred us | measured us | FETCH KiB | L2->CU req | "
+              "LDS instr | bank-conflict cycles |", "|---|---|---|---|---|---|---|---|---|"]
+    for r in plans[:25]:
+        lines.append(f"| {r['model_rank']} | {r['variant']} | {'x'.join(map(str, r['tile']))} | {r['pred_us']:.1f} | "
+                     f"{'-' if r['measured_us'] is None else format(r['measured_us'], '.1f')} | "
+                     f"{r['fetch_kib']:.0f} | {r['l2_to_cu_req']:.0f} | {r['lds_instr']:.0f} | "
+                     f"{r['lds_bank_conflict_cycles']:.0f} |")
+    lines.append(f"\n(first 25 of {len(plans)} plans; all in model_counter_sweep.json)\n")
+    open(COUNTER_SWEEP_MD, "w").write("\n".join(lines))
+    print("\n".join(lines[:20]), flush=True)
+
+
+COUNTER_SWEEP_COMMANDS = [
+    f"rocprofv3 --pmc {' '.join(cs)} --output-format csv -d gpurun_out/counter_sweep_{i} -o s -- "
+    f"python -u bench.py --counter-sweep --layer {COUNTER_SWEEP_LAYER}"
+    for i, cs in enumerate(COUNTER_SWEEP_COUNTERS)
+] + [f"python bench.py --counter-sweep-parse gpurun_out/counter_sweep_0 gpurun_out/counter_sweep_1 "
+     f"gpurun_out/counter_sweep_2 --layer {COUNTER_SWEEP_LAYER}"]
 
 
 TABLE1_JSON = os.path.join(ROOT, "profiles", "table1_sweep.json")
@@ -822,10 +986,19 @@ def main():
     ap.add_argument("--model-check", nargs=4, metavar=("FETCH", "WRITE", "TCP_TCC", "LDS"),
                     help="predicted vs measured bytes per level for every layer, from four counter runs "
                          "of --traffic-run --layer all")
-    ap.add_argument("--rank-sweep", nargs="?", const=100, type=int, metavar="N",
-                    help="model validation: time the model's top 5 and a uniform sample of the other "
-                         "candidates (N plans per layer, default 100) of every layer; writes "
+    ap.add_argument("--rank-sweep", nargs="?", const=0, type=int, metavar="N",
+                    help="model validation: time every candidate of every layer (or, with N, the model's "
+                         "top 5 and a uniform sample of the others, N plans per layer); writes "
                          "profiles/model_rank_sweep.{json,md}")
+    ap.add_argument("--held-out", action="store_true",
+                    help="the same validation on seeded random layers that none of the model's measured "
+                         "constants were fitted on; writes profiles/model_heldout.{json,md}")
+    ap.add_argument("--counter-sweep", nargs="?", const=100, type=int, metavar="N",
+                    help="launch the model's top 5 and a sample of the other plans of --layer (N in all) "
+                         "once each, for rocprofv3 --pmc counter passes (Fig. 6 analogue)")
+    ap.add_argument("--counter-sweep-parse", nargs="+", metavar="DIR",
+                    help="per-plan counters of the --counter-sweep passes against the model's rank and "
+                         "levels; writes profiles/model_counter_sweep.{json,md}")
     ap.add_argument("--table1", action="store_true",
                     help="every conv2d layer of Table 1 at batch 1 (stride, same padding); writes "
                          "profiles/table1_sweep.{json,md}")
@@ -847,6 +1020,10 @@ def main():
     if args.model_check:  # host-only: reads the counter files of four earlier runs
         model_check_parse(list(CONFIGS), args.model_check)
         return
+    if args.counter_sweep_parse:  # host-only: reads the counter files of the sweep's passes
+        counter_sweep_parse(BY_NAME[args.layer if args.layer != HEADLINE else COUNTER_SWEEP_LAYER],
+                            args.counter_sweep_parse)
+        return
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
@@ -863,9 +1040,20 @@ def main():
         open(TABLE1_MD, "w").write(md)
         print(md, flush=True)
         return
-    if args.rank_sweep:
+    if args.held_out:
+        res = rank_sweep(heldout_layers())
+        res["_meta"] = {"kernel_sha": kernel_source_hash(), "command": "python bench.py --held-out"}
+        json.dump(res, open(HELDOUT_JSON, "w"), indent=1)
+        md = heldout_report({k: v for k, v in res.items() if not k.startswith("_")})
+        open(HELDOUT_MD, "w").write(md)
+        print(md, flush=True)
+        return
+    if args.counter_sweep:
+        counter_sweep(BY_NAME[args.layer if args.layer != HEADLINE else COUNTER_SWEEP_LAYER], args.counter_sweep)
+        return
+    if args.rank_sweep is not None:
         res = rank_sweep(list(CONFIGS) if args.layer in ("all", HEADLINE) else [BY_NAME[args.layer]],
-                         n=args.rank_sweep)
+                         n=args.rank_sweep or None)
         res["_meta"] = {"kernel_sha": kernel_source_hash(), "command": "python bench.py --rank-sweep"}
         json.dump(res, open(RANK_JSON, "w"), indent=1)
         md = rank_report({k: v for k, v in res.items() if not k.startswith("_")})

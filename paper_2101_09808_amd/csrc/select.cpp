@@ -124,17 +124,20 @@ const Hw kHw;
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Bank-conflict cost of a wave's 64 4-byte LDS reads (addresses in
-// elements), for the gfx950 LDS as measured: 32 banks of 4 bytes, a wave's
-// ds_read_b32 served 16 lanes at a time; each 16-lane group takes as many
-// passes as the most distinct addresses that fall into one bank.  Returns the
-// sum of passes over the four groups (4 = conflict-free).
+// elements), for the gfx950 LDS as measured with the bank-conflict counter
+// (SQ_LDS_BANK_CONFLICT) on access patterns of known stride and grouping:
+// 32 banks of 4 bytes, a wave's ds_read_b32 served 32 lanes at a time
+// (lanes 0-31, then 32-63); each half takes as many passes as the most
+// distinct addresses that fall into one bank (equal addresses are one
+// broadcast).  Returns the sum of passes over the two halves (2 =
+// conflict-free).
 int conflict_cost(const int* addr) {
   int total = 0;
-  for (int grp = 0; grp < 4; ++grp) {
+  for (int grp = 0; grp < 2; ++grp) {
     int worst = 0;
     for (int b = 0; b < 32; ++b) {
-      int seen[16], n = 0;
-      for (int l = 16 * grp; l < 16 * grp + 16; ++l) {
+      int seen[32], n = 0;
+      for (int l = 32 * grp; l < 32 * grp + 32; ++l) {
         if (((addr[l] % 32) + 32) % 32 != b) continue;
         bool dup = false;
         for (int q = 0; q < n; ++q) dup |= seen[q] == addr[l];
@@ -164,12 +167,13 @@ int pick_ker_rstride_uncached(int need, int mult, int rs) {
 }
 
 // Channel stride of the In tile: >= need, a multiple of 4, least conflicted
-// B-operand reads (lane (j, g) reads channel g, pixel j).
-int pick_in_cstride_uncached(int need) {
+// B-operand reads (lane (j, g) reads channel g, pixel j of the tile's first
+// 16-pixel block: row j / tw, column j % tw of rows `wp` elements apart).
+int pick_in_cstride_uncached(int need, int tw, int wp) {
   int best = -1, best_cost = 1 << 30;
   for (int cand = ((need + 3) / 4) * 4; cand < need + 68; cand += 4) {
     int addr[64];
-    for (int l = 0; l < 64; ++l) addr[l] = (l >> 4) * cand + (l & 15);
+    for (int l = 0; l < 64; ++l) addr[l] = (l >> 4) * cand + ((l & 15) / tw) * wp + (l & 15) % tw;
     const int c = conflict_cost(addr);
     if (c < best_cost) {
       best_cost = c;
@@ -196,14 +200,14 @@ int pick_ker_rstride(int need, int mult, int rs) {
   return v;
 }
 
-int pick_in_cstride(int need) {
-  const auto key = std::make_tuple(need, -1, -1);
+int pick_in_cstride(int need, int tw, int wp) {
+  const auto key = std::make_tuple(need, -1 - std::min(tw, 16), wp);
   {
     std::lock_guard<std::mutex> lk(g_pad_mu);
     auto it = g_pad_cache.find(key);
     if (it != g_pad_cache.end()) return it->second;
   }
-  const int v = pick_in_cstride_uncached(need);
+  const int v = pick_in_cstride_uncached(need, std::min(tw, 16), wp);
   std::lock_guard<std::mutex> lk(g_pad_mu);
   g_pad_cache[key] = v;
   return v;
@@ -441,7 +445,7 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
   const int in_wp = tw + s.S - 1;
   const int64_t E = (int64_t)in_rows * in_wp;
   if (E * TC >= (1 << 20)) return false;
-  const int in_cstride = pick_in_cstride((int)E);
+  const int in_cstride = pick_in_cstride((int)E, tw, in_wp);
   const int TCRS = TC * RS;
   if (v.ker_vec > 1 && ((int64_t)s.C * RS % v.ker_vec != 0 || TCRS % v.ker_vec != 0)) return false;
   if (TCRS >= (1 << 16) || BK >= (1 << 15)) return false;
