@@ -698,14 +698,17 @@ def rank_report(res, title="Model-predicted rank vs measured time (Sec. 9), MI35
 
 HELDOUT_JSON = os.path.join(ROOT, "profiles", "model_heldout.json")
 HELDOUT_MD = os.path.join(ROOT, "profiles", "model_heldout.md")
+TRAIN_JSON = os.path.join(ROOT, "profiles", "model_train_sweep.json")
+TRAIN_MD = os.path.join(ROOT, "profiles", "model_train_sweep.md")
+HELDOUT_SEED, TRAIN_SEED = 78, 77
 
 
-def heldout_layers(n=10, seed=77):
-    """Seeded random layers for held-out validation: none of them is one of
-    the five configurations, the Table 1 layers or the strided layers on
-    whose timings the model's measured constants (issue efficiencies, family
-    factors, fill and drain) were fitted.  Shapes in Table 1's range: batch
-    1-32, 16-512 channels, 7-58 pixels, 1x1 and 3x3 taps, valid stride 1."""
+def heldout_layers(n=10, seed=HELDOUT_SEED):
+    """Seeded random layers.  Seed 77 (the training set) joins the five
+    configurations in the per-variant calibration of the selector; seed 78
+    (the held-out set) is used for validation only.  Shapes in Table 1's
+    range: batch 1-32, 16-512 channels, 7-58 pixels, 1x1 and 3x3 taps, valid
+    stride 1."""
     import random
 
     from paper_2101_09808_amd.workloads import ConvShape
@@ -719,15 +722,23 @@ def heldout_layers(n=10, seed=77):
         HW = rng.randint(7, 58) + RS - 1
         if N * C * HW * HW * 4 > 200e6 or N * K * HW * HW > 40e6:
             continue
-        out.append(ConvShape(f"heldout{len(out)}", N, C, K, HW, HW, RS, RS, "f32", 12000 + len(out)))
+        out.append(ConvShape(f"heldout{len(out)}" if seed == HELDOUT_SEED else f"train{len(out)}", N, C, K, HW, HW,
+                             RS, RS, "f32", 12000 + 100 * (seed - TRAIN_SEED) + len(out)))
     return out
 
 
-def heldout_report(res):
+def heldout_report(res, train=False):
+    if train:
+        return rank_report(res, title="Model rank vs measured time on the calibration layers (Sec. 9), MI355X",
+                           command="python bench.py --train-sweep",
+                           intro="Ten seeded random fp32 layers (bench.py heldout_layers, seed 77: batch 1-32, 16-512 "
+                                 "channels, 7-58 pixels, 1x1 and 3x3) that, with the five configurations, set the "
+                                 "selector's per-variant calibration (paper_2101_09808_amd/calibrate.py).")
     return rank_report(res, title="Model rank vs measured time on held-out layers (Sec. 9), MI355X",
                        command="python bench.py --held-out",
-                       intro="Ten seeded random fp32 layers (bench.py heldout_layers: batch 1-32, 16-512 channels, "
-                             "7-58 pixels, 1x1 and 3x3) that none of the model's measured constants were fitted on.")
+                       intro="Ten seeded random fp32 layers (bench.py heldout_layers, seed 78: batch 1-32, 16-512 "
+                             "channels, 7-58 pixels, 1x1 and 3x3) that none of the model's measured constants "
+                             "(calibration included) were fitted on.")
 
 
 COUNTER_SWEEP_LAYER = "conv3x3_n32_c128_k128_in30"
@@ -993,6 +1004,9 @@ def main():
     ap.add_argument("--held-out", action="store_true",
                     help="the same validation on seeded random layers that none of the model's measured "
                          "constants were fitted on; writes profiles/model_heldout.{json,md}")
+    ap.add_argument("--train-sweep", action="store_true",
+                    help="the same sweep on the seeded random layers that join the five configurations in the "
+                         "selector's calibration; writes profiles/model_train_sweep.{json,md}")
     ap.add_argument("--counter-sweep", nargs="?", const=100, type=int, metavar="N",
                     help="launch the model's top 5 and a sample of the other plans of --layer (N in all) "
                          "once each, for rocprofv3 --pmc counter passes (Fig. 6 analogue)")
@@ -1040,12 +1054,14 @@ def main():
         open(TABLE1_MD, "w").write(md)
         print(md, flush=True)
         return
-    if args.held_out:
-        res = rank_sweep(heldout_layers())
-        res["_meta"] = {"kernel_sha": kernel_source_hash(), "command": "python bench.py --held-out"}
-        json.dump(res, open(HELDOUT_JSON, "w"), indent=1)
-        md = heldout_report({k: v for k, v in res.items() if not k.startswith("_")})
-        open(HELDOUT_MD, "w").write(md)
+    if args.held_out or args.train_sweep:
+        train = bool(args.train_sweep)
+        res = rank_sweep(heldout_layers(seed=TRAIN_SEED if train else HELDOUT_SEED))
+        res["_meta"] = {"kernel_sha": kernel_source_hash(),
+                        "command": "python bench.py " + ("--train-sweep" if train else "--held-out")}
+        json.dump(res, open(TRAIN_JSON if train else HELDOUT_JSON, "w"), indent=1)
+        md = heldout_report({k: v for k, v in res.items() if not k.startswith("_")}, train=train)
+        open(TRAIN_MD if train else HELDOUT_MD, "w").write(md)
         print(md, flush=True)
         return
     if args.counter_sweep:

@@ -520,8 +520,7 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
 }
 
 namespace {
-double family_factor(int family);
-// Ranking time of a scored plan: predicted time times the kernel family's
+// Ranking time of a scored plan: predicted time times the kernel variant's
 // measured factor.
 double rank_time(const conv_plan_t& p) { return p.rank_us; }
 }  // namespace
@@ -543,7 +542,7 @@ bool phase_direct(const Variant& v, const PhaseGeom& p, int dtype, Geom* g) {
 }
 
 namespace {
-double family_factor(int family);
+double calibration(const Variant& v);
 
 // Paper's Sec. 3.2 volumes (In, Ker, Out elements) of the class
 // <{n,k,h,w},{c,r},s> representative n,k,h,w,c,r,s for extents Ne and tile T
@@ -574,7 +573,7 @@ int score_plan(const Shape& s0, conv_plan_t* plan) {
   double dv[3];
   class3_volume(Ne, Ne, 1, dv);
   p.paper_bytes[CONV_LVL_HBM] = (dv[0] + dv[1]) * e + dv[2] * 4.0;
-  p.rank_us = p.pred_total_us * family_factor(find_variant(p.variant)->family);
+  p.rank_us = p.pred_total_us * calibration(*find_variant(p.variant));
   *plan = p;
   return CONV_OK;
 }
@@ -817,25 +816,28 @@ int score_plan_impl(const Shape& s0, conv_plan_t* plan) {
   return CONV_OK;
 }
 
-// Measured correction of the model per kernel family (the model does not
-// capture latency hiding or the inner loop's issue overhead): the unrolled
-// pointwise streaming kernel and the transposing bf16 kernel run about 20%
-// faster than the direct-to-LDS pipeline at equal predicted time, the looped
-// streaming kernel about 10% slower, and the register-staged kernel from
-// about as fast (tiny grids) to nearly three times slower (layer sweeps on
-// MI355X: the five configurations, the Table 1 layers at batch 1 and the
-// strided layers at batch 32; 2 keeps it for the small layers where it wins).
-// Plans are ranked by predicted time times this factor.
-double family_factor(int family) {
-  switch (family) {
-    case FAMILY_STREAM1X1:
-    case FAMILY_STREAM1X1_BAL:
-    case FAMILY_BF16_TR: return 0.8;
-    case FAMILY_DMA:
-    case FAMILY_BF16: return 1.0;
-    case FAMILY_STREAM1X1_LOOP: return 1.1;
-    default: return 2.0;
-  }
+// Measured rate of each compiled kernel variant relative to the model
+// (variant_calibration.inc, generated by paper_2101_09808_amd/calibrate.py
+// from the rank sweep of the five layer configurations): the median over
+// the variant's timed plans of measured / predicted time.  The model's
+// levels and MFMA time do not capture how well an instance's inner loop
+// hides latency and issues (the paper measures its microkernel's rate once,
+// Sec. 6); this factor does, per instance.  A variant without enough timed
+// plans takes its family's median; an unknown one 1.
+#include "variant_calibration.inc"
+struct Calibration {
+  int id;  // variant id, or minus the family
+  double factor;
+  int plans;
+};
+const Calibration kCalibration[] = {CONV_CALIBRATION_TABLE};
+
+double calibration(const Variant& v) {
+  for (const Calibration& c : kCalibration)
+    if (c.id == v.id) return c.factor;
+  for (const Calibration& c : kCalibration)
+    if (c.id == -v.family) return c.factor;
+  return 1.0;
 }
 
 void fill_plan_fields(conv_plan_t* p, const Variant& v, int nwk, int nwp, int tr, int tw,
