@@ -471,7 +471,7 @@ def model_check_parse(layers, dirs, launches=6):
         pb = plan["pred_bytes"]
         e = 2 if c.dtype == "bf16" else 4
         in_bytes = c.N * c.C * c.H * c.W * e
-        pred_l2cu = pb["lds"] + (in_bytes if fam in (4, 5) else 0)
+        pred_l2cu = pb["lds"] + (in_bytes if fam in (4, 5, 7) else 0)
         out_bytes = c.N * c.K * c.P * c.Q * 4
         hbm = m["FETCH_SIZE"]["bytes_per_launch"] + m["WRITE_SIZE"]["bytes_per_launch"]
         l2cu = m["TCP_TCC_READ_REQ_sum"]["bytes_per_launch"]
@@ -739,6 +739,66 @@ def heldout_report(res, train=False):
                        intro="Ten seeded random fp32 layers (bench.py heldout_layers, seed 78: batch 1-32, 16-512 "
                              "channels, 7-58 pixels, 1x1 and 3x3) that none of the model's measured constants "
                              "(calibration included) were fitted on.")
+
+
+BREAKDOWN_COUNTERS = ["GRBM_GUI_ACTIVE", "SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAIT_INST_ANY",
+                      "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_ACTIVE_INST_VMEM", "SQ_ACTIVE_INST_LDS", "SQ_WAIT_INST_LDS"]
+BREAKDOWN_FILE = os.path.join(ROOT, "profiles", "cycle_breakdown_per_layer.md")
+BREAKDOWN_COMMANDS = [
+    "rocprofv3 --kernel-trace --pmc " + " ".join(BREAKDOWN_COUNTERS) +
+    " --output-format csv -d gpurun_out/breakdown -o b -- python -u bench.py --traffic-run --layer all",
+    "python bench.py --breakdown-parse gpurun_out/breakdown"]
+
+
+def breakdown_parse(layers, d, launches=6):
+    """Where each layer's waves spend their cycles (one counter pass with the
+    kernel trace): MFMA-pipe busy share of the SIMD cycles, the share of
+    wave cycles spent waiting on a dependency (memory or LDS), and the clock
+    the counters imply.  SQ_WAVE_CYCLES and SQ_WAIT_INST_* count in units of
+    four cycles (quad cycles), summed over waves; SQ_BUSY_CYCLES in cycles,
+    summed over the chip's 32 shader engines."""
+    import csv
+    import glob
+    cc = sorted(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True))[0]
+    tr = sorted(glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True))[0]
+    dur = {int(r["Dispatch_Id"]): int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in csv.DictReader(open(tr))}
+    vals, names = {}, {}
+    for r in csv.DictReader(open(cc)):
+        k = int(r["Dispatch_Id"])
+        vals.setdefault(k, {})
+        vals[k][r["Counter_Name"]] = vals[k].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        names[k] = r["Kernel_Name"]
+    conv = [k for k in sorted(vals) if "convfwd::" in names[k] and "reduce" not in names[k]]
+    if len(conv) != launches * len(layers):
+        raise SystemExit(f"expected {launches * len(layers)} conv dispatches, got {len(conv)}")
+    lines = ["# Where the waves spend their cycles, per layer (selected plans), MI355X", "",
+             "One rocprofv3 counter pass with the kernel trace over `bench.py --traffic-run --layer all` "
+             "(six launches of each layer's selected plan; the first left out):", ""]
+    lines += ["    " + x for x in BREAKDOWN_COMMANDS]
+    lines += ["", "* MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES over (SIMDs x kernel cycles), the share of the chip's "
+              "MFMA pipe time in use; kernel cycles from the trace duration at the clock below.",
+              "* Waiting: SQ_WAIT_INST_ANY over SQ_WAVE_CYCLES, the share of resident-wave time stalled on a "
+              "dependency (a load, an LDS read, a barrier); LDS waits separately (SQ_WAIT_INST_LDS).",
+              "* Clock: SQ_BUSY_CYCLES / 32 shader engines over the kernel's duration (busy time of the "
+              "shader engines, so a lower bound of the clock while the kernel runs).", "",
+              "| layer | kernel us | clock GHz (>=) | MFMA busy | waiting | LDS waits | waves |",
+              "|---|---|---|---|---|---|---|"]
+    rows = {}
+    for i, c in enumerate(layers):
+        ks = conv[i * launches + 1:(i + 1) * launches]
+        us = sum(dur[k] for k in ks) / len(ks) / 1e3
+        m = {n: sum(vals[k].get(n, 0.0) for k in ks) / len(ks) for n in BREAKDOWN_COUNTERS}
+        ghz = m["SQ_BUSY_CYCLES"] / 32 / (us * 1e3)
+        mfma = m["SQ_VALU_MFMA_BUSY_CYCLES"] / (1024 * us * 1e3 * ghz)
+        wait = m["SQ_WAIT_INST_ANY"] / max(1.0, m["SQ_WAVE_CYCLES"])
+        lwait = m["SQ_WAIT_INST_LDS"] / max(1.0, m["SQ_WAVE_CYCLES"])
+        rows[c.name] = {"kernel_us": us, "clock_ghz_lower_bound": ghz, "mfma_busy": mfma, "waiting": wait,
+                        "lds_waiting": lwait, "waves": m["SQ_WAVES"], "counters": m}
+        lines.append(f"| {c.name} | {us:.1f} | {ghz:.2f} | {100 * mfma:.0f}% | {100 * wait:.0f}% | "
+                     f"{100 * lwait:.0f}% | {m['SQ_WAVES']:.0f} |")
+    open(BREAKDOWN_FILE, "w").write("\n".join(lines) + "\n")
+    json.dump(rows, open(BREAKDOWN_FILE.replace(".md", ".json"), "w"), indent=1)
+    print("\n".join(lines), flush=True)
 
 
 COUNTER_SWEEP_LAYER = "conv3x3_n32_c128_k128_in30"
@@ -1010,6 +1070,9 @@ def main():
     ap.add_argument("--counter-sweep", nargs="?", const=100, type=int, metavar="N",
                     help="launch the model's top 5 and a sample of the other plans of --layer (N in all) "
                          "once each, for rocprofv3 --pmc counter passes (Fig. 6 analogue)")
+    ap.add_argument("--breakdown-parse", metavar="DIR",
+                    help="cycle breakdown per layer from one counter pass of --traffic-run --layer all; writes "
+                         "profiles/cycle_breakdown_per_layer.{md,json}")
     ap.add_argument("--counter-sweep-parse", nargs="+", metavar="DIR",
                     help="per-plan counters of the --counter-sweep passes against the model's rank and "
                          "levels; writes profiles/model_counter_sweep.{json,md}")
@@ -1033,6 +1096,9 @@ def main():
         return
     if args.model_check:  # host-only: reads the counter files of four earlier runs
         model_check_parse(list(CONFIGS), args.model_check)
+        return
+    if args.breakdown_parse:  # host-only: reads the counter files of one pass
+        breakdown_parse(list(CONFIGS), args.breakdown_parse)
         return
     if args.counter_sweep_parse:  # host-only: reads the counter files of the sweep's passes
         counter_sweep_parse(BY_NAME[args.layer if args.layer != HEADLINE else COUNTER_SWEEP_LAYER],
