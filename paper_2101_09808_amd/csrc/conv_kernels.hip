@@ -1948,6 +1948,8 @@ const Instance kInstances[] = {
     BF16_TR_INST(212, 4, 64, 3, 3),
     BF16_TR_INST(213, 8, 64, 3, 3),
     BF16_TR_INST(214, 8, 32, 3, 3),
+    BF16_TR_INST(215, 14, 32, 3, 3),
+    BF16_TR_INST(216, 4, 32, 3, 3),
     // ---- bf16 inputs (persistent, transposed channel-fastest LDS tiles)
     BF16_INST(201, 4, 4, 3, 3, 3),
     BF16_INST(202, 2, 4, 3, 3, 3),

@@ -772,9 +772,23 @@ int score_plan_impl(const Shape& s0, conv_plan_t* plan) {
   plan->class_lvl[CONV_LVL_LDS] = 3;
   plan->class_lvl[CONV_LVL_HBM] = 0;
 
+  // Persistent kernels (bf16 families) give each workgroup a fixed run of
+  // ceil(tiles / workgroups) tiles: the memory levels run at full rate only
+  // while every workgroup still has tiles (the load-balancing term of
+  // Algorithm 1 applied to the levels, not only to the MFMAs), and the last
+  // tile's stores of every workgroup follow its MFMAs with nothing left to
+  // overlap them.
+  const bool persistent = v->family == FAMILY_BF16 || v->family == FAMILY_BF16_TR;
+  double imbalance = 1.0, last_tile_us = kHw.drain_us;
+  if (persistent && g.num_tiles > 0) {
+    const double G = std::min<double>(g.grid, g.num_tiles);
+    imbalance = std::ceil(g.num_tiles / G) * G / g.num_tiles;
+    last_tile_us = G * (out_bytes / g.num_tiles) / kHw.bw[CONV_LVL_HBM] * 1e6;
+  }
   double tmax = 0;
   for (int l = 0; l < CONV_NUM_LVLS; ++l) {
     plan->pred_us[l] = plan->pred_bytes[l] / kHw.bw[l] * 1e6;
+    if (l == CONV_LVL_L2 || l == CONV_LVL_HBM) plan->pred_us[l] *= imbalance;
     tmax = std::max(tmax, plan->pred_us[l]);
   }
   // Compute: MFMA cycles of one wave (its channel range); a CU runs
@@ -812,7 +826,7 @@ int score_plan_impl(const Shape& s0, conv_plan_t* plan) {
   // Fill and drain: one round trip before the first step, that step's MFMAs
   // (nothing to overlap them with yet), the last stores.
   const double step_us = plan->pred_mfma_us / std::max(1, g.cps);
-  plan->pred_total_us = tmax + reduce_us + kHw.fill_us + step_us + kHw.drain_us;
+  plan->pred_total_us = tmax + reduce_us + kHw.fill_us + step_us + last_tile_us;
   return CONV_OK;
 }
 
