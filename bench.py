@@ -512,7 +512,10 @@ def model_check_parse(layers, dirs, launches=6):
     print(json.dumps(out), flush=True)
 
 
-RANK_JSON = os.path.join(ROOT, "profiles", "model_rank_sweep.json")
+# per-plan raw results of the sweeps (large; the committed summaries are the .md
+# files beside them and calibration/ratios.txt in the package)
+RAW_DIR = os.path.join(ROOT, "gpurun_out")
+RANK_JSON = os.path.join(RAW_DIR, "model_rank_sweep.json")
 RANK_MD = os.path.join(ROOT, "profiles", "model_rank_sweep.md")
 
 
@@ -696,9 +699,9 @@ def rank_report(res, title="Model-predicted rank vs measured time (Sec. 9), MI35
     return "\n".join(lines) + "\n"
 
 
-HELDOUT_JSON = os.path.join(ROOT, "profiles", "model_heldout.json")
+HELDOUT_JSON = os.path.join(RAW_DIR, "model_heldout.json")
 HELDOUT_MD = os.path.join(ROOT, "profiles", "model_heldout.md")
-TRAIN_JSON = os.path.join(ROOT, "profiles", "model_train_sweep.json")
+TRAIN_JSON = os.path.join(RAW_DIR, "model_train_sweep.json")
 TRAIN_MD = os.path.join(ROOT, "profiles", "model_train_sweep.md")
 HELDOUT_SEED, TRAIN_SEED = 78, 77
 
@@ -803,7 +806,7 @@ def breakdown_parse(layers, d, launches=6):
 
 COUNTER_SWEEP_LAYER = "conv3x3_n32_c128_k128_in30"
 COUNTER_SWEEP_COUNTERS = [["FETCH_SIZE"], ["TCP_TCC_READ_REQ_sum"], ["SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT"]]
-COUNTER_SWEEP_JSON = os.path.join(ROOT, "profiles", "model_counter_sweep.json")
+COUNTER_SWEEP_JSON = os.path.join(RAW_DIR, "model_counter_sweep.json")
 COUNTER_SWEEP_MD = os.path.join(ROOT, "profiles", "model_counter_sweep.md")
 
 
@@ -880,6 +883,7 @@ def counter_sweep_parse(c, dirs):
         out["spearman"][cnt] = e
     conflicts = sum(r["lds_bank_conflict_cycles"] for r in plans) / max(1.0, sum(r["lds_instr"] for r in plans))
     out["bank_conflict_cycles_per_lds_instr"] = conflicts
+    os.makedirs(RAW_DIR, exist_ok=True)
     json.dump(out, open(COUNTER_SWEEP_JSON, "w"), indent=1)
     lines = [f"# Counters per plan against the model (Fig. 6 analogue), {c.name}, MI355X", "",
              "The model's 5 best plans and a uniform sample of the other candidates (100 in all), each "
@@ -905,7 +909,7 @@ def counter_sweep_parse(c, dirs):
                      f"{'-' if r['measured_us'] is None else format(r['measured_us'], '.1f')} | "
                      f"{r['fetch_kib']:.0f} | {r['l2_to_cu_req']:.0f} | {r['lds_instr']:.0f} | "
                      f"{r['lds_bank_conflict_cycles']:.0f} |")
-    lines.append(f"\n(first 25 of {len(plans)} plans; all in model_counter_sweep.json)\n")
+    lines.append(f"\n(first 25 of {len(plans)} plans; the parse writes all of them to its per-plan JSON)\n")
     open(COUNTER_SWEEP_MD, "w").write("\n".join(lines))
     print("\n".join(lines[:20]), flush=True)
 
@@ -1060,13 +1064,13 @@ def main():
     ap.add_argument("--rank-sweep", nargs="?", const=0, type=int, metavar="N",
                     help="model validation: time every candidate of every layer (or, with N, the model's "
                          "top 5 and a uniform sample of the others, N plans per layer); writes "
-                         "profiles/model_rank_sweep.{json,md}")
+                         "profiles/model_rank_sweep.md (per-plan JSON: gpurun_out/)")
     ap.add_argument("--held-out", action="store_true",
                     help="the same validation on seeded random layers that none of the model's measured "
-                         "constants were fitted on; writes profiles/model_heldout.{json,md}")
+                         "constants were fitted on; writes profiles/model_heldout.md (per-plan JSON: gpurun_out/)")
     ap.add_argument("--train-sweep", action="store_true",
                     help="the same sweep on the seeded random layers that join the five configurations in the "
-                         "selector's calibration; writes profiles/model_train_sweep.{json,md}")
+                         "selector's calibration; writes profiles/model_train_sweep.md (per-plan JSON: gpurun_out/)")
     ap.add_argument("--counter-sweep", nargs="?", const=100, type=int, metavar="N",
                     help="launch the model's top 5 and a sample of the other plans of --layer (N in all) "
                          "once each, for rocprofv3 --pmc counter passes (Fig. 6 analogue)")
@@ -1075,7 +1079,7 @@ def main():
                          "profiles/cycle_breakdown_per_layer.{md,json}")
     ap.add_argument("--counter-sweep-parse", nargs="+", metavar="DIR",
                     help="per-plan counters of the --counter-sweep passes against the model's rank and "
-                         "levels; writes profiles/model_counter_sweep.{json,md}")
+                         "levels; writes profiles/model_counter_sweep.md (per-plan JSON: gpurun_out/)")
     ap.add_argument("--table1", action="store_true",
                     help="every conv2d layer of Table 1 at batch 1 (stride, same padding); writes "
                          "profiles/table1_sweep.{json,md}")
@@ -1125,6 +1129,7 @@ def main():
         res = rank_sweep(heldout_layers(seed=TRAIN_SEED if train else HELDOUT_SEED))
         res["_meta"] = {"kernel_sha": kernel_source_hash(),
                         "command": "python bench.py " + ("--train-sweep" if train else "--held-out")}
+        os.makedirs(RAW_DIR, exist_ok=True)
         json.dump(res, open(TRAIN_JSON if train else HELDOUT_JSON, "w"), indent=1)
         md = heldout_report({k: v for k, v in res.items() if not k.startswith("_")}, train=train)
         open(TRAIN_MD if train else HELDOUT_MD, "w").write(md)
@@ -1137,6 +1142,7 @@ def main():
         res = rank_sweep(list(CONFIGS) if args.layer in ("all", HEADLINE) else [BY_NAME[args.layer]],
                          n=args.rank_sweep or None)
         res["_meta"] = {"kernel_sha": kernel_source_hash(), "command": "python bench.py --rank-sweep"}
+        os.makedirs(RAW_DIR, exist_ok=True)
         json.dump(res, open(RANK_JSON, "w"), indent=1)
         md = rank_report({k: v for k, v in res.items() if not k.startswith("_")})
         open(RANK_MD, "w").write(md)
