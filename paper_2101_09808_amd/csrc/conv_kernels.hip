@@ -1903,6 +1903,14 @@ const Instance kInstances[] = {
     // small layers without a split reduction
     F32_DMA_CG(161, 2, 2, 4, 4, 16, 3, 3, 3, 7, 1, 5, 4),
     F32_DMA_CG(162, 2, 2, 8, 8, 32, 3, 3, 2, 7, 1, 5, 4),
+    // the same with fewer In loads (tiles whose In halo fits): the small
+    // 3x3 layers' plans issue no empty loads
+    F32_DMA_CG(179, 2, 2, 8, 8, 32, 3, 3, 2, 4, 1, 5, 4),
+    F32_DMA_CG(180, 2, 2, 4, 4, 16, 3, 3, 4, 4, 1, 5, 4),
+    // 32 k x 7 blocks per wave, one wave per channel group: 32 x 98-pixel
+    // tiles cover the 3x3 7x7 N32 layer in 256 workgroups with 12.5% padding
+    F32_DMA_CG(181, 2, 7, 4, 4, 16, 3, 3, 3, 11, 1, 5, 4),
+    F32_DMA_CG(182, 2, 7, 8, 8, 32, 3, 3, 2, 11, 1, 5, 4),
     F32_DMA_CG(163, 1, 4, 4, 4, 16, 3, 3, 3, 11, 1, 3, 4),
     F32_DMA_CG(164, 2, 4, 8, 4, 16, 3, 3, 2, 8, 1, 5, 4),
     F32_DMA_CG(165, 4, 4, 4, 4, 16, 3, 3, 3, 8, 1, 10, 4),
