@@ -194,6 +194,11 @@ class LayerRunner:
         return [a.elapsed_time(b) * 1e3 for a, b in evs]
 
 
+def progress(msg):
+    """A progress line on stderr (stdout carries only the result line)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def summary(ts):
     """Mean, median, standard deviation and 95% confidence half-width of the
     mean (Student t) of per-run times in us."""
@@ -1201,10 +1206,12 @@ def main():
                              f"{FLUSH_BYTES >> 20} MB and between its own HIP events"},
         "sclk": sclk,
     }
+    progress(f"headline {c.name}: {r['mean_kernel_ms'] * 1e3:.1f} us per launch back to back")
     out["empty_kernel_floor"] = empty_kernel_floor(flush)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(c)
         out["cpu_baseline_1thread"] = cpu_baseline_one_thread(CONFIGS[0])
+        progress("CPU oracle baselines done")
     if not args.no_layers:
         layers = {}
         # the bf16 layer with bf16 Out (conv_fwd_bf16_out): half the write
@@ -1262,6 +1269,7 @@ def main():
             layers[lc.name].update({"mopt5_variant": tplan["variant"], "mopt5_split_c": tplan["split_c"],
                                     "mopt5_kernel_us": tk * 1e6, "mopt5_gflops": flops(lc) / tk / 1e9,
                                     "mopt5_pct_hbm_peak": 100 * alg_bytes(lc) / tk / 1e9 / PEAK["hbm_gbs"]})
+            progress(f"layer {lc.name}: {lk * 1e6:.1f} us (MOpt-5 {tk * 1e6:.1f} us)")
             torch.cuda.empty_cache()
         layers[c5.name + "_bf16out"] = bf16out_row
         # strided, padded Table 1 layers (conv_fwd_ex: the selected stride-1
@@ -1285,6 +1293,7 @@ def main():
                 "pct_hbm_peak": 100 * alg_bytes(lc) / lk / 1e9 / PEAK["hbm_gbs"],
                 "cold": lcold,
             }
+            progress(f"layer {lc.name}: {lk * 1e6:.1f} us")
             torch.cuda.empty_cache()
         out["per_layer"] = layers
     print(json.dumps(out), flush=True)
