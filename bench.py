@@ -194,6 +194,21 @@ class LayerRunner:
         return [a.elapsed_time(b) * 1e3 for a, b in evs]
 
 
+def trace_summary(db_path, limit=20):
+    """Kernel table of a rocprofv3 results database (--kernel-trace): per
+    kernel name, calls, average / min / max duration in us and workgroups,
+    the kernels that took the most total time first."""
+    import sqlite3
+    db = sqlite3.connect(db_path)
+    q = ("select name, count(*), avg(duration), min(duration), max(duration), sum(duration), grid_x, workgroup_x "
+         "from kernels group by name order by sum(duration) desc limit ?")
+    lines = ["| kernel | calls | avg us | min us | max us | workgroups |", "|---|---|---|---|---|---|"]
+    for r in db.execute(q, (limit,)):
+        lines.append(f"| {r[0][:110]} | {r[1]} | {r[2] / 1e3:.2f} | {r[3] / 1e3:.2f} | {r[4] / 1e3:.2f} | "
+                     f"{r[6] // max(1, r[7])} |")
+    return "\n".join(lines)
+
+
 def progress(msg):
     """A progress line on stderr (stdout carries only the result line)."""
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
@@ -1085,6 +1100,9 @@ def main():
     ap.add_argument("--counter-sweep-parse", nargs="+", metavar="DIR",
                     help="per-plan counters of the --counter-sweep passes against the model's rank and "
                          "levels; writes profiles/model_counter_sweep.md (per-plan JSON: gpurun_out/)")
+    ap.add_argument("--trace-summary", metavar="RESULTS_DB",
+                    help="host only: the kernel table (calls, average/min/max us, workgroups) of a rocprofv3 "
+                         "--kernel-trace results database")
     ap.add_argument("--table1", action="store_true",
                     help="every conv2d layer of Table 1 at batch 1 (stride, same padding); writes "
                          "profiles/table1_sweep.{json,md}")
@@ -1105,6 +1123,9 @@ def main():
         return
     if args.model_check:  # host-only: reads the counter files of four earlier runs
         model_check_parse(list(CONFIGS), args.model_check)
+        return
+    if args.trace_summary:  # host-only: reads a rocprofv3 results database
+        print(trace_summary(args.trace_summary), flush=True)
         return
     if args.breakdown_parse:  # host-only: reads the counter files of one pass
         breakdown_parse(list(CONFIGS), args.breakdown_parse)
@@ -1224,7 +1245,7 @@ def main():
         del lr5
         ab = alg_bytes(c5) - c5.N * c5.K * c5.P * c5.Q * 2
         bf16out_row = {
-            "dtype": "bf16", "out_dtype": "bf16", "variant": B.conv_fwd_plan(*c5.key(), dtype=B.CONV_DTYPE_BF16)["variant"],
+            "dtype": "bf16", "out_dtype": "bf16", "variant": B.conv_fwd_bf16_out_plan(*c5.key())["variant"],
             "split_c": 1, "kernel_us": lk * 1e6, "gflops": flops(c5) / lk / 1e9,
             "pct_fp32_mfma_peak": 100 * flops(c5) / lk / 1e12 / PEAK["fp32_mfma_tflops"],
             "pct_dtype_mfma_peak": 100 * flops(c5) / lk / 1e12 / PEAK["bf16_mfma_tflops"],

@@ -152,10 +152,14 @@ int conv_fwd_bf16(int N, int C, int K, int H, int W, int R, int S,
  * bf16-input forward convolution with bf16 output: as conv_fwd_bf16 (fp32
  * products and sums), then each output rounded to the nearest bf16 (ties to
  * even), halving the bytes written.  Out : [N][K][H-R+1][W-S+1] bf16 bit
- * patterns, device.  The plan is the one conv_fwd_bf16 selects; the
- * transposing-read bf16 kernel writes bf16 directly, any other kernel
- * writes fp32 into a stream-ordered workspace (from the library's
- * pool, returned within the call) that a second kernel rounds into Out.
+ * patterns, device.  The plan is the one conv_fwd_bf16 selects, except
+ * where that plan's transposing-read kernel could not pair its stores into
+ * 16-byte pieces although Out allows them (16-byte aligned Out and
+ * (W-S+1) % 8 == 0): then the best candidate that pairs them
+ * (conv_fwd_bf16_out_plan).  The transposing-read bf16 kernel writes bf16
+ * directly, any other kernel writes fp32 into a stream-ordered workspace
+ * (from the library's pool, returned within the call) that a second kernel
+ * rounds into Out.
  * The paper states single precision only; the other entry points write
  * fp32 Out, and this one is the bf16-output refinement that makes bf16
  * layers less write-bound.  Returns a conv_status_t.
@@ -211,6 +215,14 @@ int conv_fwd_ex(int N, int C, int K, int H, int W, int R, int S,
 int conv_fwd_ex_noalloc(int N, int C, int K, int H, int W, int R, int S,
                         int stride_h, int stride_w, int pad_h, int pad_w, int dtype,
                         const void* In, const void* Ker, float* Out, void* stream);
+
+/*
+ * Host-only: the plan conv_fwd_bf16_out runs for this shape with a 16-byte
+ * aligned Out (see there).  Makes no HIP call.  Returns a conv_status_t;
+ * CONV_ENOPLAN where no bf16 kernel instance takes the shape (the call then
+ * widens the inputs and runs the fp32 plan).
+ */
+int conv_fwd_bf16_out_plan(int N, int C, int K, int H, int W, int R, int S, conv_plan_t* plan_out);
 
 /*
  * Host-only: the inner stride-1 problem conv_fwd_ex runs for these

@@ -78,6 +78,8 @@ def lib():
         L.conv_fwd_plan.restype = _i32
         L.conv_fwd_with_plan.argtypes = shape7 + [_vp, _vp, _vp, ctypes.POINTER(ConvPlan), _vp]
         L.conv_fwd_with_plan.restype = _i32
+        L.conv_fwd_bf16_out_plan.argtypes = shape7 + [ctypes.POINTER(ConvPlan)]
+        L.conv_fwd_bf16_out_plan.restype = _i32
         L.conv_fwd_score_plan.argtypes = shape7 + [ctypes.POINTER(ConvPlan)]
         L.conv_fwd_score_plan.restype = _i32
         L.conv_fwd_candidates.argtypes = shape7 + [_i32, ctypes.POINTER(ConvPlan), _i32]
@@ -286,6 +288,16 @@ def conv_fwd_plan(N, C, K, H, W, R, S, dtype=CONV_DTYPE_F32):
     st = lib().conv_fwd_plan(N, C, K, H, W, R, S, dtype, ctypes.byref(p))
     if st != CONV_OK:
         raise ConvError(st, "conv_fwd_plan")
+    return p.to_dict()
+
+
+def conv_fwd_bf16_out_plan(N, C, K, H, W, R, S):
+    """The plan conv_fwd_bf16_out runs for a shape with a 16-byte aligned
+    Out (host only), as a dict."""
+    p = ConvPlan()
+    st = lib().conv_fwd_bf16_out_plan(N, C, K, H, W, R, S, ctypes.byref(p))
+    if st != CONV_OK:
+        raise ConvError(st, "conv_fwd_bf16_out_plan")
     return p.to_dict()
 
 

@@ -103,6 +103,61 @@ int cached_entry(const Shape& s, int dtype, int align, Entry* out) {
   return CONV_OK;
 }
 
+// bf16 Out from the transposing bf16 kernel: its stores are 16 bytes only
+// when the wave tile pairs neighbouring blocks (an even number of blocks per
+// part, in rows of an even number of blocks); otherwise every output is a
+// 2-byte store, eight times slower on the 226x226 layer.  Whether a tile
+// pairs is fixed by the instance (rows max_ni, columns max_nk), as in the
+// kernel's PAIRED.
+bool pairs_bf16_out(const Variant& v) {
+  if (v.family != FAMILY_BF16_TR) return true;
+  const int cbr = v.max_nk / 16, wp = v.max_ni * cbr / 4;
+  const int npart = wp % 2 == 0 ? 2 : 1, pb = wp / npart;
+  return pb % 2 == 0 && cbr % 2 == 0;
+}
+
+// The plan of conv_fwd_bf16_out: the selected bf16 plan, unless 16-byte
+// stores are possible (Q % 8 == 0, Out 16-byte aligned) and it does not pair
+// them: then the best candidate that does.  Cached beside the other entries
+// under its own dtype code.
+constexpr int kBf16OutKey = 0x100;
+int cached_entry_bf16_out(const Shape& s, int align, bool pair_possible, Entry* out) {
+  Entry e;
+  int st = cached_entry(s, CONV_DTYPE_BF16, align, &e);
+  if (st != CONV_OK || !pair_possible || pairs_bf16_out(*e.v)) {
+    *out = e;
+    return st;
+  }
+  const Key key{s.N, s.C, s.K, s.H, s.W, s.R, s.S, CONV_DTYPE_BF16 | kBf16OutKey, align};
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_cache.find(key);
+    if (it != g_cache.end()) {
+      *out = it->second;
+      return CONV_OK;
+    }
+  }
+  std::vector<conv_plan_t> buf(4096);
+  const int n = std::min<int>(enumerate_plans(s, CONV_DTYPE_BF16, buf.data(), (int)buf.size()), (int)buf.size());
+  for (int i = 0; i < n; ++i) {
+    const Variant* w = find_variant(buf[i].variant);
+    Geom g;
+    if (!w || !variant_fits(*w, CONV_DTYPE_BF16, align) || !pairs_bf16_out(*w) ||
+        !resolve_geom(s, *w, buf[i], &g, nullptr))
+      continue;
+    e.plan = buf[i];
+    e.v = w;
+    e.g = g;
+    break;
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_cache[key] = e;
+  }
+  *out = e;
+  return CONV_OK;
+}
+
 int cached_plan(const Shape& s, int dtype, conv_plan_t* out) {
   Entry e;
   const int st = cached_entry(s, dtype, ALIGN_ALL, &e);
@@ -284,7 +339,8 @@ int conv_fwd_bf16_out(int N, int C, int K, int H, int W, int R, int S, const uin
   if (!In || !Ker || !Out) return CONV_ENULL;
   Entry e;
   const Shape sh{N, C, K, H, W, R, S};
-  st = cached_entry(sh, CONV_DTYPE_BF16, alignment_of(In, Ker), &e);
+  const bool pair_possible = (W - S + 1) % 8 == 0 && (reinterpret_cast<uintptr_t>(Out) & 15) == 0;
+  st = cached_entry_bf16_out(sh, alignment_of(In, Ker), pair_possible, &e);
   if (st == CONV_ENOPLAN) return run_bf16_widened(sh, In, Ker, Out, true, stream);
   if (st != CONV_OK) return st;
   return launch_bf16_out(*e.v, e.g, In, Ker, Out, stream);
@@ -487,6 +543,16 @@ int conv_fwd_plan(int N, int C, int K, int H, int W, int R, int S, int dtype,
   if (!plan_out) return CONV_ENULL;
   if (dtype != CONV_DTYPE_F32 && dtype != CONV_DTYPE_BF16) return CONV_EINVAL;
   return cached_plan(Shape{N, C, K, H, W, R, S}, dtype, plan_out);
+}
+
+int conv_fwd_bf16_out_plan(int N, int C, int K, int H, int W, int R, int S, conv_plan_t* plan_out) {
+  int st = validate_shape(N, C, K, H, W, R, S);
+  if (st != CONV_OK) return st;
+  if (!plan_out) return CONV_ENULL;
+  Entry e;
+  st = cached_entry_bf16_out(Shape{N, C, K, H, W, R, S}, ALIGN_ALL, (W - S + 1) % 8 == 0, &e);
+  if (st == CONV_OK) *plan_out = e.plan;
+  return st;
 }
 
 int conv_fwd_with_plan(int N, int C, int K, int H, int W, int R, int S, const void* In,

@@ -775,14 +775,19 @@ int score_plan_impl(const Shape& s0, conv_plan_t* plan) {
   // Persistent kernels (bf16 families) give each workgroup a fixed run of
   // ceil(tiles / workgroups) tiles: the memory levels run at full rate only
   // while every workgroup still has tiles (the load-balancing term of
-  // Algorithm 1 applied to the levels, not only to the MFMAs), and the last
+  // Algorithm 1 applied to the levels, not only to the MFMAs), and a tile
+  // that the layer fills only in part (columns past Q, k rows past K) takes
+  // a whole tile's phases; so the levels are charged the tile executions of
+  // the busiest workgroup over the tiles' worth of useful outputs.  The last
   // tile's stores of every workgroup follow its MFMAs with nothing left to
   // overlap them.
   const bool persistent = v->family == FAMILY_BF16 || v->family == FAMILY_BF16_TR;
   double imbalance = 1.0, last_tile_us = kHw.drain_us;
   if (persistent && g.num_tiles > 0) {
     const double G = std::min<double>(g.grid, g.num_tiles);
-    imbalance = std::ceil(g.num_tiles / G) * G / g.num_tiles;
+    const double full = (double)g.num_tiles * g.tr * g.tw * 16.0 * v->wk * g.nwk /
+                        ((double)s.N * g.P * g.Q * s.K);  // tile slots over outputs (>= 1)
+    imbalance = std::ceil(g.num_tiles / G) * G / g.num_tiles * std::max(1.0, full);
     last_tile_us = G * (out_bytes / g.num_tiles) / kHw.bw[CONV_LVL_HBM] * 1e6;
   }
   double tmax = 0;

@@ -120,3 +120,32 @@ def test_enumeration_rules_for_channel_groups_and_narrow_steps():
                 seen_narrow = True
                 assert key[1] < 16, (key, p)
     assert seen_groups and seen_narrow
+
+
+def test_bf16_out_plan_pairs_its_stores():
+    """conv_fwd_bf16_out's plan for a layer whose fastest fp32-Out tiling
+    (4 x 32) cannot pair bf16 stores into 16-byte pieces: the best candidate
+    whose wave tile pairs them (an even number of 16-pixel blocks per part,
+    in rows of an even number of blocks), as the transposing kernel does."""
+    dims = (16, 32, 64, 226, 226, 3, 3)
+
+    def pairs(p):
+        g = B.conv_fwd_geometry(*dims, p)
+        if g["family"] != 6:
+            return True
+        cbr = p["tile_cols"] // 16
+        wp = p["tile_rows"] * cbr // 4
+        pb = wp // (2 if wp % 2 == 0 else 1)
+        return pb % 2 == 0 and cbr % 2 == 0
+
+    sel = B.conv_fwd_plan(*dims, dtype=B.CONV_DTYPE_BF16)
+    out = B.conv_fwd_bf16_out_plan(*dims)
+    assert not pairs(sel)
+    assert pairs(out)
+    first = next(p for p in B.conv_fwd_candidates(*dims, dtype=B.CONV_DTYPE_BF16) if pairs(p))
+    assert (out["variant"], out["tile_rows"], out["tile_cols"]) == (first["variant"], first["tile_rows"],
+                                                                    first["tile_cols"])
+    # a shape whose selected plan pairs keeps it
+    dims2 = (2, 32, 48, 18, 42, 3, 3)
+    if pairs(B.conv_fwd_plan(*dims2, dtype=B.CONV_DTYPE_BF16)):
+        assert B.conv_fwd_bf16_out_plan(*dims2)["variant"] == B.conv_fwd_plan(*dims2, dtype=B.CONV_DTYPE_BF16)["variant"]
