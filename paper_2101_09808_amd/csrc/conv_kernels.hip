@@ -1391,9 +1391,10 @@ conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ke
 //     128-byte pieces of each channel row).  Each block accumulates over all
 //     C channels, the even and odd channel pairs of each quad in separate
 //     accumulators (four independent 32x32x2 chains keep the MFMA pipe full
-//     with one wave per SIMD); the two are added and the block is stored
-//     while the next block computes, which spreads the Out writes over the
-//     whole kernel instead of one burst at the end;
+//     with one wave per SIMD); the two are added and the block's 32 results
+//     are stored over the steps of the next block, which spreads the Out
+//     writes over the whole kernel instead of one burst per block (the last
+//     block stores at the end);
 //   * the last T pixels form one 16-pixel block (masked past PW) whose 64
 //     rows of k are split among the four waves, 16 rows each on one 16x16x4
 //     accumulator, computed alongside each wave's last block.
@@ -1402,7 +1403,8 @@ conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ke
 // (64 rows of this k tile, all C channels) is staged through registers into
 // LDS in chunks of 64 channels during the first block, each chunk requested
 // a whole chunk ahead; every load is visible to the compiler, so its waits
-// are exact.  Requires C % 64 == 0 and In below 1 GB (32-bit offsets).
+// are exact.  Requires C % 64 == 0, In below 1 GB and Out below 2 GB
+// (32-bit offsets).
 template <int NB, int D, int NQ>
 __global__ void __launch_bounds__(256)
 conv1x1_bal_kernel(const float* __restrict__ In, const float* __restrict__ Ker, float* __restrict__ Out,
@@ -1489,6 +1491,17 @@ conv1x1_bal_kernel(const float* __restrict__ In, const float* __restrict__ Ker, 
   };
   v16f acc[2][2];  // [kb][e]
   v4f acc16 = v4f{0.f, 0.f, 0.f, 0.f};
+  // A finished block's 32 results (every block but the last) are stored
+  // over the steps of the next block, results 32 q / NQ .. 32 (q + 1) / NQ - 1
+  // at step q (one every NQ / 32 steps, or 32 / NQ per step).  Stores and loads
+  // share one completion counter, so ring loads issued behind a burst of 32
+  // stores (32 KB per CU, draining at the CU's share of the HBM write rate)
+  // would wait for all of them and stall the next block.  32-bit offsets
+  // (Out below 2 GB); a masked lane's offset is past the buffer's range.
+  const __amdgpu_buffer_rsrc_t orsrc = __builtin_amdgcn_make_buffer_rsrc(
+      Out, (short)0, (int)((unsigned)g.N * (unsigned)K * (unsigned)HW * 4u), 0x00020000);
+  float pend[32];
+  unsigned pend_base = kOob;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -1520,15 +1533,41 @@ conv1x1_bal_kernel(const float* __restrict__ In, const float* __restrict__ Ker, 
         acc[kb][e] = __builtin_amdgcn_mfma_f32_32x32x2f32(a32[buf][e][kb], ring32[t % D][e], acc[kb][e], 0, 0, 0);
     if constexpr (tail) acc16 = __builtin_amdgcn_mfma_f32_16x16x4f32(a16[buf], ring16[t % D], acc16, 0, 0, 0);
     if constexpr (t + D < NSTEP) load(std::integral_constant<int, t + D>{});
+    if constexpr (j >= 1) {
+      // the previous block's results r: row 32 kb + 8 (v / 4) + 4 h32 + v % 4
+      static_for<(32 * (q + 1)) / NQ - (32 * q) / NQ>([&](auto i_c) __attribute__((always_inline)) {
+        constexpr int r = (32 * q) / NQ + decltype(i_c)::value;
+        constexpr int kb = r / 16, v = r % 16;
+        const int k = k0 + 32 * kb + 8 * (v / 4) + 4 * h32 + v % 4;
+        const float val = pend[r];
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, val), orsrc,
+                                              k < K ? pend_base + (unsigned)(k * HW) * 4u : kOob, 0, kStoreNT);
+      });
+    }
     if constexpr (chunk_end) {
       ker_store(q / 16 + 1);
       if constexpr (q / 16 + 2 < NCH) ker_load(q / 16 + 2);
       __syncthreads();
       read_a(tn % NQ, buf ^ 1, tn / NQ == NB - 1);
     }
-    if constexpr (q == NQ - 1) {
-      // block j done: add the two channel-pair halves and store 32 pixels
-      // (two rows of k per instruction, streaming hint), then restart
+    if constexpr (q == NQ - 1 && j < NB - 1) {
+      // block j done: add the two channel-pair halves into the pending
+      // results, then restart
+      const int px = P0 + 32 * (4 * j + wave) + l32;
+      const int n = px / HW, hw = px - n * HW;
+      pend_base = px < Pend ? (unsigned)(n * K * HW + hw) * 4u : kOob;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) pend[16 * kb + v] = acc[kb][0][v] + acc[kb][1][v];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 2; ++e) acc[kb][e] = v16f{};
+    }
+    if constexpr (q == NQ - 1 && j == NB - 1) {
+      // last block done: add the two channel-pair halves and store 32 pixels
+      // (two rows of k per instruction, streaming hint)
       const int px = P0 + 32 * (4 * j + wave) + l32;
       if (px < Pend) {
         const int n = px / HW, hw = px - n * HW;

@@ -321,6 +321,7 @@ bool resolve_geom(const Shape& s0, const Variant& v, const conv_plan_t& plan, Ge
     if (bytes > kHw.lds_bytes || groups * tiles_k >= (int64_t(1) << 31)) return false;
     if ((int64_t)s.N * s.C * s.W * 4 >= (int64_t(1) << 30)) return false;  // 32-bit byte offsets
     if ((int64_t)s.K * s.C * 4 >= (int64_t(1) << 31)) return false;        // below the Ker sentinel
+    if ((int64_t)s.N * s.K * s.W * 4 >= (int64_t(1) << 31)) return false;  // Out: 32-bit store offsets
     Geom q;
     std::memset(&q, 0, sizeof(q));
     q.N = s.N; q.C = s.C; q.K = s.K; q.H = s.H; q.W = s.W; q.R = 1; q.S = 1;

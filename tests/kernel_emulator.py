@@ -723,7 +723,10 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
     32x32x2 MFMAs, even and odd channel pairs in separate accumulators added
     at the store, and k rows 16 s .. 16 s + 15 of the 16-pixel tail block at
     P0 + 128 NB on 16x16x4 MFMAs.  In offsets are 32-bit byte offsets from
-    raw buffer loads (offsets at or past the buffer size read 0)."""
+    raw buffer loads (offsets at or past the buffer size read 0); every block
+    but the last is stored during the next block, results 32 q / nq ..
+    32 (q + 1) / nq - 1 at its step q, through 32-bit byte offsets of raw
+    buffer stores (past Out's size: dropped), the last through pointers."""
     N, C, K, H, W = (g[x] for x in "N C K H W".split())
     _chk(g["family"] == 7 and g["R"] == 1 and g["S"] == 1 and H == 1, "balanced pointwise geometry")
     _chk(g["threads"] == 256 and g["nwp"] == 4 and g["nwk"] == 1, "four waves per workgroup")
@@ -745,6 +748,8 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
     written = np.zeros(out_size, np.int64)
     lane = np.arange(64)
     KOOB, M32 = 0x80000000, 0xFFFFFFFF
+    out_bytes = out_size * 4
+    _chk(out_bytes < 2 ** 31, "Out byte range below 2 GB")
     cstride = 4 * HW
 
     def in_load(voff, byte_add, expect):
@@ -767,6 +772,17 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
         _chk((dst[st] >= 0).all() and (dst[st] < out_size).all(), "Out store range")
         out[dst[st]] = vals[st]
         np.add.at(written, dst[st], 1)
+
+    def store_buffer(vals, k, px, valid):
+        # pend_base + k * HW * 4, or the sentinel for masked lanes and rows
+        n, hw = px // HW, px % HW
+        base = np.where(valid, (n * K * HW + hw) * 4, KOOB)
+        off = np.where(k < K, base + k * HW * 4, KOOB) & M32
+        hit = off < out_bytes
+        _chk((hit == (valid & (k < K))).all(), "Out range check does not match the mask")
+        _chk((off[hit] % 4 == 0).all(), "misaligned Out offset")
+        out[off[hit] // 4] = vals[hit]
+        np.add.at(written, off[hit] // 4, 1)
 
     def in_off(px, c, pend):
         n, hw = px // HW, px % HW
@@ -794,11 +810,17 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
         l32, h32 = lane & 31, lane >> 5
         l16, h16 = lane & 15, lane >> 4
         for wave in range(4):
+            pending = None  # the previous block's 32 results, lane pixels and mask
             for j in range(NB):
                 px = P0 + 32 * (4 * j + wave) + l32
                 voff, valid = in_off(px, h32, pend)
                 acc = np.zeros((2, 2, 32, 32))  # [kb][e]
                 for q in range(nq):
+                    if pending is not None:
+                        vals, ppx, pvalid = pending
+                        for r in range(32 * q // nq, 32 * (q + 1) // nq):
+                            kb, v = r // 16, r % 16
+                            store_buffer(vals[r], k0 + 32 * kb + 8 * (v // 4) + 4 * h32 + v % 4, ppx, pvalid)
                     for e in range(2):
                         bv = in_load(voff, (4 * q + 2 * e) * cstride, valid)
                         for kb in range(2):
@@ -808,10 +830,14 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
                             Bm = np.zeros((2, 32))
                             Bm[h32, l32] = bv
                             acc[kb, e] += Am @ Bm
-                for kb in range(2):
-                    for v in range(16):
-                        i = 8 * (v // 4) + 4 * h32 + v % 4
-                        store(acc[kb, 0][i, l32] + acc[kb, 1][i, l32], k0 + 32 * kb + i, px, valid)
+                res = [acc[kb, 0][8 * (v // 4) + 4 * h32 + v % 4, l32] + acc[kb, 1][8 * (v // 4) + 4 * h32 + v % 4, l32]
+                       for kb in range(2) for v in range(16)]
+                if j < NB - 1:
+                    pending = (res, px, valid)
+                else:
+                    for kb in range(2):
+                        for v in range(16):
+                            store(res[16 * kb + v], k0 + 32 * kb + 8 * (v // 4) + 4 * h32 + v % 4, px, valid)
             # tail: 16 pixels at P0 + 128 NB, rows 16 wave .. 16 wave + 15
             px = P0 + 128 * NB + l16
             voff, valid = in_off(px, h16, pend)
