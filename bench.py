@@ -40,6 +40,19 @@ FLUSH_BYTES = 512 * 2 ** 20  # read between timed runs: twice the last-level cac
 PROTOCOL_RUNS = 50           # timed runs per layer (Sec. 10: 50 runs, the first excluded)
 RAMP_S = 0.1                 # back-to-back launches before any timing, independent of --warmup
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_conv1x1_n32_c256_k64_in56.json")
+SETS_MAX_BYTES = 16 * 2 ** 30  # device memory of all rotating buffer sets of one layer
+
+
+def buffer_sets(in_bytes, out_bytes):
+    """Number of In/Out buffer sets that back-to-back launches rotate through
+    so that each launch reads its In from HBM.  The kernels write Out with
+    streaming stores, which the 256 MB last-level cache does not keep, so In
+    alone must exceed twice that cache.  (Measured on the 226x226 bf16 layer:
+    with four sets, 209 MB of In in all, a launch took 66 us; once anything
+    of 48 MB or more passed through the cache between launches, 107 us.)
+    Capped at SETS_MAX_BYTES of device memory in all."""
+    want = -(-2 * MALL_BYTES // max(1, in_bytes)) + 1
+    return max(2, min(want, SETS_MAX_BYTES // max(1, in_bytes + out_bytes)))
 
 
 def flops(c):
@@ -92,8 +105,9 @@ def plan_kernel_hash(c, plan):
 
 class LayerRunner:
     """Device buffers and a raw-pointer launcher for one layer: In/Out buffer
-    sets rotate (more than twice the 256 MB last-level cache in all) so that
-    back-to-back launches read In from HBM and write Out to HBM."""
+    sets rotate (In alone more than twice the 256 MB last-level cache in
+    all, see buffer_sets) so that back-to-back launches read In from HBM and
+    write Out to HBM."""
 
     def __init__(self, c, out_bf16=False):
         import torch
@@ -102,8 +116,8 @@ class LayerRunner:
 
         self.c = c
         In0, Ker0 = make_inputs(c)
-        set_bytes = In0.numel() * In0.element_size() + c.N * c.K * c.P * c.Q * 4
-        self.nsets = max(2, -(-2 * MALL_BYTES // set_bytes) + 1)
+        self.nsets = buffer_sets(In0.numel() * In0.element_size(),
+                                 c.N * c.K * c.P * c.Q * (2 if out_bf16 else 4))
         dev = torch.device("cuda:0")
         self.Ker = Ker0.to(dev)
         self.ins = [In0.to(dev) for _ in range(self.nsets)]
@@ -360,8 +374,7 @@ def traffic_run(layers, launches=6):
             raise ValueError(f"{c.name}: the traffic run launches stride-1 valid layers only")
         bf16 = c.dtype == "bf16"
         edt = torch.bfloat16 if bf16 else torch.float32
-        set_bytes = c.N * c.C * c.H * c.W * (2 if bf16 else 4) + c.N * c.K * c.P * c.Q * 4
-        nsets = max(2, -(-2 * MALL_BYTES // set_bytes) + 1)
+        nsets = buffer_sets(c.N * c.C * c.H * c.W * (2 if bf16 else 4), c.N * c.K * c.P * c.Q * 4)
         ins = [torch.empty(c.N, c.C, c.H, c.W, device=dev).uniform_(-1, 1).to(edt) for _ in range(nsets)]
         Ker = torch.empty(c.K, c.C, c.R, c.S, device=dev).uniform_(-1, 1).to(edt)
         outs = [torch.empty(c.N, c.K, c.P, c.Q, device=dev) for _ in range(nsets)]
@@ -659,8 +672,7 @@ def rank_sweep(configs, n=None, reps=10):
         cands = all_candidates(c, dt)
         idx = list(range(len(cands))) if n is None else rank_sample(cands, n=n, seed=c.seed)
         In0, Ker0 = make_inputs(c)
-        set_bytes = In0.numel() * In0.element_size() + c.N * c.K * c.P * c.Q * 4
-        nsets = max(2, -(-2 * MALL_BYTES // set_bytes) + 1)
+        nsets = buffer_sets(In0.numel() * In0.element_size(), c.N * c.K * c.P * c.Q * 4)
         ins = [In0.cuda() for _ in range(nsets)]
         outs = [torch.empty(c.N, c.K, c.P, c.Q, device="cuda") for _ in range(nsets)]
         Ker = Ker0.cuda()
@@ -726,12 +738,16 @@ TRAIN_MD = os.path.join(ROOT, "profiles", "model_train_sweep.md")
 HELDOUT_SEED, TRAIN_SEED = 78, 77
 
 
-def heldout_layers(n=10, seed=HELDOUT_SEED):
+def heldout_layers(n=10, seed=HELDOUT_SEED, n_bf16=None):
     """Seeded random layers.  Seed 77 (the training set) joins the five
     configurations in the per-variant calibration of the selector; seed 78
-    (the held-out set) is used for validation only.  Shapes in Table 1's
-    range: batch 1-32, 16-512 channels, 7-58 pixels, 1x1 and 3x3 taps, valid
-    stride 1."""
+    (the held-out set) is used for validation only.  `n` fp32 shapes in
+    Table 1's range: batch 1-32, 16-512 channels, 7-58 pixels, 1x1 and 3x3
+    taps, valid stride 1; then `n_bf16` (default 4 for training, 3 held out)
+    bf16 first-layer shapes (32 input channels, 32-64 filters, 3x3, 58-226
+    pixels, batch 2-16: the family of the 226x226 layer, whose kernels no
+    fp32 layer runs), drawn from a stream of their own so that the fp32
+    shapes do not depend on them."""
     import random
 
     from paper_2101_09808_amd.workloads import ConvShape
@@ -747,6 +763,17 @@ def heldout_layers(n=10, seed=HELDOUT_SEED):
             continue
         out.append(ConvShape(f"heldout{len(out)}" if seed == HELDOUT_SEED else f"train{len(out)}", N, C, K, HW, HW,
                              RS, RS, "f32", 12000 + 100 * (seed - TRAIN_SEED) + len(out)))
+    if n_bf16 is None:
+        n_bf16 = 4 if seed == TRAIN_SEED else 3
+    rng = random.Random(1000 + seed)
+    while len(out) < n + n_bf16:
+        N = rng.choice([2, 4, 8, 16])
+        K = rng.choice([32, 48, 64])
+        HW = rng.choice([56, 112, 168, 224]) + 2  # Out rows divisible by 4, 7, 8 and 14
+        if N * K * (HW - 2) ** 2 * 4 > 400e6:
+            continue
+        out.append(ConvShape(f"heldout{len(out)}" if seed == HELDOUT_SEED else f"train{len(out)}", N, 32, K, HW, HW,
+                             3, 3, "bf16", 12000 + 100 * (seed - TRAIN_SEED) + len(out)))
     return out
 
 
@@ -755,13 +782,15 @@ def heldout_report(res, train=False):
         return rank_report(res, title="Model rank vs measured time on the calibration layers (Sec. 9), MI355X",
                            command="python bench.py --train-sweep",
                            intro="Ten seeded random fp32 layers (bench.py heldout_layers, seed 77: batch 1-32, 16-512 "
-                                 "channels, 7-58 pixels, 1x1 and 3x3) that, with the five configurations, set the "
-                                 "selector's per-variant calibration (paper_2101_09808_amd/calibrate.py).")
+                                 "channels, 7-58 pixels, 1x1 and 3x3) and four bf16 first layers (32 input channels, "
+                                 "3x3, 58-226 pixels) that, with the five configurations, set the selector's "
+                                 "per-variant calibration (paper_2101_09808_amd/calibrate.py).")
     return rank_report(res, title="Model rank vs measured time on held-out layers (Sec. 9), MI355X",
                        command="python bench.py --held-out",
                        intro="Ten seeded random fp32 layers (bench.py heldout_layers, seed 78: batch 1-32, 16-512 "
-                             "channels, 7-58 pixels, 1x1 and 3x3) that none of the model's measured constants "
-                             "(calibration included) were fitted on.")
+                             "channels, 7-58 pixels, 1x1 and 3x3) and three bf16 first layers (32 input channels, "
+                             "3x3, 58-226 pixels) that none of the model's measured constants (calibration "
+                             "included) were fitted on.")
 
 
 BREAKDOWN_COUNTERS = ["GRBM_GUI_ACTIVE", "SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAIT_INST_ANY",

@@ -388,7 +388,7 @@ def emulate(g, In, Ker, wgs=None):
 
 
 # ---------------------------------------------------------------------------
-# bf16 family (conv_bf16_kernel): persistent workgroups over tile ranges,
+# bf16 family (conv_bf16_kernel): persistent workgroups over every G-th tile,
 # channel-fastest swizzled LDS images, 16x16x32 MFMA.
 
 def _swz(chunk, idx):
@@ -433,8 +433,6 @@ def emulate_bf16(g, In, Ker, wgs=None, in_aligned=True, out_aligned=True, out_bf
     for b in (range(G) if wgs is None else wgs):
         G8 = G & ~7
         L = (b & 7) * (G8 >> 3) + (b >> 3) if b < G8 else b
-        per = -(-tiles // G)
-        t_begin, t_end = L * per, min(tiles, L * per + per)
         lds = np.full(lds_bytes // 2, np.nan)  # bf16 slots
 
         def stage_ker(k0, c0):
@@ -494,7 +492,7 @@ def emulate_bf16(g, In, Ker, wgs=None, in_aligned=True, out_aligned=True, out_bf
 
         if resident:
             stage_ker(0, 0)
-        for T in range(t_begin, t_end):
+        for T in range(L, tiles, G):  # tiles L, L + G, ...
             _chk(not seen[T], "tile processed twice")
             seen[T] = True
             acc = {}
@@ -912,7 +910,6 @@ def emulate_bf16_tr(g, In, Ker, wgs=None, out_aligned=True, out_bf16=False):
     written = np.zeros(out_size, np.int64)
     tiles = g["tiles_rows"] * g["tiles_cols"]
     G = g["grid"]
-    per = -(-tiles // G)
     # Ker: thread t, vector i covers elements 8v .. 8v+7 (v = t + 256 i) of
     # the natural order (rows past K lie past the buffer and read zeros); the
     # vectors go to the In region in that order, then thread items
@@ -944,7 +941,7 @@ def emulate_bf16_tr(g, In, Ker, wgs=None, out_aligned=True, out_bf16=False):
     for b in (range(G) if wgs is None else wgs):
         G8 = G & ~7
         L = (b & 7) * (G8 >> 3) + (b >> 3) if b < G8 else b
-        for T in range(L * per, min(tiles, (L + 1) * per)):
+        for T in range(L, tiles, G):  # tiles L, L + G, ...
             ct, rt = T % g["tiles_cols"], T // g["tiles_cols"]
             rho0 = rt * TR
             n, p0 = divmod(rho0, P)

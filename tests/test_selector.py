@@ -123,11 +123,12 @@ def test_enumeration_rules_for_channel_groups_and_narrow_steps():
 
 
 def test_bf16_out_plan_pairs_its_stores():
-    """conv_fwd_bf16_out's plan for a layer whose fastest fp32-Out tiling
-    (4 x 32) cannot pair bf16 stores into 16-byte pieces: the best candidate
-    whose wave tile pairs them (an even number of 16-pixel blocks per part,
-    in rows of an even number of blocks), as the transposing kernel does."""
-    dims = (16, 32, 64, 226, 226, 3, 3)
+    """conv_fwd_bf16_out's plan for a layer whose selected fp32-Out tiling
+    (here 7 x 64) cannot pair bf16 stores into 16-byte pieces: the best
+    candidate whose wave tile pairs them (an even number of 16-pixel blocks
+    per part, in rows of an even number of blocks), as the transposing kernel
+    does."""
+    dims = (8, 32, 48, 226, 226, 3, 3)
 
     def pairs(p):
         g = B.conv_fwd_geometry(*dims, p)
