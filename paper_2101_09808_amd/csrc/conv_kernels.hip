@@ -1149,19 +1149,36 @@ conv_bf16_tr_kernel(const unsigned short* __restrict__ In, const unsigned short*
             const int kl = kb * 16 + j;
             kop[kb] = *reinterpret_cast<const v8bf*>(lker + ((size_t)kl * KPITCH + rs) * 64 + chunk_swz(gq, kl) * 16);
           }
-#pragma unroll
-          for (int bi = 0; bi < PB; ++bi) {
-            // block b: tile row b / CBR, columns 16 * (b % CBR) ..
+          // block bi's In operand: block b = tile row b / CBR, columns 16 * (b % CBR) ..
+          auto read_iop = [&](int bi) __attribute__((always_inline)) {
             const int b = wave * WP + decltype(part)::value * PB + bi;
             const unsigned short* src =
                 lin + sx * 32 * CP + src_c * CP + (b / CBR + r) * TW + 16 * (b % CBR) + src_x;
             const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(src));
             const v4s hi =
                 __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(src + 4 * CP));
-            const v8bf iop = __builtin_bit_cast(v8bf, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+            return __builtin_bit_cast(v8bf, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+          };
+          if constexpr (NPART == 1) {
+            // one part per tile (an odd number of blocks per wave): every
+            // block's operand is read first, then the MFMAs (measured 3-7%
+            // faster on the 14x32 and 7x64 tilings; slower with two parts)
+            v8bf iop[PB];
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-              acc[bi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(iop, kop[kb], acc[bi][kb], 0, 0, 0);
+            for (int bi = 0; bi < PB; ++bi) iop[bi] = read_iop(bi);
+#pragma unroll
+            for (int bi = 0; bi < PB; ++bi)
+#pragma unroll
+              for (int kb = 0; kb < 4; ++kb)
+                acc[bi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(iop[bi], kop[kb], acc[bi][kb], 0, 0, 0);
+          } else {
+#pragma unroll
+            for (int bi = 0; bi < PB; ++bi) {
+              const v8bf iop = read_iop(bi);
+#pragma unroll
+              for (int kb = 0; kb < 4; ++kb)
+                acc[bi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(iop, kop[kb], acc[bi][kb], 0, 0, 0);
+            }
           }
           // this tap's share of the previous part's stores (for the first
           // part, those not issued during the copies)
