@@ -82,3 +82,36 @@ def test_plan_kernel_hash_follows_the_launched_kernel_and_plan():
     other_variant = next(p for p in cands if p["variant"] != p0["variant"])
     assert bench.plan_kernel_hash(c, other_tile) != h0
     assert bench.plan_kernel_hash(c, other_variant) != h0
+
+
+def test_buffer_sets_put_twice_the_last_level_cache_of_in_behind_every_launch():
+    """Out's streaming stores do not stay in the last-level cache, so the
+    rotation is sized by In alone: at least 2 x 256 MB of In across the sets
+    (a launch then reads In that the cache has evicted), within the cap on
+    device memory."""
+    mall = bench.MALL_BYTES
+    for in_b, out_b in [(52_301_824, 205_520_896), (102_760_448, 25_690_112), (861_184, 802_816),
+                        (14_745_600, 12_845_056)]:
+        n = bench.buffer_sets(in_b, out_b)
+        assert n * in_b >= 2 * mall + in_b, (in_b, n)
+        assert (n - 1) * in_b < 2 * mall + in_b, (in_b, n)  # no more than needed
+        assert n * (in_b + out_b) <= bench.SETS_MAX_BYTES
+    # a huge Out caps the count (and never below two sets)
+    assert bench.buffer_sets(1 << 20, 4 << 30) == 3  # 16 GB / (4 GB + 1 MB)
+    assert bench.buffer_sets(1 << 30, 8 << 30) == 2
+
+
+def test_bf16_calibration_layers_admit_every_transposing_tiling():
+    """The bf16 first layers of the training and held-out sets have Out rows
+    divisible by every transposing tiling's rows, so each tiling is timed on
+    each of them."""
+    from paper_2101_09808_amd import conv as B
+
+    for seed in (bench.TRAIN_SEED, bench.HELDOUT_SEED):
+        layers = [c for c in bench.heldout_layers(seed=seed) if c.dtype == "bf16"]
+        assert len(layers) == (4 if seed == bench.TRAIN_SEED else 3)
+        for c in layers:
+            assert c.C == 32 and c.R == c.S == 3 and c.P % 56 == 0
+            n = B.lib().conv_fwd_candidates(*c.key(), B.CONV_DTYPE_BF16, None, 0)
+            cands = B.conv_fwd_candidates(*c.key(), dtype=B.CONV_DTYPE_BF16, cap=n)
+            assert {211, 212, 213, 214, 215, 216} <= {p["variant"] for p in cands}, c
