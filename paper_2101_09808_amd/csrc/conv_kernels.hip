@@ -1457,8 +1457,9 @@ conv1x1_stream_kernel(const float* __restrict__ In, const float* __restrict__ Ke
 // (64 rows of this k tile, all C channels) is staged through registers into
 // LDS in chunks of 64 channels during the first block, each chunk requested
 // a whole chunk ahead; every load is visible to the compiler, so its waits
-// are exact.  Requires C % 64 == 0, In below 1 GB and Out below 2 GB
-// (32-bit offsets).
+// are exact.  Strided or padded 1x1 layers read In through the phase
+// mapping (no separate pass).  Requires C % 64 == 0, In below 1 GB and Out
+// below 2 GB (32-bit offsets).
 template <int NB, int D, int NQ>
 __global__ void __launch_bounds__(256)
 conv1x1_bal_kernel(const float* __restrict__ In, const float* __restrict__ Ker, float* __restrict__ Out,
@@ -1487,10 +1488,18 @@ conv1x1_bal_kernel(const float* __restrict__ In, const float* __restrict__ Ker, 
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(In), (short)0, (int)g.in_bytes, 0x00020000);
   __amdgpu_buffer_rsrc_t krsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(Ker), (short)0, (int)g.ker_bytes, 0x00020000);
-  const unsigned cstride = 4u * (unsigned)HW;  // bytes between channels
+  // Strided or padded 1x1 layers (conv_fwd_ex, g.nph = 1) read the
+  // caller's In through the phase mapping: inner pixel (yi, xi) of image n
+  // is In pixel (yi sh - ph, xi sw - pw), zero outside the image.
+  const unsigned cstride = 4u * (unsigned)(g.nph ? g.H0 * g.W0 : HW);  // bytes between channels
   auto in_off = [&](int px, int c) __attribute__((always_inline)) {
     const int n = px / HW, hw = px - n * HW;
-    return (px < Pend) ? (unsigned)((n * C + c) * HW + hw) * 4u : kOob;
+    if (px >= Pend) return kOob;
+    if (g.nph == 0) return (unsigned)((n * C + c) * HW + hw) * 4u;
+    const int yi = fdiv(hw, g.dv_Wi), xi = hw - yi * g.Wi;
+    const int iy = yi * g.sh - g.ph, ix = xi * g.sw - g.pw;
+    if (iy < 0 || iy >= g.H0 || ix < 0 || ix >= g.W0) return kOob;
+    return (unsigned)(((n * g.C0 + c) * g.H0 + iy) * g.W0 + ix) * 4u;
   };
   unsigned off32[NB];
 #pragma unroll

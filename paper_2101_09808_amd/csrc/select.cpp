@@ -528,9 +528,16 @@ double rank_time(const conv_plan_t& p) { return p.rank_us; }
 
 bool phase_direct(const Variant& v, const PhaseGeom& p, int dtype, Geom* g) {
   const int nph = p.na * p.nb;
-  if (dtype != CONV_DTYPE_F32 || v.family != FAMILY_DMA || v.in_vec != 1 || v.tc % nph) return false;
+  if (dtype != CONV_DTYPE_F32) return false;
   const int64_t in_bytes = (int64_t)p.N * p.C * p.H * p.W * 4;
-  if (in_bytes >= (int64_t(1) << 31)) return false;  // 32-bit byte offsets below the out-of-range marker
+  if (v.family == FAMILY_STREAM1X1_BAL) {
+    // a 1x1 layer has one phase; each lane's In offset is mapped once, and
+    // the kernel's channel steps keep its offsets below 2^32 for In < 1 GB
+    if (nph != 1 || p.Rp != 1 || p.Sp != 1 || in_bytes >= (int64_t(1) << 30)) return false;
+  } else {
+    if (v.family != FAMILY_DMA || v.in_vec != 1 || v.tc % nph) return false;
+    if (in_bytes >= (int64_t(1) << 31)) return false;  // 32-bit byte offsets below the out-of-range marker
+  }
   g->nph = nph;
   g->na = p.na; g->nb = p.nb;
   g->sh = p.sh; g->sw = p.sw;

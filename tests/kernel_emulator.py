@@ -724,9 +724,16 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
     raw buffer loads (offsets at or past the buffer size read 0); every block
     but the last is stored during the next block, results 32 q / nq ..
     32 (q + 1) / nq - 1 at its step q, through 32-bit byte offsets of raw
-    buffer stores (past Out's size: dropped), the last through pointers."""
+    buffer stores (past Out's size: dropped), the last through pointers.
+    With g["nph"] (conv_fwd_ex, one phase) In is the caller's outer tensor,
+    read through the phase mapping: inner pixel (yi, xi) is In pixel
+    (yi sh - ph, xi sw - pw), zero outside the image."""
     N, C, K, H, W = (g[x] for x in "N C K H W".split())
     _chk(g["family"] == 7 and g["R"] == 1 and g["S"] == 1 and H == 1, "balanced pointwise geometry")
+    nph = g.get("nph", 0)
+    if nph:
+        _chk(nph == 1 and g["na"] == 1 and g["nb"] == 1 and g["C0"] == C and g["Wi"] > 0 and W % g["Wi"] == 0,
+             "one phase of a 1x1 layer")
     _chk(g["threads"] == 256 and g["nwp"] == 4 and g["nwk"] == 1, "four waves per workgroup")
     NB = g["max_ni"]
     _chk(g["tc"] == C and C % 64 == 0 and g["wp"] == 2 * NB + 1, "instance for this channel count")
@@ -739,6 +746,8 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
     total_px = N * HW
     _chk(g["tiles_rows"] == -(-total_px // pw) and g["grid"] == g["tiles_rows"] * g["tiles_k"], "grid")
     in_size, ker_size, out_size = N * C * HW, K * C, N * K * HW
+    if nph:
+        in_size = N * C * g["H0"] * g["W0"]
     _chk(In.size == in_size and Ker.size == ker_size, "input sizes")
     _chk(g["in_bytes"] == in_size * 4 and in_size * 4 < 2 ** 30, "In byte range below 1 GB")
     _chk(g["ker_bytes"] == ker_size * 4 and ker_size * 4 < 2 ** 31, "Ker byte range below the sentinel")
@@ -748,7 +757,7 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
     KOOB, M32 = 0x80000000, 0xFFFFFFFF
     out_bytes = out_size * 4
     _chk(out_bytes < 2 ** 31, "Out byte range below 2 GB")
-    cstride = 4 * HW
+    cstride = 4 * (g["H0"] * g["W0"] if nph else HW)
 
     def in_load(voff, byte_add, expect):
         off = (voff + byte_add) & M32
@@ -784,7 +793,13 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
 
     def in_off(px, c, pend):
         n, hw = px // HW, px % HW
-        return np.where(px < pend, ((n * C + c) * HW + hw) * 4, KOOB), px < pend
+        if not nph:
+            return np.where(px < pend, ((n * C + c) * HW + hw) * 4, KOOB), px < pend
+        yi, xi = hw // g["Wi"], hw % g["Wi"]
+        iy, ix = yi * g["sh"] - g["ph"], xi * g["sw"] - g["pw"]
+        inside = (px < pend) & (iy >= 0) & (iy < g["H0"]) & (ix >= 0) & (ix < g["W0"])
+        off = ((n * g["C0"] + c) * g["H0"] + iy) * g["W0"] + ix
+        return np.where(inside, off * 4, KOOB), inside
 
     for b in (range(g["grid"]) if wgs is None else wgs):
         kt, pg = b % g["tiles_k"], b // g["tiles_k"]
@@ -811,7 +826,8 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
             pending = None  # the previous block's 32 results, lane pixels and mask
             for j in range(NB):
                 px = P0 + 32 * (4 * j + wave) + l32
-                voff, valid = in_off(px, h32, pend)
+                voff, inside = in_off(px, h32, pend)
+                valid = px < pend
                 acc = np.zeros((2, 2, 32, 32))  # [kb][e]
                 for q in range(nq):
                     if pending is not None:
@@ -820,7 +836,7 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
                             kb, v = r // 16, r % 16
                             store_buffer(vals[r], k0 + 32 * kb + 8 * (v // 4) + 4 * h32 + v % 4, ppx, pvalid)
                     for e in range(2):
-                        bv = in_load(voff, (4 * q + 2 * e) * cstride, valid)
+                        bv = in_load(voff, (4 * q + 2 * e) * cstride, inside)
                         for kb in range(2):
                             av = lds_read(lds, (kb * 32 + l32) * pitch + 4 * q + 2 * e + h32)
                             Am = np.zeros((32, 2))
@@ -838,10 +854,11 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
                             store(res[16 * kb + v], k0 + 32 * kb + 8 * (v // 4) + 4 * h32 + v % 4, px, valid)
             # tail: 16 pixels at P0 + 128 NB, rows 16 wave .. 16 wave + 15
             px = P0 + 128 * NB + l16
-            voff, valid = in_off(px, h16, pend)
+            voff, inside = in_off(px, h16, pend)
+            valid = px < pend
             acc16 = np.zeros((16, 16))
             for q in range(nq):
-                bv = in_load(voff, 4 * q * cstride, valid)
+                bv = in_load(voff, 4 * q * cstride, inside)
                 av = lds_read(lds, (16 * wave + l16) * pitch + 4 * q + h16)
                 Am = np.zeros((16, 4))
                 Am[l16, h16] = av

@@ -493,6 +493,21 @@ def test_strided_full_config_full_compare(cfg):
     assert rel_err(out, ref) <= TOL["f32"]
 
 
+def test_strided_padded_1x1_direct_full_compare():
+    """A padded stride-2 1x1 layer whose plan is the balanced pointwise
+    kernel reading In through the phase mapping (border pixels read zeros
+    and are still stored): every output against the oracle."""
+    shape = ConvShape("s2p1_1x1_n8_c64_k64_in56", 8, 64, 64, 56, 56, 1, 1, "f32", 75, 2, 1)
+    p, direct = B.conv_fwd_ex_plan(*shape.key(), shape.stride, shape.pad)
+    assert direct and B.conv_fwd_ex_geometry(*shape.key(), (2, 2), (1, 1), p)["family"] == 7
+    In, Ker = make_inputs(shape)
+    say(f"[gpu] strided padded 1x1 {shape.name} v{p['variant']}")
+    out = host(B.conv_fwd_ex(In.to(DEV), Ker.to(DEV), 2, 1))
+    ref = oconv.conv_fwd_ex(host(In), host(Ker), (2, 2), (1, 1))
+    assert out.shape == ref.shape
+    assert rel_err(out, ref) <= TOL["f32"]
+
+
 @pytest.mark.parametrize("cfg", __import__("paper_2101_09808_amd.workloads", fromlist=["x"]).TABLE1,
                          ids=lambda c: c.name)
 def test_table1_layer_full_compare(cfg):

@@ -268,7 +268,10 @@ def _direct_cases():
     cases = [s for s in STRIDED_SHAPES if s.dtype == "f32"]
     # stride 1 with same padding, and a 1x1 stride-2 layer on a channel-group kernel
     cases += [ConvShape("pad1_3x3", 2, 24, 40, 13, 11, 3, 3, "f32", 71, 1, 1),
-              ConvShape("s2_1x1_c64", 1, 64, 72, 14, 12, 1, 1, "f32", 72, 2, 0)]
+              ConvShape("s2_1x1_c64", 1, 64, 72, 14, 12, 1, 1, "f32", 72, 2, 0),
+              # a padded 1x1 layer: the balanced pointwise kernel reads zeros
+              # for the border pixels and still stores them
+              ConvShape("s2p1_1x1_c128", 2, 128, 40, 15, 13, 1, 1, "f32", 73, 2, 1)]
     return cases
 
 
@@ -303,6 +306,38 @@ def test_direct_phase_addressing_indexing(shape):
     sel = B.conv_fwd_plan(*inner[:7])
     if B.conv_fwd_geometry(*inner[:7], sel)["family"] == 2:
         assert B.conv_fwd_ex_geometry(*shape.key(), st, pd, sel)["nph"] in (0, inner[1] // shape.C)
+
+
+@pytest.mark.parametrize("shape", [
+    ConvShape("s2_1x1_n32_c64_k128_in56", 32, 64, 128, 56, 56, 1, 1, "f32", 74, 2, 0),
+    ConvShape("s2p1_1x1_n8_c64_k64_in56", 8, 64, 64, 56, 56, 1, 1, "f32", 75, 2, 1),
+], ids=lambda s: s.name)
+def test_bal_direct_phase_addressing_indexing(shape):
+    """conv_fwd_ex's plan for strided (and padded) 1x1 layers of this size:
+    the balanced pointwise kernel reading the caller's In through the phase
+    mapping; the first, a middle and the last workgroups, every output they
+    store against the strided, padded oracle (the others store nothing)."""
+    p, direct = B.conv_fwd_ex_plan(*shape.key(), shape.stride, shape.pad)
+    st, pd = (shape.stride, shape.stride), (shape.pad, shape.pad)
+    g = B.conv_fwd_ex_geometry(*shape.key(), st, pd, p)
+    assert direct and g["family"] == 7 and g["nph"] == 1
+    In, Ker = make_inputs(shape)
+    In64, Ker64 = In.numpy().astype(np.float64), Ker.numpy().astype(np.float64)
+    ref = oconv.conv_fwd_ex(In.numpy(), Ker.numpy(), st, pd).reshape(-1)
+    G = g["grid"]
+    out, written = emulate(g, In64.reshape(-1), Ker64.reshape(-1), wgs=[0, G // 2, G - 1])
+    assert written.max() == 1 and written.sum() > 0
+    hit = written == 1
+    assert np.max(np.abs(out[hit] - ref[hit])) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
+    # every output of those workgroups' pixel ranges and 64-row k tiles is stored
+    PQ = ref.size // (shape.N * shape.K)
+    i = np.arange(ref.size)
+    px, k = i % PQ + (i // (shape.K * PQ)) * PQ, (i // PQ) % shape.K
+    mine = np.zeros(ref.size, bool)
+    for b in (0, G // 2, G - 1):
+        kt, pg = b % g["tiles_k"], b // g["tiles_k"]
+        mine |= (px >= pg * g["tw"]) & (px < (pg + 1) * g["tw"]) & (k // 64 == kt)
+    assert np.array_equal(hit, mine)
 
 
 @pytest.mark.parametrize("shape_index,aligned", [(2, True), (4, True), (2, False)])
