@@ -184,9 +184,13 @@ int conv_fwd_bf16_out(int N, int C, int K, int H, int W, int R, int S,
  * becomes min(sh,R) x min(sw,S) phase images; Ker gets ceil(R/sh) x
  * ceil(S/sw) taps, zero where no original tap lands) and runs the selected
  * stride-1 plan of the inner problem (see conv_fwd_ex_inner_shape and
- * conv_fwd_ex_plan).  For fp32 plans on the direct-to-LDS kernel the kernel
- * reads In through the phase mapping (see conv_fwd_ex_geometry); otherwise a
- * small kernel writes the phase images into a workspace first.  With more
+ * conv_fwd_ex_plan).  For fp32 plans on the direct-to-LDS kernel (and on
+ * the balanced pointwise kernel for 1x1 layers) the kernel reads In through
+ * the phase mapping (see conv_fwd_ex_geometry); otherwise a small kernel
+ * writes the phase images into a workspace first.  For stride-2 layers with
+ * odd taps (R = 2 ceil(R/2) - 1, likewise S) the plan may be a phase-skip
+ * variant of the direct-to-LDS kernel, which leaves out the zero taps of the
+ * phases (3x3: 7 of 16).  With more
  * than one phase per channel, another small kernel writes the rearranged
  * Ker into a workspace.  Workspaces are the per-stream ones described under
  * Ownership.  Asynchronous like conv_fwd.  Returns a conv_status_t.
@@ -250,7 +254,8 @@ int conv_fwd_plan(int N, int C, int K, int H, int W, int R, int S, int dtype,
  * floats.  `In`/`Ker` are fp32
  * or bf16 per plan->dtype.  Returns CONV_EINVAL for a plan the kernels cannot
  * run -- including a plan whose vector loads need 16-byte aligned In or Ker
- * when the tensors passed are not -- else as conv_fwd.
+ * when the tensors passed are not, and a phase-skip plan (conv_fwd_ex
+ * only) -- else as conv_fwd.
  */
 int conv_fwd_with_plan(int N, int C, int K, int H, int W, int R, int S,
                        const void* In, const void* Ker, float* Out,
@@ -332,7 +337,10 @@ int conv_model_volume(const int perm[7], const int64_t N[7], const int64_t T[7],
  *   pointwise streaming unrolled / looped), In vector
  *   width, pipeline stages, LDS elements per stage (family 3: LDS bytes), In
  *   elements per stage (family 2), In and Ker bytes, workgroups launched;
- *   three reserved zeros; channel ranges of the reduction, pipeline steps
+ *   1 if the kernel skips the zero taps of a stride-2 odd-tap layer's phases
+ *   (family 2; such plans run only through conv_fwd_ex, and
+ *   conv_fwd_geometry rejects them), then two reserved zeros; channel ranges
+ *   of the reduction, pipeline steps
  *   per range; 1 if the inner loop is on 32x32x2 MFMAs (family 2); groups
  *   of waves that split each pipeline step's channels inside the workgroup
  *   (family 2; 1 otherwise); then the direct phase addressing of

@@ -342,7 +342,7 @@ GEOM_FIELDS = (
     "lds_in_elems", "lds_ker_elems", "ni_in", "ni_ker", "nchunks",
     "wk", "wp", "tc", "rc", "sc", "max_ni", "max_nk", "ker_vec", "threads", "lds_bytes",
     "family", "in_vec", "stages", "stage_elems", "in_region", "in_bytes", "ker_bytes", "grid",
-    "reserved0", "reserved1", "reserved2", "split", "cps", "mfma32", "nwc",
+    "phase_skip", "reserved1", "reserved2", "split", "cps", "mfma32", "nwc",
     "nph", "na", "nb", "sh", "sw", "ph", "pw", "C0", "H0", "W0", "Wi",
 ) + tuple(f"dv_{d}_{x}" for d in ("in_cstride", "in_wp", "H", "ker_rstride", "tw", "P", "nph", "nb", "Wi",
                                   "tiles_k", "tiles_cols", "tiles_rows") for x in ("m", "s"))

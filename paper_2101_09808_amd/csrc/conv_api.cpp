@@ -168,7 +168,7 @@ int cached_plan(const Shape& s, int dtype, conv_plan_t* out) {
 int run(const Shape& s, const void* In, const void* Ker, float* Out, const conv_plan_t& plan,
         void* stream) {
   const Variant* v = find_variant(plan.variant);
-  if (!v || v->dtype != plan.dtype) return CONV_EINVAL;
+  if (!v || v->dtype != plan.dtype || v->phase_skip) return CONV_EINVAL;  // phase skip: conv_fwd_ex only
   if (!variant_fits(*v, plan.dtype, alignment_of(In, Ker))) return CONV_EINVAL;
   Geom g;
   if (!resolve_geom(s, *v, plan, &g, nullptr)) return CONV_EINVAL;
@@ -228,14 +228,20 @@ int select_ex_entry(const PhaseGeom& p, int align_direct, int align_split, ExEnt
   // (Ranking the candidates with the phase-split pass charged to plans that
   // cannot read In directly picked worse plans on the small layers, whose
   // predicted times are least reliable: Table 1's R1 28 -> 54 us.)
+  // Stride-2 layers with odd taps also get the phase-skip variants, which
+  // run only reading In directly.
+  const bool skip_ok = p.na == 2 && p.nb == 2 && p.sh == 2 && p.sw == 2 && p.R == 2 * p.Rp - 1 &&
+                       p.S == 2 * p.Sp - 1;
   std::vector<conv_plan_t> buf(4096);
-  const int n = std::min<int>(enumerate_plans(inner, CONV_DTYPE_F32, buf.data(), (int)buf.size()), (int)buf.size());
+  const int n =
+      std::min<int>(enumerate_plans(inner, CONV_DTYPE_F32, buf.data(), (int)buf.size(), skip_ok), (int)buf.size());
   for (int i = 0; i < n; ++i) {
     const Variant* v = find_variant(buf[i].variant);
     Geom g;
     if (!v || !resolve_geom(inner, *v, buf[i], &g, nullptr)) continue;
     Geom gd = g;
     const bool direct = variant_fits(*v, CONV_DTYPE_F32, align_direct) && phase_direct(*v, p, CONV_DTYPE_F32, &gd);
+    if (v->phase_skip && !direct) continue;
     if (!direct && !variant_fits(*v, CONV_DTYPE_F32, align_split)) continue;
     out->e.plan = buf[i];
     out->e.v = v;
@@ -301,7 +307,7 @@ int export_geometry(const Variant& vr, const Geom& g, int lds, int32_t* out, int
       g.lds_in_elems, g.lds_ker_elems, g.ni_in, g.ni_ker, g.nchunks,
       v->wk, v->wp, v->tc, v->rc, v->sc, v->max_ni, v->max_nk, v->ker_vec, v->threads, lds,
       v->family, v->in_vec, v->stages, g.stage_elems, g.in_region, (int32_t)g.in_bytes,
-      (int32_t)g.ker_bytes, g.grid, 0, 0, 0, g.split, g.cps, v->mfma32, v->groups(),
+      (int32_t)g.ker_bytes, g.grid, v->phase_skip, 0, 0, g.split, g.cps, v->mfma32, v->groups(),
       g.nph, g.na, g.nb, g.sh, g.sw, g.ph, g.pw, g.C0, g.H0, g.W0, g.Wi,
       (int32_t)g.dv_in_cstride.m, g.dv_in_cstride.s, (int32_t)g.dv_in_wp.m, g.dv_in_wp.s,
       (int32_t)g.dv_H.m, g.dv_H.s, (int32_t)g.dv_ker_rstride.m, g.dv_ker_rstride.s,
@@ -650,7 +656,7 @@ int conv_fwd_geometry(int N, int C, int K, int H, int W, int R, int S, const con
   if (st != CONV_OK) return st;
   if (!plan || (cap > 0 && !out)) return CONV_ENULL;
   const Variant* v = find_variant(plan->variant);
-  if (!v) return CONV_EINVAL;
+  if (!v || v->phase_skip) return CONV_EINVAL;  // phase skip: conv_fwd_ex_geometry only
   Geom g;
   int lds = 0;
   if (!resolve_geom(Shape{N, C, K, H, W, R, S}, *v, *plan, &g, &lds)) return CONV_EINVAL;
@@ -670,7 +676,8 @@ int conv_fwd_ex_geometry(int N, int C, int K, int H, int W, int R, int S, int st
   const Shape inner{N, C * p.na * p.nb, K, p.Hp, p.Wp, p.Rp, p.Sp};
   if (!resolve_geom(inner, *v, *plan, &g, &lds)) return CONV_EINVAL;
   const bool rewrite = stride_h > 1 || stride_w > 1 || pad_h > 0 || pad_w > 0;
-  if (rewrite) phase_direct(*v, p, plan->dtype, &g);  // leaves nph = 0 where it does not apply
+  const bool direct = rewrite && phase_direct(*v, p, plan->dtype, &g);  // nph stays 0 where it does not apply
+  if (v->phase_skip && !direct) return CONV_EINVAL;  // phase skip runs only reading In directly
   return export_geometry(*v, g, lds, out, cap);
 }
 

@@ -46,6 +46,8 @@ struct Variant {
   int stages;     // pipeline depth (LDS buffers)
   int mfma32;     // DMA: 1 = 32x32x2 inner loop (64-row k tile, 32-pixel blocks)
   int nwc;        // DMA: groups of waves splitting each step's channels (0 = 1, no split)
+  int phase_skip; // DMA: skips the zero taps of a stride-2 odd-tap layer's phases; runs only
+                  // through conv_fwd_ex, reading In through the phase mapping
   int groups() const { return nwc > 1 ? nwc : 1; }
 };
 
@@ -172,7 +174,9 @@ int time_launches(const Variant& v, const Geom& g, const void* In, const void* K
 
 // Selector entry points (host only, no HIP calls).
 int select_plan(const Shape& s, int dtype, conv_plan_t* out);
-int enumerate_plans(const Shape& s, int dtype, conv_plan_t* plans, int cap);
+// phase_skip: also the phase-skip variants (conv_fwd_ex's stride-2 odd-tap
+// layers, read through the phase mapping; they are wrong for any other use)
+int enumerate_plans(const Shape& s, int dtype, conv_plan_t* plans, int cap, bool phase_skip = false);
 int score_plan(const Shape& s, conv_plan_t* plan);  // fills the derived fields of a plan
 
 // Paper model, Sec. 3.2: per-array volumes for a permutation (codes n=0..w=6).

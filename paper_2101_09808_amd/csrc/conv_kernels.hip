@@ -337,6 +337,23 @@ __device__ __forceinline__ void wait_vmcnt_opaque() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Pipeline steps st = (channel group cs, tap rs) of one chunk that the
+// phase-skip kernel runs: group cs holds phase f = cs / GPP (GPP groups of
+// four channels per phase); with PS false, every step.
+template <int NSTEP, int RC, int SC, int GPP, bool PS>
+struct PhaseSteps {
+  int st[NSTEP > 0 ? NSTEP : 1];
+  int n;
+  constexpr PhaseSteps() : st{}, n(0) {
+    for (int i = 0; i < NSTEP; ++i) {
+      const int cs = i / (RC * SC), rs = i % (RC * SC), r = rs / SC, s = rs % SC;
+      const int f = PS ? cs / GPP : 0, a = f >> 1, b = f & 1;
+      if (PS && ((a == 1 && r == RC - 1) || (b == 1 && s == SC - 1))) continue;
+      st[n++] = i;
+    }
+  }
+};
+
 // MF32 selects the inner loop: false, WK x WP blocks of 16x16 on
 // v_mfma_f32_16x16x4f32 (four channels per step); true, a 64-row k tile
 // (WK = 4) times WP/2 blocks of 32 pixels on v_mfma_f32_32x32x2f32 (two
@@ -349,14 +366,28 @@ __device__ __forceinline__ void wait_vmcnt_opaque() {
 // accumulators are summed through LDS at the end (in group order, so the
 // result is deterministic).  Small layers then keep every SIMD busy without
 // a second, reducing kernel.
+//
+// PS (phase skip) is for the polyphase rewrite of a stride-2 layer with odd
+// taps R = 2 RC - 1, S = 2 SC - 1, run through conv_fwd_ex with In read by
+// the phase mapping (four phases (a, b) per input channel).  Tap (r', s') of
+// phase (a, b) is a real tap unless a = 1 and r' = RC - 1, or b = 1 and
+// s' = SC - 1; the rearranged Ker is zero there (3x3: 7 of 16 taps).  A
+// chunk of TC inner channels is laid out phase-major in LDS (position
+// f * TC/4 + c holds phase f of the chunk's input channel c), so that each
+// step's four channels share one phase, and the steps of zero taps are left
+// out of the unrolled loop.
 template <int WK, int WP, int NW, int TC, int RC, int SC, int NS, int NLI, int KVI, int NLK, int KVK,
-          bool MF32 = false, int NWC = 1>
+          bool MF32 = false, int NWC = 1, bool PS = false>
 __global__ void __launch_bounds__(NW * 64)
 conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
                     float* __restrict__ Out, const Geom g) {
   static_assert(NS >= 2 && NS <= 4, "pipeline depth");
   static_assert(NWC == 1 || (!MF32 && NW % NWC == 0 && TC % (4 * NWC) == 0),
                 "channel groups: 16x16x4 loop, whole waves and whole channel quads per group");
+  static_assert(!PS || (!MF32 && NWC == 1 && TC % 16 == 0 && RC > 1 && SC > 1 && KVI == 1 &&
+                        (RC * SC) % KVK == 0),
+                "phase skip: 16x16x4 loop, four input channels per phase and step, Ker vectors within a tap row");
+  constexpr int TCO = TC / 4;  // PS: input channels per chunk
   extern __shared__ __align__(16) float lds[];
   constexpr int IN_REGION = NLI * NW * 64 * KVI;
   constexpr int KER_REGION = NLK * NW * 64 * KVK;
@@ -399,7 +430,10 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
             in_goff[i] = ((n * C + cl) * H + y) * W + t.q0 + x;
           } else {
             // phase (a, b) of input channel c: a chunk holds whole channels
-            const int c = fdiv(cl, g.dv_nph), f = cl - c * g.nph, a = fdiv(f, g.dv_nb), b = f - a * g.nb;
+            // (PS: LDS position cl is phase cl / TCO of channel cl % TCO)
+            const int c = PS ? cl % TCO : fdiv(cl, g.dv_nph);
+            const int f = PS ? cl / TCO : cl - c * g.nph;
+            const int a = fdiv(f, g.dv_nb), b = f - a * g.nb;
             int yi = y, xi = t.q0 + x;
             if (g.Wi) {  // 1x1 kernel view: one row of H' x W' pixels
               yi = fdiv(xi, g.dv_Wi);
@@ -407,8 +441,9 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
             }
             const int iy = yi * g.sh + a - g.ph, ix = xi * g.sw + b - g.pw;
             if (iy >= 0 && iy < g.H0 && ix >= 0 && ix < g.W0) in_goff[i] = ((n * g.C0 + c) * g.H0 + iy) * g.W0 + ix;
+            if (PS) in_cl[i] = c * 4 + f;  // the inner channel, for the channel-count check
           }
-          in_cl[i] = cl;
+          if (!PS || g.nph == 0) in_cl[i] = cl;
         }
       }
     }
@@ -424,8 +459,11 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
     ker_goff[i] = -1;
     ker_m[i] = 0;
     if (kl < BK && m < TCRS && t.k0 + kl < K) {
-      ker_goff[i] = (t.k0 + kl) * C * RS + m;
-      ker_m[i] = m;
+      // PS: LDS position (f * TCO + c) * RS + rs holds the rearranged Ker's
+      // inner channel c * 4 + f (a vector stays within one channel's taps)
+      const int mg = PS ? ((m / RS % TCO) * 4 + m / RS / TCO) * RS + m % RS : m;
+      ker_goff[i] = (t.k0 + kl) * C * RS + mg;
+      ker_m[i] = mg;
     }
   }
   static_assert(!MF32 || (WK == 4 && WP % 2 == 0), "32x32 blocks: 64 k rows, pixel blocks in pairs of 16");
@@ -506,11 +544,13 @@ conv_f32_dma_kernel(const float* __restrict__ In, const float* __restrict__ Ker,
 #pragma unroll
       for (int pb = 0; pb < NPB; ++pb) b[slot][pb] = lin_c[poff[pb]];
     };
-    fetch(0, 0);
+    // PS: only the steps of real taps, in order (see the template's comment)
+    constexpr PhaseSteps<NSTEP, RC, SC, TCO / 4, PS> steps{};
+    fetch(steps.st[0], 0);
 #pragma unroll
-    for (int st = 0; st < NSTEP; ++st) {
-      const int cur = st & 1;
-      if (st + 1 < NSTEP) fetch(st + 1, cur ^ 1);
+    for (int i = 0; i < steps.n; ++i) {
+      const int cur = i & 1;
+      if (i + 1 < steps.n) fetch(steps.st[i + 1], cur ^ 1);
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
@@ -1905,6 +1945,13 @@ widen_bf16_kernel(const unsigned short* __restrict__ src, float* __restrict__ ds
                    NS, 0, NWC},                                                                  \
            &conv_f32_dma_kernel<WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK, false, NWC>, nullptr}
 
+// the same pipeline skipping the zero taps of a stride-2 odd-tap layer's
+// phases (conv_fwd_ex only)
+#define F32_DMA_PS(ID, WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK)                           \
+  Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_DMA, WK, WP, TC, RC, SC, NLI, NLK, KVK, KVI, NW * 64, \
+                   NS, 0, 1, 1},                                                                 \
+           &conv_f32_dma_kernel<WK, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK, false, 1, true>, nullptr}
+
 // the same pipeline with the 32x32x2 inner loop (WK = 4, WP even)
 #define F32_DMA32(ID, WP, NW, TC, RC, SC, NS, NLI, KVI, NLK, KVK)                                \
   Instance{Variant{ID, CONV_DTYPE_F32, FAMILY_DMA, 4, WP, TC, RC, SC, NLI, NLK, KVK, KVI, NW * 64, \
@@ -1990,6 +2037,9 @@ const Instance kInstances[] = {
     F32_DMA(116, 2, 4, 8, 4, 4, 4, 2, 3, 1, 3, 4),
     F32_DMA(117, 4, 4, 4, 16, 2, 2, 3, 6, 1, 5, 4),
     F32_DMA(118, 2, 4, 8, 16, 2, 2, 3, 10, 1, 3, 4),
+    // phase-skip twin of 118 for stride-2 3x3 layers (four input channels
+    // per phase and step)
+    F32_DMA_PS(192, 2, 4, 8, 16, 2, 2, 3, 10, 1, 3, 4),
     // squat wave tiles (4 k blocks x 4..8 pixel blocks), Ker rows loaded
     // element-wise so their LDS pitch can be conflict-free
     F32_DMA(141, 4, 4, 4, 8, 3, 3, 3, 7, 1, 19, 1),

@@ -538,6 +538,11 @@ bool phase_direct(const Variant& v, const PhaseGeom& p, int dtype, Geom* g) {
     if (v.family != FAMILY_DMA || v.in_vec != 1 || v.tc % nph) return false;
     if (in_bytes >= (int64_t(1) << 31)) return false;  // 32-bit byte offsets below the out-of-range marker
   }
+  // phase skip: stride 2 along both axes with odd taps (four phases whose
+  // zero taps are the last row / column of the odd phases)
+  if (v.phase_skip && !(p.na == 2 && p.nb == 2 && p.sh == 2 && p.sw == 2 && p.R == 2 * p.Rp - 1 &&
+                        p.S == 2 * p.Sp - 1 && v.tc % 16 == 0))
+    return false;
   g->nph = nph;
   g->na = p.na; g->nb = p.nb;
   g->sh = p.sh; g->sw = p.sw;
@@ -699,6 +704,8 @@ int score_plan_impl(const Shape& s0, conv_plan_t* plan) {
     double dv[3];
     class3_volume(Nr, Tr, 0, dv);
     plan->pred_bytes[CONV_LVL_REG] = (dv[0] + dv[1]) * e;
+    if (v->phase_skip)  // the operands of the zero-tap steps are not read
+      plan->pred_bytes[CONV_LVL_REG] *= (2.0 * v->rc - 1) * (2.0 * v->sc - 1) / (4.0 * v->rc * v->sc);
     plan->paper_bytes[CONV_LVL_REG] = plan->pred_bytes[CONV_LVL_REG];
   }
 
@@ -814,6 +821,8 @@ int score_plan_impl(const Shape& s0, conv_plan_t* plan) {
   const double per_cu = std::ceil((double)g.num_tiles * g.split / kHw.cus);
   const double waves_per_simd = per_cu * (g.nwk * g.nwp * groups) / kHw.simds_per_cu;
   plan->pred_mfma_us = waves_per_simd * wave_cycles / kHw.clock_hz * 1e6;
+  // phase skip: the steps of zero taps are not run (3x3 stride 2: 9 of 16)
+  if (v->phase_skip) plan->pred_mfma_us *= (2.0 * v->rc - 1) * (2.0 * v->sc - 1) / (4.0 * v->rc * v->sc);
   if (plan->dtype == CONV_DTYPE_F32) {
     // Issue efficiency of the fp32 inner loop.  Each step of a WK x WP wave
     // tile reads WK + WP operands from LDS for WK * WP MFMAs; measured
@@ -908,7 +917,7 @@ bool better(const conv_plan_t& a, const conv_plan_t& b) {
 }
 }  // namespace
 
-int enumerate_plans(const Shape& s0, int dtype, conv_plan_t* plans, int cap) {
+int enumerate_plans(const Shape& s0, int dtype, conv_plan_t* plans, int cap, bool phase_skip) {
   const Shape s = kernel_view(s0);
   int nv = 0;
   const Variant* vs = variants(&nv);
@@ -917,6 +926,7 @@ int enumerate_plans(const Shape& s0, int dtype, conv_plan_t* plans, int cap) {
   for (int vi = 0; vi < nv; ++vi) {
     const Variant& v = vs[vi];
     if (v.dtype != dtype) continue;
+    if (v.phase_skip && !phase_skip) continue;  // only for conv_fwd_ex's stride-2 odd-tap layers
     if (v.rc && (s.R != v.rc || s.S != v.sc)) continue;
     if (v.family == FAMILY_STREAM1X1 || v.family == FAMILY_STREAM1X1_LOOP) {
       // pixels per wave so that the workgroup count lands near a multiple

@@ -98,6 +98,12 @@ def emulate(g, In, Ker, wgs=None):
         _chk(g["family"] == 2 and g["in_vec"] == 1 and g["tc"] % nph == 0, "direct phase addressing")
         _chk(nph == g["na"] * g["nb"] and C == g["C0"] * nph, "phase counts")
         in_size = N * g["C0"] * g["H0"] * g["W0"]
+    # phase skip: chunks laid out phase-major in LDS (position f * TC/4 + c
+    # holds phase f of the chunk's input channel c), zero-tap steps left out
+    PSK = bool(g.get("phase_skip", 0))
+    if PSK:
+        _chk(nph == 4 and g["na"] == 2 and g["nb"] == 2 and g["sh"] == 2 and g["sw"] == 2, "four phases, stride 2")
+        _chk(g["tc"] % 16 == 0 and g["in_vec"] == 1 and R * S % g["ker_vec"] == 0, "phase-skip instance")
     _chk(In.size == in_size and Ker.size == ker_size, "input sizes")
     dma = g["family"] == 2
     MF32 = bool(g.get("mfma32", 0))
@@ -225,8 +231,13 @@ def emulate(g, In, Ker, wgs=None):
                 if nph:
                     # chunk-local input channel and phase, as the kernel splits them
                     _chk(c0 % nph == 0, "a pipeline step splits a channel's phases")
-                    cr = fdiv(cl, g, "nph")
-                    f = cl - cr * nph
+                    if PSK:
+                        cr, f = cl % (TC // 4), cl // (TC // 4)
+                        # the channel-count check on the inner channel
+                        valid = (e < TC * g["in_cstride"]) & (row < t["nrows"]) & (x < ncols) & (c0 + cr * 4 + f < C)
+                    else:
+                        cr = fdiv(cl, g, "nph")
+                        f = cl - cr * nph
                     a = fdiv(f, g, "nb")
                     b = f - a * g["nb"]
                     yi, xi = y, t["q0"] + x
@@ -256,7 +267,11 @@ def emulate(g, In, Ker, wgs=None):
                 e = ((i * NW + wave) * 64 + lane_t) * KV
                 kl = fdiv(e, g, "ker_rstride")
                 m = e - kl * g["ker_rstride"]
-                valid = (kl < BK) & (m < TCRS) & (t["k0"] + kl < K) & (m < mlim)
+                if PSK:  # LDS position (f * TC/4 + c) * RS + rs <- inner channel c * 4 + f
+                    m = ((m // RS) % (TC // 4) * 4 + (m // RS) // (TC // 4)) * RS + m % RS
+                    valid = (kl < BK) & (e - kl * g["ker_rstride"] < TCRS) & (t["k0"] + kl < K) & (m < mlim)
+                else:
+                    valid = (kl < BK) & (m < TCRS) & (t["k0"] + kl < K) & (m < mlim)
                 if KV > 1:
                     _chk(~valid | (m + KV <= mlim), "Ker vector straddles the channel range")
                     _chk(g["ker_rstride"] % KV == 0, "Ker vector straddles an LDS row")
@@ -266,6 +281,7 @@ def emulate(g, In, Ker, wgs=None):
                     vals = np.where(valid, Ker[np.clip(src, 0, ker_size - 1)], 0.0)
                     dst = e + q
                     _chk(dst < lker_n, "Ker DMA writes past its region")
+                    _chk(~valid | (m % RS + q < RS) if PSK else True, "phase-skip Ker vector leaves its channel")
                     _chk(np.isnan(fresh_k[dst]), "two lanes write one LDS Ker element")
                     fresh_k[dst] = vals
             lker[buf][:] = fresh_k
@@ -304,6 +320,10 @@ def emulate(g, In, Ker, wgs=None):
                 for cs in range(wv["wc"] * per, (wv["wc"] + 1) * per):
                     for r in range(R):
                         for s in range(S):
+                            if PSK:
+                                f = cs * CG // (TC // 4)  # the group's phase (a, b)
+                                if (f >> 1 == 1 and r == R - 1) or (f & 1 == 1 and s == S - 1):
+                                    continue  # a zero tap of this phase: the kernel leaves the step out
                             tap = r * g["in_wp"] + s
                             rs = r * S + s
                             A = []

@@ -493,6 +493,27 @@ def test_strided_full_config_full_compare(cfg):
     assert rel_err(out, ref) <= TOL["f32"]
 
 
+@pytest.mark.parametrize("shape", [
+    ConvShape("s2p0_3x3_c18_partial_chunk", 2, 18, 40, 113, 113, 3, 3, "f32", 91, 2, 0),
+    ConvShape("s2p1_3x3_c30", 2, 30, 64, 112, 112, 3, 3, "f32", 92, 2, 1),
+    ConvShape("s2p1_3x3_c16_k128", 1, 16, 128, 112, 112, 3, 3, "f32", 93, 2, 1),
+], ids=lambda s: s.name)
+def test_phase_skip_full_compare(shape):
+    """Stride-2 3x3 layers whose plan is the phase-skip variant of the
+    direct-to-LDS kernel (zero taps of the phases left out, In read through
+    the phase mapping; one with a partial last chunk of input channels):
+    every output against the oracle."""
+    p, direct = B.conv_fwd_ex_plan(*shape.key(), shape.stride, shape.pad)
+    g = B.conv_fwd_ex_geometry(*shape.key(), (2, 2), (shape.pad,) * 2, p)
+    assert direct and g["phase_skip"] == 1
+    In, Ker = make_inputs(shape)
+    say(f"[gpu] phase skip {shape.name} v{p['variant']}")
+    out = host(B.conv_fwd_ex(In.to(DEV), Ker.to(DEV), 2, shape.pad))
+    ref = oconv.conv_fwd_ex(host(In), host(Ker), (2, 2), (shape.pad,) * 2)
+    assert out.shape == ref.shape
+    assert rel_err(out, ref) <= TOL["f32"]
+
+
 def test_strided_padded_1x1_direct_full_compare():
     """A padded stride-2 1x1 layer whose plan is the balanced pointwise
     kernel reading In through the phase mapping (border pixels read zeros

@@ -340,6 +340,70 @@ def test_bal_direct_phase_addressing_indexing(shape):
     assert np.array_equal(hit, mine)
 
 
+PS_TWINS = {118: 192, 111: 192}  # regular variant -> phase-skip variant, same wave tile
+
+
+@pytest.mark.parametrize("shape", [
+    ConvShape("s2p1_3x3_c16", 2, 16, 32, 20, 20, 3, 3, "f32", 81, 2, 1),
+    ConvShape("s2p0_3x3_c12_odd", 1, 12, 24, 17, 15, 3, 3, "f32", 82, 2, 0),
+    ConvShape("s2p1_3x3_c36", 2, 36, 40, 13, 16, 3, 3, "f32", 83, 2, 1),
+    ConvShape("s2p0_3x3_c18_partial_chunk", 1, 18, 24, 21, 21, 3, 3, "f32", 84, 2, 0),
+], ids=lambda s: s.name)
+def test_phase_skip_indexing(shape):
+    """Phase-skip variants (stride-2 odd-tap layers through conv_fwd_ex):
+    each tiling of the inner problem's candidates on the twin with four input
+    channels per step, phase-major LDS chunks and the zero-tap steps left
+    out, against the strided, padded oracle (a wrongly skipped tap, or a
+    channel or phase mixed up, changes the result)."""
+    from tests.kernel_emulator import emulate_phase_split
+    In, Ker = make_inputs(shape)
+    In64, Ker64 = In.float().numpy().astype(np.float64), Ker.float().numpy().astype(np.float64)
+    st, pd = (shape.stride, shape.stride), (shape.pad, shape.pad)
+    _, Kp, inner = emulate_phase_split(In64, Ker64, st, pd)
+    ref = oconv.conv_fwd_ex(In64.astype(np.float32), Ker64.astype(np.float32), st, pd).reshape(-1)
+    done = set()
+    for p in B.conv_fwd_candidates(*inner[:7]):
+        ps = PS_TWINS.get(p["variant"])
+        key = (ps, p["tile_rows"], p["tile_cols"], p["waves_k"], p["split_c"])
+        if ps is None or key in done:
+            continue
+        q = dict(p, variant=ps)
+        try:
+            g = B.conv_fwd_ex_geometry(*shape.key(), st, pd, q)
+        except B.ConvError:
+            continue
+        done.add(key)
+        assert g["phase_skip"] == 1 and g["nph"] == 4
+        with pytest.raises(B.ConvError):
+            B.conv_fwd_geometry(*inner[:7], q)  # never on the plain problem
+        out, written = emulate(g, In64.reshape(-1), Kp.reshape(-1))
+        assert np.all(written == 1), q
+        assert np.max(np.abs(out - ref)) <= 1e-9 * max(1.0, np.max(np.abs(ref))), q
+    assert {k[0] for k in done} == {192}, done
+
+
+def test_phase_skip_selected_for_the_strided_3x3_layer():
+    """conv_fwd_ex's plan for the 3x3 stride-2 layer at batch 32 is a
+    phase-skip variant reading In directly; three of its workgroups emulated
+    against the oracle."""
+    from tests.kernel_emulator import emulate_phase_split
+    from paper_2101_09808_amd.workloads import BY_NAME
+    shape = BY_NAME["conv3x3s2p1_n32_c64_k128_in56"]
+    p, direct = B.conv_fwd_ex_plan(*shape.key(), shape.stride, shape.pad)
+    st, pd = (shape.stride,) * 2, (shape.pad,) * 2
+    g = B.conv_fwd_ex_geometry(*shape.key(), st, pd, p)
+    assert direct and g["phase_skip"] == 1
+    In, Ker = make_inputs(shape)
+    In64, Ker64 = In.numpy().astype(np.float64), Ker.numpy().astype(np.float64)
+    _, Kp, _ = emulate_phase_split(In64[:1], Ker64, st, pd)  # the rearranged Ker (batch-independent)
+    ref = oconv.conv_fwd_ex(In.numpy(), Ker.numpy(), st, pd).reshape(-1)
+    T = g["num_tiles"]
+    out, written = emulate(g, In64.reshape(-1), Kp.reshape(-1), wgs=[0, T // 2, T - 1])
+    hit = written == 1
+    assert written.max() == 1 and hit.sum() > 0
+    assert np.max(np.abs(out[hit] - ref[hit])) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
+
+
 @pytest.mark.parametrize("shape_index,aligned", [(2, True), (4, True), (2, False)])
 def test_bf16_transposing_bf16_out_indexing(shape_index, aligned):
     """Family 6 writing bf16 Out: 16-byte stores of eight pixels from lane
