@@ -733,14 +733,16 @@ def emulate_stream1x1(g, In, Ker, wgs=None):
 def emulate_stream1x1_bal(g, In, Ker, wgs=None):
     """The balanced pointwise kernel (family 7, conv1x1_bal_kernel).
 
-    Per workgroup PW = tw consecutive pixels from P0 = group * PW, with
-    128 NB < PW <= 128 NB + 16 (NB = max_ni).  Ker rows [k][c] go to LDS
+    PW = tw with 128 NB < PW <= 128 NB + 16 (NB = max_ni) sets the grid,
+    G = ceil(pixels / PW) workgroups per k tile; workgroup p takes 128-pixel
+    block j at (j G + p) 128 and the 16-pixel tail at NB G 128 + 16 p, pixels
+    past the end masked.  Ker rows [k][c] go to LDS
     (pitch C + 1) from 16-byte loads: lane (wave, i, lane) row
     16 wave + 4 i + lane // 16, channels 64 ch + 4 (lane % 16) .. + 3.
-    Wave s computes the 32-pixel blocks at P0 + 32 (4 j + s), j < NB, on
+    Wave s computes the 32-pixel blocks at (j G + p) 128 + 32 s, j < NB, on
     32x32x2 MFMAs, even and odd channel pairs in separate accumulators added
-    at the store, and k rows 16 s .. 16 s + 15 of the 16-pixel tail block at
-    P0 + 128 NB on 16x16x4 MFMAs.  In offsets are 32-bit byte offsets from
+    at the store, and k rows 16 s .. 16 s + 15 of the tail block on 16x16x4
+    MFMAs.  In offsets are 32-bit byte offsets from
     raw buffer loads (offsets at or past the buffer size read 0); every block
     but the last is stored during the next block, results 32 q / nq ..
     32 (q + 1) / nq - 1 at its step q, through 32-bit byte offsets of raw
@@ -824,8 +826,8 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
     for b in (range(g["grid"]) if wgs is None else wgs):
         kt, pg = b % g["tiles_k"], b // g["tiles_k"]
         k0 = kt * 64
-        P0 = pg * pw
-        pend = min(P0 + pw, total_px)
+        GP = g["tiles_rows"]
+        pend = total_px
         lds = np.full(64 * pitch, np.nan)  # the pad column is never read
         for wave in range(4):
             for ch in range(C // 64):
@@ -845,7 +847,7 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
         for wave in range(4):
             pending = None  # the previous block's 32 results, lane pixels and mask
             for j in range(NB):
-                px = P0 + 32 * (4 * j + wave) + l32
+                px = (j * GP + pg) * 128 + 32 * wave + l32
                 voff, inside = in_off(px, h32, pend)
                 valid = px < pend
                 acc = np.zeros((2, 2, 32, 32))  # [kb][e]
@@ -872,8 +874,8 @@ def emulate_stream1x1_bal(g, In, Ker, wgs=None):
                     for kb in range(2):
                         for v in range(16):
                             store(res[16 * kb + v], k0 + 32 * kb + 8 * (v // 4) + 4 * h32 + v % 4, px, valid)
-            # tail: 16 pixels at P0 + 128 NB, rows 16 wave .. 16 wave + 15
-            px = P0 + 128 * NB + l16
+            # tail: 16 pixels at NB G 128 + 16 p, rows 16 wave .. 16 wave + 15
+            px = NB * GP * 128 + 16 * pg + l16
             voff, inside = in_off(px, h16, pend)
             valid = px < pend
             acc16 = np.zeros((16, 16))

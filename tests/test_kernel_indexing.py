@@ -329,14 +329,20 @@ def test_bal_direct_phase_addressing_indexing(shape):
     assert written.max() == 1 and written.sum() > 0
     hit = written == 1
     assert np.max(np.abs(out[hit] - ref[hit])) <= 1e-9 * max(1.0, np.max(np.abs(ref)))
-    # every output of those workgroups' pixel ranges and 64-row k tiles is stored
+    # every output of those workgroups' pixels (128-pixel block j at
+    # (j G + p) 128, the 16-pixel tail at NB G 128 + 16 p) and 64-row k
+    # tiles is stored
     PQ = ref.size // (shape.N * shape.K)
     i = np.arange(ref.size)
     px, k = i % PQ + (i // (shape.K * PQ)) * PQ, (i // PQ) % shape.K
+    GP, NB = g["tiles_rows"], g["max_ni"]
     mine = np.zeros(ref.size, bool)
     for b in (0, G // 2, G - 1):
         kt, pg = b % g["tiles_k"], b // g["tiles_k"]
-        mine |= (px >= pg * g["tw"]) & (px < (pg + 1) * g["tw"]) & (k // 64 == kt)
+        own = (px >= NB * GP * 128 + 16 * pg) & (px < NB * GP * 128 + 16 * pg + 16)
+        for j in range(NB):
+            own |= (px >= (j * GP + pg) * 128) & (px < (j * GP + pg + 1) * 128)
+        mine |= own & (k // 64 == kt)
     assert np.array_equal(hit, mine)
 
 
