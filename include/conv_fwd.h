@@ -91,7 +91,10 @@ enum {
  * channels staged per pipeline step (all R x S taps at once).  The wave
  * (register-level) tile is `wave_k` x `wave_px`; accumulators stay in
  * registers for the whole reduction (the Out-stationary classes
- * <{n,k,h,w},{c,r},s> / <{n,k,h,w},{c,s},r> of Sec. 4).
+ * <{n,k,h,w},{c,r},s> / <{n,k,h,w},{c,s},r> of Sec. 4).  Exception: the
+ * balanced pointwise kernel of 1x1 layers takes `tile_cols` pixels of the
+ * flattened n*H*W index per workgroup, not as one range but as 128-pixel
+ * blocks handed out in grid stride plus one 16-pixel tail block.
  */
 typedef struct {
   int dtype;          /* CONV_DTYPE_*                                        */
