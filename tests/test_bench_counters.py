@@ -115,3 +115,45 @@ def test_bf16_calibration_layers_admit_every_transposing_tiling():
             n = B.lib().conv_fwd_candidates(*c.key(), B.CONV_DTYPE_BF16, None, 0)
             cands = B.conv_fwd_candidates(*c.key(), dtype=B.CONV_DTYPE_BF16, cap=n)
             assert {211, 212, 213, 214, 215, 216} <= {p["variant"] for p in cands}, c
+
+
+def _selected(c):
+    from paper_2101_09808_amd import conv as B
+    dt = B.CONV_DTYPE_BF16 if c.dtype == "bf16" else B.CONV_DTYPE_F32
+    return B.conv_fwd_plan(*c.key(), dtype=dt)
+
+
+def test_committed_counter_profiles_match_the_selected_kernels():
+    """The committed counter figures (model vs counters, the headline's HBM
+    traffic) were taken on the kernels and plans that the current sources
+    select: a change to a selected kernel, its instance or its plan leaves
+    them stale, and this fails until they are measured again."""
+    import json
+    from paper_2101_09808_amd.workloads import BY_NAME
+    prof = os.path.join(bench.ROOT, "profiles")
+    mv = json.load(open(os.path.join(prof, "model_vs_counters.json")))
+    assert {l["workload"] for l in mv["layers"]} == {c.name for c in CONFIGS}
+    for l in mv["layers"]:
+        c = BY_NAME[l["workload"]]
+        p = _selected(c)
+        assert (p["variant"], bench.plan_kernel_hash(c, p)) == (l["plan_variant"], l["plan_kernel_sha"]), c.name
+    t = json.load(open(bench.TRAFFIC_FILE))
+    c = BY_NAME[bench.HEADLINE]
+    p = _selected(c)
+    assert (p["variant"], bench.plan_kernel_hash(c, p)) == (t["plan_variant"], t["kernel_sha"])
+
+
+def test_model_levels_bracket_the_measured_traffic():
+    """Acceptance band of the per-level model against the counters (the paper
+    validates rank only; this band is the build's own): for every layer the
+    fabric bytes measured (FETCH_SIZE + WRITE_SIZE, copy-scaled) lie between
+    the model's compulsory bytes (its HBM level, less 2% for counter
+    rounding) and 1.3x its L2 level plus Out, the traffic if no tile's
+    operands were shared through the L2; and the L2->CU read requests lie
+    within 0.7-1.3x the model's LDS level in 128-byte lines."""
+    import json
+    mv = json.load(open(os.path.join(bench.ROOT, "profiles", "model_vs_counters.json")))
+    for l in mv["layers"]:
+        assert l["hbm_meas"] >= 0.98 * l["hbm_pred"], l["workload"]
+        assert l["hbm_meas"] <= 1.3 * max(l["l2_pred"], l["hbm_pred"]), l["workload"]
+        assert 0.7 <= l["l2cu_meas"] / l["l2cu_pred"] <= 1.3, l["workload"]
