@@ -720,6 +720,7 @@ int score_plan_impl(const Shape& s0, conv_plan_t* plan) {
   const double line = 128.0;
   auto run_bytes = [&](double L) { return L > 0 ? L + line - e : 0.0; };
   double in_tiles = 0;  // sum over pixel tiles of the halo footprint, bytes per channel, in lines
+  std::vector<double> tile_halo((size_t)g.tiles_rows * g.tiles_cols);  // the same per tile rt * tiles_cols + ct
   for (int64_t rt = 0; rt < g.tiles_rows; ++rt) {
     const int64_t r0 = rt * g.tr, r1 = std::min<int64_t>(r0 + g.tr, NP) - 1;
     const int64_t nu0 = (r0 / g.P) * s.H + r0 % g.P, nu1 = (r1 / g.P) * s.H + r1 % g.P + s.R - 1;
@@ -727,7 +728,9 @@ int score_plan_impl(const Shape& s0, conv_plan_t* plan) {
     for (int64_t ct = 0; ct < g.tiles_cols; ++ct) {
       const int64_t cols = std::min<int64_t>(g.tw, g.Q - ct * g.tw) + s.S - 1;
       const double span = run_bytes(((rows - 1) * s.W + cols) * e);
-      in_tiles += std::min(span, rows * run_bytes((double)cols * e));
+      const double t = std::min(span, rows * run_bytes((double)cols * e));
+      tile_halo[(size_t)(rt * g.tiles_cols + ct)] = t * s.C;
+      in_tiles += t;
     }
   }
   const double in_halo_bytes = in_tiles * s.C;          // one pass over all pixel tiles
@@ -758,7 +761,41 @@ int score_plan_impl(const Shape& s0, conv_plan_t* plan) {
   // L2: outer tile-loop order of the grid, per XCD.
   const double in_bytes = (double)s.N * s.C * s.H * s.W * e;
   const double out_bytes = (double)s.N * s.K * g.P * g.Q * 4.0;
-  if (plan->grid_order == 0) {
+  const bool one_tile_per_wg = v->family == FAMILY_DMA || v->family == FAMILY_STAGED;
+  if (one_tile_per_wg && g.split == 1 && g.grid == g.num_tiles && g.grid <= kHw.cus) {
+    // One round: every tile is in flight at once.  Workgroup b runs on XCD
+    // b mod 8 and takes tile L = xcd_remap(b), so each XCD holds one
+    // contiguous range of L (and at most one of the last G mod 8 tiles); its
+    // L2 fetches each In halo tile and each k slice of Ker that the range
+    // touches once.  With k tiles innermost (order 0) a range spans few
+    // pixel tiles and every k slice; with pixel tiles innermost (order 1),
+    // the reverse.
+    const int64_t G = g.num_tiles, G8 = G & ~int64_t(7), per = G8 / 8;
+    const double ker_slice = ker_line_bytes / g.tiles_k;
+    std::vector<char> seen_px(tile_halo.size()), seen_k((size_t)g.tiles_k);
+    double l2 = 0;
+    auto take = [&](int64_t L) {
+      int64_t kt, px;
+      if (plan->grid_order == 0) {
+        kt = L % g.tiles_k;
+        px = L / g.tiles_k;
+      } else {
+        const int64_t ct = L % g.tiles_cols, rest = L / g.tiles_cols;
+        kt = rest / g.tiles_rows;
+        px = (rest % g.tiles_rows) * g.tiles_cols + ct;
+      }
+      if (!seen_px[(size_t)px]) seen_px[(size_t)px] = 1, l2 += tile_halo[(size_t)px];
+      if (!seen_k[(size_t)kt]) seen_k[(size_t)kt] = 1, l2 += ker_slice;
+    };
+    for (int x = 0; x < 8; ++x) {
+      std::fill(seen_px.begin(), seen_px.end(), 0);
+      std::fill(seen_k.begin(), seen_k.end(), 0);
+      for (int64_t L = x * per; L < (x + 1) * per; ++L) take(L);
+      if (G8 + x < G) take(G8 + x);
+    }
+    plan->pred_bytes[CONV_LVL_L2] = l2;
+    plan->class_lvl[CONV_LVL_L2] = plan->grid_order == 0 ? 5 : 1;
+  } else if (plan->grid_order == 0) {
     // k tiles innermost: each pixel tile's halo is fetched once.  Every XCD
     // needs the whole kernel tensor; it stays resident if it fits in half the
     // XCD's L2, else it is re-fetched once per group of pixel tiles that are
