@@ -2020,6 +2020,8 @@ const Instance kInstances[] = {
     F32_STREAM1X1_BAL(328, 2, 16, 16),
     F32_STREAM1X1_BAL(329, 2, 16, 128),
     F32_STREAM1X1_BAL(330, 1, 16, 128),
+    F32_STREAM1X1_BAL(331, 3, 16, 96),
+    F32_STREAM1X1_BAL(332, 2, 16, 96),
     F32_STREAM1X1_LOOP(311, 4, 3, 8),
     F32_STREAM1X1_LOOP(312, 4, 0, 8),
     F32_STREAM1X1_LOOP(313, 2, 2, 8),

@@ -269,6 +269,7 @@ VARIANT_SHAPES = [
     ConvShape("var1x1_bal_c128", 2, 128, 64, 18, 22, 1, 1, "f32", 41),
     ConvShape("var1x1_bal_c256", 2, 256, 80, 18, 22, 1, 1, "f32", 42),
     ConvShape("var1x1_bal_c512", 2, 512, 64, 18, 22, 1, 1, "f32", 43),
+    ConvShape("var1x1_bal_c384", 2, 384, 64, 18, 22, 1, 1, "f32", 44),
 ]
 
 
